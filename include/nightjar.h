@@ -1,0 +1,232 @@
+/*
+ * nightjar.h -- C ABI of the batched speculative verify step on MI355X (gfx950).
+ *
+ * Nightjar (arXiv 2512.22420) serves requests with speculative decoding whose
+ * speculative length gamma is chosen per batch size B by a bandit planner
+ * (Sec. 5), gamma = 0 meaning plain decoding (Sec. 4).  The computation whose
+ * cost that planner trades off is the verify step: the target model scores
+ * all gamma drafts of each of the B sequences in one forward pass (Sec. 2.2),
+ * the acceptance test keeps the longest accepted prefix and adds one corrected
+ * or bonus token (Sec. 3.1; Sec. 5.1 "committed tokens"), and only accepted
+ * tokens' keys and values are committed to the paged KV cache before the next
+ * step (PagedAttention, Sec. 2.1; step-level finalisation, Sec. 6.5).
+ *
+ * In this header gamma is written k.  The target is a Llama-style decoder:
+ * RMSNorm, rotate-half RoPE, grouped-query attention, SwiGLU FFN, untied LM
+ * head, no biases.
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ * - Pointers marked "device" are device memory on the current HIP device and
+ *   stay owned by the caller; descriptor structs and pointer arrays inside them
+ *   are host memory, read during the call only.
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *   stream) and makes no device allocation; scratch lives in the caller's
+ *   workspace.
+ * - Return value: NJ_OK (0) on success, otherwise a negative NJ_E* code and
+ *   nightjar_last_error() describes the problem.  Argument errors are found on
+ *   the host before anything is enqueued.  Bad data found by the kernels (token
+ *   or block ids out of range, a context that does not fit the block table)
+ *   is skipped without any out-of-bounds access and recorded in the workspace;
+ *   nightjar_device_error() reports it.  Outputs are undefined after an error.
+ * - Element types: dtype NJ_BF16 stores weights, KV pages and window K/V as
+ *   bf16 (round-to-nearest-even); NJ_F32 stores them as fp32.  Logits,
+ *   draft probabilities and uniforms are fp32 in both; ids are int32.
+ *
+ * Layouts (row-major, reduction dimension contiguous)
+ * ----------------------------------------------------
+ *   embed, lm_head     [V][d]
+ *   w_qkv              [(H + 2*Hkv) * D][d]   query rows, then key rows, then value rows
+ *   w_o                [d][H * D]
+ *   w_gate_up          [2F][d]                gate rows, then up rows
+ *   w_down             [d][F]
+ *   norms              [d]
+ *   k_pages[l]         [num_blocks][Hkv][block_size][D]
+ *   v_pages[l]         [num_blocks][Hkv][D][block_size]   (dim-major inside a block)
+ *   block_table        [B][max_blocks]   logical block j of sequence b -> physical block
+ *   Cached K is stored after RoPE; V as is.  Token t of sequence b lives in
+ *   block block_table[b][t / block_size], slot t % block_size.  block_size
+ *   must be 16.
+ */
+#ifndef NIGHTJAR_H
+#define NIGHTJAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { NJ_F32 = 0, NJ_BF16 = 1 };
+
+enum {
+  NJ_OK = 0,
+  NJ_EINVAL = -1,  /* bad argument (null pointer, bad size, workspace too small, ...) */
+  NJ_EDEVICE = -2, /* the kernels found bad data (see nightjar_device_error)          */
+  NJ_EHIP = -3     /* a HIP runtime call failed                                       */
+};
+
+/* Device-side error bits reported by nightjar_device_error(). */
+enum {
+  NJ_DEV_BAD_TOKEN = 1,   /* a window or draft token id outside [0, V)                 */
+  NJ_DEV_BAD_BLOCK = 2,   /* a needed block-table entry outside [0, num_blocks)          */
+  NJ_DEV_BAD_CONTEXT = 4, /* context_lens[b] < 0 or context_lens[b]+k+1 > max_blocks*16  */
+  NJ_DEV_BAD_ACCEPT = 8   /* kv_append: accepted_len[b] outside [0, k]                   */
+};
+
+typedef struct nj_model_desc {
+  int32_t n_layers;   /* L                      */
+  int32_t d_model;    /* d                      */
+  int32_t n_heads;    /* H query heads          */
+  int32_t n_kv_heads; /* Hkv; H % Hkv == 0      */
+  int32_t head_dim;   /* D (even)               */
+  int32_t ffn_dim;    /* F                      */
+  int32_t vocab;      /* V                      */
+  int32_t block_size; /* tokens per KV block: 16 */
+  float rms_eps;
+  float rope_theta;
+  int32_t dtype;      /* NJ_F32 or NJ_BF16      */
+} nj_model_desc;
+
+typedef struct nj_layer_weights {
+  const void* attn_norm; /* [d]                    */
+  const void* w_qkv;     /* [(H+2Hkv)*D][d]        */
+  const void* w_o;       /* [d][H*D]               */
+  const void* ffn_norm;  /* [d]                    */
+  const void* w_gate_up; /* [2F][d]                */
+  const void* w_down;    /* [d][F]                 */
+} nj_layer_weights;
+
+typedef struct nj_weights {
+  const void* embed;              /* device [V][d]                      */
+  const void* final_norm;         /* device [d]                         */
+  const void* lm_head;            /* device [V][d]                      */
+  const nj_layer_weights* layers; /* host array of n_layers; entries are device pointers */
+} nj_weights;
+
+typedef struct nj_kv_cache {
+  void* const* k_pages; /* host array of n_layers device pointers: [num_blocks][Hkv][16][D] */
+  void* const* v_pages; /* host array of n_layers device pointers: [num_blocks][Hkv][D][16] */
+  int32_t num_blocks;
+} nj_kv_cache;
+
+/*
+ * Bytes of workspace a verify step with up to max_B sequences and up to max_k
+ * drafts each needs (0 if the descriptor is invalid).  A workspace sized for
+ * (max_B, max_k) serves every smaller (B, k).
+ */
+size_t nightjar_workspace_bytes(const nj_model_desc* desc, int32_t max_B, int32_t max_k);
+
+/*
+ * Prepare a fresh workspace (clears its device error word).  Call once after
+ * allocating it; device memory, workspace_bytes from nightjar_workspace_bytes.
+ */
+int nightjar_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * nightjar_verify_step -- one speculative verify step for B sequences with k
+ * drafts each (Sec. 2.2 "verifying": all k drafts scored in one target forward;
+ * Sec. 3.1: n accepted plus one token committed).
+ *
+ * Window of sequence b: token 0 is last_tokens[b] (the last committed token,
+ * whose KV is not yet cached), tokens 1..k are draft_tokens[b][0..k-1]; window
+ * token i sits at position context_lens[b] + i and attends to every cached
+ * token of b and to window tokens 0..i.  Target row i gives p_i, the target
+ * distribution of the token after window token i (softmax of the logits,
+ * temperature 1, no truncation).
+ *
+ * Acceptance (the standard speculative-sampling test the paper cites; its
+ * output distribution is the target's, Sec. 1 and Sec. 6.5): for i = 0..k-1,
+ * draft x = draft_tokens[b][i] is accepted iff uniforms[b][i] < p_i(x) / q_i(x)
+ * with q_i(x) = draft_probs[b][i][x] (q_i(x) == 0 counts as accepted); the
+ * first rejection at n stops the loop and one token is drawn from
+ * max(0, p_n - q_n) (from p_n if that is all zero); if all k are accepted the
+ * bonus token is drawn from p_k.  The draw uses uniforms[b][k]: the smallest j
+ * whose running sum of weights (index order) exceeds uniforms[b][k] times the
+ * total.
+ *
+ *   desc, w, kv         model and cache (see layouts above)
+ *   block_table         device int32 [B][max_blocks]
+ *   context_lens        device int32 [B]   cached tokens per sequence (not modified)
+ *   last_tokens         device int32 [B]
+ *   draft_tokens        device int32 [B][k]      may be NULL when k == 0
+ *   draft_probs         device fp32  [B][k][V]   may be NULL when k == 0
+ *   uniforms            device fp32  [B][k+1]    values in [0, 1)
+ *   B >= 1, 0 <= k <= 15 (the window fits one 16-token block)
+ *   accepted_len        device int32 [B]         out: n_b
+ *   next_tokens         device int32 [B][k+1]    out: drafts[0..n_b-1], the drawn token, then -1
+ *   target_logits       device fp32  [B][k+1][V] out, or NULL (then kept in the workspace)
+ *   workspace           device, >= nightjar_workspace_bytes(desc, B, k) bytes; it also
+ *                       keeps the window K/V for the following nightjar_kv_append
+ */
+int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv,
+                         const int32_t* block_table, int32_t max_blocks, const int32_t* context_lens,
+                         const int32_t* last_tokens, const int32_t* draft_tokens, const float* draft_probs,
+                         const float* uniforms, int32_t B, int32_t k,
+                         int32_t* accepted_len, int32_t* next_tokens, float* target_logits,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * nightjar_kv_append -- commit the accepted window rows (Sec. 6.5: a step is
+ * finalised before the next begins; rejected drafts leave no KV behind).
+ *
+ * For each b, window rows 0..accepted_len[b] (the last committed token plus the
+ * accepted drafts) are written to positions context_lens[b] + j of the pages,
+ * then context_lens[b] += accepted_len[b] + 1 on the device.  The emitted token
+ * is not appended: it is the next step's last token.  Must follow the
+ * nightjar_verify_step that filled `workspace`, with the same desc, kv,
+ * block_table, max_blocks, B and k, before another verify step reuses it.
+ *
+ *   context_lens   device int32 [B], in/out
+ *   accepted_len   device int32 [B]
+ */
+int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const int32_t* block_table,
+                       int32_t max_blocks, int32_t* context_lens, const int32_t* accepted_len,
+                       int32_t B, int32_t k, const void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Waits for `stream`, then returns the NJ_DEV_* bits the kernels recorded in
+ * `workspace` since the last call (and clears them), or a negative NJ_E* code.
+ */
+int nightjar_device_error(void* workspace, size_t workspace_bytes, void* stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* nightjar_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * Stage entry points: single stages of the verify step, with the kernels the
+ * step uses, for stage-level parity tests and kernel timing.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * Acceptance alone, from given target logits (the acceptance rule above).
+ *   logits [B][k+1][V] fp32, draft_tokens [B][k], draft_probs [B][k][V],
+ *   uniforms [B][k+1]; outputs as in nightjar_verify_step.  workspace from
+ *   nightjar_workspace_bytes(desc, B, k) (only desc->vocab is read).
+ */
+int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_t* draft_tokens,
+                    const float* draft_probs, const float* uniforms, int32_t B, int32_t k,
+                    int32_t* accepted_len, int32_t* next_tokens, void* workspace, size_t workspace_bytes,
+                    void* stream);
+
+/* Epilogues of nightjar_gemm. */
+enum {
+  NJ_GEMM_STORE = 0,    /* y[m][n] = acc (fp32 out)                                  */
+  NJ_GEMM_RESIDUAL = 1, /* y[m][n] += acc (fp32 in/out)                              */
+  NJ_GEMM_SWIGLU = 2    /* N = 2F weight rows; y[m][f] = silu(acc_f) * acc_{F+f}, y in
+                           the weight dtype, [M][F]                                 */
+};
+
+/*
+ * y = x . w^T with the step's GEMM kernels.  x [M][K] and w [N][K] in `dtype`
+ * (NJ_BF16 or NJ_F32); y as the epilogue says.  M >= 1; K % 32 == 0 for bf16.
+ */
+int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
+                  int32_t epilogue, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NIGHTJAR_H */

@@ -4,5 +4,5 @@ Only the tests, the smoke check and the benchmark's CPU-baseline leg use it;
 the HIP library never does.
 """
 from .verify_step import (accept, attention, forward_window, gather_cache, invcdf,  # noqa: F401
-                          kv_append, rms_norm, rope, silu, softmax, verify_step, widen,
-                          window_tokens, Weights64)
+                          kv_append, linear, rms_norm, rope, silu, softmax, verify_step, widen,
+                          window_tokens)

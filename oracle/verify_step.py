@@ -26,7 +26,7 @@ What it computes (Nightjar, arXiv 2512.22420):
 The target is a Llama-style decoder (RMSNorm, rotate-half RoPE, grouped-query
 attention, SwiGLU FFN, untied LM head).  Every floating-point step runs in
 fp64 on the exact stored weight values (bf16 bit patterns are widened
-exactly).  Readings of points the paper leaves open are listed where they are
+exactly; large matrices are widened one block of rows at a time).  Readings of points the paper leaves open are listed where they are
 used; all of them are also collected in the design notes of the repository.
 
 Parity: the acceptance rule and the inverse-CDF draw are pinned by exact
@@ -132,57 +132,52 @@ def attention(q: np.ndarray, k_cache: np.ndarray, v_cache: np.ndarray,
 # --------------------------------------------------------------------------
 # Forward over the verify window
 # --------------------------------------------------------------------------
-class Weights64:
-    """Model weights widened once to fp64."""
-
-    def __init__(self, weights: Dict, shape):
-        dt = shape.dtype
-        self.shape = shape
-        self.embed = widen(weights["embed"], dt)
-        self.lm_head = widen(weights["lm_head"], dt)
-        self.final_norm = widen(weights["final_norm"], dt)
-        self.layers = [{name: widen(arr, dt) for name, arr in lw.items()} for lw in weights["layers"]]
+def linear(x: np.ndarray, w: np.ndarray, dtype: str, rows: int = 8192) -> np.ndarray:
+    """x @ W^T for a weight stored [N, K]; W is widened to fp64 one block of rows
+    at a time so that no full fp64 copy of a large matrix is made."""
+    out = np.empty((x.shape[0], w.shape[0]))
+    for r0 in range(0, w.shape[0], rows):
+        out[:, r0: r0 + rows] = x @ widen(w[r0: r0 + rows], dtype).T
+    return out
 
 
-def forward_window(w: Weights64, k_pages: Sequence[np.ndarray], v_pages: Sequence[np.ndarray],
+def forward_window(weights: Dict, shape, k_pages: Sequence[np.ndarray], v_pages: Sequence[np.ndarray],
                    block_table: np.ndarray, context_lens: np.ndarray,
                    tokens: np.ndarray) -> Tuple[np.ndarray, List[np.ndarray], List[np.ndarray]]:
     """Target forward over each sequence's window tokens against its paged cache.
 
     tokens [B, T]: window token ids (last committed token, then the drafts);
-    window row i sits at position context_lens[b] + i.
+    window row i of sequence b sits at position context_lens[b] + i.  The
+    linear layers act on every row independently, so all B*T rows go through
+    them together; attention is per sequence.
     Returns logits [B, T, V] and, per layer, the window's post-RoPE keys and
     its values, each [B, T, Hkv, D].
     """
-    s = w.shape
+    s, dt = shape, shape.dtype
     H, Hkv, D, F = s.n_heads, s.n_kv_heads, s.head_dim, s.ffn_dim
     B, T = tokens.shape
-    logits = np.empty((B, T, s.vocab))
-    win_k = [np.empty((B, T, Hkv, D)) for _ in range(s.n_layers)]
-    win_v = [np.empty((B, T, Hkv, D)) for _ in range(s.n_layers)]
-    for b in range(B):
-        ctx = int(context_lens[b])
-        pos = ctx + np.arange(T)
-        h = w.embed[tokens[b]].copy()                       # [T, d]
-        for l, lw in enumerate(w.layers):
-            x = rms_norm(h, lw["attn_norm"], s.rms_eps)
-            qkv = x @ lw["w_qkv"].T
-            q = qkv[:, : H * D].reshape(T, H, D)
-            k = qkv[:, H * D: (H + Hkv) * D].reshape(T, Hkv, D)
-            v = qkv[:, (H + Hkv) * D:].reshape(T, Hkv, D)
-            q = rope(q, pos, s.rope_theta)
-            k = rope(k, pos, s.rope_theta)
-            win_k[l][b], win_v[l][b] = k, v
-            kc, vc = gather_cache(k_pages[l], v_pages[l], block_table[b], ctx, s.block_size)
-            kc, vc = widen(kc, s.dtype), widen(vc, s.dtype)
-            o = attention(q, kc, vc, k, v)
-            h = h + o.reshape(T, H * D) @ lw["w_o"].T
-            x = rms_norm(h, lw["ffn_norm"], s.rms_eps)
-            gu = x @ lw["w_gate_up"].T
-            a = silu(gu[:, :F]) * gu[:, F:]
-            h = h + a @ lw["w_down"].T
-        x = rms_norm(h, w.final_norm, s.rms_eps)
-        logits[b] = x @ w.lm_head.T
+    pos = (np.asarray(context_lens, dtype=np.int64)[:, None] + np.arange(T)[None, :]).reshape(-1)
+    h = widen(weights["embed"][np.asarray(tokens).reshape(-1)], dt)     # [B*T, d]
+    win_k, win_v = [], []
+    for l, lw in enumerate(weights["layers"]):
+        x = rms_norm(h, widen(lw["attn_norm"], dt), s.rms_eps)
+        qkv = linear(x, lw["w_qkv"], dt)
+        q = rope(qkv[:, : H * D].reshape(-1, H, D), pos, s.rope_theta)
+        k = rope(qkv[:, H * D: (H + Hkv) * D].reshape(-1, Hkv, D), pos, s.rope_theta)
+        v = qkv[:, (H + Hkv) * D:].reshape(-1, Hkv, D)
+        o = np.empty_like(q)
+        for b in range(B):
+            rows = slice(b * T, (b + 1) * T)
+            kc, vc = gather_cache(k_pages[l], v_pages[l], block_table[b], int(context_lens[b]), s.block_size)
+            o[rows] = attention(q[rows], widen(kc, dt), widen(vc, dt), k[rows], v[rows])
+        win_k.append(k.reshape(B, T, Hkv, D))
+        win_v.append(v.reshape(B, T, Hkv, D))
+        h = h + linear(o.reshape(-1, H * D), lw["w_o"], dt)
+        x = rms_norm(h, widen(lw["ffn_norm"], dt), s.rms_eps)
+        gu = linear(x, lw["w_gate_up"], dt)
+        h = h + linear(silu(gu[:, :F]) * gu[:, F:], lw["w_down"], dt)
+    x = rms_norm(h, widen(weights["final_norm"], dt), s.rms_eps)
+    logits = linear(x, weights["lm_head"], dt).reshape(B, T, s.vocab)
     return logits, win_k, win_v
 
 
@@ -249,18 +244,17 @@ def window_tokens(last_tokens: np.ndarray, draft_tokens: np.ndarray) -> np.ndarr
 
 
 def verify_step(weights, shape, k_pages, v_pages, block_table, context_lens,
-                last_tokens, draft_tokens, draft_probs, uniforms, w64: Optional[Weights64] = None) -> Dict:
+                last_tokens, draft_tokens, draft_probs, uniforms) -> Dict:
     """One verify step for B sequences with gamma drafts each.
 
     Returns accepted_len [B], next_tokens [B, gamma+1] (-1 past the n+1
     emitted tokens), logits [B, gamma+1, V], target probabilities, and the
     window keys/values that a KV append would commit.
     """
-    w64 = w64 if w64 is not None else Weights64(weights, shape)
     B = len(last_tokens)
     toks = window_tokens(last_tokens, draft_tokens)
     gamma = toks.shape[1] - 1
-    logits, win_k, win_v = forward_window(w64, k_pages, v_pages, block_table, context_lens, toks)
+    logits, win_k, win_v = forward_window(weights, shape, k_pages, v_pages, block_table, context_lens, toks)
     probs = softmax(logits)
     acc = np.zeros(B, dtype=np.int32)
     nxt = np.full((B, gamma + 1), -1, dtype=np.int32)

@@ -1,0 +1,135 @@
+"""ctypes binding of libnightjar.so: the C ABI of ``include/nightjar.h`` with the
+same names.  Argument marshalling only; every step runs in the HIP library.
+Device pointers are passed as Python ints (e.g. ``tensor.data_ptr()``), the
+stream as a ``hipStream_t`` int (``torch.cuda.current_stream().cuda_stream``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnightjar.so")
+
+NJ_F32, NJ_BF16 = 0, 1
+NJ_OK, NJ_EINVAL, NJ_EDEVICE, NJ_EHIP = 0, -1, -2, -3
+NJ_DEV_BAD_TOKEN, NJ_DEV_BAD_BLOCK, NJ_DEV_BAD_CONTEXT, NJ_DEV_BAD_ACCEPT = 1, 2, 4, 8
+NJ_GEMM_STORE, NJ_GEMM_RESIDUAL, NJ_GEMM_SWIGLU = 0, 1, 2
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_sz = ctypes.c_size_t
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32), ("n_kv_heads", _i32),
+                ("head_dim", _i32), ("ffn_dim", _i32), ("vocab", _i32), ("block_size", _i32),
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("dtype", _i32)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [("attn_norm", _vp), ("w_qkv", _vp), ("w_o", _vp), ("ffn_norm", _vp),
+                ("w_gate_up", _vp), ("w_down", _vp)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [("embed", _vp), ("final_norm", _vp), ("lm_head", _vp), ("layers", ctypes.POINTER(LayerWeights))]
+
+
+class KvCache(ctypes.Structure):
+    _fields_ = [("k_pages", ctypes.POINTER(_vp)), ("v_pages", ctypes.POINTER(_vp)), ("num_blocks", _i32)]
+
+
+class NightjarError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"nightjar error {code}: {msg}")
+        self.code = code
+
+
+_LIB = None
+
+_SIGS = {
+    "nightjar_workspace_bytes": (_sz, [ctypes.POINTER(ModelDesc), _i32, _i32]),
+    "nightjar_workspace_init": (ctypes.c_int, [_vp, _sz, _vp]),
+    "nightjar_verify_step": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.POINTER(KvCache),
+                                            _vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp,
+                                            _vp, _sz, _vp]),
+    "nightjar_kv_append": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(KvCache), _vp, _i32, _vp, _vp,
+                                          _i32, _i32, _vp, _sz, _vp]),
+    "nightjar_device_error": (ctypes.c_int, [_vp, _sz, _vp]),
+    "nightjar_last_error": (ctypes.c_char_p, []),
+    "nightjar_accept": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp,
+                                       _sz, _vp]),
+    "nightjar_gemm": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Load the built library; fails loudly if it is missing (there is no fallback)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2512_22420_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = res, args
+        _LIB = L
+    return _LIB
+
+
+def last_error() -> str:
+    return lib().nightjar_last_error().decode()
+
+
+def _check(rc: int) -> int:
+    if rc < 0:
+        raise NightjarError(rc, last_error())
+    return rc
+
+
+def workspace_bytes(desc: ModelDesc, max_B: int, max_k: int) -> int:
+    n = lib().nightjar_workspace_bytes(ctypes.byref(desc), max_B, max_k)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def workspace_init(workspace: int, nbytes: int, stream: int = 0) -> None:
+    _check(lib().nightjar_workspace_init(workspace, nbytes, stream))
+
+
+def verify_step(desc, weights, kv, block_table, max_blocks, context_lens, last_tokens, draft_tokens, draft_probs,
+                uniforms, B, k, accepted_len, next_tokens, target_logits, workspace, workspace_nbytes,
+                stream: int = 0) -> None:
+    _check(lib().nightjar_verify_step(ctypes.byref(desc), ctypes.byref(weights), ctypes.byref(kv), block_table,
+                                      max_blocks, context_lens, last_tokens, draft_tokens, draft_probs, uniforms,
+                                      B, k, accepted_len, next_tokens, target_logits, workspace, workspace_nbytes,
+                                      stream))
+
+
+def kv_append(desc, kv, block_table, max_blocks, context_lens, accepted_len, B, k, workspace, workspace_nbytes,
+              stream: int = 0) -> None:
+    _check(lib().nightjar_kv_append(ctypes.byref(desc), ctypes.byref(kv), block_table, max_blocks, context_lens,
+                                    accepted_len, B, k, workspace, workspace_nbytes, stream))
+
+
+def device_error(workspace: int, workspace_nbytes: int, stream: int = 0) -> int:
+    return _check(lib().nightjar_device_error(workspace, workspace_nbytes, stream))
+
+
+def accept(desc, logits, draft_tokens, draft_probs, uniforms, B, k, accepted_len, next_tokens, workspace,
+           workspace_nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_accept(ctypes.byref(desc), logits, draft_tokens, draft_probs, uniforms, B, k,
+                                 accepted_len, next_tokens, workspace, workspace_nbytes, stream))
+
+
+def gemm(dtype, x, w, y, M, N, K, epilogue, stream: int = 0) -> None:
+    _check(lib().nightjar_gemm(dtype, x, w, y, M, N, K, epilogue, stream))
+
+
+def header_functions(header_path: str):
+    """Names of the functions declared in the C header (used by the ABI tests)."""
+    import re
+    text = open(header_path).read()
+    return sorted(set(re.findall(r"\b(nightjar_[a-z_]+)\s*\(", text)))

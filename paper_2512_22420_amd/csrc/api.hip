@@ -1,0 +1,294 @@
+// C ABI of the verify step: argument checks, workspace layout, and the kernel
+// sequence of one step on one stream (no host synchronisation inside a step).
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <string>
+#include <unordered_map>
+
+#include "../../include/nightjar.h"
+#include "kernels.h"
+
+using namespace nj;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(NJ_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+constexpr int kMaxK = 15;
+constexpr int kMaxVocab = 524288;
+
+size_t al(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct Layout {
+  size_t err, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats, total;
+  size_t win_layer_bytes;
+};
+
+bool desc_ok(const nj_model_desc* d) {
+  if (!d) return !fail(NJ_EINVAL, "desc is NULL");
+  if (d->n_layers < 1 || d->d_model < 1 || d->n_heads < 1 || d->n_kv_heads < 1 || d->head_dim < 2 ||
+      d->ffn_dim < 1 || d->vocab < 1)
+    return !fail(NJ_EINVAL, "model dimensions must be positive");
+  if (d->n_heads % d->n_kv_heads) return !fail(NJ_EINVAL, "n_heads %% n_kv_heads != 0");
+  if (d->head_dim % 2) return !fail(NJ_EINVAL, "head_dim must be even");
+  if (d->block_size != 16) return !fail(NJ_EINVAL, "block_size must be 16");
+  if (d->dtype != NJ_F32 && d->dtype != NJ_BF16) return !fail(NJ_EINVAL, "dtype must be NJ_F32 or NJ_BF16");
+  if (d->vocab > kMaxVocab) return !fail(NJ_EINVAL, "vocab > %d", kMaxVocab);
+  if (!(d->rms_eps >= 0.f) || !(d->rope_theta > 0.f)) return !fail(NJ_EINVAL, "bad rms_eps or rope_theta");
+  if (d->dtype == NJ_BF16) {
+    const int qkv = (d->n_heads + 2 * d->n_kv_heads) * d->head_dim;
+    if (d->head_dim != 128) return !fail(NJ_EINVAL, "bf16 path needs head_dim 128");
+    if (d->d_model % 32 || d->ffn_dim % 32 || (d->n_heads * d->head_dim) % 32)
+      return !fail(NJ_EINVAL, "bf16 path needs d_model, ffn_dim, H*D multiples of 32");
+    if (qkv % 16 || d->vocab % 16 || d->d_model % 16 || d->ffn_dim % 16)
+      return !fail(NJ_EINVAL, "bf16 path needs GEMM output widths (qkv, d, F, V) multiples of 16");
+  }
+  return true;
+}
+
+Layout layout(const nj_model_desc& d, int B, int k) {
+  const size_t e = d.dtype == NJ_BF16 ? 2 : 4;
+  const size_t T = k + 1, M = (size_t)B * T;
+  const size_t HD = (size_t)d.n_heads * d.head_dim;
+  const size_t qkv = (size_t)(d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
+  const int G = d.n_heads / d.n_kv_heads;
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += al(bytes);
+    return o;
+  };
+  L.err = take(kAlign);
+  L.h = take(M * d.d_model * 4);
+  L.x = take(M * d.d_model * e);
+  L.qkv = take(M * qkv * 4);
+  L.q = take(M * HD * e);
+  L.win_layer_bytes = (size_t)B * d.n_kv_heads * 16 * d.head_dim * e;
+  L.win_k = take(L.win_layer_bytes * d.n_layers);
+  L.win_v = take(L.win_layer_bytes * d.n_layers);
+  const size_t pf = d.dtype == NJ_BF16 ? attention_partial_floats(B, d.n_kv_heads, (int)T, G, d.head_dim) : 0;
+  const size_t pml = pf ? pf / (d.head_dim + 2) * 2 : 0;
+  L.part_o = take(pf * 4);
+  L.part_ml = take(pml * 4);
+  L.o = take(M * HD * e);
+  L.act = take(M * d.ffn_dim * e);
+  L.logits = take(M * d.vocab * 4);
+  L.stats = take(M * accept_chunks(d.vocab) * 2 * 4);
+  L.total = off;
+  return L;
+}
+
+struct StepRecord {
+  int B, k, n_layers;
+};
+std::mutex g_mu;
+std::unordered_map<const void*, StepRecord> g_steps;
+
+}  // namespace
+
+extern "C" {
+
+const char* nightjar_last_error(void) { return g_err.c_str(); }
+
+size_t nightjar_workspace_bytes(const nj_model_desc* desc, int32_t max_B, int32_t max_k) {
+  if (!desc_ok(desc) || max_B < 1 || max_k < 0 || max_k > kMaxK) return 0;
+  return layout(*desc, max_B, max_k).total;
+}
+
+int nightjar_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace || workspace_bytes < kAlign) return fail(NJ_EINVAL, "workspace NULL or smaller than %zu", kAlign);
+  hipError_t e = launch_fill_i32(static_cast<int32_t*>(workspace), 0, 1, (hipStream_t)stream);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "workspace_init");
+}
+
+int nightjar_device_error(void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace || workspace_bytes < kAlign) return fail(NJ_EINVAL, "workspace NULL or too small");
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "device_error: stream sync");
+  int32_t v = 0;
+  e = hipMemcpy(&v, workspace, sizeof v, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "device_error: read");
+  if (v) {
+    e = launch_fill_i32(static_cast<int32_t*>(workspace), 0, 1, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "device_error: clear");
+  }
+  return v;
+}
+
+int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv,
+                         const int32_t* block_table, int32_t max_blocks, const int32_t* context_lens,
+                         const int32_t* last_tokens, const int32_t* draft_tokens, const float* draft_probs,
+                         const float* uniforms, int32_t B, int32_t k, int32_t* accepted_len, int32_t* next_tokens,
+                         float* target_logits, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc)) return NJ_EINVAL;
+  const nj_model_desc& d = *desc;
+  if (B < 1) return fail(NJ_EINVAL, "B must be >= 1");
+  if (k < 0 || k > kMaxK) return fail(NJ_EINVAL, "k must be in [0, %d]", kMaxK);
+  if (max_blocks < 1) return fail(NJ_EINVAL, "max_blocks must be >= 1");
+  if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers) return fail(NJ_EINVAL, "weights incomplete");
+  if (!kv || !kv->k_pages || !kv->v_pages || kv->num_blocks < 1) return fail(NJ_EINVAL, "kv cache incomplete");
+  if (!block_table || !context_lens || !last_tokens || !uniforms || !accepted_len || !next_tokens || !workspace)
+    return fail(NJ_EINVAL, "a required pointer is NULL");
+  if (k > 0 && (!draft_tokens || !draft_probs)) return fail(NJ_EINVAL, "k > 0 needs draft_tokens and draft_probs");
+  const int T = k + 1, M = B * T, G = d.n_heads / d.n_kv_heads;
+  const bool bf = d.dtype == NJ_BF16;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const nj_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(NJ_EINVAL, "layer %d weights incomplete", l);
+    if (!kv->k_pages[l] || !kv->v_pages[l]) return fail(NJ_EINVAL, "layer %d pages NULL", l);
+    if (bf && !(aligned16(lw.w_qkv) && aligned16(lw.w_o) && aligned16(lw.w_gate_up) && aligned16(lw.w_down) &&
+                aligned16(kv->k_pages[l]) && aligned16(kv->v_pages[l])))
+      return fail(NJ_EINVAL, "layer %d: weights and pages must be 16-byte aligned", l);
+  }
+  if (bf && !aligned16(w->lm_head)) return fail(NJ_EINVAL, "lm_head must be 16-byte aligned");
+  if (target_logits && !aligned16(target_logits)) return fail(NJ_EINVAL, "target_logits must be 16-byte aligned");
+  if (bf && T * G > 64) return fail(NJ_EINVAL, "(k+1) * (H/Hkv) = %d exceeds 64 query rows per KV head", T * G);
+  if (!bf && (size_t)max_blocks * 16 * 4 > 65536) return fail(NJ_EINVAL, "fp32 path supports max_blocks <= 1024");
+  const Layout L = layout(d, B, k);
+  if (workspace_bytes < L.total)
+    return fail(NJ_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, L.total);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = static_cast<char*>(workspace);
+  int* err = reinterpret_cast<int*>(ws + L.err);
+  float* h = reinterpret_cast<float*>(ws + L.h);
+  void* x = ws + L.x;
+  float* qkv = reinterpret_cast<float*>(ws + L.qkv);
+  void* q = ws + L.q;
+  void* o = ws + L.o;
+  void* act = ws + L.act;
+  float* logits = target_logits ? target_logits : reinterpret_cast<float*>(ws + L.logits);
+  const int dt = bf ? kBF16 : kF32;
+  const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
+
+  int nsplit = 1, bps = max_blocks;
+  if (bf) attention_plan(B, d.n_kv_heads, T, G, max_blocks, &nsplit, &bps);
+
+  hipError_t e;
+#define NJ_TRY(call, what)                   \
+  do {                                       \
+    e = (call);                              \
+    if (e != hipSuccess) return hip_fail(e, what); \
+  } while (0)
+
+  NJ_TRY(launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
+                           d.vocab, d.rms_eps, err, s),
+         "embed");
+  for (int l = 0; l < d.n_layers; ++l) {
+    const nj_layer_weights& lw = w->layers[l];
+    if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s), "attn_norm");
+    NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, s), "qkv gemm");
+    void* wk = ws + L.win_k + l * L.win_layer_bytes;
+    void* wv = ws + L.win_v + l * L.win_layer_bytes;
+    NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
+                              wk, wv, s),
+           "rope");
+    AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
+                kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
+                reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml), nsplit, bps,
+                o, err};
+    NJ_TRY(launch_attention(aa, s), "attention");
+    NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, s), "o gemm");
+    NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s), "ffn_norm");
+    NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu, s), "gate_up gemm");
+    NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, s), "down gemm");
+  }
+  NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s), "final_norm");
+  NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, s), "lm_head gemm");
+  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, reinterpret_cast<float*>(ws + L.stats),
+                accepted_len, next_tokens, err};
+  NJ_TRY(launch_accept(ac, s), "accept");
+#undef NJ_TRY
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    g_steps[workspace] = StepRecord{B, k, d.n_layers};
+  }
+  return NJ_OK;
+}
+
+int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const int32_t* block_table,
+                       int32_t max_blocks, int32_t* context_lens, const int32_t* accepted_len, int32_t B, int32_t k,
+                       const void* workspace, size_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc)) return NJ_EINVAL;
+  const nj_model_desc& d = *desc;
+  if (!kv || !kv->k_pages || !kv->v_pages || kv->num_blocks < 1) return fail(NJ_EINVAL, "kv cache incomplete");
+  if (!block_table || !context_lens || !accepted_len || !workspace) return fail(NJ_EINVAL, "a required pointer is NULL");
+  if (B < 1 || k < 0 || k > kMaxK || max_blocks < 1) return fail(NJ_EINVAL, "bad B, k or max_blocks");
+  for (int l = 0; l < d.n_layers; ++l)
+    if (!kv->k_pages[l] || !kv->v_pages[l]) return fail(NJ_EINVAL, "layer %d pages NULL", l);
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    auto it = g_steps.find(workspace);
+    if (it == g_steps.end()) return fail(NJ_EINVAL, "no verify step has filled this workspace");
+    if (it->second.B != B || it->second.k != k || it->second.n_layers != d.n_layers)
+      return fail(NJ_EINVAL, "B/k/layers differ from the verify step that filled the workspace");
+  }
+  const Layout L = layout(d, B, k);
+  if (workspace_bytes < L.total) return fail(NJ_EINVAL, "workspace too small");
+  const char* ws = static_cast<const char*>(workspace);
+  KvAppendArgs a{d.dtype == NJ_BF16 ? kBF16 : kF32, kv->k_pages, kv->v_pages, ws + L.win_k, ws + L.win_v,
+                 block_table, max_blocks, kv->num_blocks, context_lens, accepted_len, d.n_layers, B, k,
+                 d.n_kv_heads, d.head_dim, reinterpret_cast<int*>(const_cast<char*>(ws) + L.err)};
+  hipError_t e = launch_kv_append(a, (hipStream_t)stream);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "kv_append");
+}
+
+int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_t* draft_tokens,
+                    const float* draft_probs, const float* uniforms, int32_t B, int32_t k, int32_t* accepted_len,
+                    int32_t* next_tokens, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!desc || desc->vocab < 1 || desc->vocab > kMaxVocab) return fail(NJ_EINVAL, "bad desc or vocab");
+  if (B < 1 || k < 0 || k > kMaxK) return fail(NJ_EINVAL, "bad B or k");
+  if (!logits || !uniforms || !accepted_len || !next_tokens || !workspace)
+    return fail(NJ_EINVAL, "a required pointer is NULL");
+  if (k > 0 && (!draft_tokens || !draft_probs)) return fail(NJ_EINVAL, "k > 0 needs draft_tokens and draft_probs");
+  const size_t M = (size_t)B * (k + 1);
+  const size_t need = kAlign + al(M * accept_chunks(desc->vocab) * 2 * 4);
+  if (workspace_bytes < need) return fail(NJ_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, need);
+  char* ws = static_cast<char*>(workspace);
+  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, reinterpret_cast<float*>(ws + kAlign),
+               accepted_len, next_tokens, reinterpret_cast<int*>(ws)};
+  hipError_t e = launch_accept(a, (hipStream_t)stream);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "accept");
+}
+
+int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
+                  int32_t epilogue, void* stream) {
+  if (dtype != NJ_F32 && dtype != NJ_BF16) return fail(NJ_EINVAL, "bad dtype");
+  if (!x || !w || !y) return fail(NJ_EINVAL, "NULL operand");
+  if (M < 1 || N < 1 || K < 1) return fail(NJ_EINVAL, "M, N, K must be >= 1");
+  if (epilogue < NJ_GEMM_STORE || epilogue > NJ_GEMM_SWIGLU) return fail(NJ_EINVAL, "bad epilogue");
+  if (epilogue == NJ_GEMM_SWIGLU && N % 2) return fail(NJ_EINVAL, "SwiGLU needs an even N");
+  const int Nout = epilogue == NJ_GEMM_SWIGLU ? N / 2 : N;
+  if (dtype == NJ_BF16) {
+    if (K % 32) return fail(NJ_EINVAL, "bf16 GEMM needs K %% 32 == 0");
+    if (Nout % 16) return fail(NJ_EINVAL, "bf16 GEMM needs output width %% 16 == 0");
+    if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(NJ_EINVAL, "operands must be 16-byte aligned");
+  }
+  hipError_t e = launch_gemm(dtype == NJ_BF16 ? kBF16 : kF32, x, w, y, M, N, K, epilogue, (hipStream_t)stream);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "gemm");
+}
+
+}  // extern "C"

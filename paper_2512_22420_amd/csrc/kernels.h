@@ -1,0 +1,85 @@
+// Host-side launchers of the verify-step kernels.  Each enqueues on `s` and
+// returns the launch status; shapes are checked by the caller (api.cpp).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nj {
+
+enum { kF32 = 0, kBF16 = 1 };
+enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2 };
+
+// y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]).
+hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
+                       hipStream_t s);
+
+// h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
+hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
+                             const void* embed, const void* gain, float* h, void* x, int d, int V,
+                             float eps, int* err, hipStream_t s);
+
+// x[r] = rmsnorm(h[r]) * gain
+hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, int M, int d, float eps,
+                          hipStream_t s);
+
+// RoPE on q and k rows of qkv at positions ctx[b] + i; q -> q_out [M][H][D];
+// k, v -> one 16-slot window block per (b, kv head).
+hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv,
+                              int D, float theta, void* q_out, void* win_k, void* win_v, hipStream_t s);
+
+struct AttnArgs {
+  int dtype;
+  const void* q;        // [M][H][D]
+  const void* k_pages;  // [nb][Hkv][16][D]
+  const void* v_pages;  // [nb][Hkv][D][16]
+  const void* win_k;    // [B][Hkv][16][D]
+  const void* win_v;    // [B][Hkv][D][16]
+  const int32_t* block_table;
+  int max_blocks;
+  const int32_t* ctx;
+  int num_blocks, B, T, H, Hkv, D;
+  float* part_o;        // split partials (bf16 path)
+  float* part_ml;
+  int nsplit, blocks_per_split;
+  void* out;            // [M][H*D]
+  int* err;
+};
+// Number of KV splits the bf16 path uses, and the partial buffer floats it needs.
+void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, int* blocks_per_split);
+size_t attention_partial_floats(int B, int Hkv, int T, int G, int D);
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+// Acceptance from logits [B*T][V].
+struct AcceptArgs {
+  const float* logits;
+  const int32_t* drafts;    // [B][k]
+  const float* dprobs;      // [B][k][V]
+  const float* uniforms;    // [B][k+1]
+  int B, k, V;
+  float* stats;             // [B*T][nch][2]
+  int32_t* accepted_len;
+  int32_t* next_tokens;
+  int* err;
+};
+int accept_chunks(int V);
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+
+struct KvAppendArgs {
+  int dtype;
+  void* const* k_pages;      // host array of L device pointers
+  void* const* v_pages;
+  const void* win_k;         // [L][B][Hkv][16][D]
+  const void* win_v;         // [L][B][Hkv][D][16]
+  const int32_t* block_table;
+  int max_blocks, num_blocks;
+  int32_t* ctx;
+  const int32_t* accepted_len;
+  int L, B, k, Hkv, D;
+  int* err;
+};
+hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s);
+
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s);
+
+}  // namespace nj

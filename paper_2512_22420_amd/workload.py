@@ -77,7 +77,7 @@ SHAPES = {s.name: s for s in (TINY_F32, LLAMA8B_LAYER, LLAMA8B, QWEN7B)}
 
 
 def _rng(seed: int, *keys: int) -> np.random.Generator:
-    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed, spawn_key=tuple(keys))))
+    return np.random.Generator(np.random.SFC64(np.random.SeedSequence(seed, spawn_key=tuple(keys))))
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -101,6 +101,22 @@ def _normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
     return out
 
 
+_CHUNK = 1 << 24
+
+
+def _normal_store(rng: np.random.Generator, shape, std: float, dtype: str) -> np.ndarray:
+    """N(0, std^2) draws stored in `dtype`, generated in chunks (no full fp32 copy)."""
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16 if dtype == "bf16" else np.float32)
+    buf = np.empty(min(_CHUNK, n), dtype=np.float32)
+    for s0 in range(0, n, _CHUNK):
+        m = min(_CHUNK, n - s0)
+        rng.standard_normal(out=buf[:m], dtype=np.float32)
+        buf[:m] *= np.float32(std)
+        out[s0: s0 + m] = f32_to_bf16_bits(buf[:m]) if dtype == "bf16" else buf[:m]
+    return out.reshape(shape)
+
+
 def _ones(n: int, dtype: str) -> np.ndarray:
     return _store(np.ones(n, dtype=np.float32), dtype)
 
@@ -119,8 +135,8 @@ def make_weights(shape: ModelShape, seed: int = 0, std: float = 0.02) -> Dict:
     """
     s, dt = shape, shape.dtype
     w = {
-        "embed": _store(_normal(_rng(seed, _K_WEIGHT, 0, 0), (s.vocab, s.d_model), std), dt),
-        "lm_head": _store(_normal(_rng(seed, _K_WEIGHT, 0, 1), (s.vocab, s.d_model), std), dt),
+        "embed": _normal_store(_rng(seed, _K_WEIGHT, 0, 0), (s.vocab, s.d_model), std, dt),
+        "lm_head": _normal_store(_rng(seed, _K_WEIGHT, 0, 1), (s.vocab, s.d_model), std, dt),
         "final_norm": _ones(s.d_model, dt),
         "layers": [],
     }
@@ -128,11 +144,11 @@ def make_weights(shape: ModelShape, seed: int = 0, std: float = 0.02) -> Dict:
         key = 1 + l
         w["layers"].append({
             "attn_norm": _ones(s.d_model, dt),
-            "w_qkv": _store(_normal(_rng(seed, _K_WEIGHT, key, 0), (s.qkv_dim, s.d_model), std), dt),
-            "w_o": _store(_normal(_rng(seed, _K_WEIGHT, key, 1), (s.d_model, s.n_heads * s.head_dim), std), dt),
+            "w_qkv": _normal_store(_rng(seed, _K_WEIGHT, key, 0), (s.qkv_dim, s.d_model), std, dt),
+            "w_o": _normal_store(_rng(seed, _K_WEIGHT, key, 1), (s.d_model, s.n_heads * s.head_dim), std, dt),
             "ffn_norm": _ones(s.d_model, dt),
-            "w_gate_up": _store(_normal(_rng(seed, _K_WEIGHT, key, 2), (2 * s.ffn_dim, s.d_model), std), dt),
-            "w_down": _store(_normal(_rng(seed, _K_WEIGHT, key, 3), (s.d_model, s.ffn_dim), std), dt),
+            "w_gate_up": _normal_store(_rng(seed, _K_WEIGHT, key, 2), (2 * s.ffn_dim, s.d_model), std, dt),
+            "w_down": _normal_store(_rng(seed, _K_WEIGHT, key, 3), (s.d_model, s.ffn_dim), std, dt),
         })
     return w
 
@@ -185,8 +201,8 @@ def make_context(shape: ModelShape, ctx: Sequence[int], k_max: int, seed: int = 
     for l in range(s.n_layers):
         kshape = (num_blocks, s.n_kv_heads, bs, s.head_dim)
         vshape = (num_blocks, s.n_kv_heads, s.head_dim, bs)
-        k_pages.append(_store(_normal(_rng(seed, _K_KV, B, l, 0), kshape, kv_std), s.dtype))
-        v_pages.append(_store(_normal(_rng(seed, _K_KV, B, l, 1), vshape, kv_std), s.dtype))
+        k_pages.append(_normal_store(_rng(seed, _K_KV, B, l, 0), kshape, kv_std, s.dtype))
+        v_pages.append(_normal_store(_rng(seed, _K_KV, B, l, 1), vshape, kv_std, s.dtype))
     return {"k_pages": k_pages, "v_pages": v_pages, "block_table": table,
             "context_lens": ctx.copy(), "num_blocks": num_blocks, "max_blocks": max_blocks}
 

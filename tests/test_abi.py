@@ -1,0 +1,80 @@
+"""The C-ABI library loads, exports every entry point the header declares, and
+rejects bad arguments on the host (no device work is needed for these)."""
+import ctypes
+import os
+
+import pytest
+
+from paper_2512_22420_amd import binding as nb
+from paper_2512_22420_amd import workload as W
+from paper_2512_22420_amd.device import model_desc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nightjar.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(nb.LIB_PATH), reason="libnightjar.so not built")
+
+
+def test_exports_every_declared_function():
+    names = nb.header_functions(HEADER)
+    assert "nightjar_verify_step" in names and "nightjar_kv_append" in names
+    L = nb.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_struct_sizes_match_header_layout():
+    assert ctypes.sizeof(nb.ModelDesc) == 11 * 4
+    assert ctypes.sizeof(nb.LayerWeights) == 6 * 8
+    assert ctypes.sizeof(nb.Weights) == 4 * 8
+    assert ctypes.sizeof(nb.KvCache) == 3 * 8
+
+
+def test_workspace_bytes_monotone_and_validating():
+    d = model_desc(W.LLAMA8B_LAYER)
+    small = nb.workspace_bytes(d, 1, 0)
+    big = nb.workspace_bytes(d, 8, 5)
+    assert 0 < small < big
+    assert big % 256 == 0
+    with pytest.raises(nb.NightjarError):
+        nb.workspace_bytes(d, 1, 16)  # the window must fit one 16-token block
+    bad = model_desc(W.LLAMA8B_LAYER)
+    bad.block_size = 32
+    assert nb.lib().nightjar_workspace_bytes(ctypes.byref(bad), 1, 0) == 0
+    assert "block_size" in nb.last_error()
+    bad = model_desc(W.LLAMA8B_LAYER)
+    bad.n_kv_heads = 5
+    assert nb.lib().nightjar_workspace_bytes(ctypes.byref(bad), 1, 0) == 0
+
+
+def test_verify_step_rejects_bad_arguments_on_host():
+    d = model_desc(W.TINY_F32)
+    w = nb.Weights()
+    kv = nb.KvCache()
+    rc = nb.lib().nightjar_verify_step(ctypes.byref(d), ctypes.byref(w), ctypes.byref(kv), 0, 1, 0, 0, 0, 0, 0,
+                                       2, 3, 0, 0, 0, 0, 0, 0)
+    assert rc == nb.NJ_EINVAL and "weights" in nb.last_error()
+    rc = nb.lib().nightjar_verify_step(None, ctypes.byref(w), ctypes.byref(kv), 0, 1, 0, 0, 0, 0, 0,
+                                       2, 3, 0, 0, 0, 0, 0, 0)
+    assert rc == nb.NJ_EINVAL and "desc" in nb.last_error()
+    rc = nb.lib().nightjar_verify_step(ctypes.byref(d), ctypes.byref(w), ctypes.byref(kv), 0, 1, 0, 0, 0, 0, 0,
+                                       2, 16, 0, 0, 0, 0, 0, 0)
+    assert rc == nb.NJ_EINVAL and "k must be" in nb.last_error()
+
+
+def test_gemm_rejects_bad_shapes_on_host():
+    L = nb.lib()
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 32, 40, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL  # K % 32
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 24, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL  # N % 16
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 30, 64, nb.NJ_GEMM_SWIGLU, 0) == nb.NJ_EINVAL
+    assert L.nightjar_gemm(nb.NJ_BF16, 0, 16, 16, 4, 32, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 0, 32, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL
+    assert L.nightjar_gemm(7, 16, 16, 16, 1, 32, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL
+
+
+def test_kv_append_requires_a_preceding_verify_step():
+    d = model_desc(W.TINY_F32)
+    ptrs = (ctypes.c_void_p * 1)(16)
+    kv = nb.KvCache(ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)), 4)
+    rc = nb.lib().nightjar_kv_append(ctypes.byref(d), ctypes.byref(kv), 16, 4, 16, 16, 2, 3, 256, 1 << 20, 0)
+    assert rc == nb.NJ_EINVAL and "no verify step" in nb.last_error()

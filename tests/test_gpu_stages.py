@@ -1,0 +1,160 @@
+"""Stage-level GPU parity: the step's GEMM kernels and its acceptance kernel,
+called through the C ABI, against the plain definitions / the oracle."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2512_22420_amd import binding as nb
+from paper_2512_22420_amd import workload as W
+from paper_2512_22420_amd.device import model_desc
+
+from parity import compare
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(a):
+    a = np.ascontiguousarray(a)
+    return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).cuda()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 16, 32), (5, 48, 96), (16, 4096, 4096), (17, 272, 4096), (48, 6144, 4096),
+                                   (64, 1040, 512), (100, 512, 1024), (3, 4096, 14336), (48, 128256, 4096)])
+def test_gemm_bf16_store(M, N, K):
+    rng = np.random.default_rng(M * 7 + N + K)
+    x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
+    y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    nb.gemm(nb.NJ_BF16, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_STORE, _stream())
+    torch.cuda.synchronize()
+    ref = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
+    err = np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max()
+    assert err < 2e-5, err
+
+
+@pytest.mark.parametrize("M,N,K", [(7, 64, 128), (48, 4096, 14336), (33, 2048, 4096)])
+def test_gemm_bf16_residual(M, N, K):
+    rng = np.random.default_rng(11 + M)
+    x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
+    h0 = rng.standard_normal((M, N), dtype=np.float32)
+    y = _dev(h0.copy())
+    nb.gemm(nb.NJ_BF16, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_RESIDUAL,
+            _stream())
+    torch.cuda.synchronize()
+    ref = h0 + oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
+    assert np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max() < 2e-5
+
+
+@pytest.mark.parametrize("M,F,K", [(6, 64, 256), (48, 14336, 4096), (20, 688, 256)])
+def test_gemm_bf16_swiglu(M, F, K):
+    rng = np.random.default_rng(5 + M)
+    x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = W.f32_to_bf16_bits(rng.standard_normal((2 * F, K), dtype=np.float32) * 0.05)
+    y = torch.empty((M, F), dtype=torch.int16, device="cuda")
+    nb.gemm(nb.NJ_BF16, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, 2 * F, K, nb.NJ_GEMM_SWIGLU,
+            _stream())
+    torch.cuda.synchronize()
+    gu = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
+    ref = oracle.silu(gu[:, :F]) * gu[:, F:]
+    got = oracle.widen(y.cpu().numpy().view(np.uint16), "bf16")
+    # bf16 output: one rounding (2^-9 relative) on top of fp32 accumulation
+    assert np.abs(got - ref).max() <= 2 ** -8 * np.abs(ref).max() + 1e-6
+
+
+@pytest.mark.parametrize("M,N,K,epi", [(3, 50, 70, nb.NJ_GEMM_STORE), (8, 768, 256, nb.NJ_GEMM_RESIDUAL),
+                                       (8, 2 * 688, 256, nb.NJ_GEMM_SWIGLU)])
+def test_gemm_f32(M, N, K, epi):
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((M, K), dtype=np.float32)
+    w = rng.standard_normal((N, K), dtype=np.float32) * 0.05
+    Nout = N // 2 if epi == nb.NJ_GEMM_SWIGLU else N
+    y0 = rng.standard_normal((M, Nout), dtype=np.float32)
+    y = _dev(y0.copy())
+    nb.gemm(nb.NJ_F32, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, N, K, epi, _stream())
+    torch.cuda.synchronize()
+    acc = x.astype(np.float64) @ w.astype(np.float64).T
+    ref = {nb.NJ_GEMM_STORE: acc, nb.NJ_GEMM_RESIDUAL: y0 + acc,
+           nb.NJ_GEMM_SWIGLU: oracle.silu(acc[:, :Nout]) * acc[:, Nout:] if epi == nb.NJ_GEMM_SWIGLU else None}[epi]
+    assert np.abs(y.cpu().numpy() - ref).max() < 1e-4 * max(1.0, np.abs(ref).max())
+
+
+# --------------------------------------------------------------------------
+# acceptance kernel alone, fed fp32 logits; the oracle runs on the same values
+# --------------------------------------------------------------------------
+def _accept_case(B, k, V, seed, logit_std, beta):
+    rng = np.random.default_rng(seed)
+    logits = (rng.standard_normal((B, k + 1, V)) * logit_std).astype(np.float32)
+    # draft distributions correlated with the target so that accept and reject both occur
+    z = beta * logits[:, :k, :].astype(np.float64) + (1 - beta) * rng.standard_normal((B, k, V)) * 2.0
+    q = oracle.softmax(z).astype(np.float32)
+    drafts = np.zeros((B, k), dtype=np.int32)
+    for b in range(B):
+        for i in range(k):
+            drafts[b, i] = oracle.invcdf(q[b, i].astype(np.float64), rng.random())
+    u = rng.random((B, k + 1), dtype=np.float32)
+    return logits, drafts, q, u
+
+
+def _run_accept(V, logits, drafts, q, u):
+    B, T, _ = logits.shape
+    k = T - 1
+    shape = dataclasses.replace(W.TINY_F32, vocab=V)
+    desc = model_desc(shape)
+    nbytes = 256 + ((B * T * ((V + 8191) // 8192) * 8 + 255) // 256) * 256
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    acc = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    nxt = torch.full((B, T), -7, dtype=torch.int32, device="cuda")
+    dl = _dev(logits)
+    dd = _dev(drafts) if k else None
+    dq = _dev(q) if k else None
+    du = _dev(u)
+    nb.accept(desc, dl.data_ptr(), dd.data_ptr() if k else 0, dq.data_ptr() if k else 0, du.data_ptr(), B, k,
+              acc.data_ptr(), nxt.data_ptr(), ws.data_ptr(), nbytes, _stream())
+    assert nb.device_error(ws.data_ptr(), nbytes, _stream()) == 0
+    return acc.cpu().numpy(), nxt.cpu().numpy()
+
+
+@pytest.mark.parametrize("B,k,V,std,beta", [
+    (64, 3, 2048, 2.0, 0.8), (32, 5, 128256, 2.0, 0.7), (16, 1, 152064, 3.0, 0.9), (40, 0, 4096, 1.0, 0.0),
+    (24, 7, 1000, 0.5, 0.95), (8, 15, 300, 1.0, 0.5), (3, 2, 5, 1.0, 0.5)])
+def test_accept_matches_oracle(B, k, V, std, beta):
+    logits, drafts, q, u = _accept_case(B, k, V, 100 + B + k, std, beta)
+    acc, nxt = _run_accept(V, logits, drafts, q, u)
+    res = compare(acc, nxt, logits, drafts, q, u)
+    assert not res["mismatches"], res["mismatches"][:5]
+    assert res["checked"] >= B // 2
+    assert np.all((acc >= 0) & (acc <= k))
+
+
+def test_accept_identical_draft_accepts_everything():
+    B, k, V = 16, 4, 4096
+    rng = np.random.default_rng(7)
+    logits = (rng.standard_normal((B, k + 1, V)) * 2).astype(np.float32)
+    q = oracle.softmax(logits[:, :k].astype(np.float64)).astype(np.float32)
+    drafts = np.stack([[oracle.invcdf(q[b, i].astype(np.float64), rng.random()) for i in range(k)]
+                       for b in range(B)]).astype(np.int32)
+    u = rng.random((B, k + 1), dtype=np.float32) * 0.99  # ratio = 1 up to rounding, u < 0.99
+    acc, nxt = _run_accept(V, logits, drafts, q, u)
+    assert np.all(acc == k)
+    assert np.array_equal(nxt[:, :k], drafts)
+
+
+def test_accept_edge_uniforms():
+    """u = 0 rejects a zero-probability draft; u just below 1 still draws a positive-weight token."""
+    V, k = 64, 2
+    logits = np.zeros((2, k + 1, V), dtype=np.float32)
+    logits[:, :, 5] = -1e30  # p(5) = 0
+    q = np.full((2, k, V), 1.0 / V, dtype=np.float32)
+    drafts = np.array([[5, 1], [1, 2]], dtype=np.int32)
+    u = np.array([[0.0, 0.5, np.nextafter(np.float32(1), np.float32(0))], [0.0, 0.0, 0.0]], dtype=np.float32)
+    acc, nxt = _run_accept(V, logits, drafts, q, u)
+    assert acc[0] == 0 and nxt[0, 0] != 5 and nxt[0, 0] == V - 1  # residual p - q > 0 everywhere but token 5
+    assert acc[1] == 2 and nxt[1, 2] == 0  # bonus draw with u = 0 takes the first positive weight

@@ -104,7 +104,7 @@ def test_window_logits_match_library_model(shape):
     for b, ids in enumerate(seqs):
         _write_prefix(cd, shape, b, _hf_prefill(m, ids[: ctx[b]]))
     toks = np.stack([ids[c: c + k + 1] for ids, c in zip(seqs, ctx)])
-    logits, win_k, win_v = oracle.forward_window(oracle.Weights64(weights, shape), cd["k_pages"], cd["v_pages"],
+    logits, win_k, win_v = oracle.forward_window(weights, shape, cd["k_pages"], cd["v_pages"],
                                                  cd["block_table"], ctx, toks)
     for b, ids in enumerate(seqs):
         ref = _hf_logits(m, ids)[ctx[b]:]
@@ -134,7 +134,7 @@ def test_planted_mistakes_are_caught_by_library_comparison():
     vs = __import__("sys").modules["oracle.verify_step"]
 
     def run():
-        lg, _, _ = vs.forward_window(vs.Weights64(weights, shape), cd["k_pages"], cd["v_pages"],
+        lg, _, _ = vs.forward_window(weights, shape, cd["k_pages"], cd["v_pages"],
                                      cd["block_table"], np.array([19]), ids[None, 19:])
         return np.abs(lg[0] - ref).max() / np.abs(ref).max()
 
@@ -155,7 +155,7 @@ def test_planted_mistakes_are_caught_by_library_comparison():
         vs.rope, vs.attention = orig_rope, orig_attn
     w2 = {**weights, "layers": [dict(weights["layers"][0], w_o=np.ascontiguousarray(weights["layers"][0]["w_o"].T)),
                                 weights["layers"][1]]}
-    lg, _, _ = vs.forward_window(vs.Weights64(w2, shape), cd["k_pages"], cd["v_pages"], cd["block_table"],
+    lg, _, _ = vs.forward_window(w2, shape, cd["k_pages"], cd["v_pages"], cd["block_table"],
                                  np.array([19]), ids[None, 19:])
     assert np.abs(lg[0] - ref).max() / np.abs(ref).max() > 1e-3
 
@@ -165,7 +165,6 @@ def test_gamma0_chain_reproduces_autoregressive_sampling():
     shape = SHAPES[1]
     weights = W.make_weights(shape, seed=4, std=0.05)
     m = _hf_model(shape, weights)
-    w64 = oracle.Weights64(weights, shape)
     steps = 20
     cd = W.make_context(shape, [0], steps, seed=4)
     kp = [np.asarray(a, dtype=np.float64).copy() for a in cd["k_pages"]]
@@ -177,7 +176,7 @@ def test_gamma0_chain_reproduces_autoregressive_sampling():
         u = rng.random(1).astype(np.float32)
         r = oracle.verify_step(weights, shape, kp, vp, cd["block_table"], ctx, np.array([seq[-1]]),
                                np.zeros((1, 0), np.int32), np.zeros((1, 0, shape.vocab), np.float32),
-                               u[None, :], w64=w64)
+                               u[None, :])
         assert r["accepted_len"][0] == 0
         y = int(r["next_tokens"][0, 0])
         # library model: full forward, softmax, inverse CDF by searchsorted
@@ -212,11 +211,10 @@ def test_window_row_depends_only_on_its_prefix():
     """Causality in the window: row i's logits do not depend on drafts after i."""
     x = W.tiny_inputs(seed=3, k=5)
     s = x["shape"]
-    w64 = oracle.Weights64(x["weights"], s)
     toks = oracle.window_tokens(x["last_tokens"], x["draft_tokens"])
-    full, _, _ = oracle.forward_window(w64, x["k_pages"], x["v_pages"], x["block_table"], x["context_lens"], toks)
+    full, _, _ = oracle.forward_window(x["weights"], s, x["k_pages"], x["v_pages"], x["block_table"], x["context_lens"], toks)
     for T in (1, 3):
-        part, _, _ = oracle.forward_window(w64, x["k_pages"], x["v_pages"], x["block_table"], x["context_lens"],
+        part, _, _ = oracle.forward_window(x["weights"], s, x["k_pages"], x["v_pages"], x["block_table"], x["context_lens"],
                                            toks[:, :T])
         np.testing.assert_allclose(part, full[:, :T], rtol=0, atol=1e-12)
 
