@@ -32,7 +32,8 @@ def test_gemm_bf16_store(M, N, K):
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     y = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    nb.gemm(nb.NJ_BF16, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_STORE, _stream())
+    dx, dw = _dev(x), _dev(w)  # keep the device copies alive across the call
+    nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_STORE, _stream())
     torch.cuda.synchronize()
     ref = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     err = np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max()
@@ -46,8 +47,8 @@ def test_gemm_bf16_residual(M, N, K):
     w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     h0 = rng.standard_normal((M, N), dtype=np.float32)
     y = _dev(h0.copy())
-    nb.gemm(nb.NJ_BF16, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_RESIDUAL,
-            _stream())
+    dx, dw = _dev(x), _dev(w)
+    nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_RESIDUAL, _stream())
     torch.cuda.synchronize()
     ref = h0 + oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     assert np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max() < 2e-5
@@ -59,8 +60,8 @@ def test_gemm_bf16_swiglu(M, F, K):
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((2 * F, K), dtype=np.float32) * 0.05)
     y = torch.empty((M, F), dtype=torch.int16, device="cuda")
-    nb.gemm(nb.NJ_BF16, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, 2 * F, K, nb.NJ_GEMM_SWIGLU,
-            _stream())
+    dx, dw = _dev(x), _dev(w)
+    nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, 2 * F, K, nb.NJ_GEMM_SWIGLU, _stream())
     torch.cuda.synchronize()
     gu = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     ref = oracle.silu(gu[:, :F]) * gu[:, F:]
@@ -78,11 +79,16 @@ def test_gemm_f32(M, N, K, epi):
     Nout = N // 2 if epi == nb.NJ_GEMM_SWIGLU else N
     y0 = rng.standard_normal((M, Nout), dtype=np.float32)
     y = _dev(y0.copy())
-    nb.gemm(nb.NJ_F32, _dev(x).data_ptr(), _dev(w).data_ptr(), y.data_ptr(), M, N, K, epi, _stream())
+    dx, dw = _dev(x), _dev(w)
+    nb.gemm(nb.NJ_F32, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, epi, _stream())
     torch.cuda.synchronize()
     acc = x.astype(np.float64) @ w.astype(np.float64).T
-    ref = {nb.NJ_GEMM_STORE: acc, nb.NJ_GEMM_RESIDUAL: y0 + acc,
-           nb.NJ_GEMM_SWIGLU: oracle.silu(acc[:, :Nout]) * acc[:, Nout:] if epi == nb.NJ_GEMM_SWIGLU else None}[epi]
+    if epi == nb.NJ_GEMM_STORE:
+        ref = acc
+    elif epi == nb.NJ_GEMM_RESIDUAL:
+        ref = y0 + acc
+    else:
+        ref = oracle.silu(acc[:, :Nout]) * acc[:, Nout:]
     assert np.abs(y.cpu().numpy() - ref).max() < 1e-4 * max(1.0, np.abs(ref).max())
 
 
