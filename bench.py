@@ -107,15 +107,21 @@ def main():
     x = torch.zeros((M, shape.d_model), dtype=torch.int16, device="cuda")
     y = torch.empty((M, shape.vocab), dtype=torch.float32, device="cuda")
     s = stream.cuda_stream
-    for _ in range(5):
+    gws_n = nb.gemm_workspace_bytes(nb.NJ_BF16, M, shape.vocab, shape.d_model, nb.NJ_GEMM_STORE)
+    gws = torch.empty(gws_n, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(gws.data_ptr(), gws_n, s)
+
+    def lm_head():
         nb.gemm(nb.NJ_BF16, x.data_ptr(), model.lm_head.data_ptr(), y.data_ptr(), M, shape.vocab, shape.d_model,
-                nb.NJ_GEMM_STORE, s)
+                nb.NJ_GEMM_STORE, gws.data_ptr(), gws_n, s)
+
+    for _ in range(5):
+        lm_head()
     reps = max(20, args.steps)
     g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     g0.record(stream)
     for _ in range(reps):
-        nb.gemm(nb.NJ_BF16, x.data_ptr(), model.lm_head.data_ptr(), y.data_ptr(), M, shape.vocab, shape.d_model,
-                nb.NJ_GEMM_STORE, s)
+        lm_head()
     g1.record(stream)
     torch.cuda.synchronize()
     lm_us = g0.elapsed_time(g1) / reps * 1e3
@@ -126,7 +132,7 @@ def main():
                 "bound": "hbm", "achieved": round(lm_gbs, 1), "peak": R.HBM_BYTES_PER_S / 1e9, "unit": "GB/s",
                 "frac": round(lm_gbs / (R.HBM_BYTES_PER_S / 1e9), 4), "traffic": None,
                 "algorithmic_bytes_per_launch": lm_bytes, "avg_launch_us": round(lm_us, 2)}
-    del x, y
+    del x, y, gws
 
     # ---------------- the (B, k) cost table ----------------
     grid = []

@@ -119,8 +119,9 @@ typedef struct nj_kv_cache {
 size_t nightjar_workspace_bytes(const nj_model_desc* desc, int32_t max_B, int32_t max_k);
 
 /*
- * Prepare a fresh workspace (clears its device error word).  Call once after
- * allocating it; device memory, workspace_bytes from nightjar_workspace_bytes.
+ * Prepare a fresh workspace: zero-fills it (the device error word and the
+ * split-K arrival counters must start at zero).  Call once after allocating
+ * it; device memory, 256-byte aligned.
  */
 int nightjar_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 
@@ -202,9 +203,12 @@ const char* nightjar_last_error(void);
 /*
  * Acceptance alone, from given target logits (the acceptance rule above).
  *   logits [B][k+1][V] fp32, draft_tokens [B][k], draft_probs [B][k][V],
- *   uniforms [B][k+1]; outputs as in nightjar_verify_step.  workspace from
- *   nightjar_workspace_bytes(desc, B, k) (only desc->vocab is read).
+ *   uniforms [B][k+1]; outputs as in nightjar_verify_step.  Only desc->vocab
+ *   is read.  workspace: device, 256-byte aligned, at least
+ *   nightjar_accept_workspace_bytes(vocab, B, k) bytes, zero-filled once by
+ *   nightjar_workspace_init.
  */
+size_t nightjar_accept_workspace_bytes(int32_t vocab, int32_t B, int32_t k);
 int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_t* draft_tokens,
                     const float* draft_probs, const float* uniforms, int32_t B, int32_t k,
                     int32_t* accepted_len, int32_t* next_tokens, void* workspace, size_t workspace_bytes,
@@ -220,10 +224,15 @@ enum {
 
 /*
  * y = x . w^T with the step's GEMM kernels.  x [M][K] and w [N][K] in `dtype`
- * (NJ_BF16 or NJ_F32); y as the epilogue says.  M >= 1; K % 32 == 0 for bf16.
+ * (NJ_BF16 or NJ_F32), device, 16-byte aligned; y as the epilogue says.
+ * M >= 1; for bf16 K % 32 == 0 and the output width % 16 == 0.  workspace:
+ * device, 256-byte aligned, at least nightjar_gemm_workspace_bytes(...) bytes,
+ * prepared once with nightjar_workspace_init (split-K counters start at zero
+ * and are left at zero by every call).
  */
+size_t nightjar_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue);
 int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
-                  int32_t epilogue, void* stream);
+                  int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

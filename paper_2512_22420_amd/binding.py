@@ -60,7 +60,9 @@ _SIGS = {
     "nightjar_last_error": (ctypes.c_char_p, []),
     "nightjar_accept": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp,
                                        _sz, _vp]),
-    "nightjar_gemm": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp]),
+    "nightjar_gemm": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
+    "nightjar_gemm_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "nightjar_accept_workspace_bytes": (_sz, [_i32, _i32, _i32]),
 }
 
 
@@ -118,14 +120,28 @@ def device_error(workspace: int, workspace_nbytes: int, stream: int = 0) -> int:
     return _check(lib().nightjar_device_error(workspace, workspace_nbytes, stream))
 
 
+def accept_workspace_bytes(vocab, B, k) -> int:
+    n = lib().nightjar_accept_workspace_bytes(vocab, B, k)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
 def accept(desc, logits, draft_tokens, draft_probs, uniforms, B, k, accepted_len, next_tokens, workspace,
            workspace_nbytes, stream: int = 0) -> None:
     _check(lib().nightjar_accept(ctypes.byref(desc), logits, draft_tokens, draft_probs, uniforms, B, k,
                                  accepted_len, next_tokens, workspace, workspace_nbytes, stream))
 
 
-def gemm(dtype, x, w, y, M, N, K, epilogue, stream: int = 0) -> None:
-    _check(lib().nightjar_gemm(dtype, x, w, y, M, N, K, epilogue, stream))
+def gemm_workspace_bytes(dtype, M, N, K, epilogue) -> int:
+    n = lib().nightjar_gemm_workspace_bytes(dtype, M, N, K, epilogue)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def gemm(dtype, x, w, y, M, N, K, epilogue, workspace, workspace_nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_gemm(dtype, x, w, y, M, N, K, epilogue, workspace, workspace_nbytes, stream))
 
 
 def header_functions(header_path: str):

@@ -1,21 +1,23 @@
 // Acceptance test of speculative sampling on the target logits.
 //
-// Stage 1 (accept_stats): per (window row, 8192-wide vocab chunk) the chunk
-// max and the sum of exp(logit - max): the softmax normaliser of every row
-// without a full-row pass in one workgroup.
+// The test for draft i only needs p_i(x_i) and q_i(x_i), so all k tests are
+// independent; the accepted length n is the index of the first failure.  The
+// draw after it needs a running sum over one full vocabulary row, which is
+// where the bandwidth goes.  Three kernels:
 //
-// Stage 2 (accept_finalize): one workgroup of 16 waves per sequence.
-//   - row statistics from the chunk partials (fixed order);
-//   - the accept loop over drafts: x_i is accepted iff u_i < p_i(x_i)/q_i(x_i)
-//     (q_i(x_i) == 0 accepts), stopping at the first rejection n;
-//   - the weights of the final draw, w = max(0, p_n - q_n) after a rejection
-//     (p_n if that is all zero) or w = p_k for the bonus token;
-//   - the inverse CDF: the smallest j with sum_{i<=j} w_i > u_k * sum(w),
-//     found by fp64 sums over 256-wide tiles (one per wave step), a wave
-//     prefix scan over the tile sums to locate the tile, and a wave prefix
-//     scan inside that tile.  Every sum is accumulated in fp64 in a fixed order,
-//     so the draw is reproducible; against a sequential fp64 running sum of the
-//     same fp32 weights only the summation order differs (~1e-15 relative).
+//   accept_stats   (rows x 8192-wide chunks): chunk max and sum of exp(l - max).
+//   accept_tiles   (rows x tile blocks): every window row i of every sequence is
+//                  a candidate draw row -- weights max(0, p_i - q_i) for i < k
+//                  (the residual after a rejection at i), p_k for the bonus row
+//                  -- and gets fp64 sums over 256-wide tiles.  Done for all
+//                  rows at once, since n is not known yet.
+//   accept_finalize (one wave per sequence): lanes run the k accept tests in
+//                  parallel (u_i < p_i(x_i) / q_i(x_i), q == 0 accepts), n =
+//                  first failure; then the smallest j whose running sum of
+//                  row n's weights exceeds u_k times their total: a prefix scan
+//                  over lane-contiguous tile sums finds the tile, a prefix scan
+//                  over that tile's 256 weights finds the entry.  All sums are
+//                  fp64 in a fixed order, so the draw is reproducible.
 #include "common.h"
 #include "kernels.h"
 
@@ -24,23 +26,47 @@ namespace {
 
 constexpr int kChunk = 8192;
 constexpr int kStatThreads = 256;
-constexpr int kAccThreads = 1024;
-constexpr int kAccWaves = kAccThreads / kWave;
-constexpr int kTile = 256;       // elements per wave step (4 per lane)
-constexpr int kMaxTiles = 2048;  // V <= 524288
-constexpr int kMaxT = 16;
+constexpr int kTile = 256;          // weights per tile (4 per lane of a wave)
+constexpr int kTilesPerBlock = 32;  // tiles per accept_tiles workgroup
+constexpr int kMaxTiles = 2048;     // V <= 524288
 
+// One pass: each thread holds its 32 values of the chunk in registers.
 __global__ __launch_bounds__(kStatThreads) void accept_stats_kernel(const float* __restrict__ logits, int V, int nch,
                                                                     float* __restrict__ stats) {
+  constexpr int PER = kChunk / kStatThreads / 4;  // float4 groups per thread
   __shared__ float sh[kStatThreads / kWave];
   const int row = blockIdx.x, c = blockIdx.y;
   const float* x = logits + (size_t)row * V;
   const int lo = c * kChunk, hi = min(lo + kChunk, V);
+  float v[PER][4];
   float mx = -INFINITY;
-  for (int j = lo + threadIdx.x; j < hi; j += kStatThreads) mx = fmaxf(mx, x[j]);
+  if ((V & 3) == 0) {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int j = lo + (it * kStatThreads + threadIdx.x) * 4;
+      const f32x4 q = j < hi ? *reinterpret_cast<const f32x4*>(x + j) : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[it][e] = q[e];
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < PER; ++it)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = lo + (it * kStatThreads + threadIdx.x) * 4 + e;
+        v[it][e] = j < hi ? x[j] : -INFINITY;
+      }
+  }
+#pragma unroll
+  for (int it = 0; it < PER; ++it)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, v[it][e]);
   mx = block_max<kStatThreads>(mx, sh);
   float s = 0.f;
-  for (int j = lo + threadIdx.x; j < hi; j += kStatThreads) s += expf(x[j] - mx);
+#pragma unroll
+  for (int it = 0; it < PER; ++it)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s += (v[it][e] == -INFINITY) ? 0.f : expf(v[it][e] - mx);
   s = block_sum<kStatThreads>(s, sh);
   if (threadIdx.x == 0) {
     stats[((size_t)row * nch + c) * 2] = mx;
@@ -48,220 +74,257 @@ __global__ __launch_bounds__(kStatThreads) void accept_stats_kernel(const float*
   }
 }
 
-struct AccK {
-  const float* logits;
-  const int32_t* drafts;
-  const float* dprobs;
-  const float* uniforms;
-  const float* stats;
-  int32_t* accepted_len;
-  int32_t* next_tokens;
-  int* err;
-  int k, V, nch;
-};
+// Row max and 1/sum from the chunk statistics, in chunk order.
+__device__ __forceinline__ void row_stats(const float* __restrict__ st, int nch, float* m, float* inv_s) {
+  float mx = -INFINITY;
+  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, st[2 * c]);
+  float s = 0.f;
+  for (int c = 0; c < nch; ++c) s += st[2 * c + 1] * expf(st[2 * c] - mx);
+  *m = mx;
+  *inv_s = 1.0f / s;
+}
 
-// weight of vocab entry j for the final draw
+// Weight of vocabulary entry j in a draw row: p_j, or max(0, p_j - q_j).
 __device__ __forceinline__ float draw_weight(const float* __restrict__ lrow, const float* __restrict__ qrow,
                                              float m, float inv_s, bool resid, int j) {
   const float p = expf(lrow[j] - m) * inv_s;
   return resid ? fmaxf(0.f, p - qrow[j]) : p;
 }
 
-__global__ __launch_bounds__(kAccThreads) void accept_finalize_kernel(AccK a) {
-  __shared__ float row_m[kMaxT], row_is[kMaxT];
-  __shared__ double tsum[kMaxTiles];
-  __shared__ int sh_n, sh_resid, sh_y;
-  __shared__ double sh_total;
+struct AccK {
+  const float* logits;    // [B*T][V]
+  const int32_t* drafts;  // [B][k]
+  const float* dprobs;    // [B][k][V]
+  const float* uniforms;  // [B][T]
+  const float* stats;     // [B*T][nch][2]
+  float* rowstat;         // [B*T][2]: max, 1/sum
+  double* tsum;           // [B*T][ntile]
+  int32_t* accepted_len;
+  int32_t* next_tokens;
+  int* err;
+  int k, V, nch, ntile;
+};
 
-  const int b = blockIdx.x, T = a.k + 1, V = a.V;
+__global__ __launch_bounds__(256) void accept_tiles_kernel(AccK a) {
+  const int row = blockIdx.x, T = a.k + 1, b = row / T, i = row % T;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-
-  if (threadIdx.x < T) {
-    const float* st = a.stats + (size_t)(b * T + threadIdx.x) * a.nch * 2;
-    float mx = -INFINITY;
-    for (int c = 0; c < a.nch; ++c) mx = fmaxf(mx, st[2 * c]);
-    float s = 0.f;
-    for (int c = 0; c < a.nch; ++c) s += st[2 * c + 1] * expf(st[2 * c] - mx);
-    row_m[threadIdx.x] = mx;
-    row_is[threadIdx.x] = 1.0f / s;
+  float m, inv_s;
+  row_stats(a.stats + (size_t)row * a.nch * 2, a.nch, &m, &inv_s);
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    a.rowstat[row * 2] = m;
+    a.rowstat[row * 2 + 1] = inv_s;
   }
-  __syncthreads();
-
-  if (threadIdx.x == 0) {
-    int n = 0;
-    for (; n < a.k; ++n) {
-      const int x = a.drafts[b * a.k + n];
-      if (x < 0 || x >= V) {
-        flag_error(a.err, kErrToken);
-        break;
+  const bool resid = i < a.k;
+  const float* lrow = a.logits + (size_t)row * a.V;
+  const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + i) * a.V : lrow;
+  const int t0 = blockIdx.y * kTilesPerBlock, t1 = min(t0 + kTilesPerBlock, a.ntile);
+  const bool vec = (a.V & 3) == 0;
+  for (int t = t0 + wave; t < t1; t += 4) {
+    const int j0 = t * kTile + lane * 4;
+    double ls = 0.0;
+    if (vec && j0 + 3 < a.V) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lrow + j0);
+      const f32x4 q4 = *reinterpret_cast<const f32x4*>(qrow + j0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = expf(l4[e] - m) * inv_s;
+        ls += (double)(resid ? fmaxf(0.f, p - q4[e]) : p);
       }
-      const float p = expf(a.logits[(size_t)(b * T + n) * V + x] - row_m[n]) * row_is[n];
-      const float q = a.dprobs[((size_t)b * a.k + n) * V + x];
-      const bool acc = (q <= 0.f) || (a.uniforms[b * T + n] < p / q);
-      if (!acc) break;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j0 + e < a.V) ls += (double)draw_weight(lrow, qrow, m, inv_s, resid, j0 + e);
     }
-    sh_n = n;
-    sh_resid = n < a.k;
+    ls = wave_sum_d(ls);
+    if (lane == 0) a.tsum[(size_t)row * a.ntile + t] = ls;
   }
-  __syncthreads();
+}
 
-  const int n = sh_n;
-  const float* lrow = a.logits + (size_t)(b * T + n) * V;
-  // draft row of the rejected position (only read when there is a rejection)
-  const float* qrow = (n < a.k) ? a.dprobs + ((size_t)b * a.k + n) * V : lrow;
-  const float m = row_m[n], inv_s = row_is[n];
-  const int ntile = (V + kTile - 1) / kTile;
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ double wave_incl_scan(double v) {
+  const int lane = threadIdx.x & 63;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const double up = __shfl_up(v, o);
+    if (lane >= o) v += up;
+  }
+  return v;
+}
 
-  for (int pass = 0; pass < 2; ++pass) {
-    const bool resid = sh_resid;
-    for (int t = wave; t < ntile; t += kAccWaves) {
-      double ls = 0.0;
+__global__ __launch_bounds__(64) void accept_finalize_kernel(AccK a) {
+  __shared__ double fb_tsum[kMaxTiles];  // only for an all-zero residual
+  const int b = blockIdx.x, T = a.k + 1, V = a.V, lane = threadIdx.x;
+
+  // the k accept tests, one per lane (lanes 0..k-1), then n = first failure
+  bool ok = true;
+  if (lane < a.k) {
+    const int x = a.drafts[b * a.k + lane];
+    if (x < 0 || x >= V) {
+      flag_error(a.err, kErrToken);
+      ok = false;
+    } else {
+      const int r = b * T + lane;
+      const float p = expf(a.logits[(size_t)r * V + x] - a.rowstat[r * 2]) * a.rowstat[r * 2 + 1];
+      const float q = a.dprobs[((size_t)b * a.k + lane) * V + x];
+      ok = (q <= 0.f) || (a.uniforms[b * T + lane] < p / q);
+    }
+  }
+  const unsigned long long fails = __ballot(lane < a.k && !ok);
+  const int n = fails ? __ffsll((long long)fails) - 1 : a.k;
+
+  const int row = b * T + n;
+  bool resid = n < a.k;
+  const float* lrow = a.logits + (size_t)row * V;
+  const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * V : lrow;
+  const float m = a.rowstat[row * 2], inv_s = a.rowstat[row * 2 + 1];
+  const int ntile = a.ntile;
+  const double* ts = a.tsum + (size_t)row * ntile;
+
+  // lane-contiguous tile ranges; the total is the last inclusive prefix, so it
+  // is made of exactly the additions the search below walks through
+  const int per = (ntile + kWave - 1) / kWave;
+  const int t0 = min(lane * per, ntile), t1 = min(t0 + per, ntile);
+  double ls = 0.0;
+  for (int t = t0; t < t1; ++t) ls += ts[t];
+  double incl = wave_incl_scan(ls);
+  double total = __shfl(incl, kWave - 1);
+  if (resid && !(total > 0.0)) {
+    // max(0, p_n - q_n) vanished (only rounding can do that): draw from p_n
+    resid = false;
+    qrow = lrow;
+    for (int t = 0; t < ntile; ++t) {
+      double s = 0.0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int j = t * kTile + lane * 4 + e;
-        if (j < V) ls += (double)draw_weight(lrow, qrow, m, inv_s, resid, j);
+        if (j < V) s += (double)draw_weight(lrow, qrow, m, inv_s, false, j);
       }
-      ls = wave_sum_d(ls);
-      if (lane == 0) tsum[t] = ls;
-    }
-    __syncthreads();
-    if (wave == 0) {
-      double s = 0.0;
-      for (int t = lane; t < ntile; t += kWave) s += tsum[t];
       s = wave_sum_d(s);
-      if (lane == 0) {
-        sh_total = s;
-        // an all-zero residual (only rounding makes p_n <= q_n everywhere) falls back to p_n
-        if (pass == 0 && resid && !(s > 0.0)) sh_resid = 0;
-      }
+      if (lane == 0) fb_tsum[t] = s;
     }
     __syncthreads();
-    if (!(pass == 0 && resid && !sh_resid)) break;
+    ts = fb_tsum;
+    ls = 0.0;
+    for (int t = t0; t < t1; ++t) ls += ts[t];
+    incl = wave_incl_scan(ls);
+    total = __shfl(incl, kWave - 1);
   }
+  const double target = (double)a.uniforms[b * T + a.k] * total;
 
-  if (wave == 0) {
-    const bool resid = sh_resid;
-    const double target = (double)a.uniforms[b * T + a.k] * sh_total;
-    // contiguous tiles per lane, then a wave prefix scan over the lane sums
-    const int per = (ntile + kWave - 1) / kWave;
-    const int t0 = min(lane * per, ntile), t1 = min(t0 + per, ntile);
-    double ls = 0.0;
-    for (int t = t0; t < t1; ++t) ls += tsum[t];
-    double incl = ls;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const double up = __shfl_up(incl, o);
-      if (lane >= o) incl += up;
-    }
-    const unsigned long long hit = __ballot(incl > target);
-    int tile = -1;
-    double base = 0.0;
-    bool want_last = false;  // take the last positive entry of `tile` instead of searching
-    if (hit) {
-      const int L = __ffsll((long long)hit) - 1;
-      if (lane == L) {
-        double cum = incl - ls;
-        for (int t = t0; t < t1; ++t) {
-          if (cum + tsum[t] > target) {
-            tile = t;
-            base = cum;
-            break;
-          }
-          cum += tsum[t];
-        }
-      }
-      tile = __shfl(tile, L);
-      base = __shfl(base, L);
-      if (tile < 0) {
-        // the lane-level and tile-level sums round differently and the target
-        // fell between them: the last positive tile of lane L's range
-        int tl = -1;
-        if (lane == L)
-          for (int t = t1 - 1; t >= t0; --t)
-            if (tsum[t] > 0.0) {
-              tl = t;
-              break;
-            }
-        tile = __shfl(tl, L);
-        want_last = true;
-      }
-    } else {
-      // no running sum exceeds u*S (u close to 1): the last positive weight
-      int tl = -1;
-      for (int t = ntile - 1 - lane; t >= 0; t -= kWave)
-        if (tsum[t] > 0.0) {
-          tl = t;
+  int tile = -1;
+  double base = 0.0;
+  int want_last = 0;  // take the last positive entry of `tile` instead of searching
+  const unsigned long long hit = __ballot(incl > target);
+  if (hit) {
+    const int L = __ffsll((long long)hit) - 1;
+    if (lane == L) {
+      double cum = incl - ls;
+      for (int t = t0; t < t1; ++t) {
+        if (cum + ts[t] > target) {
+          tile = t;
+          base = cum;
           break;
         }
-      for (int o = 32; o > 0; o >>= 1) tl = max(tl, __shfl_xor(tl, o));
-      tile = tl;
-      want_last = true;
-    }
-    if (tile < 0) tile = 0;
-    float w4[4];
-    double lsum = 0.0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = tile * kTile + lane * 4 + e;
-      w4[e] = (j < V) ? draw_weight(lrow, qrow, m, inv_s, resid, j) : 0.f;
-      lsum += (double)w4[e];
-    }
-    int cand = -1;
-    if (!want_last) {
-      double inc = lsum;
-      for (int o = 1; o < kWave; o <<= 1) {
-        const double up = __shfl_up(inc, o);
-        if (lane >= o) inc += up;
+        cum += ts[t];
       }
-      const unsigned long long h2 = __ballot(base + inc > target);
-      if (h2) {
-        const int L = __ffsll((long long)h2) - 1;
-        if (lane == L) {
-          double cum = base + inc - lsum;
-          for (int e = 0; e < 4; ++e) {
-            cum += (double)w4[e];
-            if (w4[e] > 0.f && cum > target) {
-              cand = tile * kTile + lane * 4 + e;
-              break;
-            }
+      if (tile < 0) {  // rounding: the last positive tile of this lane's range
+        for (int t = t1 - 1; t >= t0; --t)
+          if (ts[t] > 0.0) {
+            tile = t;
+            break;
+          }
+        want_last = 1;
+      }
+    }
+    tile = __shfl(tile, L);
+    base = __shfl(base, L);
+    want_last = __shfl(want_last, L);
+  } else {
+    // no running sum exceeds u*S (u close to 1): the last positive weight
+    int tl = -1;
+    for (int t = ntile - 1 - lane; t >= 0; t -= kWave)
+      if (ts[t] > 0.0) {
+        tl = t;
+        break;
+      }
+    for (int o = 32; o > 0; o >>= 1) tl = max(tl, __shfl_xor(tl, o));
+    tile = tl;
+    want_last = 1;
+  }
+  if (tile < 0) tile = 0;
+
+  float w4[4];
+  double lsum = 0.0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int j = tile * kTile + lane * 4 + e;
+    w4[e] = (j < V) ? draw_weight(lrow, qrow, m, inv_s, resid, j) : 0.f;
+    lsum += (double)w4[e];
+  }
+  int cand = -1;
+  if (!want_last) {
+    const double inc = wave_incl_scan(lsum);
+    const unsigned long long h2 = __ballot(base + inc > target);
+    if (h2) {
+      const int L = __ffsll((long long)h2) - 1;
+      if (lane == L) {
+        double cum = base + inc - lsum;
+        for (int e = 0; e < 4; ++e) {
+          cum += (double)w4[e];
+          if (w4[e] > 0.f && cum > target) {
+            cand = tile * kTile + lane * 4 + e;
+            break;
           }
         }
       }
-      for (int o = 32; o > 0; o >>= 1) cand = max(cand, __shfl_xor(cand, o));
     }
-    if (cand < 0) {
-      int lastpos = -1;
+    for (int o = 32; o > 0; o >>= 1) cand = max(cand, __shfl_xor(cand, o));
+  }
+  if (cand < 0) {
+    int lastpos = -1;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (w4[e] > 0.f) lastpos = tile * kTile + lane * 4 + e;
-      for (int o = 32; o > 0; o >>= 1) lastpos = max(lastpos, __shfl_xor(lastpos, o));
-      cand = lastpos < 0 ? tile * kTile : lastpos;
-    }
-    const int y = cand;
-    if (lane == 0) sh_y = y;
+    for (int e = 0; e < 4; ++e)
+      if (w4[e] > 0.f) lastpos = tile * kTile + lane * 4 + e;
+    for (int o = 32; o > 0; o >>= 1) lastpos = max(lastpos, __shfl_xor(lastpos, o));
+    cand = lastpos < 0 ? tile * kTile : lastpos;
   }
-  __syncthreads();
-  if (threadIdx.x < T) {
-    const int t = threadIdx.x;
+
+  if (lane < T) {
     int v = -1;
-    if (t < n) v = a.drafts[b * a.k + t];
-    else if (t == n) v = sh_y;
-    a.next_tokens[b * T + t] = v;
+    if (lane < n) v = a.drafts[b * a.k + lane];
+    else if (lane == n) v = cand;
+    a.next_tokens[b * T + lane] = v;
   }
-  if (threadIdx.x == 0) a.accepted_len[b] = n;
+  if (lane == 0) a.accepted_len[b] = n;
 }
+
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
 int accept_chunks(int V) { return (V + kChunk - 1) / kChunk; }
 
+size_t accept_workspace_bytes(int rows, int V) {
+  const int ntile = (V + kTile - 1) / kTile;
+  return al256((size_t)rows * accept_chunks(V) * 2 * 4) + al256((size_t)rows * 2 * 4) +
+         al256((size_t)rows * ntile * 8);
+}
+
 hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
-  const int T = x.k + 1, nch = accept_chunks(x.V);
-  hipLaunchKernelGGL(accept_stats_kernel, dim3(x.B * T, nch), dim3(kStatThreads), 0, s, x.logits, x.V, nch,
-                     x.stats);
+  const int T = x.k + 1, rows = x.B * T, nch = accept_chunks(x.V), ntile = (x.V + kTile - 1) / kTile;
+  char* ws = static_cast<char*>(x.scratch);
+  float* stats = reinterpret_cast<float*>(ws);
+  float* rowstat = reinterpret_cast<float*>(ws + al256((size_t)rows * nch * 2 * 4));
+  double* tsum = reinterpret_cast<double*>(ws + al256((size_t)rows * nch * 2 * 4) + al256((size_t)rows * 2 * 4));
+  hipLaunchKernelGGL(accept_stats_kernel, dim3(rows, nch), dim3(kStatThreads), 0, s, x.logits, x.V, nch, stats);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, x.stats, x.accepted_len, x.next_tokens, x.err, x.k, x.V, nch};
-  hipLaunchKernelGGL(accept_finalize_kernel, dim3(x.B), dim3(kAccThreads), 0, s, a);
+  AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, stats, rowstat, tsum, x.accepted_len, x.next_tokens, x.err,
+         x.k, x.V, nch, ntile};
+  hipLaunchKernelGGL(accept_tiles_kernel, dim3(rows, (ntile + kTilesPerBlock - 1) / kTilesPerBlock), dim3(256), 0,
+                     s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_finalize_kernel, dim3(x.B), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

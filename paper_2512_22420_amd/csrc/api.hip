@@ -3,6 +3,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -38,9 +39,22 @@ size_t al(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
-  size_t err, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats, total;
+  size_t err, gemm_cnt, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats, gemm_part, total;
   size_t win_layer_bytes;
 };
+
+// The step's GEMMs, in order: (N, K, epilogue).
+struct GemmShape {
+  int N, K, epi;
+};
+void step_gemms(const nj_model_desc& d, GemmShape out[5]) {
+  const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
+  out[0] = {QKV, d.d_model, kEpiStore};
+  out[1] = {d.d_model, HD, kEpiResidual};
+  out[2] = {2 * d.ffn_dim, d.d_model, kEpiSwiglu};
+  out[3] = {d.d_model, d.ffn_dim, kEpiResidual};
+  out[4] = {d.vocab, d.d_model, kEpiStore};
+}
 
 bool desc_ok(const nj_model_desc* d) {
   if (!d) return !fail(NJ_EINVAL, "desc is NULL");
@@ -53,6 +67,8 @@ bool desc_ok(const nj_model_desc* d) {
   if (d->dtype != NJ_F32 && d->dtype != NJ_BF16) return !fail(NJ_EINVAL, "dtype must be NJ_F32 or NJ_BF16");
   if (d->vocab > kMaxVocab) return !fail(NJ_EINVAL, "vocab > %d", kMaxVocab);
   if (!(d->rms_eps >= 0.f) || !(d->rope_theta > 0.f)) return !fail(NJ_EINVAL, "bad rms_eps or rope_theta");
+  if (d->d_model % 4 || d->d_model > 8192) return !fail(NJ_EINVAL, "d_model must be a multiple of 4, at most 8192");
+  if (d->head_dim > 512) return !fail(NJ_EINVAL, "head_dim > 512");
   if (d->dtype == NJ_BF16) {
     const int qkv = (d->n_heads + 2 * d->n_kv_heads) * d->head_dim;
     if (d->head_dim != 128) return !fail(NJ_EINVAL, "bf16 path needs head_dim 128");
@@ -78,6 +94,19 @@ Layout layout(const nj_model_desc& d, int B, int k) {
     return o;
   };
   L.err = take(kAlign);
+  // split-K arrival counters of the step's GEMMs: one region at a fixed place,
+  // zeroed by nightjar_workspace_init and left at zero by every GEMM
+  size_t cnt = 0, part = 0;
+  if (d.dtype == NJ_BF16) {
+    GemmShape gs[5];
+    step_gemms(d, gs);
+    for (const GemmShape& g : gs) {
+      const GemmPlan p = gemm_plan((int)M, g.N, g.K, g.epi);
+      cnt = std::max(cnt, p.counter_bytes);
+      part = std::max(part, p.part_bytes);
+    }
+  }
+  L.gemm_cnt = take(cnt);
   L.h = take(M * d.d_model * 4);
   L.x = take(M * d.d_model * e);
   L.qkv = take(M * qkv * 4);
@@ -92,7 +121,8 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   L.o = take(M * HD * e);
   L.act = take(M * d.ffn_dim * e);
   L.logits = take(M * d.vocab * 4);
-  L.stats = take(M * accept_chunks(d.vocab) * 2 * 4);
+  L.stats = take(accept_workspace_bytes((int)M, d.vocab));
+  L.gemm_part = take(part);  // split-K partials (GEMMs run one after another)
   L.total = off;
   return L;
 }
@@ -116,7 +146,9 @@ size_t nightjar_workspace_bytes(const nj_model_desc* desc, int32_t max_B, int32_
 
 int nightjar_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
   if (!workspace || workspace_bytes < kAlign) return fail(NJ_EINVAL, "workspace NULL or smaller than %zu", kAlign);
-  hipError_t e = launch_fill_i32(static_cast<int32_t*>(workspace), 0, 1, (hipStream_t)stream);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+  if (workspace_bytes / 4 > (size_t)INT32_MAX) return fail(NJ_EINVAL, "workspace too large");
+  hipError_t e = launch_fill_i32(static_cast<int32_t*>(workspace), 0, (int)(workspace_bytes / 4), (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "workspace_init");
 }
 
@@ -180,6 +212,8 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   void* q = ws + L.q;
   void* o = ws + L.o;
   void* act = ws + L.act;
+  int* gcnt = reinterpret_cast<int*>(ws + L.gemm_cnt);
+  float* gpart = reinterpret_cast<float*>(ws + L.gemm_part);
   float* logits = target_logits ? target_logits : reinterpret_cast<float*>(ws + L.logits);
   const int dt = bf ? kBF16 : kF32;
   const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
@@ -200,7 +234,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   for (int l = 0; l < d.n_layers; ++l) {
     const nj_layer_weights& lw = w->layers[l];
     if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s), "attn_norm");
-    NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, s), "qkv gemm");
+    NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s), "qkv gemm");
     void* wk = ws + L.win_k + l * L.win_layer_bytes;
     void* wv = ws + L.win_v + l * L.win_layer_bytes;
     NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
@@ -211,15 +245,15 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml), nsplit, bps,
                 o, err};
     NJ_TRY(launch_attention(aa, s), "attention");
-    NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, s), "o gemm");
+    NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s), "o gemm");
     NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s), "ffn_norm");
-    NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu, s), "gate_up gemm");
-    NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, s), "down gemm");
+    NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu, gcnt, gpart, s), "gate_up gemm");
+    NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s), "down gemm");
   }
   NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s), "final_norm");
-  NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, s), "lm_head gemm");
-  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, reinterpret_cast<float*>(ws + L.stats),
-                accepted_len, next_tokens, err};
+  NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
+  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, accepted_len, next_tokens,
+                err};
   NJ_TRY(launch_accept(ac, s), "accept");
 #undef NJ_TRY
   {
@@ -256,6 +290,14 @@ int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const i
   return e == hipSuccess ? NJ_OK : hip_fail(e, "kv_append");
 }
 
+size_t nightjar_accept_workspace_bytes(int32_t vocab, int32_t B, int32_t k) {
+  if (vocab < 1 || vocab > kMaxVocab || B < 1 || k < 0 || k > kMaxK) {
+    fail(NJ_EINVAL, "bad vocab, B or k");
+    return 0;
+  }
+  return kAlign + accept_workspace_bytes(B * (k + 1), vocab);
+}
+
 int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_t* draft_tokens,
                     const float* draft_probs, const float* uniforms, int32_t B, int32_t k, int32_t* accepted_len,
                     int32_t* next_tokens, void* workspace, size_t workspace_bytes, void* stream) {
@@ -264,20 +306,18 @@ int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_
   if (!logits || !uniforms || !accepted_len || !next_tokens || !workspace)
     return fail(NJ_EINVAL, "a required pointer is NULL");
   if (k > 0 && (!draft_tokens || !draft_probs)) return fail(NJ_EINVAL, "k > 0 needs draft_tokens and draft_probs");
-  const size_t M = (size_t)B * (k + 1);
-  const size_t need = kAlign + al(M * accept_chunks(desc->vocab) * 2 * 4);
+  const size_t need = nightjar_accept_workspace_bytes(desc->vocab, B, k);
   if (workspace_bytes < need) return fail(NJ_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, need);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
   char* ws = static_cast<char*>(workspace);
-  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, reinterpret_cast<float*>(ws + kAlign),
-               accepted_len, next_tokens, reinterpret_cast<int*>(ws)};
+  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, ws + kAlign, accepted_len, next_tokens,
+               reinterpret_cast<int*>(ws)};
   hipError_t e = launch_accept(a, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "accept");
 }
 
-int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
-                  int32_t epilogue, void* stream) {
+static int gemm_args_ok(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue) {
   if (dtype != NJ_F32 && dtype != NJ_BF16) return fail(NJ_EINVAL, "bad dtype");
-  if (!x || !w || !y) return fail(NJ_EINVAL, "NULL operand");
   if (M < 1 || N < 1 || K < 1) return fail(NJ_EINVAL, "M, N, K must be >= 1");
   if (epilogue < NJ_GEMM_STORE || epilogue > NJ_GEMM_SWIGLU) return fail(NJ_EINVAL, "bad epilogue");
   if (epilogue == NJ_GEMM_SWIGLU && N % 2) return fail(NJ_EINVAL, "SwiGLU needs an even N");
@@ -285,9 +325,31 @@ int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t 
   if (dtype == NJ_BF16) {
     if (K % 32) return fail(NJ_EINVAL, "bf16 GEMM needs K %% 32 == 0");
     if (Nout % 16) return fail(NJ_EINVAL, "bf16 GEMM needs output width %% 16 == 0");
-    if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(NJ_EINVAL, "operands must be 16-byte aligned");
   }
-  hipError_t e = launch_gemm(dtype == NJ_BF16 ? kBF16 : kF32, x, w, y, M, N, K, epilogue, (hipStream_t)stream);
+  return NJ_OK;
+}
+
+size_t nightjar_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue) {
+  if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return 0;
+  if (dtype != NJ_BF16) return kAlign;
+  const GemmPlan p = gemm_plan(M, N, K, epilogue);
+  return kAlign + p.counter_bytes + p.part_bytes;
+}
+
+int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
+                  int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream) {
+  if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
+  if (!x || !w || !y) return fail(NJ_EINVAL, "NULL operand");
+  if (dtype == NJ_BF16 && (!aligned16(x) || !aligned16(w) || !aligned16(y)))
+    return fail(NJ_EINVAL, "operands must be 16-byte aligned");
+  const size_t need = nightjar_gemm_workspace_bytes(dtype, M, N, K, epilogue);
+  if (!workspace || workspace_bytes < need) return fail(NJ_EINVAL, "workspace NULL or smaller than %zu bytes", need);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+  char* ws = static_cast<char*>(workspace) + kAlign;  // [counters][partials]
+  size_t cnt_bytes = 0;
+  if (dtype == NJ_BF16) cnt_bytes = gemm_plan(M, N, K, epilogue).counter_bytes;
+  hipError_t e = launch_gemm(dtype == NJ_BF16 ? kBF16 : kF32, x, w, y, M, N, K, epilogue, reinterpret_cast<int*>(ws),
+                             reinterpret_cast<float*>(ws + cnt_bytes), (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "gemm");
 }
 

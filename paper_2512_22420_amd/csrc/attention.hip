@@ -215,27 +215,25 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnK a) {
 }
 
 // Merge KV-split partials in split order: out = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
-__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
-                                                           const float* __restrict__ part_ml,
-                                                           bf16_t* __restrict__ out, int nsplit, int rpad, int T,
-                                                           int H, int Hkv) {
-  const int pair = blockIdx.x, b = pair / Hkv, kvh = pair % Hkv;
-  const int G = H / Hkv, R = T * G;
-  for (int idx = threadIdx.x; idx < R * kD; idx += blockDim.x) {
-    const int qr = idx / kD, d = idx % kD;
-    float mx = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, part_ml[(((size_t)pair * nsplit + s) * rpad + qr) * 2]);
-    float acc = 0.f, wsum = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const size_t base = ((size_t)pair * nsplit + s) * rpad + qr;
-      const float m = part_ml[base * 2];
-      const float f = (m == -INFINITY) ? 0.f : exp2f(m - mx);
-      wsum += f * part_ml[base * 2 + 1];
-      acc += f * part_o[base * kD + d];
-    }
-    const int i = qr / G, hh = qr % G;
-    out[((size_t)(b * T + i) * H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
+// One workgroup per (sequence, KV head, query row), one thread per head dim.
+__global__ __launch_bounds__(kD) void attn_combine_kernel(const float* __restrict__ part_o,
+                                                          const float* __restrict__ part_ml,
+                                                          bf16_t* __restrict__ out, int nsplit, int rpad, int T,
+                                                          int H, int Hkv) {
+  const int pair = blockIdx.x, qr = blockIdx.y, d = threadIdx.x;
+  const int b = pair / Hkv, kvh = pair % Hkv, G = H / Hkv;
+  float mx = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, part_ml[(((size_t)pair * nsplit + s) * rpad + qr) * 2]);
+  float acc = 0.f, wsum = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const size_t base = ((size_t)pair * nsplit + s) * rpad + qr;
+    const float m = part_ml[base * 2];
+    const float f = (m == -INFINITY) ? 0.f : exp2f(m - mx);
+    wsum += f * part_ml[base * 2 + 1];
+    acc += f * part_o[base * kD + d];
   }
+  const int i = qr / G, hh = qr % G;
+  out[((size_t)(b * T + i) * H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
 }
 
 // fp32 path: one workgroup per (sequence, query head, window position); scores
@@ -365,7 +363,7 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || x.nsplit == 1) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(x.B * x.Hkv), dim3(256), 0, s, x.part_o, x.part_ml,
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(x.B * x.Hkv, R), dim3(kD), 0, s, x.part_o, x.part_ml,
                      static_cast<bf16_t*>(x.out), x.nsplit, RT * 16, x.T, x.H, x.Hkv);
   return hipGetLastError();
 }

@@ -8,16 +8,53 @@ namespace nj {
 namespace {
 
 constexpr int kNormThreads = 256;
+constexpr int kNormMaxPer = 8;  // float4 groups per thread: d <= 8192
 
-// x = h / sqrt(mean(h^2) + eps) * gain, one row per workgroup.
+__device__ __forceinline__ void load4(const float* p, float* v) {
+  const f32x4 q = *reinterpret_cast<const f32x4*>(p);
+  v[0] = q[0], v[1] = q[1], v[2] = q[2], v[3] = q[3];
+}
+__device__ __forceinline__ void load4(const bf16_t* p, float* v) {
+  const u32x2 q = *reinterpret_cast<const u32x2*>(p);
+  v[0] = __uint_as_float(q[0] << 16), v[1] = __uint_as_float(q[0] & 0xffff0000u);
+  v[2] = __uint_as_float(q[1] << 16), v[3] = __uint_as_float(q[1] & 0xffff0000u);
+}
+__device__ __forceinline__ void store4(float* p, const float* v) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+}
+__device__ __forceinline__ void store4(bf16_t* p, const float* v) {
+  u32x2 q;
+  q[0] = pack_bf16x2(v[0], v[1]);
+  q[1] = pack_bf16x2(v[2], v[3]);
+  *reinterpret_cast<u32x2*>(p) = q;
+}
+
+// x = h / sqrt(mean(h^2) + eps) * gain for one row held in registers
+// (d % 4 == 0, d <= 4 * kNormThreads * kNormMaxPer).
 template <typename T>
-__device__ __forceinline__ void norm_row(const float* __restrict__ h, const T* __restrict__ gain,
+__device__ __forceinline__ void norm_row(const float (&hv)[kNormMaxPer][4], const T* __restrict__ gain,
                                          T* __restrict__ x, int d, float eps, float* sh) {
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += kNormThreads) ss = fmaf(h[i], h[i], ss);
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+    if (j < d)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ss = fmaf(hv[it][e], hv[it][e], ss);
+  }
   ss = block_sum<kNormThreads>(ss, sh);
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += kNormThreads) x[i] = from_f<T>(h[i] * r * to_f(gain[i]));
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+    if (j < d) {
+      float gv[4], o[4];
+      load4(gain + j, gv);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = hv[it][e] * r * gv[e];
+      store4(x + j, o);
+    }
+  }
 }
 
 template <typename T>
@@ -34,9 +71,16 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
   }
   const T* e = embed + (size_t)tok * d;
   float* hr = h + (size_t)row * d;
-  for (int j = threadIdx.x; j < d; j += kNormThreads) hr[j] = to_f(e[j]);
-  __syncthreads();
-  norm_row<T>(hr, gain, x + (size_t)row * d, d, eps, sh);
+  float hv[kNormMaxPer][4];
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+    if (j < d) {
+      load4(e + j, hv[it]);
+      store4(hr + j, hv[it]);
+    }
+  }
+  norm_row<T>(hv, gain, x + (size_t)row * d, d, eps, sh);
 }
 
 template <typename T>
@@ -44,30 +88,50 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
                                                                const T* __restrict__ gain, T* __restrict__ x,
                                                                int d, float eps) {
   __shared__ float sh[kNormThreads / kWave];
-  norm_row<T>(h + (size_t)blockIdx.x * d, gain, x + (size_t)blockIdx.x * d, d, eps, sh);
+  const float* hr = h + (size_t)blockIdx.x * d;
+  float hv[kNormMaxPer][4];
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+    if (j < d) load4(hr + j, hv[it]);
+  }
+  norm_row<T>(hv, gain, x + (size_t)blockIdx.x * d, d, eps, sh);
 }
 
 // One workgroup per window row.  Pair (j, j + D/2) of every q and k head turns
-// by pos * theta^(-2j/D), angle and sin/cos evaluated in fp64 (positions reach
-// several thousand radians).  k goes to win_k[b][g][i][:], v to
+// by pos * theta^(-2j/D); the D/2 angles of the row and their sin/cos are
+// evaluated once, in fp64 (positions reach several thousand radians), and
+// shared through LDS by all heads.  k goes to win_k[b][g][i][:], v to
 // win_v[b][g][:][i]; the row i == 0 workgroup also zeroes the unused slots
 // T..15 of the window block so that masked lanes never see stale data.
+constexpr int kMaxHalfDim = 256;
+
 template <typename T>
 __global__ __launch_bounds__(128) void rope_window_kernel(const float* __restrict__ qkv,
                                                           const int32_t* __restrict__ ctx, int T_, int H,
                                                           int Hkv, int D, float theta, T* __restrict__ q_out,
                                                           T* __restrict__ win_k, T* __restrict__ win_v) {
+  __shared__ float s_cos[kMaxHalfDim], s_sin[kMaxHalfDim];
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   const int half = D / 2;
   const double pos = (double)(max(ctx[b], 0) + i);
   const double ltheta = log((double)theta);
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    // angle in fp64, reduced to [-pi, pi] in fp64 (2*pi split in two parts),
+    // then an fp32 sin/cos of the small argument
+    const double ang = pos * exp(-(2.0 * j / D) * ltheta);
+    const double kq = rint(ang * 0.15915494309189535);
+    const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
+    float sn, cs;
+    sincosf((float)red, &sn, &cs);
+    s_cos[j] = cs;
+    s_sin[j] = sn;
+  }
+  __syncthreads();
   const float* src = qkv + (size_t)row * (H + 2 * Hkv) * D;
   for (int idx = threadIdx.x; idx < (H + Hkv) * half; idx += blockDim.x) {
     const int hd = idx / half, j = idx % half;
-    const double ang = pos * exp(-(2.0 * j / D) * ltheta);
-    double sd, cd;
-    sincos(ang, &sd, &cd);
-    const float c = (float)cd, sn = (float)sd;
+    const float c = s_cos[j], sn = s_sin[j];
     const float a = src[hd * D + j], bb = src[hd * D + j + half];
     const float ra = a * c - bb * sn, rb = bb * c + a * sn;
     if (hd < H) {
@@ -96,21 +160,23 @@ __global__ __launch_bounds__(128) void rope_window_kernel(const float* __restric
   }
 }
 
-constexpr int kMaxAppendLayers = 32;
+constexpr int kMaxAppendLayers = 64;
 struct PagePtrs {
   void* k[kMaxAppendLayers];
   void* v[kMaxAppendLayers];
 };
 
-// grid (B, layers of this chunk): copy window rows 0..n_b into their slots.
+// One workgroup per sequence: copy window rows 0..n_b of layers [layer0,
+// layer0 + nl) into their slots; the launch holding the last layer then
+// advances context_lens[b] (all readers of it are in this workgroup).
 template <typename T>
-__global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int layer0, const T* __restrict__ win_k,
-                                                        const T* __restrict__ win_v,
+__global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int layer0, int nl, bool last_chunk,
+                                                        const T* __restrict__ win_k, const T* __restrict__ win_v,
                                                         const int32_t* __restrict__ table, int max_blocks,
-                                                        int num_blocks, const int32_t* __restrict__ ctx,
+                                                        int num_blocks, int32_t* __restrict__ ctx,
                                                         const int32_t* __restrict__ acc, int B, int k, int Hkv,
                                                         int D, int* __restrict__ err) {
-  const int b = blockIdx.x, lc = blockIdx.y, l = layer0 + lc;
+  const int b = blockIdx.x;
   const int n = acc[b], c = ctx[b];
   if (n < 0 || n > k) {
     if (threadIdx.x == 0) flag_error(err, kErrAccept);
@@ -120,32 +186,30 @@ __global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int laye
     if (threadIdx.x == 0) flag_error(err, kErrContext);
     return;
   }
-  T* kp = static_cast<T*>(pages.k[lc]);
-  T* vp = static_cast<T*>(pages.v[lc]);
-  const size_t wbase = ((size_t)l * B + b) * Hkv;
-  for (int j = 0; j <= n; ++j) {
-    const int pos = c + j;
-    const int phys = table[(size_t)b * max_blocks + pos / kBlock];
-    if (phys < 0 || phys >= num_blocks) {
-      if (threadIdx.x == 0) flag_error(err, kErrBlock);
-      continue;
-    }
-    const int slot = pos % kBlock;
-    for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
-      const int g = idx / D, dd = idx % D;
-      kp[(((size_t)phys * Hkv + g) * kBlock + slot) * D + dd] = win_k[((wbase + g) * kBlock + j) * D + dd];
-      vp[(((size_t)phys * Hkv + g) * D + dd) * kBlock + slot] = win_v[((wbase + g) * D + dd) * kBlock + j];
+  for (int lc = 0; lc < nl; ++lc) {
+    const int l = layer0 + lc;
+    T* kp = static_cast<T*>(pages.k[lc]);
+    T* vp = static_cast<T*>(pages.v[lc]);
+    const size_t wbase = ((size_t)l * B + b) * Hkv;
+    for (int j = 0; j <= n; ++j) {
+      const int pos = c + j;
+      const int phys = table[(size_t)b * max_blocks + pos / kBlock];
+      if (phys < 0 || phys >= num_blocks) {
+        if (threadIdx.x == 0) flag_error(err, kErrBlock);
+        continue;
+      }
+      const int slot = pos % kBlock;
+      for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
+        const int g = idx / D, dd = idx % D;
+        kp[(((size_t)phys * Hkv + g) * kBlock + slot) * D + dd] = win_k[((wbase + g) * kBlock + j) * D + dd];
+        vp[(((size_t)phys * Hkv + g) * D + dd) * kBlock + slot] = win_v[((wbase + g) * D + dd) * kBlock + j];
+      }
     }
   }
-}
-
-__global__ void ctx_update_kernel(int32_t* __restrict__ ctx, const int32_t* __restrict__ acc, int B, int k,
-                                  int max_blocks) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  const int n = acc[b], c = ctx[b];
-  if (n < 0 || n > k || c < 0 || c + k + 1 > max_blocks * kBlock) return;
-  ctx[b] = c + n + 1;
+  if (last_chunk) {
+    __syncthreads();  // every thread has read ctx[b]
+    if (threadIdx.x == 0) ctx[b] = c + n + 1;
+  }
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
@@ -194,26 +258,24 @@ hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, i
 hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s) {
   for (int l0 = 0; l0 < a.L; l0 += kMaxAppendLayers) {
     const int nl = (a.L - l0 < kMaxAppendLayers) ? a.L - l0 : kMaxAppendLayers;
+    const bool last = l0 + nl >= a.L;
     PagePtrs p{};
     for (int i = 0; i < nl; ++i) {
       p.k[i] = a.k_pages[l0 + i];
       p.v[i] = a.v_pages[l0 + i];
     }
     if (a.dtype == kF32)
-      hipLaunchKernelGGL(kv_append_kernel<float>, dim3(a.B, nl), dim3(256), 0, s, p, l0,
+      hipLaunchKernelGGL(kv_append_kernel<float>, dim3(a.B), dim3(256), 0, s, p, l0, nl, last,
                          static_cast<const float*>(a.win_k), static_cast<const float*>(a.win_v), a.block_table,
                          a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
     else
-      hipLaunchKernelGGL(kv_append_kernel<bf16_t>, dim3(a.B, nl), dim3(256), 0, s, p, l0,
-                         static_cast<const bf16_t*>(a.win_k), static_cast<const bf16_t*>(a.win_v),
-                         a.block_table, a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D,
-                         a.err);
+      hipLaunchKernelGGL(kv_append_kernel<bf16_t>, dim3(a.B), dim3(256), 0, s, p, l0, nl, last,
+                         static_cast<const bf16_t*>(a.win_k), static_cast<const bf16_t*>(a.win_v), a.block_table,
+                         a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(ctx_update_kernel, dim3((a.B + 255) / 256), dim3(256), 0, s, a.ctx, a.accepted_len, a.B, a.k,
-                     a.max_blocks);
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s) {

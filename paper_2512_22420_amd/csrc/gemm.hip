@@ -1,14 +1,25 @@
 // GEMMs of the verify step: y = x . w^T over the B*(k+1) window rows.
 //
 // bf16 path: weight-streaming MFMA kernel.  At verify-step sizes M = B*(k+1)
-// is 1..~768 while N*K reaches 5e8 (LM head), so below M ~ 300 the kernel is
-// bound by reading each weight byte once from HBM.  Each wave owns 16 weight
-// rows (the A operand of v_mfma_f32_16x16x32_bf16) and streams them along K
-// with 16-byte loads, four 32-wide k-steps per pipeline stage, double
-// buffered; the activation rows (B operand, M padded to 16) come from L2.
-// Workgroups that would be too few to fill 256 CUs split K across their
-// waves and reduce through LDS in a fixed order.  Epilogues: store fp32,
-// residual add into the fp32 residual stream, SwiGLU into bf16 activations.
+// is 1..~768 while N*K reaches 5e8 (LM head), so below M ~ 300 the work is
+// bound by reading each weight byte once from HBM.
+//
+// - Each wave owns 16 weight rows -- the A operand of v_mfma_f32_16x16x32_bf16
+//   -- and streams them along K with 16-byte loads, eight 32-wide k-steps per
+//   stage, with the next stage's loads in flight while the current one is
+//   multiplied (two register buffers, no copies between them).
+// - The activation rows (B operand, M padded to 16) are staged per stage in
+//   LDS, loaded once per workgroup and shared by all its waves (4 or 8), with
+//   a 16-byte row pad against bank conflicts.  Reading them from L2 per wave
+//   instead costs half the bandwidth at M = 48.
+// - When 16-row tiles alone give too few workgroups to fill 256 CUs (small N),
+//   K is split across workgroups: each writes an fp32 partial, and the last
+//   workgroup of a tile to arrive (device-scope counter) adds the partials in
+//   chunk order and applies the epilogue, so results do not depend on arrival
+//   order.  Counters reset themselves for the next launch.
+// - Epilogues: store fp32, add into the fp32 residual stream, or SwiGLU
+//   (gate rows n and up rows Nout + n are two row groups of the same wave)
+//   stored as bf16.
 //
 // Operand layout (16x16x32 bf16): lane l supplies row (l & 15) of A and
 // column (l & 15) of B, eight consecutive k of k-group (l >> 4); the result
@@ -20,7 +31,10 @@
 namespace nj {
 namespace {
 
-constexpr int kU = 4;  // 32-wide k-steps per pipeline stage
+constexpr int kU = 8;                     // 32-wide k-steps per stage
+constexpr int kStageK = 32 * kU;          // 256
+constexpr int kRowStride = kStageK + 8;   // LDS row stride in elements (+16 bytes)
+constexpr int kTargetWorkgroups = 512;
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -28,28 +42,40 @@ __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
 
 __device__ __forceinline__ float silu_mul(float gte, float up) { return gte / (1.0f + expf(-gte)) * up; }
 
-// MT: 16-row tiles of x per workgroup; NG: weight row groups (2 for SwiGLU:
-// gate rows n and up rows Nout + n); KSPLIT: waves sharing one 16-row weight
-// tile along K; NW: waves per workgroup.
-template <int MT, int NG, int KSPLIT, int NW, int EPI>
-__global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(const bf16_t* __restrict__ X,
-                                                            const bf16_t* __restrict__ W,
-                                                            void* __restrict__ Y, int M, int Nout, int K) {
-  constexpr int WN = NW / KSPLIT;
+struct GemmK {
+  const bf16_t* X;
+  const bf16_t* W;
+  void* Y;
+  float* part;    // [nkc][M][NG][Nout] fp32 partials (split K only)
+  int* counters;  // [mblocks][ntiles] arrival counters (split K only), zero between launches
+  int M, Nout, K, stages_per_chunk;
+};
+
+// MT: 16-row x tiles per workgroup; NG: weight row groups (2 for SwiGLU);
+// NW: waves per workgroup (each owns 16 weight rows of every group).
+template <int MT, int NG, int NW, int EPI>
+__global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
+  constexpr int ROWS = MT * 16, NTH = NW * 64;
+  constexpr int CHUNKS = ROWS * kStageK / 8;  // 16-byte pieces of one x stage
+  constexpr int PER_T = (CHUNKS + NTH - 1) / NTH;
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kRowStride];
+  __shared__ int s_last;
+
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ks = wave % KSPLIT, ns = wave / KSPLIT;
   const int r = lane & 15, g = lane >> 4;
-  const int n0 = (blockIdx.x * WN + ns) * 16;
-  const int m0 = blockIdx.y * (MT * 16);
+  const int tile = blockIdx.x, mb = blockIdx.y, kc = blockIdx.z, nkc = gridDim.z;
+  const int M = a.M, Nout = a.Nout, K = a.K;
+  const int n0 = (tile * NW + wave) * 16;
+  const int m0 = mb * ROWS;
   const bool active = n0 < Nout;
+  const int S = K / 32;
+  const int nst = (S + kU - 1) / kU;
+  const int st0 = kc * a.stages_per_chunk, st1 = min(nst, st0 + a.stages_per_chunk);
 
   const int nrow = min(n0 + r, Nout - 1);
   const bf16_t* wp[NG];
 #pragma unroll
-  for (int q = 0; q < NG; ++q) wp[q] = W + (size_t)(q * Nout + nrow) * K + g * 8;
-  const bf16_t* xp[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) xp[mt] = X + (size_t)min(m0 + mt * 16 + r, M - 1) * K + g * 8;
+  for (int q = 0; q < NG; ++q) wp[q] = a.W + (size_t)(q * Nout + nrow) * K + g * 8;
 
   f32x4 acc[MT][NG];
 #pragma unroll
@@ -57,94 +83,148 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(const bf16_t* __rest
 #pragma unroll
     for (int q = 0; q < NG; ++q) acc[mt][q] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (active) {
-    const int S = K / 32;
-    const int s0 = (S * ks) / KSPLIT, s1 = (S * (ks + 1)) / KSPLIT;
-    const int nfull = (s1 - s0) / kU;
-    int s = s0;
-    if (nfull > 0) {
-      bf16x8 wa[NG][kU], xa[MT][kU];
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-#pragma unroll
-        for (int q = 0; q < NG; ++q) wa[q][u] = ld8(wp[q] + (s + u) * 32);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) xa[mt][u] = ld8(xp[mt] + (s + u) * 32);
-      }
-      for (int it = 0; it < nfull; ++it) {
-        // prefetch the next stage (the last iteration re-reads its own stage)
-        const int sn = (it + 1 < nfull) ? s + kU : s;
-        bf16x8 wb[NG][kU], xb[MT][kU];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-#pragma unroll
-          for (int q = 0; q < NG; ++q) wb[q][u] = ld8(wp[q] + (sn + u) * 32);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) xb[mt][u] = ld8(xp[mt] + (sn + u) * 32);
-        }
-#pragma unroll
-        for (int u = 0; u < kU; ++u)
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int q = 0; q < NG; ++q)
-              acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[q][u], xa[mt][u], acc[mt][q], 0, 0, 0);
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-#pragma unroll
-          for (int q = 0; q < NG; ++q) wa[q][u] = wb[q][u];
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) xa[mt][u] = xb[mt][u];
-        }
-        s += kU;
-      }
-    }
-    for (; s < s1; ++s) {
-      bf16x8 wv[NG], xv[MT];
-#pragma unroll
-      for (int q = 0; q < NG; ++q) wv[q] = ld8(wp[q] + s * 32);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) xv[mt] = ld8(xp[mt] + s * 32);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int q = 0; q < NG; ++q)
-          acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wv[q], xv[mt], acc[mt][q], 0, 0, 0);
-    }
+  u32x4 xr[PER_T];
+  bf16x8 wbuf[2][NG][kU];
+
+#define NJ_GLOAD_X(st)                                                                           \
+  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
+    const int idx = threadIdx.x + c * NTH;                                                       \
+    if (idx < CHUNKS) {                                                                          \
+      const int row = idx / (kStageK / 8), kk = (st) * kStageK + (idx % (kStageK / 8)) * 8;      \
+      xr[c] = kk < K ? *reinterpret_cast<const u32x4*>(a.X + (size_t)min(m0 + row, M - 1) * K + kk) \
+                     : u32x4{0u, 0u, 0u, 0u};                                                    \
+    }                                                                                            \
+  }
+#define NJ_SSTORE_X(buf)                                                                         \
+  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
+    const int idx = threadIdx.x + c * NTH;                                                       \
+    if (idx < CHUNKS) {                                                                          \
+      const int row = idx / (kStageK / 8), col = (idx % (kStageK / 8)) * 8;                      \
+      *reinterpret_cast<u32x4*>(&xs[buf][row * kRowStride + col]) = xr[c];                       \
+    }                                                                                            \
+  }
+#define NJ_LOAD_W(B, st)                                                                         \
+  if (active) {                                                                                  \
+    _Pragma("unroll") for (int u = 0; u < kU; ++u) {                                             \
+      if ((st) * kU + u < S) {                                                                   \
+        _Pragma("unroll") for (int q = 0; q < NG; ++q) wbuf[B][q][u] = ld8(wp[q] + ((st) * kU + u) * 32); \
+      }                                                                                          \
+    }                                                                                            \
+  }
+#define NJ_COMPUTE(B, buf, st)                                                                   \
+  if (active) {                                                                                  \
+    _Pragma("unroll") for (int u = 0; u < kU; ++u) {                                             \
+      if ((st) * kU + u < S) {                                                                   \
+        _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                      \
+          const bf16x8 xv = __builtin_bit_cast(                                                  \
+              bf16x8, *reinterpret_cast<const u32x4*>(&xs[buf][(mt * 16 + r) * kRowStride + u * 32 + g * 8])); \
+          _Pragma("unroll") for (int q = 0; q < NG; ++q) acc[mt][q] =                            \
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(wbuf[B][q][u], xv, acc[mt][q], 0, 0, 0);   \
+        }                                                                                        \
+      }                                                                                          \
+    }                                                                                            \
+  }
+  // one stage: stage st+1's x (global -> registers) and w loads go out, stage
+  // st is multiplied, stage st+1's x goes to the other LDS buffer
+#define NJ_STAGE(B, BN)                                       \
+  {                                                           \
+    const bool more = st + 1 < st1;                           \
+    if (more) {                                               \
+      NJ_GLOAD_X(st + 1);                                     \
+      NJ_LOAD_W(BN, st + 1);                                  \
+    }                                                         \
+    NJ_COMPUTE(B, (st - st0) & 1, st);                        \
+    if (more) NJ_SSTORE_X((st + 1 - st0) & 1);                \
+    __syncthreads();                                          \
+    ++st;                                                     \
+    if (st >= st1) break;                                     \
   }
 
-  if constexpr (KSPLIT > 1) {
-    __shared__ f32x4 red[NW][MT * NG][64];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int q = 0; q < NG; ++q) red[wave][mt * NG + q][lane] = acc[mt][q];
+  if (st0 < st1) {
+    NJ_GLOAD_X(st0);
+    NJ_LOAD_W(0, st0);
+    NJ_SSTORE_X(0);
     __syncthreads();
-    if (ks != 0) return;
-    for (int k2 = 1; k2 < KSPLIT; ++k2)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int q = 0; q < NG; ++q) acc[mt][q] += red[wave + k2][mt * NG + q][lane];
+    int st = st0;
+    for (;;) {
+      NJ_STAGE(0, 1)
+      NJ_STAGE(1, 0)
+    }
   }
-  if (!active) return;
+#undef NJ_GLOAD_X
+#undef NJ_SSTORE_X
+#undef NJ_LOAD_W
+#undef NJ_COMPUTE
+#undef NJ_STAGE
 
   const int n = n0 + 4 * g;
+  if (nkc > 1) {
+    // Split K: publish this chunk's partial, and the last chunk to arrive
+    // finishes the tile.  Partials are written and read with device-scope
+    // (L2 write-through / coherent) accesses, so the hand-off needs neither an
+    // L2 writeback nor an L2 invalidate: each thread waits until its partial
+    // stores are acknowledged, then one counter increment publishes them.
+    if (active) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = m0 + mt * 16 + r;
+        if (m < M)
+#pragma unroll
+          for (int q = 0; q < NG; ++q) {
+            float* dst = a.part + (((size_t)kc * M + m) * NG + q) * Nout + n;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              __hip_atomic_store(dst + i, acc[mt][q][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+      }
+    }
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    int* cnt = a.counters + (size_t)mb * gridDim.x + tile;
+    if (threadIdx.x == 0)
+      s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nkc - 1);
+    __syncthreads();
+    if (!s_last) return;
+    if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
+    if (!active) return;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = m0 + mt * 16 + r;
+      if (m >= M) continue;
+#pragma unroll
+      for (int q = 0; q < NG; ++q) {
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < nkc; ++j) {
+          if (j == kc) {
+            s += acc[mt][q];
+          } else {
+            const float* src = a.part + (((size_t)j * M + m) * NG + q) * Nout + n;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[i] += __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+        acc[mt][q] = s;
+      }
+    }
+  } else if (!active) {
+    return;
+  }
+
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int m = m0 + mt * 16 + r;
     if (m >= M) continue;
     if constexpr (EPI == kEpiStore) {
-      *reinterpret_cast<f32x4*>(static_cast<float*>(Y) + (size_t)m * Nout + n) = acc[mt][0];
+      *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) = acc[mt][0];
     } else if constexpr (EPI == kEpiResidual) {
-      f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(Y) + (size_t)m * Nout + n);
+      f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
       *p = *p + acc[mt][0];
     } else {
-      const f32x4 a = acc[mt][0], b = acc[mt][1];
+      const f32x4 gt = acc[mt][0], up = acc[mt][1];
       u32x2 o;
-      o[0] = pack_bf16x2(silu_mul(a[0], b[0]), silu_mul(a[1], b[1]));
-      o[1] = pack_bf16x2(silu_mul(a[2], b[2]), silu_mul(a[3], b[3]));
-      *reinterpret_cast<u32x2*>(static_cast<bf16_t*>(Y) + (size_t)m * Nout + n) = o;
+      o[0] = pack_bf16x2(silu_mul(gt[0], up[0]), silu_mul(gt[1], up[1]));
+      o[1] = pack_bf16x2(silu_mul(gt[2], up[2]), silu_mul(gt[3], up[3]));
+      *reinterpret_cast<u32x2*>(static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n) = o;
     }
   }
 }
@@ -178,44 +258,57 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
-template <int MT, int NG, int KSPLIT, int NW, int EPI>
-hipError_t launch_bf16_cfg(const void* x, const void* w, void* y, int M, int Nout, int K, hipStream_t s) {
-  constexpr int WN = NW / KSPLIT;
-  const int ntiles = Nout / 16;
-  dim3 grid((ntiles + WN - 1) / WN, (M + MT * 16 - 1) / (MT * 16));
-  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, KSPLIT, NW, EPI>), grid, dim3(NW * 64), 0, s,
-                     static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, M, Nout, K);
+template <int MT, int NG, int NW, int EPI>
+hipError_t launch_cfg(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI>), dim3(p.ntiles, p.mblocks, p.nkc), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
 }
 
-template <int MT, int NG, int EPI>
-hipError_t launch_bf16_mt(const void* x, const void* w, void* y, int M, int Nout, int K, int ksplit,
-                          hipStream_t s) {
-  switch (ksplit) {
-    case 1: return launch_bf16_cfg<MT, NG, 1, 4, EPI>(x, w, y, M, Nout, K, s);
-    case 2: return launch_bf16_cfg<MT, NG, 2, 4, EPI>(x, w, y, M, Nout, K, s);
-    case 4: return launch_bf16_cfg<MT, NG, 4, 4, EPI>(x, w, y, M, Nout, K, s);
-    default:
-      if constexpr (NG == 1) return launch_bf16_cfg<MT, NG, 8, 8, EPI>(x, w, y, M, Nout, K, s);
-      else return launch_bf16_cfg<MT, NG, 4, 4, EPI>(x, w, y, M, Nout, K, s);
+template <int NG, int EPI>
+hipError_t launch_epi(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+  if (p.nw == 4) {
+    switch (p.mt) {
+      case 1: return launch_cfg<1, NG, 4, EPI>(a, p, s);
+      case 2: return launch_cfg<2, NG, 4, EPI>(a, p, s);
+      case 3: return launch_cfg<3, NG, 4, EPI>(a, p, s);
+      default: return launch_cfg<4, NG, 4, EPI>(a, p, s);
+    }
+  }
+  switch (p.mt) {
+    case 1: return launch_cfg<1, NG, 8, EPI>(a, p, s);
+    case 2: return launch_cfg<2, NG, 8, EPI>(a, p, s);
+    case 3: return launch_cfg<3, NG, 8, EPI>(a, p, s);
+    default: return launch_cfg<4, NG, 8, EPI>(a, p, s);
   }
 }
 
-template <int NG, int EPI>
-hipError_t launch_bf16_epi(const void* x, const void* w, void* y, int M, int Nout, int K, int mt, int ksplit,
-                           hipStream_t s) {
-  switch (mt) {
-    case 1: return launch_bf16_mt<1, NG, EPI>(x, w, y, M, Nout, K, ksplit, s);
-    case 2: return launch_bf16_mt<2, NG, EPI>(x, w, y, M, Nout, K, ksplit, s);
-    case 3: return launch_bf16_mt<3, NG, EPI>(x, w, y, M, Nout, K, ksplit, s);
-    default: return launch_bf16_mt<4, NG, EPI>(x, w, y, M, Nout, K, ksplit, s);
-  }
-}
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
+GemmPlan gemm_plan(int M, int N, int K, int epi) {
+  GemmPlan p{};
+  const int NG = epi == kEpiSwiglu ? 2 : 1;
+  const int Nout = N / NG;
+  p.mt = M >= 64 ? 4 : (M + 15) / 16;
+  p.mblocks = (M + p.mt * 16 - 1) / (p.mt * 16);
+  const int tiles16 = (Nout + 15) / 16;
+  // 8 waves share each staged x tile when it is large; small N keeps 4 so
+  // that there are more workgroups before splitting K
+  p.nw = (p.mt >= 3 && tiles16 / 8 * p.mblocks >= 256) ? 8 : 4;
+  p.ntiles = (tiles16 + p.nw - 1) / p.nw;
+  const int nst = (K / 32 + kU - 1) / kU;
+  int nkc = 1;
+  while ((long)p.ntiles * p.mblocks * nkc < kTargetWorkgroups && nst / (nkc * 2) >= 2) nkc *= 2;
+  p.stages_per_chunk = (nst + nkc - 1) / nkc;
+  p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
+  p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
+  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * 4) : 0;
+  return p;
+}
+
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
-                       hipStream_t s) {
+                       int* counters, float* part, hipStream_t s) {
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   if (dtype == kF32) {
     dim3 grid((Nout + 3) / 4);
@@ -226,17 +319,12 @@ hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, 
     else hipLaunchKernelGGL(gemm_f32_kernel<kEpiSwiglu>, grid, dim3(256), 0, s, xf, wf, y, M, Nout, K);
     return hipGetLastError();
   }
-  // bf16: 16-row x tiles per workgroup, then split K until ~2048 waves are in flight
-  const int mt = M >= 64 ? 4 : (M + 15) / 16;
-  const int mblocks = (M + mt * 16 - 1) / (mt * 16);
-  const long tiles = (long)(Nout / 16) * mblocks;
-  const int steps = K / 32;
-  int ksplit = 1;
-  while (ksplit < 8 && tiles * ksplit < 2048 && steps / (ksplit * 2) >= 8) ksplit *= 2;
-  if (epi == kEpiSwiglu && ksplit > 4) ksplit = 4;
-  if (epi == kEpiStore) return launch_bf16_epi<1, kEpiStore>(x, w, y, M, Nout, K, mt, ksplit, s);
-  if (epi == kEpiResidual) return launch_bf16_epi<1, kEpiResidual>(x, w, y, M, Nout, K, mt, ksplit, s);
-  return launch_bf16_epi<2, kEpiSwiglu>(x, w, y, M, Nout, K, mt, ksplit, s);
+  const GemmPlan p = gemm_plan(M, N, K, epi);
+  GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.stages_per_chunk};
+  if (epi == kEpiStore) return launch_epi<1, kEpiStore>(a, p, s);
+  if (epi == kEpiResidual) return launch_epi<1, kEpiResidual>(a, p, s);
+  return launch_epi<2, kEpiSwiglu>(a, p, s);
 }
 
 }  // namespace nj

@@ -10,9 +10,22 @@ namespace nj {
 enum { kF32 = 0, kBF16 = 1 };
 enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2 };
 
-// y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]).
+// How the bf16 GEMM splits its work: 16-row x tiles per workgroup (mt),
+// waves per workgroup (nw), workgroups along N (ntiles) and M (mblocks), K
+// chunks across workgroups (nkc, stages_per_chunk), and the workspace the
+// split-K partials and arrival counters take.
+struct GemmPlan {
+  int mt, nw, ntiles, mblocks, nkc, stages_per_chunk;
+  size_t part_bytes, counter_bytes;
+};
+GemmPlan gemm_plan(int M, int N, int K, int epi);
+
+// y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]).  `counters`
+// (plan.counter_bytes, zero on entry and on exit) and `part`
+// (plan.part_bytes) are scratch; GEMMs that run one after another on a stream
+// may share both as long as the counters are never overwritten by anything else.
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
-                       hipStream_t s);
+                       int* counters, float* part, hipStream_t s);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
@@ -57,12 +70,13 @@ struct AcceptArgs {
   const float* dprobs;      // [B][k][V]
   const float* uniforms;    // [B][k+1]
   int B, k, V;
-  float* stats;             // [B*T][nch][2]
+  void* scratch;            // accept_workspace_bytes(B*T, V) bytes
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
 };
 int accept_chunks(int V);
+size_t accept_workspace_bytes(int rows, int V);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
 struct KvAppendArgs {

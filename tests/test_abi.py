@@ -64,12 +64,18 @@ def test_verify_step_rejects_bad_arguments_on_host():
 
 def test_gemm_rejects_bad_shapes_on_host():
     L = nb.lib()
-    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 32, 40, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL  # K % 32
-    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 24, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL  # N % 16
-    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 30, 64, nb.NJ_GEMM_SWIGLU, 0) == nb.NJ_EINVAL
-    assert L.nightjar_gemm(nb.NJ_BF16, 0, 16, 16, 4, 32, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL
-    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 0, 32, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL
-    assert L.nightjar_gemm(7, 16, 16, 16, 1, 32, 64, nb.NJ_GEMM_STORE, 0) == nb.NJ_EINVAL
+    big = 1 << 30
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 32, 40, nb.NJ_GEMM_STORE, 256, big, 0) == nb.NJ_EINVAL  # K % 32
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 24, 64, nb.NJ_GEMM_STORE, 256, big, 0) == nb.NJ_EINVAL  # N % 16
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 4, 30, 64, nb.NJ_GEMM_SWIGLU, 256, big, 0) == nb.NJ_EINVAL
+    assert L.nightjar_gemm(nb.NJ_BF16, 0, 16, 16, 4, 32, 64, nb.NJ_GEMM_STORE, 256, big, 0) == nb.NJ_EINVAL
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 0, 32, 64, nb.NJ_GEMM_STORE, 256, big, 0) == nb.NJ_EINVAL
+    assert L.nightjar_gemm(7, 16, 16, 16, 1, 32, 64, nb.NJ_GEMM_STORE, 256, big, 0) == nb.NJ_EINVAL
+    # a workspace smaller than the split-K scratch is refused before any launch
+    need = nb.gemm_workspace_bytes(nb.NJ_BF16, 48, 4096, 14336, nb.NJ_GEMM_RESIDUAL)
+    assert need > 256
+    assert L.nightjar_gemm(nb.NJ_BF16, 16, 16, 16, 48, 4096, 14336, nb.NJ_GEMM_RESIDUAL, 256, need - 256, 0) == nb.NJ_EINVAL
+    assert "workspace" in nb.last_error()
 
 
 def test_kv_append_requires_a_preceding_verify_step():

@@ -25,22 +25,31 @@ def _stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+def _gemm(dtype, x, w, y, M, N, K, epi):
+    """Run the library GEMM with a freshly prepared workspace."""
+    nbytes = nb.gemm_workspace_bytes(dtype, M, N, K, epi)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(ws.data_ptr(), nbytes, _stream())
+    nb.gemm(dtype, x.data_ptr(), w.data_ptr(), y.data_ptr(), M, N, K, epi, ws.data_ptr(), nbytes, _stream())
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("M,N,K", [(1, 16, 32), (5, 48, 96), (16, 4096, 4096), (17, 272, 4096), (48, 6144, 4096),
-                                   (64, 1040, 512), (100, 512, 1024), (3, 4096, 14336), (48, 128256, 4096)])
+                                   (64, 1040, 512), (100, 512, 1024), (3, 4096, 14336), (48, 128256, 4096),
+                                   (2, 4096, 4096), (33, 1024, 800), (130, 6144, 4096), (48, 4096, 14336)])
 def test_gemm_bf16_store(M, N, K):
     rng = np.random.default_rng(M * 7 + N + K)
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     y = torch.empty((M, N), dtype=torch.float32, device="cuda")
     dx, dw = _dev(x), _dev(w)  # keep the device copies alive across the call
-    nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_STORE, _stream())
-    torch.cuda.synchronize()
+    _gemm(nb.NJ_BF16, dx, dw, y, M, N, K, nb.NJ_GEMM_STORE)
     ref = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     err = np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max()
     assert err < 2e-5, err
 
 
-@pytest.mark.parametrize("M,N,K", [(7, 64, 128), (48, 4096, 14336), (33, 2048, 4096)])
+@pytest.mark.parametrize("M,N,K", [(7, 64, 128), (48, 4096, 14336), (33, 2048, 4096), (1, 4096, 4096), (80, 4096, 14336)])
 def test_gemm_bf16_residual(M, N, K):
     rng = np.random.default_rng(11 + M)
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
@@ -48,21 +57,19 @@ def test_gemm_bf16_residual(M, N, K):
     h0 = rng.standard_normal((M, N), dtype=np.float32)
     y = _dev(h0.copy())
     dx, dw = _dev(x), _dev(w)
-    nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_RESIDUAL, _stream())
-    torch.cuda.synchronize()
+    _gemm(nb.NJ_BF16, dx, dw, y, M, N, K, nb.NJ_GEMM_RESIDUAL)
     ref = h0 + oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     assert np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max() < 2e-5
 
 
-@pytest.mark.parametrize("M,F,K", [(6, 64, 256), (48, 14336, 4096), (20, 688, 256)])
+@pytest.mark.parametrize("M,F,K", [(6, 64, 256), (48, 14336, 4096), (20, 688, 256), (1, 14336, 4096), (70, 1024, 512)])
 def test_gemm_bf16_swiglu(M, F, K):
     rng = np.random.default_rng(5 + M)
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((2 * F, K), dtype=np.float32) * 0.05)
     y = torch.empty((M, F), dtype=torch.int16, device="cuda")
     dx, dw = _dev(x), _dev(w)
-    nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, 2 * F, K, nb.NJ_GEMM_SWIGLU, _stream())
-    torch.cuda.synchronize()
+    _gemm(nb.NJ_BF16, dx, dw, y, M, 2 * F, K, nb.NJ_GEMM_SWIGLU)
     gu = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     ref = oracle.silu(gu[:, :F]) * gu[:, F:]
     got = oracle.widen(y.cpu().numpy().view(np.uint16), "bf16")
@@ -80,8 +87,7 @@ def test_gemm_f32(M, N, K, epi):
     y0 = rng.standard_normal((M, Nout), dtype=np.float32)
     y = _dev(y0.copy())
     dx, dw = _dev(x), _dev(w)
-    nb.gemm(nb.NJ_F32, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, epi, _stream())
-    torch.cuda.synchronize()
+    _gemm(nb.NJ_F32, dx, dw, y, M, N, K, epi)
     acc = x.astype(np.float64) @ w.astype(np.float64).T
     if epi == nb.NJ_GEMM_STORE:
         ref = acc
@@ -114,8 +120,9 @@ def _run_accept(V, logits, drafts, q, u):
     k = T - 1
     shape = dataclasses.replace(W.TINY_F32, vocab=V)
     desc = model_desc(shape)
-    nbytes = 256 + ((B * T * ((V + 8191) // 8192) * 8 + 255) // 256) * 256
-    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    nbytes = nb.accept_workspace_bytes(V, B, k)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(ws.data_ptr(), nbytes, _stream())
     acc = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     nxt = torch.full((B, T), -7, dtype=torch.int32, device="cuda")
     dl = _dev(logits)
@@ -164,3 +171,26 @@ def test_accept_edge_uniforms():
     acc, nxt = _run_accept(V, logits, drafts, q, u)
     assert acc[0] == 0 and nxt[0, 0] != 5 and nxt[0, 0] == V - 1  # residual p - q > 0 everywhere but token 5
     assert acc[1] == 2 and nxt[1, 2] == 0  # bonus draw with u = 0 takes the first positive weight
+
+
+def test_gemm_split_k_is_deterministic_and_reusable():
+    """Split-K partials are summed in chunk order by whichever workgroup arrives
+    last, and the arrival counters are left at zero: repeated calls on one
+    workspace give bitwise-identical results."""
+    M, N, K = 48, 4096, 14336
+    rng = np.random.default_rng(99)
+    dx = _dev(W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32)))
+    dw = _dev(W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02))
+    nbytes = nb.gemm_workspace_bytes(nb.NJ_BF16, M, N, K, nb.NJ_GEMM_STORE)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(ws.data_ptr(), nbytes, _stream())
+    outs = []
+    for _ in range(4):
+        y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        nb.gemm(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_STORE, ws.data_ptr(),
+                nbytes, _stream())
+        outs.append(y)
+    torch.cuda.synchronize()
+    for y in outs[1:]:
+        assert torch.equal(y, outs[0])
+    assert not torch.isnan(outs[0]).any()
