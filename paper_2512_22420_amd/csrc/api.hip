@@ -94,19 +94,17 @@ Layout layout(const nj_model_desc& d, int B, int k) {
     return o;
   };
   L.err = take(kAlign);
-  // split-K arrival counters of the step's GEMMs: one region at a fixed place,
-  // zeroed by nightjar_workspace_init and left at zero by every GEMM
-  size_t cnt = 0, part = 0;
+  // Split-K arrival counters of the step's GEMMs: a fixed-size region at a
+  // fixed offset, whatever B and k, so that steps of different sizes on one
+  // workspace never write activations over them.  Zeroed by
+  // nightjar_workspace_init and left at zero by every GEMM.
+  L.gemm_cnt = take(kGemmCounterBytes);
+  size_t part = 0;
   if (d.dtype == NJ_BF16) {
     GemmShape gs[5];
     step_gemms(d, gs);
-    for (const GemmShape& g : gs) {
-      const GemmPlan p = gemm_plan((int)M, g.N, g.K, g.epi);
-      cnt = std::max(cnt, p.counter_bytes);
-      part = std::max(part, p.part_bytes);
-    }
+    for (const GemmShape& g : gs) part = std::max(part, gemm_plan((int)M, g.N, g.K, g.epi).part_bytes);
   }
-  L.gemm_cnt = take(cnt);
   L.h = take(M * d.d_model * 4);
   L.x = take(M * d.d_model * e);
   L.qkv = take(M * qkv * 4);

@@ -98,65 +98,59 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
   norm_row<T>(hv, gain, x + (size_t)blockIdx.x * d, d, eps, sh);
 }
 
-// One workgroup per window row.  Pair (j, j + D/2) of every q and k head turns
-// by pos * theta^(-2j/D); the D/2 angles of the row and their sin/cos are
-// evaluated once, in fp64 (positions reach several thousand radians), and
-// shared through LDS by all heads.  k goes to win_k[b][g][i][:], v to
-// win_v[b][g][:][i]; the row i == 0 workgroup also zeroes the unused slots
-// T..15 of the window block so that masked lanes never see stale data.
-constexpr int kMaxHalfDim = 256;
-
+// RoPE and the window K/V store.  One thread per rotation pair (j, j + D/2) of
+// one head of one window row; workgroups cover (row, group of heads), so no
+// thread walks a loop of dependent loads.  The pair turns by
+// pos * theta^(-2j/D): theta^(-2j/D) comes from the host in fp64, the angle is
+// formed and reduced to [-pi, pi] in fp64 (positions reach thousands of
+// radians), then an fp32 sin/cos of the small argument.  q goes to
+// q_out[row][h][:], k to win_k[b][g][i][:], v to win_v[b][g][:][i]; workgroups of
+// row i == 0 also zero the unused slots T..15 of the window blocks so that
+// masked lanes never read stale data.
 template <typename T>
-__global__ __launch_bounds__(128) void rope_window_kernel(const float* __restrict__ qkv,
+__global__ __launch_bounds__(256) void rope_window_kernel(const float* __restrict__ qkv,
                                                           const int32_t* __restrict__ ctx, int T_, int H,
-                                                          int Hkv, int D, float theta, T* __restrict__ q_out,
+                                                          int Hkv, int D, RopeFreq f, T* __restrict__ q_out,
                                                           T* __restrict__ win_k, T* __restrict__ win_v) {
-  __shared__ float s_cos[kMaxHalfDim], s_sin[kMaxHalfDim];
-  const int row = blockIdx.x, b = row / T_, i = row % T_;
   const int half = D / 2;
-  const double pos = (double)(max(ctx[b], 0) + i);
-  const double ltheta = log((double)theta);
-  for (int j = threadIdx.x; j < half; j += blockDim.x) {
-    // angle in fp64, reduced to [-pi, pi] in fp64 (2*pi split in two parts),
-    // then an fp32 sin/cos of the small argument
-    const double ang = pos * exp(-(2.0 * j / D) * ltheta);
+  const int hpb = blockDim.x / half;  // heads per workgroup
+  const int row = blockIdx.x, b = row / T_, i = row % T_;
+  const int hd = blockIdx.y * hpb + threadIdx.x / half, j = threadIdx.x % half;
+  if (hd >= H + 2 * Hkv) return;
+  const float* src = qkv + (size_t)row * (H + 2 * Hkv) * D + (size_t)hd * D;
+  if (hd < H + Hkv) {
+    const double ang = (double)(max(ctx[b], 0) + i) * f.inv_freq[j];
     const double kq = rint(ang * 0.15915494309189535);
     const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
     float sn, cs;
     sincosf((float)red, &sn, &cs);
-    s_cos[j] = cs;
-    s_sin[j] = sn;
-  }
-  __syncthreads();
-  const float* src = qkv + (size_t)row * (H + 2 * Hkv) * D;
-  for (int idx = threadIdx.x; idx < (H + Hkv) * half; idx += blockDim.x) {
-    const int hd = idx / half, j = idx % half;
-    const float c = s_cos[j], sn = s_sin[j];
-    const float a = src[hd * D + j], bb = src[hd * D + j + half];
-    const float ra = a * c - bb * sn, rb = bb * c + a * sn;
+    const float a = src[j], bb = src[j + half];
+    const float ra = a * cs - bb * sn, rb = bb * cs + a * sn;
+    T* dst;
     if (hd < H) {
-      T* qo = q_out + ((size_t)row * H + hd) * D;
-      qo[j] = from_f<T>(ra);
-      qo[j + half] = from_f<T>(rb);
+      dst = q_out + ((size_t)row * H + hd) * D;
     } else {
       const int g = hd - H;
-      T* ko = win_k + (((size_t)b * Hkv + g) * kBlock + i) * D;
-      ko[j] = from_f<T>(ra);
-      ko[j + half] = from_f<T>(rb);
+      dst = win_k + (((size_t)b * Hkv + g) * kBlock + i) * D;
+      if (i == 0)
+        for (int slot = T_; slot < kBlock; ++slot) {
+          T* z = win_k + (((size_t)b * Hkv + g) * kBlock + slot) * D;
+          z[j] = from_f<T>(0.f);
+          z[j + half] = from_f<T>(0.f);
+        }
     }
-  }
-  const float* vs = src + (H + Hkv) * D;
-  for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
-    const int g = idx / D, dd = idx % D;
-    win_v[(((size_t)b * Hkv + g) * D + dd) * kBlock + i] = from_f<T>(vs[idx]);
-  }
-  if (i == 0) {
-    for (int idx = threadIdx.x; idx < Hkv * D * (kBlock - T_); idx += blockDim.x) {
-      const int g = idx / (D * (kBlock - T_)), rem = idx % (D * (kBlock - T_));
-      const int slot = T_ + rem / D, dd = rem % D;
-      win_k[(((size_t)b * Hkv + g) * kBlock + slot) * D + dd] = from_f<T>(0.f);
-      win_v[(((size_t)b * Hkv + g) * D + dd) * kBlock + slot] = from_f<T>(0.f);
-    }
+    dst[j] = from_f<T>(ra);
+    dst[j + half] = from_f<T>(rb);
+  } else {
+    const int g = hd - H - Hkv;
+    T* vb = win_v + ((size_t)b * Hkv + g) * D * kBlock;
+    vb[(size_t)j * kBlock + i] = from_f<T>(src[j]);
+    vb[(size_t)(j + half) * kBlock + i] = from_f<T>(src[j + half]);
+    if (i == 0)
+      for (int slot = T_; slot < kBlock; ++slot) {
+        vb[(size_t)j * kBlock + slot] = from_f<T>(0.f);
+        vb[(size_t)(j + half) * kBlock + slot] = from_f<T>(0.f);
+      }
   }
 }
 
@@ -166,50 +160,52 @@ struct PagePtrs {
   void* v[kMaxAppendLayers];
 };
 
-// One workgroup per sequence: copy window rows 0..n_b of layers [layer0,
-// layer0 + nl) into their slots; the launch holding the last layer then
-// advances context_lens[b] (all readers of it are in this workgroup).
+// grid (B, layers of this launch): copy window rows 0..n_b of one layer into
+// their slots, one element per thread step.
 template <typename T>
-__global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int layer0, int nl, bool last_chunk,
-                                                        const T* __restrict__ win_k, const T* __restrict__ win_v,
+__global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int layer0, const T* __restrict__ win_k,
+                                                        const T* __restrict__ win_v,
                                                         const int32_t* __restrict__ table, int max_blocks,
-                                                        int num_blocks, int32_t* __restrict__ ctx,
+                                                        int num_blocks, const int32_t* __restrict__ ctx,
                                                         const int32_t* __restrict__ acc, int B, int k, int Hkv,
                                                         int D, int* __restrict__ err) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x, lc = blockIdx.y, l = layer0 + lc;
   const int n = acc[b], c = ctx[b];
   if (n < 0 || n > k) {
-    if (threadIdx.x == 0) flag_error(err, kErrAccept);
+    if (threadIdx.x == 0 && lc == 0) flag_error(err, kErrAccept);
     return;
   }
   if (c < 0 || c + k + 1 > max_blocks * kBlock) {
-    if (threadIdx.x == 0) flag_error(err, kErrContext);
+    if (threadIdx.x == 0 && lc == 0) flag_error(err, kErrContext);
     return;
   }
-  for (int lc = 0; lc < nl; ++lc) {
-    const int l = layer0 + lc;
-    T* kp = static_cast<T*>(pages.k[lc]);
-    T* vp = static_cast<T*>(pages.v[lc]);
-    const size_t wbase = ((size_t)l * B + b) * Hkv;
-    for (int j = 0; j <= n; ++j) {
-      const int pos = c + j;
-      const int phys = table[(size_t)b * max_blocks + pos / kBlock];
-      if (phys < 0 || phys >= num_blocks) {
-        if (threadIdx.x == 0) flag_error(err, kErrBlock);
-        continue;
-      }
-      const int slot = pos % kBlock;
-      for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
-        const int g = idx / D, dd = idx % D;
-        kp[(((size_t)phys * Hkv + g) * kBlock + slot) * D + dd] = win_k[((wbase + g) * kBlock + j) * D + dd];
-        vp[(((size_t)phys * Hkv + g) * D + dd) * kBlock + slot] = win_v[((wbase + g) * D + dd) * kBlock + j];
-      }
+  T* kp = static_cast<T*>(pages.k[lc]);
+  T* vp = static_cast<T*>(pages.v[lc]);
+  const size_t wbase = ((size_t)l * B + b) * Hkv;
+  const int per_row = Hkv * D, total = (n + 1) * per_row;
+#pragma unroll 4
+  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
+    const int j = idx / per_row, rem = idx % per_row, g = rem / D, dd = rem % D;
+    const int pos = c + j;
+    const int phys = table[(size_t)b * max_blocks + pos / kBlock];
+    if (phys < 0 || phys >= num_blocks) {
+      flag_error(err, kErrBlock);
+      continue;
     }
+    const int slot = pos % kBlock;
+    kp[(((size_t)phys * Hkv + g) * kBlock + slot) * D + dd] = win_k[((wbase + g) * kBlock + j) * D + dd];
+    vp[(((size_t)phys * Hkv + g) * D + dd) * kBlock + slot] = win_v[((wbase + g) * D + dd) * kBlock + j];
   }
-  if (last_chunk) {
-    __syncthreads();  // every thread has read ctx[b]
-    if (threadIdx.x == 0) ctx[b] = c + n + 1;
-  }
+}
+
+// context_lens[b] += n_b + 1, after every layer's append (a separate launch).
+__global__ void ctx_update_kernel(int32_t* __restrict__ ctx, const int32_t* __restrict__ acc, int B, int k,
+                                  int max_blocks) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int n = acc[b], c = ctx[b];
+  if (n < 0 || n > k || c < 0 || c + k + 1 > max_blocks * kBlock) return;
+  ctx[b] = c + n + 1;
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
@@ -246,11 +242,16 @@ hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, 
 
 hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv, int D,
                               float theta, void* q_out, void* win_k, void* win_v, hipStream_t s) {
+  RopeFreq f{};
+  const int half = D / 2;
+  for (int j = 0; j < half && j < kMaxHalfDim; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / D);
+  const int hpb = half >= 256 ? 1 : 256 / half;
+  dim3 grid(B * T, (H + 2 * Hkv + hpb - 1) / hpb), block(hpb * half);
   if (dtype == kF32)
-    hipLaunchKernelGGL(rope_window_kernel<float>, dim3(B * T), dim3(128), 0, s, qkv, ctx, T, H, Hkv, D, theta,
+    hipLaunchKernelGGL(rope_window_kernel<float>, grid, block, 0, s, qkv, ctx, T, H, Hkv, D, f,
                        static_cast<float*>(q_out), static_cast<float*>(win_k), static_cast<float*>(win_v));
   else
-    hipLaunchKernelGGL(rope_window_kernel<bf16_t>, dim3(B * T), dim3(128), 0, s, qkv, ctx, T, H, Hkv, D, theta,
+    hipLaunchKernelGGL(rope_window_kernel<bf16_t>, grid, block, 0, s, qkv, ctx, T, H, Hkv, D, f,
                        static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(win_k), static_cast<bf16_t*>(win_v));
   return hipGetLastError();
 }
@@ -258,24 +259,25 @@ hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, i
 hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s) {
   for (int l0 = 0; l0 < a.L; l0 += kMaxAppendLayers) {
     const int nl = (a.L - l0 < kMaxAppendLayers) ? a.L - l0 : kMaxAppendLayers;
-    const bool last = l0 + nl >= a.L;
     PagePtrs p{};
     for (int i = 0; i < nl; ++i) {
       p.k[i] = a.k_pages[l0 + i];
       p.v[i] = a.v_pages[l0 + i];
     }
     if (a.dtype == kF32)
-      hipLaunchKernelGGL(kv_append_kernel<float>, dim3(a.B), dim3(256), 0, s, p, l0, nl, last,
+      hipLaunchKernelGGL(kv_append_kernel<float>, dim3(a.B, nl), dim3(256), 0, s, p, l0,
                          static_cast<const float*>(a.win_k), static_cast<const float*>(a.win_v), a.block_table,
                          a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
     else
-      hipLaunchKernelGGL(kv_append_kernel<bf16_t>, dim3(a.B), dim3(256), 0, s, p, l0, nl, last,
+      hipLaunchKernelGGL(kv_append_kernel<bf16_t>, dim3(a.B, nl), dim3(256), 0, s, p, l0,
                          static_cast<const bf16_t*>(a.win_k), static_cast<const bf16_t*>(a.win_v), a.block_table,
                          a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  return hipSuccess;
+  hipLaunchKernelGGL(ctx_update_kernel, dim3((a.B + 255) / 256), dim3(256), 0, s, a.ctx, a.accepted_len, a.B, a.k,
+                     a.max_blocks);
+  return hipGetLastError();
 }
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s) {

@@ -34,7 +34,7 @@ namespace {
 constexpr int kU = 8;                     // 32-wide k-steps per stage
 constexpr int kStageK = 32 * kU;          // 256
 constexpr int kRowStride = kStageK + 8;   // LDS row stride in elements (+16 bytes)
-constexpr int kTargetWorkgroups = 512;
+constexpr int kSplitTargetWorkgroups = 256;
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -53,7 +53,11 @@ struct GemmK {
 
 // MT: 16-row x tiles per workgroup; NG: weight row groups (2 for SwiGLU);
 // NW: waves per workgroup (each owns 16 weight rows of every group).
-template <int MT, int NG, int NW, int EPI>
+// FULL: K % 256 == 0 and every wave owns 16 real weight rows, so the stage loop
+// needs no guards at all; the prefetch of the stage after the last one simply
+// re-reads the last one (an L1/L2 hit).  Branches inside the loop would make
+// the compiler drain all outstanding loads at every join.
+template <int MT, int NG, int NW, int EPI, int DEPTH, bool FULL>
 __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
   constexpr int ROWS = MT * 16, NTH = NW * 64;
   constexpr int CHUNKS = ROWS * kStageK / 8;  // 16-byte pieces of one x stage
@@ -84,7 +88,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
     for (int q = 0; q < NG; ++q) acc[mt][q] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   u32x4 xr[PER_T];
-  bf16x8 wbuf[2][NG][kU];
+  bf16x8 wbuf[DEPTH + 1][NG][kU];
 
 #define NJ_GLOAD_X(st)                                                                           \
   _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
@@ -124,15 +128,14 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
       }                                                                                          \
     }                                                                                            \
   }
-  // one stage: stage st+1's x (global -> registers) and w loads go out, stage
-  // st is multiplied, stage st+1's x goes to the other LDS buffer
+  // One stage: stage st+1's x (global -> registers) and the w loads of stage
+  // st+DEPTH go out, stage st is multiplied, stage st+1's x goes to the other
+  // LDS buffer.  w stage s lives in register buffer s % (DEPTH + 1).
 #define NJ_STAGE(B, BN)                                       \
   {                                                           \
     const bool more = st + 1 < st1;                           \
-    if (more) {                                               \
-      NJ_GLOAD_X(st + 1);                                     \
-      NJ_LOAD_W(BN, st + 1);                                  \
-    }                                                         \
+    if (more) NJ_GLOAD_X(st + 1);                             \
+    if (st + DEPTH < st1) NJ_LOAD_W(BN, st + DEPTH);          \
     NJ_COMPUTE(B, (st - st0) & 1, st);                        \
     if (more) NJ_SSTORE_X((st + 1 - st0) & 1);                \
     __syncthreads();                                          \
@@ -140,15 +143,76 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
     if (st >= st1) break;                                     \
   }
 
-  if (st0 < st1) {
+  if constexpr (FULL) {
+    // branch-free stage loop (ping-pong over two w register buffers and two x LDS buffers)
+#define NJ_FGLOAD_X(st)                                                                          \
+  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
+    const int idx = threadIdx.x + c * NTH;                                                       \
+    const int row = idx / (kStageK / 8), kk = (st) * kStageK + (idx % (kStageK / 8)) * 8;        \
+    xr[c] = *reinterpret_cast<const u32x4*>(a.X + (size_t)min(m0 + row, M - 1) * K + kk);        \
+  }
+#define NJ_FSSTORE_X(buf)                                                                        \
+  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
+    const int idx = threadIdx.x + c * NTH;                                                       \
+    const int row = idx / (kStageK / 8), col = (idx % (kStageK / 8)) * 8;                        \
+    *reinterpret_cast<u32x4*>(&xs[buf][row * kRowStride + col]) = xr[c];                         \
+  }
+#define NJ_FLOAD_W(B, st)                                                                        \
+  _Pragma("unroll") for (int u = 0; u < kU; ++u)                                                 \
+    _Pragma("unroll") for (int q = 0; q < NG; ++q) wbuf[B][q][u] = ld8(wp[q] + ((st) * kU + u) * 32);
+#define NJ_FCOMPUTE(B, buf)                                                                      \
+  _Pragma("unroll") for (int u = 0; u < kU; ++u) {                                               \
+    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                          \
+      const bf16x8 xv = __builtin_bit_cast(                                                      \
+          bf16x8, *reinterpret_cast<const u32x4*>(&xs[buf][(mt * 16 + r) * kRowStride + u * 32 + g * 8])); \
+      _Pragma("unroll") for (int q = 0; q < NG; ++q) acc[mt][q] =                                \
+          __builtin_amdgcn_mfma_f32_16x16x32_bf16(wbuf[B][q][u], xv, acc[mt][q], 0, 0, 0);       \
+    }                                                                                            \
+  }
+    static_assert(CHUNKS % NTH == 0, "x stage must split evenly over the workgroup");
+    NJ_FGLOAD_X(st0);
+    NJ_FLOAD_W(0, st0);
+    NJ_FSSTORE_X(0);
+    __syncthreads();
+    for (int st = st0; st < st1; st += 2) {
+      const int s1 = min(st + 1, st1 - 1);
+      NJ_FGLOAD_X(s1);
+      NJ_FLOAD_W(1, s1);
+      __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the multiplies
+      NJ_FCOMPUTE(0, 0);
+      NJ_FSSTORE_X(1);
+      __syncthreads();
+      if (st + 1 >= st1) break;
+      const int s2 = min(st + 2, st1 - 1);
+      NJ_FGLOAD_X(s2);
+      NJ_FLOAD_W(0, s2);
+      __builtin_amdgcn_sched_barrier(0);
+      NJ_FCOMPUTE(1, 1);
+      NJ_FSSTORE_X(0);
+      __syncthreads();
+    }
+#undef NJ_FGLOAD_X
+#undef NJ_FSSTORE_X
+#undef NJ_FLOAD_W
+#undef NJ_FCOMPUTE
+  } else if (st0 < st1) {
     NJ_GLOAD_X(st0);
     NJ_LOAD_W(0, st0);
+    if (DEPTH > 1 && st0 + 1 < st1) NJ_LOAD_W(1 % (DEPTH + 1), st0 + 1);
     NJ_SSTORE_X(0);
     __syncthreads();
     int st = st0;
-    for (;;) {
-      NJ_STAGE(0, 1)
-      NJ_STAGE(1, 0)
+    if constexpr (DEPTH == 1) {
+      for (;;) {
+        NJ_STAGE(0, 1)
+        NJ_STAGE(1, 0)
+      }
+    } else {
+      for (;;) {
+        NJ_STAGE(0, 2 % (DEPTH + 1))
+        NJ_STAGE(1, 3 % (DEPTH + 1))
+        NJ_STAGE(2 % (DEPTH + 1), 4 % (DEPTH + 1))
+      }
     }
   }
 #undef NJ_GLOAD_X
@@ -260,7 +324,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 template <int MT, int NG, int NW, int EPI>
 hipError_t launch_cfg(const GemmK& a, const GemmPlan& p, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI>), dim3(p.ntiles, p.mblocks, p.nkc), dim3(NW * 64), 0, s, a);
+  const dim3 grid(p.ntiles, p.mblocks, p.nkc), block(NW * 64);
+  const bool full = a.K % kStageK == 0 && (a.Nout / 16) % NW == 0 && a.Nout % 16 == 0;
+  if (full)
+    hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI, 1, true>), grid, block, 0, s, a);
+  else if (NG == 1 && p.depth == 2)
+    hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI, 2, false>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI, 1, false>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
@@ -293,18 +364,34 @@ GemmPlan gemm_plan(int M, int N, int K, int epi) {
   p.mt = M >= 64 ? 4 : (M + 15) / 16;
   p.mblocks = (M + p.mt * 16 - 1) / (p.mt * 16);
   const int tiles16 = (Nout + 15) / 16;
-  // 8 waves share each staged x tile when it is large; small N keeps 4 so
-  // that there are more workgroups before splitting K
-  p.nw = (p.mt >= 3 && tiles16 / 8 * p.mblocks >= 256) ? 8 : 4;
+  // 8 waves share each staged x tile when it is large and N is wide enough to
+  // keep 512+ workgroups; otherwise 4 waves (more workgroups)
+  p.nw = (p.mt >= 3 && tiles16 / 8 * p.mblocks >= 512) ? 8 : 4;
   p.ntiles = (tiles16 + p.nw - 1) / p.nw;
   const int nst = (K / 32 + kU - 1) / kU;
+  const long base = (long)p.ntiles * p.mblocks;
+  // Split K until ~256 workgroups run (one per CU), keeping >= 4 stages per
+  // chunk so that the x staging and the partial hand-off are amortised (a
+  // measured sweep over the verify step's shapes puts the optimum there).
   int nkc = 1;
-  while ((long)p.ntiles * p.mblocks * nkc < kTargetWorkgroups && nst / (nkc * 2) >= 2) nkc *= 2;
+  while (base * nkc * 2 <= kSplitTargetWorkgroups && nst / (nkc * 2) >= 4) nkc *= 2;
   p.stages_per_chunk = (nst + nkc - 1) / nkc;
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
+  p.depth = 1;
   p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
   p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * 4) : 0;
+  static_assert(kSplitTargetWorkgroups / 2 * 4 <= kGemmCounterBytes, "counter region too small");
   return p;
+}
+
+hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
+                            int* counters, float* part, hipStream_t s) {
+  const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
+  GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.stages_per_chunk};
+  if (epi == kEpiStore) return launch_epi<1, kEpiStore>(a, p, s);
+  if (epi == kEpiResidual) return launch_epi<1, kEpiResidual>(a, p, s);
+  return launch_epi<2, kEpiSwiglu>(a, p, s);
 }
 
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
@@ -319,12 +406,7 @@ hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, 
     else hipLaunchKernelGGL(gemm_f32_kernel<kEpiSwiglu>, grid, dim3(256), 0, s, xf, wf, y, M, Nout, K);
     return hipGetLastError();
   }
-  const GemmPlan p = gemm_plan(M, N, K, epi);
-  GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.stages_per_chunk};
-  if (epi == kEpiStore) return launch_epi<1, kEpiStore>(a, p, s);
-  if (epi == kEpiResidual) return launch_epi<1, kEpiResidual>(a, p, s);
-  return launch_epi<2, kEpiSwiglu>(a, p, s);
+  return launch_gemm_plan(x, w, y, M, N, K, epi, gemm_plan(M, N, K, epi), counters, part, s);
 }
 
 }  // namespace nj

@@ -16,9 +16,13 @@ enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2 };
 // split-K partials and arrival counters take.
 struct GemmPlan {
   int mt, nw, ntiles, mblocks, nkc, stages_per_chunk;
+  int depth;  // weight stages in flight ahead of the one being multiplied (1 or 2)
   size_t part_bytes, counter_bytes;
 };
 GemmPlan gemm_plan(int M, int N, int K, int epi);
+// Split K only happens when ntiles * mblocks <= 256, so every GEMM's arrival
+// counters fit in this many bytes (a fixed region, whatever M, N, K).
+constexpr size_t kGemmCounterBytes = 4096;
 
 // y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]).  `counters`
 // (plan.counter_bytes, zero on entry and on exit) and `part`
@@ -26,6 +30,9 @@ GemmPlan gemm_plan(int M, int N, int K, int epi);
 // may share both as long as the counters are never overwritten by anything else.
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
                        int* counters, float* part, hipStream_t s);
+// bf16 GEMM with an explicit plan (nw 4 or 8, mt 1..4, any nkc/stages_per_chunk).
+hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
+                            int* counters, float* part, hipStream_t s);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
@@ -37,7 +44,11 @@ hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, 
                           hipStream_t s);
 
 // RoPE on q and k rows of qkv at positions ctx[b] + i; q -> q_out [M][H][D];
-// k, v -> one 16-slot window block per (b, kv head).
+// k, v -> one 16-slot window block per (b, kv head).  D <= 2 * kMaxHalfDim.
+constexpr int kMaxHalfDim = 256;
+struct RopeFreq {
+  double inv_freq[kMaxHalfDim];  // theta^(-2j/D)
+};
 hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv,
                               int D, float theta, void* q_out, void* win_k, void* win_v, hipStream_t s);
 

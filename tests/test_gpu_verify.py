@@ -237,3 +237,20 @@ def test_hip_graph_replay_matches_eager():
         assert torch.equal(io.accepted_len, eager[2]), rep
         verify(model, cache, io, ws)  # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_steps_of_different_sizes_share_one_workspace():
+    """A workspace sized for the largest step serves smaller and larger steps in
+    any order: results equal those on a fresh workspace, bitwise."""
+    shape = SMALL_BF16
+    weights = W.make_weights(shape, 11)
+    model = DeviceModel(shape, weights)
+    shared = Workspace(shape, 6, 7)
+    sizes = [(2, 1), (6, 7), (1, 0), (4, 3), (6, 7), (3, 5)]
+    for B, k in sizes:
+        x = _inputs(shape, np.arange(B, dtype=np.int32) * 37 + 5, k, seed=B * 10 + k, weights=weights)
+        _, _, io_s, _, err_s = _run(shape, x, model=model, ws=shared)
+        _, _, io_f, _, err_f = _run(shape, x, model=model)
+        assert err_s == 0 and err_f == 0
+        assert torch.equal(io_s.logits, io_f.logits), (B, k)
+        assert torch.equal(io_s.next_tokens, io_f.next_tokens), (B, k)
