@@ -234,6 +234,31 @@ size_t nightjar_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_
 int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
                   int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Kernel choices of nightjar_gemm_with_plan. */
+enum {
+  NJ_GEMM_AUTO = 0,         /* the kernel and split nightjar_gemm picks              */
+  NJ_GEMM_STREAM = 1,       /* weight-streaming kernel (windows up to ~128 rows)     */
+  NJ_GEMM_TILE_256x256 = 2, /* LDS-tiled kernel; output tile = x rows x weight rows  */
+  NJ_GEMM_TILE_128x256 = 3,
+  NJ_GEMM_TILE_128x128 = 4
+};
+
+/*
+ * nightjar_gemm with the kernel and the number of K chunks chosen by the
+ * caller, for parity tests of every kernel shape and for tuning.  split_k = 0
+ * lets the kernel's planner choose; split_k >= 1 is capped so that every chunk
+ * has work (256 k per chunk at least for NJ_GEMM_STREAM, 64 for the tiled
+ * kernels).  The tiled kernels need K % 64 == 0, and a split run may cover at
+ * most 1024 output tiles; otherwise NJ_EINVAL.  Operands, epilogues and errors
+ * as in nightjar_gemm; the workspace must hold
+ * nightjar_gemm_plan_workspace_bytes(...) bytes (0 = invalid arguments).
+ */
+size_t nightjar_gemm_plan_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue,
+                                          int32_t kernel, int32_t split_k);
+int nightjar_gemm_with_plan(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
+                            int32_t epilogue, int32_t kernel, int32_t split_k, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,6 +15,7 @@ NJ_F32, NJ_BF16 = 0, 1
 NJ_OK, NJ_EINVAL, NJ_EDEVICE, NJ_EHIP = 0, -1, -2, -3
 NJ_DEV_BAD_TOKEN, NJ_DEV_BAD_BLOCK, NJ_DEV_BAD_CONTEXT, NJ_DEV_BAD_ACCEPT = 1, 2, 4, 8
 NJ_GEMM_STORE, NJ_GEMM_RESIDUAL, NJ_GEMM_SWIGLU = 0, 1, 2
+NJ_GEMM_AUTO, NJ_GEMM_STREAM, NJ_GEMM_TILE_256x256, NJ_GEMM_TILE_128x256, NJ_GEMM_TILE_128x128 = 0, 1, 2, 3, 4
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -62,6 +63,9 @@ _SIGS = {
                                        _sz, _vp]),
     "nightjar_gemm": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
     "nightjar_gemm_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "nightjar_gemm_with_plan": (ctypes.c_int, [_i32, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _sz,
+                                               _vp]),
+    "nightjar_gemm_plan_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32, _i32]),
     "nightjar_accept_workspace_bytes": (_sz, [_i32, _i32, _i32]),
 }
 
@@ -142,6 +146,19 @@ def gemm_workspace_bytes(dtype, M, N, K, epilogue) -> int:
 
 def gemm(dtype, x, w, y, M, N, K, epilogue, workspace, workspace_nbytes, stream: int = 0) -> None:
     _check(lib().nightjar_gemm(dtype, x, w, y, M, N, K, epilogue, workspace, workspace_nbytes, stream))
+
+
+def gemm_plan_workspace_bytes(dtype, M, N, K, epilogue, kernel, split_k) -> int:
+    n = lib().nightjar_gemm_plan_workspace_bytes(dtype, M, N, K, epilogue, kernel, split_k)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace, workspace_nbytes,
+                   stream: int = 0) -> None:
+    _check(lib().nightjar_gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace,
+                                         workspace_nbytes, stream))
 
 
 def header_functions(header_path: str):

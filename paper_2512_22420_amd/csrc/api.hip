@@ -351,4 +351,64 @@ int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t 
   return e == hipSuccess ? NJ_OK : hip_fail(e, "gemm");
 }
 
+static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue, int32_t kernel, int32_t split,
+                     GemmPlan* out) {
+  if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
+  if (split < 0) return fail(NJ_EINVAL, "split_k must be >= 0");
+  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_TILE_128x128) return fail(NJ_EINVAL, "bad kernel choice");
+  if (dtype != NJ_BF16) {
+    if (kernel != NJ_GEMM_AUTO || split) return fail(NJ_EINVAL, "the fp32 GEMM has a single kernel and no split");
+    *out = GemmPlan{};
+    return NJ_OK;
+  }
+  if (kernel == NJ_GEMM_AUTO) {
+    if (split) return fail(NJ_EINVAL, "split_k needs an explicit kernel");
+    *out = gemm_plan(M, N, K, epilogue);
+    return NJ_OK;
+  }
+  GemmPlan p;
+  if (kernel == NJ_GEMM_STREAM) {
+    p = gemm_stream_plan(M, N, K, epilogue, split);
+  } else {
+    if (!tile_fits(M, N, K)) return fail(NJ_EINVAL, "the tiled kernels need K %% 64 == 0 and M*K, N*K < 2^31");
+    const int tile = kernel == NJ_GEMM_TILE_256x256 ? kTile256x256
+                     : kernel == NJ_GEMM_TILE_128x256 ? kTile128x256 : kTile128x128;
+    p = split ? gemm_tile_plan(M, N, K, epilogue, tile, std::min(split, K / 64))
+              : gemm_tile_choose(M, N, K, epilogue, tile);
+  }
+  if (p.nkc > 1 && p.counter_bytes > kGemmCounterBytes)
+    return fail(NJ_EINVAL, "a split-K run may cover at most %zu output tiles", kGemmCounterBytes / 4);
+  if (p.part_bytes >= kMaxPartBytes) return fail(NJ_EINVAL, "split-K partials would take 2 GiB or more");
+  *out = p;
+  return NJ_OK;
+}
+
+size_t nightjar_gemm_plan_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue,
+                                          int32_t kernel, int32_t split_k) {
+  GemmPlan p;
+  if (plan_with(dtype, M, N, K, epilogue, kernel, split_k, &p) != NJ_OK) return 0;
+  return dtype == NJ_BF16 ? kAlign + p.counter_bytes + p.part_bytes : kAlign;
+}
+
+int nightjar_gemm_with_plan(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
+                            int32_t epilogue, int32_t kernel, int32_t split_k, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  GemmPlan p;
+  if (plan_with(dtype, M, N, K, epilogue, kernel, split_k, &p) != NJ_OK) return NJ_EINVAL;
+  if (!x || !w || !y) return fail(NJ_EINVAL, "NULL operand");
+  if (dtype == NJ_BF16 && (!aligned16(x) || !aligned16(w) || !aligned16(y)))
+    return fail(NJ_EINVAL, "operands must be 16-byte aligned");
+  const size_t need = dtype == NJ_BF16 ? kAlign + p.counter_bytes + p.part_bytes : kAlign;
+  if (!workspace || workspace_bytes < need) return fail(NJ_EINVAL, "workspace NULL or smaller than %zu bytes", need);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+  char* ws = static_cast<char*>(workspace) + kAlign;  // [counters][partials]
+  hipError_t e;
+  if (dtype == NJ_BF16)
+    e = launch_gemm_plan(x, w, y, M, N, K, epilogue, p, reinterpret_cast<int*>(ws),
+                         reinterpret_cast<float*>(ws + p.counter_bytes), (hipStream_t)stream);
+  else
+    e = launch_gemm(kF32, x, w, y, M, N, K, epilogue, nullptr, nullptr, (hipStream_t)stream);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "gemm");
+}
+
 }  // extern "C"

@@ -14,6 +14,21 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+// Split-K partials are exchanged between workgroups that may sit on different
+// XCDs (separate L2s).  They are written and read as 16-byte buffer accesses
+// with the device-coherence cache policy (sc1, the policy of agent-scope
+// atomics), so no L2 writeback or invalidate is needed for the hand-off.
+// Accesses past num_bytes are dropped (stores) or read as zero (loads).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(void* base, int num_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, num_bytes, 0x00020000);
+}
+__device__ __forceinline__ void coherent_store(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, 16 /* sc1 */);
+}
+__device__ __forceinline__ f32x4 coherent_load(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 16 /* sc1 */));
+}
+
 constexpr int kWave = 64;
 constexpr int kBlock = 16;  // tokens per KV block
 

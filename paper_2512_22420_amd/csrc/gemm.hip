@@ -25,6 +25,9 @@
 // column (l & 15) of B, eight consecutive k of k-group (l >> 4); the result
 // lane l holds rows 4*(l >> 4) + i, column l & 15.  Any k permutation applied
 // to both operands leaves the product unchanged.
+#include <algorithm>
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -35,6 +38,8 @@ constexpr int kU = 8;                     // 32-wide k-steps per stage
 constexpr int kStageK = 32 * kU;          // 256
 constexpr int kRowStride = kStageK + 8;   // LDS row stride in elements (+16 bytes)
 constexpr int kSplitTargetWorkgroups = 256;
+// windows of at least this many rows may use the LDS-tiled kernel
+constexpr int kTileMinRows = 64;
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -49,6 +54,7 @@ struct GemmK {
   float* part;    // [nkc][M][NG][Nout] fp32 partials (split K only)
   int* counters;  // [mblocks][ntiles] arrival counters (split K only), zero between launches
   int M, Nout, K, stages_per_chunk;
+  int part_bytes;
 };
 
 // MT: 16-row x tiles per workgroup; NG: weight row groups (2 for SwiGLU);
@@ -224,22 +230,19 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
   const int n = n0 + 4 * g;
   if (nkc > 1) {
     // Split K: publish this chunk's partial, and the last chunk to arrive
-    // finishes the tile.  Partials are written and read with device-scope
-    // (L2 write-through / coherent) accesses, so the hand-off needs neither an
-    // L2 writeback nor an L2 invalidate: each thread waits until its partial
-    // stores are acknowledged, then one counter increment publishes them.
+    // finishes the tile.  Partials are written and read with device-coherent
+    // accesses, so the hand-off needs neither an L2 writeback nor an L2
+    // invalidate: each thread waits until its partial stores are acknowledged,
+    // then one counter increment publishes them.
+    const __amdgpu_buffer_rsrc_t prs = coherent_rsrc(a.part, a.part_bytes);
+    auto poff = [&](int j, int m, int q) { return (uint32_t)((((size_t)j * M + m) * NG + q) * Nout + n) * 4u; };
     if (active) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = m0 + mt * 16 + r;
         if (m < M)
 #pragma unroll
-          for (int q = 0; q < NG; ++q) {
-            float* dst = a.part + (((size_t)kc * M + m) * NG + q) * Nout + n;
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              __hip_atomic_store(dst + i, acc[mt][q][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
+          for (int q = 0; q < NG; ++q) coherent_store(prs, poff(kc, m, q), acc[mt][q]);
       }
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -251,23 +254,16 @@ __global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
     if (!s_last) return;
     if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
     if (!active) return;
+    // sum all nkc partials (this workgroup's own included, read back) in chunk order
+    for (int j = 0; j < nkc; ++j) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = m0 + mt * 16 + r;
-      if (m >= M) continue;
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = min(m0 + mt * 16 + r, M - 1);  // rows past M: read in range, dropped below
 #pragma unroll
-      for (int q = 0; q < NG; ++q) {
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int j = 0; j < nkc; ++j) {
-          if (j == kc) {
-            s += acc[mt][q];
-          } else {
-            const float* src = a.part + (((size_t)j * M + m) * NG + q) * Nout + n;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) s[i] += __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
+        for (int q = 0; q < NG; ++q) {
+          const f32x4 v = coherent_load(prs, poff(j, m, q));
+          acc[mt][q] = j == 0 ? v : acc[mt][q] + v;
         }
-        acc[mt][q] = s;
       }
     }
   } else if (!active) {
@@ -353,12 +349,84 @@ hipError_t launch_epi(const GemmK& a, const GemmPlan& p, hipStream_t s) {
   }
 }
 
-size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
-
 }  // namespace
 
-GemmPlan gemm_plan(int M, int N, int K, int epi) {
+static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc) {
   GemmPlan p{};
+  const int NG = epi == kEpiSwiglu ? 2 : 1;
+  const int Nout = N / NG;
+  p.tile = tile;
+  const int bm = tile_bm(tile), bno = tile_bn(tile) / NG;
+  p.mblocks = (M + bm - 1) / bm;
+  p.ntiles = (Nout + bno - 1) / bno;
+  const int nst = K / 64;
+  p.stages_per_chunk = (nst + nkc - 1) / nkc;
+  p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
+  p.depth = 1;
+  p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
+  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * 4) : 0;
+  return p;
+}
+
+namespace {
+// Cost models (seconds) used to pick the kernel for windows of 64+ rows,
+// with constants fitted to a sweep of the 8B- and 7B-shaped GEMMs at 64..2048
+// rows (the chosen plan is within 15% of the best measured one everywhere).
+// Tiled kernel: rounds of resident workgroups times one tile's MFMA time at
+// the tile shape's sustained fraction of peak, plus, when K is split, the
+// last arriver's reduction (one CU reads nkc partial tiles) and the partial
+// traffic.
+constexpr double kLaunch = 5e-6;
+double tile_cost(const GemmPlan& p, int M, int N, int K) {
+  const int bm = tile_bm(p.tile), bn = tile_bn(p.tile);
+  const double slots = p.tile == kTile128x128 ? 512.0 : 256.0;  // resident workgroups
+  const double eff = p.tile == kTile256x256 ? 0.5 : p.tile == kTile128x256 ? 0.38 : 0.25;
+  const double rounds = std::ceil((double)p.ntiles * p.mblocks * p.nkc / slots);
+  double t = rounds * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (2.5e15 / slots * eff);
+  if (p.nkc > 1) t += 2.0 * p.nkc * bm * bn * 4 / 1e11 + 2.0 * p.nkc * (double)M * N * 4 / 5e12;
+  return t + kLaunch;
+}
+// Weight-streaming kernel: one pass over the weights per 64-row block, later
+// passes partly served from the caches.
+double stream_cost(int M, int N, int K) {
+  const int mb = (M + 63) / 64;
+  return (double)N * K * 2 * (1.0 + 0.7 * (mb - 1)) / 4e12 + kLaunch;
+}
+}  // namespace
+
+GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile) {
+  GemmPlan best{};
+  double bc = 1e30;
+  for (int tile : {kTile256x256, kTile128x256, kTile128x128}) {
+    if (only_tile != kTileNone && tile != only_tile) continue;
+    for (int nkc = 1; nkc <= 8; nkc *= 2) {
+      if (nkc > 1 && K / 64 / nkc < 8) break;
+      const GemmPlan p = gemm_tile_plan(M, N, K, epi, tile, nkc);
+      if (p.nkc > 1 && (p.counter_bytes > kGemmCounterBytes || p.part_bytes >= kMaxPartBytes)) continue;
+      const double c = tile_cost(p, M, N, K);
+      if (c < bc) bc = c, best = p;
+    }
+  }
+  return best;
+}
+
+bool tile_fits(int M, int N, int K) {
+  return K % 64 == 0 && (long)M * K < (1L << 31) && (long)N * K < (1L << 31);
+}
+
+GemmPlan gemm_plan(int M, int N, int K, int epi) {
+  if (M >= kTileMinRows && tile_fits(M, N, K)) {
+    const GemmPlan t = gemm_tile_choose(M, N, K, epi, kTileNone);
+    if (tile_cost(t, M, N, K) < stream_cost(M, N, K)) return t;
+  }
+  return gemm_stream_plan(M, N, K, epi, 0);
+}
+
+GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split) {
+  GemmPlan p{};
+  p.tile = kTileNone;
   const int NG = epi == kEpiSwiglu ? 2 : 1;
   const int Nout = N / NG;
   p.mt = M >= 64 ? 4 : (M + 15) / 16;
@@ -374,7 +442,10 @@ GemmPlan gemm_plan(int M, int N, int K, int epi) {
   // chunk so that the x staging and the partial hand-off are amortised (a
   // measured sweep over the verify step's shapes puts the optimum there).
   int nkc = 1;
-  while (base * nkc * 2 <= kSplitTargetWorkgroups && nst / (nkc * 2) >= 4) nkc *= 2;
+  if (split > 0) nkc = std::min(split, nst);
+  else
+    while (base * nkc * 2 <= kSplitTargetWorkgroups && nst / (nkc * 2) >= 4) nkc *= 2;
+  if (split <= 0 && (size_t)nkc * M * N * 4 >= kMaxPartBytes) nkc = 1;
   p.stages_per_chunk = (nst + nkc - 1) / nkc;
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
   p.depth = 1;
@@ -386,9 +457,10 @@ GemmPlan gemm_plan(int M, int N, int K, int epi) {
 
 hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s) {
+  if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s);
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.stages_per_chunk};
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.stages_per_chunk, (int)p.part_bytes};
   if (epi == kEpiStore) return launch_epi<1, kEpiStore>(a, p, s);
   if (epi == kEpiResidual) return launch_epi<1, kEpiResidual>(a, p, s);
   return launch_epi<2, kEpiSwiglu>(a, p, s);

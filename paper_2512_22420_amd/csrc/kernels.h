@@ -10,19 +10,39 @@ namespace nj {
 enum { kF32 = 0, kBF16 = 1 };
 enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2 };
 
-// How the bf16 GEMM splits its work: 16-row x tiles per workgroup (mt),
-// waves per workgroup (nw), workgroups along N (ntiles) and M (mblocks), K
-// chunks across workgroups (nkc, stages_per_chunk), and the workspace the
-// split-K partials and arrival counters take.
+// Output tiles of the LDS-tiled kernel for large windows: x rows x weight rows.
+enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
+
+// How the bf16 GEMM splits its work.  Weight-streaming kernel (tile ==
+// kTileNone): 16-row x tiles per workgroup (mt), waves per workgroup (nw),
+// workgroups along N (ntiles) and M (mblocks).  LDS-tiled kernel: tile shape,
+// ntiles / mblocks output tiles along N and M.  Both: K chunks across
+// workgroups (nkc, stages_per_chunk; a stage is 256 k for the streaming kernel,
+// 64 for the tiled one), and the workspace the split-K partials and arrival
+// counters take.
 struct GemmPlan {
+  int tile;
   int mt, nw, ntiles, mblocks, nkc, stages_per_chunk;
   int depth;  // weight stages in flight ahead of the one being multiplied (1 or 2)
   size_t part_bytes, counter_bytes;
 };
 GemmPlan gemm_plan(int M, int N, int K, int epi);
+// Plan of the LDS-tiled kernel with a given tile shape and K split.
+GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc);
+// The tiled kernel needs K % 64 == 0 and operands of fewer than 2^31 elements.
+bool tile_fits(int M, int N, int K);
+// Best tiled plan by the cost model (only_tile = kTileNone: any tile shape).
+GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile);
+// Plan of the weight-streaming kernel; split > 0 forces that many K chunks
+// (at most one per 256-k stage), 0 picks the split.
+GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split);
+int tile_bm(int tile);
+int tile_bn(int tile);
 // Split K only happens when ntiles * mblocks <= 256, so every GEMM's arrival
 // counters fit in this many bytes (a fixed region, whatever M, N, K).
 constexpr size_t kGemmCounterBytes = 4096;
+// Split-K partials are addressed with 32-bit buffer offsets.
+constexpr size_t kMaxPartBytes = (size_t)1 << 31;
 
 // y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]).  `counters`
 // (plan.counter_bytes, zero on entry and on exit) and `part`
@@ -30,8 +50,12 @@ constexpr size_t kGemmCounterBytes = 4096;
 // may share both as long as the counters are never overwritten by anything else.
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
                        int* counters, float* part, hipStream_t s);
-// bf16 GEMM with an explicit plan (nw 4 or 8, mt 1..4, any nkc/stages_per_chunk).
+// bf16 GEMM with an explicit plan (either kernel; for the streaming one nw 4
+// or 8, mt 1..4, any nkc/stages_per_chunk).
 hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
+                            int* counters, float* part, hipStream_t s);
+// The LDS-tiled kernel alone (K % 64 == 0).
+hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.

@@ -84,3 +84,28 @@ def test_kv_append_requires_a_preceding_verify_step():
     kv = nb.KvCache(ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)), 4)
     rc = nb.lib().nightjar_kv_append(ctypes.byref(d), ctypes.byref(kv), 16, 4, 16, 16, 2, 3, 256, 1 << 20, 0)
     assert rc == nb.NJ_EINVAL and "no verify step" in nb.last_error()
+
+
+def test_gemm_with_plan_rejects_impossible_plans_on_host():
+    L = nb.lib()
+    ws = 1 << 30
+    st = nb.NJ_GEMM_STORE
+    # tiled kernels need K % 64 == 0
+    assert L.nightjar_gemm_with_plan(nb.NJ_BF16, 16, 16, 16, 200, 256, 96, st, nb.NJ_GEMM_TILE_128x128, 0, 256, ws, 0) \
+        == nb.NJ_EINVAL
+    assert "K % 64" in nb.last_error()
+    # a split run may cover at most 1024 output tiles
+    assert nb.lib().nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 768, 128256, 4096, st, nb.NJ_GEMM_TILE_128x128, 2) == 0
+    assert "output tiles" in nb.last_error()
+    # auto plan takes no split; fp32 has one kernel; bad kernel id
+    assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, nb.NJ_GEMM_AUTO, 2) == 0
+    assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_F32, 64, 256, 256, st, nb.NJ_GEMM_STREAM, 0) == 0
+    assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, 9, 0) == 0
+    assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, nb.NJ_GEMM_STREAM, -1) == 0
+    # the workspace grows with the split (fp32 partials per chunk)
+    a = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, 384, 4096, 4096, st, nb.NJ_GEMM_TILE_256x256, 1)
+    b = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, 384, 4096, 4096, st, nb.NJ_GEMM_TILE_256x256, 4)
+    assert b >= a + 4 * 384 * 4096 * 4
+    # a workspace one byte short is refused before any launch
+    assert L.nightjar_gemm_with_plan(nb.NJ_BF16, 16, 16, 16, 384, 4096, 4096, st, nb.NJ_GEMM_TILE_256x256, 4, 256,
+                                     b - 1, 0) == nb.NJ_EINVAL

@@ -77,6 +77,98 @@ def test_gemm_bf16_swiglu(M, F, K):
     assert np.abs(got - ref).max() <= 2 ** -8 * np.abs(ref).max() + 1e-6
 
 
+def _gemm_ref(x, w, epi, y0=None):
+    acc = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
+    if epi == nb.NJ_GEMM_STORE:
+        return acc
+    if epi == nb.NJ_GEMM_RESIDUAL:
+        return y0 + acc
+    F = w.shape[0] // 2
+    return oracle.silu(acc[:, :F]) * acc[:, F:]
+
+
+def _gemm_case(M, N, K, epi, seed):
+    rng = np.random.default_rng(seed)
+    x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.03)
+    Nout = N // 2 if epi == nb.NJ_GEMM_SWIGLU else N
+    y0 = rng.standard_normal((M, Nout), dtype=np.float32) if epi == nb.NJ_GEMM_RESIDUAL else None
+    return x, w, y0
+
+
+def _gemm_out(y, epi):
+    if epi == nb.NJ_GEMM_SWIGLU:
+        return oracle.widen(y.cpu().numpy().view(np.uint16), "bf16")
+    return y.cpu().numpy().astype(np.float64)
+
+
+def _gemm_tol(ref, epi):
+    # fp32 accumulation; the SwiGLU output adds one bf16 rounding (2^-9 relative)
+    scale = np.abs(ref).max()
+    return 2 ** -8 * scale + 1e-6 if epi == nb.NJ_GEMM_SWIGLU else 2e-5 * scale
+
+
+@pytest.mark.parametrize("kernel,split,M,N,K,epi", [
+    (nb.NJ_GEMM_TILE_256x256, 0, 300, 1040, 512, nb.NJ_GEMM_STORE),        # ragged M and N
+    (nb.NJ_GEMM_TILE_256x256, 4, 384, 4096, 4096, nb.NJ_GEMM_RESIDUAL),    # split K
+    (nb.NJ_GEMM_TILE_256x256, 2, 64, 2 * 336, 4096, nb.NJ_GEMM_SWIGLU),    # ragged F, split
+    (nb.NJ_GEMM_TILE_128x256, 0, 200, 4112, 1024, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_128x256, 2, 130, 2 * 688, 1024, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_128x256, 8, 129, 512, 4096, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_128x128, 3, 257, 1024, 2048, nb.NJ_GEMM_RESIDUAL),    # split that is not a power of 2
+    (nb.NJ_GEMM_TILE_128x128, 0, 768, 2 * 1024, 512, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_128x128, 0, 1, 272, 64, nb.NJ_GEMM_STORE),            # one row, one stage
+    (nb.NJ_GEMM_STREAM, 3, 48, 4096, 4096, nb.NJ_GEMM_STORE),              # streaming kernel, forced split
+    (nb.NJ_GEMM_STREAM, 1, 200, 1024, 1024, nb.NJ_GEMM_RESIDUAL),          # streaming kernel past 64 rows
+    (nb.NJ_GEMM_AUTO, 0, 768, 6144, 4096, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_AUTO, 0, 320, 4096, 14336, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_AUTO, 0, 256, 2 * 2048, 3584, nb.NJ_GEMM_SWIGLU),
+])
+def test_gemm_every_kernel_shape(kernel, split, M, N, K, epi):
+    x, w, y0 = _gemm_case(M, N, K, epi, seed=M + 3 * N + K + kernel)
+    Nout = N // 2 if epi == nb.NJ_GEMM_SWIGLU else N
+    if epi == nb.NJ_GEMM_SWIGLU:
+        y = torch.empty((M, Nout), dtype=torch.int16, device="cuda")
+    elif epi == nb.NJ_GEMM_RESIDUAL:
+        y = _dev(y0.copy())
+    else:
+        y = torch.full((M, Nout), float("nan"), dtype=torch.float32, device="cuda")
+    dx, dw = _dev(x), _dev(w)
+    nbytes = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, M, N, K, epi, kernel, split)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(ws.data_ptr(), nbytes, _stream())
+    for rep in range(2):  # the second call checks that the split-K counters were left at zero
+        if epi == nb.NJ_GEMM_RESIDUAL:
+            y.copy_(torch.from_numpy(y0))
+        nb.gemm_with_plan(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, epi, kernel, split,
+                          ws.data_ptr(), nbytes, _stream())
+        torch.cuda.synchronize()
+        ref = _gemm_ref(x, w, epi, y0)
+        got = _gemm_out(y, epi)
+        assert np.isfinite(got).all()
+        assert np.abs(got - ref).max() <= _gemm_tol(ref, epi), (rep, np.abs(got - ref).max())
+
+
+def test_gemm_lm_head_large_window_sampled():
+    """The LM-head shape at the largest window of the large-batch grid (768 rows
+    x 128256 x 4096, auto plan), checked on sampled rows and a column band."""
+    M, N, K = 768, 128256, 4096
+    rng = np.random.default_rng(768)
+    x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
+    y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    dx, dw = _dev(x), _dev(w)
+    _gemm(nb.NJ_BF16, dx, dw, y, M, N, K, nb.NJ_GEMM_STORE)
+    rows = np.sort(rng.choice(M, 12, replace=False))
+    rows[-1] = M - 1
+    ref = oracle.widen(x[rows], "bf16") @ oracle.widen(w, "bf16").T
+    got = y[torch.from_numpy(rows).cuda()].cpu().numpy()
+    assert np.abs(got - ref).max() <= 2e-5 * np.abs(ref).max()
+    cols = slice(N - 300, N)
+    ref_c = oracle.widen(x, "bf16") @ oracle.widen(w[cols], "bf16").T
+    assert np.abs(y[:, cols].cpu().numpy() - ref_c).max() <= 2e-5 * np.abs(ref_c).max()
+
+
 @pytest.mark.parametrize("M,N,K,epi", [(3, 50, 70, nb.NJ_GEMM_STORE), (8, 768, 256, nb.NJ_GEMM_RESIDUAL),
                                        (8, 2 * 688, 256, nb.NJ_GEMM_SWIGLU)])
 def test_gemm_f32(M, N, K, epi):

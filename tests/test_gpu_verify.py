@@ -23,6 +23,9 @@ pytestmark = pytest.mark.gpu
 # two-layer bf16 GQA model with the production head dim; vocab not a multiple of 256
 SMALL_BF16 = dataclasses.replace(W.LLAMA8B_LAYER, name="bf16-small", n_layers=2, d_model=512, n_heads=8,
                                  n_kv_heads=2, ffn_dim=1024, vocab=4112)
+# Qwen-like grouping: 7 query heads per KV head (k=7 packs 56 query rows per KV head)
+QWEN_SMALL = dataclasses.replace(W.QWEN7B, name="qwen-small", n_layers=2, d_model=1792, n_heads=14, n_kv_heads=2,
+                                 ffn_dim=1536, vocab=6016)
 
 
 def _oracle(x, shape):
@@ -78,6 +81,34 @@ def test_small_bf16_ragged_contexts(k):
     gl = io.logits.cpu().numpy()
     assert rel_l2_rows(gl, ref["logits"]).max() <= 1e-2
     _decisions_ok(io, ref, x, gpu_logits=gl)
+
+
+@pytest.mark.parametrize("k", [2, 4, 7])
+def test_qwen_grouping_many_query_rows(k):
+    """G = 7: k=2 -> 21 query rows per KV head (2 tiles), k=4 -> 35 (3), k=7 -> 56 (4)."""
+    ctx = np.array([300, 0, 47, 129], dtype=np.int32)
+    x = _inputs(QWEN_SMALL, ctx, k, seed=20 + k)
+    _, _, io, _, err = _run(QWEN_SMALL, x)
+    assert err == 0
+    ref = _oracle(x, QWEN_SMALL)
+    gl = io.logits.cpu().numpy()
+    assert rel_l2_rows(gl, ref["logits"]).max() <= 1e-2
+    _decisions_ok(io, ref, x, gpu_logits=gl)
+
+
+def test_large_batch_lognormal_contexts():
+    """B=24, k=5 (M = 144 rows: three 64-row blocks in every GEMM), contexts
+    lognormal (median 768, sigma 0.5, clipped to [128, 2048]) as in the large-batch grid."""
+    B, k = 24, 5
+    ctx = W.ctx_lengths("lognormal", B, seed=3, median=768, sigma=0.5, lo=128, hi=2048)
+    x = _inputs(SMALL_BF16, ctx, k, seed=31)
+    _, _, io, _, err = _run(SMALL_BF16, x)
+    assert err == 0
+    ref = _oracle(x, SMALL_BF16)
+    gl = io.logits.cpu().numpy()
+    assert rel_l2_rows(gl, ref["logits"]).max() <= 1e-2
+    res = _decisions_ok(io, ref, x, gpu_logits=gl)
+    assert res["checked"] >= B // 2
 
 
 @pytest.fixture(scope="module")
