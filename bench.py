@@ -48,6 +48,167 @@ def measured_traffic(M):
     return rec.get("hbm_bytes_per_launch")
 
 
+# --------------------------------------------------------------------------
+# Report mode: cost table of the large-batch / full-depth configurations
+# --------------------------------------------------------------------------
+def report(args):
+    """Time the verify step over a workload's (B, k) grid and print one JSON
+    line with the cost table.  Inputs are generated on the GPU with torch's
+    seeded generator (same distributions as the CPU generator, not the same
+    bits: these runs are timed, not checked; the parity tests use the CPU
+    generator).  Drafts follow the beta-mixed draft model,
+    q_i = softmax(beta * l_i + (1 - beta) * N(0, 4)), with the target logits l_i
+    of a device pre-pass over the window."""
+    import torch
+
+    from paper_2512_22420_amd import binding as nb
+    from paper_2512_22420_amd import roofline as R
+    from paper_2512_22420_amd import workload as W
+    from paper_2512_22420_amd.device import DeviceCache, DeviceModel, Workspace, device_error, kv_append, verify
+
+    wl = W.WORKLOADS[args.workload]
+    shape = wl.shape
+    grid = list(wl.grid)
+    if args.points:
+        keep = {tuple(int(v) for v in p.split("x")) for p in args.points.split(",")}
+        grid = [g for g in grid if g in keep]
+    betas = [float(b) for b in args.beta.split(",")]
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+
+    def normal_bf16(shape_, std):
+        out = torch.empty(shape_, dtype=torch.bfloat16, device="cuda")
+        flat = out.view(-1)
+        step = 1 << 26
+        for i in range(0, flat.numel(), step):  # bounded fp32 temporaries
+            n = min(step, flat.numel() - i)
+            flat[i:i + n] = (torch.randn(n, generator=gen, device="cuda") * std).to(torch.bfloat16)
+        return out.view(torch.int16)
+
+    t0 = time.time()
+    ones = torch.ones(shape.d_model, dtype=torch.bfloat16, device="cuda").view(torch.int16)
+    w = {"embed": normal_bf16((shape.vocab, shape.d_model), 0.02),
+         "lm_head": normal_bf16((shape.vocab, shape.d_model), 0.02), "final_norm": ones, "layers": []}
+    for _ in range(shape.n_layers):
+        w["layers"].append({"attn_norm": ones, "ffn_norm": ones,
+                            "w_qkv": normal_bf16((shape.qkv_dim, shape.d_model), 0.02),
+                            "w_o": normal_bf16((shape.d_model, shape.n_heads * shape.head_dim), 0.02),
+                            "w_gate_up": normal_bf16((2 * shape.ffn_dim, shape.d_model), 0.02),
+                            "w_down": normal_bf16((shape.d_model, shape.ffn_dim), 0.02)})
+    model = DeviceModel(shape, w)
+    torch.cuda.synchronize()
+    log(f"{wl.name}: weights generated on the device in {time.time() - t0:.1f} s")
+    B_max = max(B for B, _ in grid)
+    k_max = max(k for _, k in grid)
+    ws = Workspace(shape, B_max, k_max)
+    s = stream.cuda_stream
+
+    class IO:
+        pass
+
+    rows = []
+    for (B, k) in grid:
+        ctx = wl.ctx(B, seed=0)
+        table, num_blocks, max_blocks = W.make_block_table(shape, ctx, k_max, seed=0)
+        c = {"k_pages": [normal_bf16((num_blocks, shape.n_kv_heads, 16, shape.head_dim), 0.5)
+                         for _ in range(shape.n_layers)],
+             "v_pages": [normal_bf16((num_blocks, shape.n_kv_heads, shape.head_dim, 16), 0.5)
+                         for _ in range(shape.n_layers)],
+             "block_table": torch.from_numpy(table).cuda(), "context_lens": torch.from_numpy(ctx).cuda(),
+             "num_blocks": num_blocks}
+        cache = DeviceCache(c)
+        cache.max_blocks = max_blocks
+        ctx0 = cache.context_lens.clone()
+        for beta in (betas if k else [None]):
+            io = IO()
+            io.B, io.k = B, k
+            io.last_tokens = torch.randint(0, shape.vocab, (B,), generator=gen, device="cuda", dtype=torch.int32)
+            io.uniforms = torch.rand((B, k + 1), generator=gen, device="cuda")
+            io.accepted_len = torch.zeros(B, dtype=torch.int32, device="cuda")
+            io.next_tokens = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+            io.draft_tokens = torch.zeros((B, k), dtype=torch.int32, device="cuda") if k else None
+            io.draft_probs = torch.full((B, k, shape.vocab), 1.0 / shape.vocab, device="cuda") if k else None
+            io.logits = torch.empty((B, k + 1, shape.vocab), dtype=torch.float32, device="cuda") if k else None
+            for i in range(k):  # beta-mixed drafts from a causal pre-pass
+                verify(model, cache, io, ws)
+                z = beta * io.logits[:, i, :] + (1.0 - beta) * 2.0 * torch.randn(
+                    (B, shape.vocab), generator=gen, device="cuda")
+                q = torch.softmax(z, dim=-1)
+                io.draft_probs[:, i] = q
+                io.draft_tokens[:, i] = torch.multinomial(q, 1, generator=gen).squeeze(1).to(torch.int32)
+            io.logits = None
+            verify(model, cache, io, ws)
+            torch.cuda.synchronize()
+            assert device_error(ws) == 0, "device error"
+            reps = args.grid_reps
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            tv, ts = [], []
+            for _ in range(reps):
+                ev[0].record(stream)
+                verify(model, cache, io, ws)
+                ev[1].record(stream)
+                kv_append(model, cache, io, ws)
+                ev[2].record(stream)
+                cache.context_lens.copy_(ctx0)
+                torch.cuda.synchronize()
+                tv.append(ev[0].elapsed_time(ev[1]) * 1e3)
+                ts.append(ev[0].elapsed_time(ev[2]) * 1e3)
+            assert device_error(ws) == 0, "device error"
+            acc = io.accepted_len.cpu().numpy()
+            t_us = float(np.median(tv))
+            mp = R.step_model(shape, B, k, ctx)
+            # the step's GEMMs alone, with layer 0's weights (every layer has the same shapes)
+            M = B * (k + 1)
+            x = normal_bf16((M, max(shape.d_model, shape.ffn_dim, shape.n_heads * shape.head_dim)), 1.0)
+            y = torch.zeros((M, max(shape.vocab, 2 * shape.ffn_dim, shape.qkv_dim)), dtype=torch.float32,
+                            device="cuda")
+            lw = model.layers[0]
+            gl = [(lw["w_qkv"], shape.qkv_dim, shape.d_model, nb.NJ_GEMM_STORE, shape.n_layers),
+                  (lw["w_o"], shape.d_model, shape.n_heads * shape.head_dim, nb.NJ_GEMM_RESIDUAL, shape.n_layers),
+                  (lw["w_gate_up"], 2 * shape.ffn_dim, shape.d_model, nb.NJ_GEMM_SWIGLU, shape.n_layers),
+                  (lw["w_down"], shape.d_model, shape.ffn_dim, nb.NJ_GEMM_RESIDUAL, shape.n_layers),
+                  (model.lm_head, shape.vocab, shape.d_model, nb.NJ_GEMM_STORE, 1)]
+            gemm_us = 0.0
+            for wt, N, K, epi, mult in gl:
+                n = nb.gemm_workspace_bytes(nb.NJ_BF16, M, N, K, epi)
+                gws = torch.empty(n, dtype=torch.uint8, device="cuda")
+                nb.workspace_init(gws.data_ptr(), n, s)
+                call = lambda: nb.gemm(nb.NJ_BF16, x.data_ptr(), wt.data_ptr(), y.data_ptr(), M, N, K, epi,
+                                       gws.data_ptr(), n, s)
+                call()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(5):
+                    call()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                gemm_us += e0.elapsed_time(e1) / 5 * 1e3 * mult
+            del x, y
+            gemm_roof_us = max(mp["weight_bytes"] / R.HBM_BYTES_PER_S, mp["gemm_flops"] / R.BF16_MFMA_FLOPS) * 1e6
+            row = {"B": B, "k": k, "M": M, "beta": beta, "verify_us": round(t_us, 1),
+                   "step_us": round(float(np.median(ts)), 1),
+                   "verified_tok_s": round(M / (t_us * 1e-6)),
+                   "goodput_tok_s": round(float((acc + 1).sum()) / (t_us * 1e-6)),
+                   "acceptance": round(float(acc.sum()) / (B * k), 3) if k else None,
+                   "roofline_us": round(mp["t_roof_s"] * 1e6, 1),
+                   "roofline_frac": round(mp["t_roof_s"] * 1e6 / t_us, 3),
+                   "gemm_us": round(gemm_us, 1), "gemm_roofline_us": round(gemm_roof_us, 1),
+                   "gemm_mfma_frac": round(mp["gemm_flops"] / R.BF16_MFMA_FLOPS * 1e6 / gemm_us, 3),
+                   "gemm_share": round(gemm_us / t_us, 3),
+                   "kv_gb": round(mp["kv_bytes"] / 1e9, 3), "ctx_mean": round(float(np.mean(ctx)), 1)}
+            rows.append(row)
+            log(f"{wl.name} B={B} k={k} beta={beta}: verify {t_us:.1f} us, step {row['step_us']} us, "
+                f"{row['verified_tok_s']} tok/s, roofline {row['roofline_us']} us ({row['roofline_frac']:.2f}), "
+                f"GEMMs {gemm_us:.1f} us at {row['gemm_mfma_frac']:.2f} of MFMA peak, acceptance {row['acceptance']}")
+        del cache, c
+        torch.cuda.empty_cache()
+    print(json.dumps({"report": wl.name, "unit": "verified tokens/s", "dtype": "bf16",
+                      "data": "synthetic, generated on the device (torch seeded generator)", "grid": rows}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -60,11 +221,21 @@ def main():
     ap.add_argument("--k", type=int, default=5)
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--workload", default="llama8b-layer-small-batch",
+                    help="another workload prints its (B, k) cost table instead of the headline line: "
+                         "llama8b-layer-large-batch, llama8b-32layer, qwen7b-28layer")
+    ap.add_argument("--points", default="", help="report mode: only these grid points, e.g. 64x4,128x5")
+    ap.add_argument("--beta", default="0.7", help="report mode: beta(s) of the beta-mixed draft model")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the verify step shards by sequence "
               "across GPUs without any exchange, which this single-GPU build does not implement.", file=sys.stderr)
         sys.exit(2)
+    if args.workload != "llama8b-layer-small-batch":
+        if args.grid_reps == 30:
+            args.grid_reps = 10
+        report(args)
+        return
 
     import torch
 

@@ -18,6 +18,8 @@
 // Softmax is online in the log2 domain; blocks are dealt round-robin to the 4
 // waves, merged through LDS, and, when the grid splits the KV range, written
 // as partials that a combine kernel merges in split order.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -25,7 +27,7 @@ namespace nj {
 namespace {
 
 constexpr int kD = 128;  // head dim of the bf16 path
-constexpr int kTargetWorkgroups = 512;
+constexpr int kMaxExtraSplits = 4096;  // KV-split workgroups beyond one per (sequence, KV head)
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -214,6 +216,259 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnK a) {
   }
 }
 
+// LDS-staged variant for long contexts and many query rows.  The workgroup
+// streams its KV range in chunks of kCB blocks: all 256 threads load the next
+// chunk (coalesced 16-byte pieces) while the current one is multiplied out of
+// LDS, so one chunk per workgroup is always in flight.  Waves are split into
+// RTW row tiles x (4 / RTW) token phases: a wave multiplies its row tile
+// against every (4/RTW)-th block of the chunk, and the phases of a tile are
+// merged at the end.  LDS rows are XOR-swizzled in 16-byte (K) and 8-byte (V)
+// units so that the fragment reads of 16 consecutive rows hit distinct banks.
+constexpr int kCB = 4;  // cached blocks per chunk
+constexpr int kKPieces = kBlock * kD / 8;  // 16-byte pieces per K (or V) block: 256
+
+__device__ __forceinline__ int k_lds(int tok, int chunk16) {  // element offset in a K block [16][128]
+  return tok * kD + ((chunk16 ^ tok) & 15) * 8;
+}
+__device__ __forceinline__ int v_lds(int dim, int unit8) {  // element offset in a V block [128][16]
+  return dim * kBlock + ((unit8 ^ (((dim >> 3) & 1) << 1)) & 3) * 4;
+}
+
+template <int RTW>
+__global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
+  constexpr int NTP = 4 / RTW;  // token phases per row tile
+  constexpr int KV_ELEMS = kCB * kBlock * kD;  // one chunk of K (or V)
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * 2 * KV_ELEMS];  // [buf][K|V][chunk], 64 KB
+  const int pair = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
+  const int b = pair / a.Hkv, kvh = pair % a.Hkv;
+  const int G = a.H / a.Hkv, R = a.T * G, RT = (R + 15) / 16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int rt = wave % RTW, tp = wave / RTW;
+
+  int ctx = a.ctx[b];
+  if (ctx < 0 || ctx + a.T > a.max_blocks * kBlock) {
+    if (threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
+    ctx = max(0, min(ctx, a.max_blocks * kBlock - a.T));
+  }
+  const int nb_ctx = (ctx + kBlock - 1) / kBlock;
+  const int c0 = split * a.bps, c1 = min(c0 + a.bps, nb_ctx);
+  const int ncached = max(0, c1 - c0);
+  const int ncc = (ncached + kCB - 1) / kCB;      // cached chunks
+  const int nchunks = ncc + (split == 0 ? 1 : 0);  // split 0 also takes the window block, as a last chunk
+
+  if (nchunks == 0) {  // a split past this sequence's context: mark its rows empty for the combine
+    for (int qr = threadIdx.x; qr < R; qr += 256)
+      a.part_ml[(((size_t)pair * nsplit + split) * (RT * 16) + qr) * 2] = -INFINITY;
+    return;
+  }
+  bf16x8 qf[4];
+  int qpos;
+  {
+    const int qc = min(rt * 16 + r16, R - 1);  // padding rows repeat the last real row
+    const int i = qc / G, hh = qc % G;
+    const bf16_t* src = a.q + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + 32 * g;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = ld8(src + 8 * s);
+    qpos = i;
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // chunk ch: blocks [j0, j0 + nblk) of the cached range, or the window block
+  auto chunk_blocks = [&](int ch, int& j0, int& nblk) {
+    if (ch < ncc) {
+      j0 = c0 + ch * kCB;
+      nblk = min(kCB, c1 - j0);
+    } else {
+      j0 = -1;
+      nblk = 1;
+    }
+  };
+  // Thread t loads piece t of each block of the chunk (K: token t/16, 16-byte
+  // column t%16; V: dim t/2, tokens 8*(t%2)..+7).  Branch-free: every piece is
+  // loaded from a valid address (blocks past the chunk or with a bad id read
+  // the window block) and zeroed when stored.  The block ids of a chunk are
+  // read one chunk ahead of its pages.
+  const bf16_t* win_k = a.wk + ((size_t)b * a.Hkv + kvh) * (kBlock * kD);
+  const bf16_t* win_v = a.wv + ((size_t)b * a.Hkv + kvh) * (kBlock * kD);
+  const int32_t* trow = a.table + (size_t)b * a.max_blocks;
+  u32x4 kr[kCB], vr[kCB];
+  bool okb[kCB];
+  int ph[kCB];
+  auto tload = [&](int ch, int (&dst)[kCB]) {
+    int j0, nblk;
+    chunk_blocks(ch, j0, nblk);
+#pragma unroll
+    for (int bi = 0; bi < kCB; ++bi) dst[bi] = trow[max(0, min(j0 + bi, c1 - 1))];
+  };
+  auto gload = [&](int ch) {
+    int j0, nblk;
+    chunk_blocks(ch, j0, nblk);
+    bool bad = false;
+#pragma unroll
+    for (int bi = 0; bi < kCB; ++bi) {
+      const bool used = j0 >= 0 && bi < nblk;
+      const bool valid = ph[bi] >= 0 && ph[bi] < a.num_blocks;
+      bad |= used && !valid;
+      okb[bi] = (used && valid) || (j0 < 0 && bi == 0);
+      const size_t off = ((size_t)(used && valid ? ph[bi] : 0) * a.Hkv + kvh) * (kBlock * kD);
+      const bf16_t* kb = (used && valid) ? a.kp + off : win_k;
+      const bf16_t* vb = (used && valid) ? a.vp + off : win_v;
+      kr[bi] = *reinterpret_cast<const u32x4*>(kb + threadIdx.x * 8);
+      vr[bi] = *reinterpret_cast<const u32x4*>(vb + threadIdx.x * 8);
+    }
+    if (bad && threadIdx.x == 0) flag_error(a.err, kErrBlock);
+  };
+  auto sstore = [&](int buf) {
+    bf16_t* ks = smem + buf * 2 * KV_ELEMS;
+    bf16_t* vs = ks + KV_ELEMS;
+    const int t = threadIdx.x;
+    const u32x4 z = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int bi = 0; bi < kCB; ++bi) {
+      *reinterpret_cast<u32x4*>(ks + bi * kBlock * kD + k_lds(t >> 4, t & 15)) = okb[bi] ? kr[bi] : z;
+      *reinterpret_cast<u32x4*>(vs + bi * kBlock * kD + v_lds(t >> 1, (t & 1) * 2)) = okb[bi] ? vr[bi] : z;
+    }
+  };
+
+  if (nchunks > 0) {
+    tload(0, ph);
+    gload(0);
+    tload(min(1, nchunks - 1), ph);
+    sstore(0);
+  }
+  __syncthreads();
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const int buf = ch & 1;
+    // ids of chunk ch+2 first (older in the load queue, so waiting for them
+    // never waits for the pages), then the pages of chunk ch+1; the chunk
+    // after the last re-loads the last one into the idle buffer (unread),
+    // which keeps the loop free of branches around the loads
+    int ph2[kCB];
+    tload(min(ch + 2, nchunks - 1), ph2);
+    gload(min(ch + 1, nchunks - 1));
+    int j0, nblk;
+    chunk_blocks(ch, j0, nblk);
+    const bool win = j0 < 0;
+    const bf16_t* ks = smem + buf * 2 * KV_ELEMS;
+    const bf16_t* vs = ks + KV_ELEMS;
+    if (rt < RT) {
+      for (int bi = tp; bi < nblk; bi += NTP) {
+        const int nvalid = win ? a.T : min(kBlock, ctx - (j0 + bi) * kBlock);
+        const bf16_t* kb = ks + bi * kBlock * kD;
+        const bf16_t* vb = vs + bi * kBlock * kD;
+        bf16x8 kf[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) kf[s] = ld8(kb + k_lds(r16, 4 * g + s));
+        u32x2 vf[8];
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) vf[dt] = *reinterpret_cast<const u32x2*>(vb + v_lds(16 * dt + r16, g));
+        if (4 * g + 3 >= nvalid) {  // tokens past the valid ones may hold anything: zero them
+          const int keep = nvalid - 4 * g;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) {
+            uint32_t lo = vf[dt][0], hi = vf[dt][1];
+            if (keep <= 0) lo = 0u;
+            else if (keep == 1) lo &= 0xffffu;
+            if (keep <= 2) hi = 0u;
+            else if (keep == 3) hi &= 0xffffu;
+            vf[dt][0] = lo;
+            vf[dt][1] = hi;
+          }
+        }
+        f32x4 st = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qf[s], st, 0, 0, 0);
+        float sc[4];
+        float bm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 4 * g + i;
+          const bool ok = tok < nvalid && (!win || tok <= qpos);
+          sc[i] = ok ? st[i] * a.scale_log2 : -INFINITY;
+          bm = fmaxf(bm, sc[i]);
+        }
+        bm = fmaxf(bm, __shfl_xor(bm, 16));
+        bm = fmaxf(bm, __shfl_xor(bm, 32));
+        const float mn = fmaxf(m_run, bm);
+        const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m_run - mn);
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = (sc[i] == -INFINITY) ? 0.f : exp2f(sc[i] - mn);
+        l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+        m_run = mn;
+        u32x2 pp;
+        pp[0] = pack_bf16x2(p[0], p[1]);
+        pp[1] = pack_bf16x2(p[2], p[3]);
+        const bf16x4 pf = __builtin_bit_cast(bf16x4, pp);
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+          o[dt] *= alpha;
+          o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vf[dt]), pf, o[dt], 0, 0, 0);
+        }
+      }
+    }
+    sstore(buf ^ 1);
+    __syncthreads();
+#pragma unroll
+    for (int bi = 0; bi < kCB; ++bi) ph[bi] = ph2[bi];
+  }
+
+  // merge the token phases of each row tile (LDS reused), then store or write partials
+  float* s_o = reinterpret_cast<float*>(smem);  // [NTP][kD][17]
+  float* s_m = s_o + NTP * kD * 17;             // [NTP][16]
+  float* s_l = s_m + NTP * 16;
+  for (int t = 0; t < RT; ++t) {
+    if (rt == t) {
+      float lsum = l_run;
+      lsum += __shfl_xor(lsum, 16);
+      lsum += __shfl_xor(lsum, 32);
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s_o[(tp * kD + 16 * dt + 4 * g + i) * 17 + r16] = o[dt][i];
+      if (g == 0) {
+        s_m[tp * 16 + r16] = m_run;
+        s_l[tp * 16 + r16] = lsum;
+      }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 16 * kD; idx += 256) {
+      const int qr16 = idx / kD, d = idx % kD;
+      const int qr = t * 16 + qr16;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < NTP; ++w) mx = fmaxf(mx, s_m[w * 16 + qr16]);
+      float acc = 0.f, wsum = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < NTP; ++w) {
+          const float f = (s_m[w * 16 + qr16] == -INFINITY) ? 0.f : exp2f(s_m[w * 16 + qr16] - mx);
+          wsum += f * s_l[w * 16 + qr16];
+          acc += f * s_o[(w * kD + d) * 17 + qr16];
+        }
+      }
+      if (qr < R) {
+        if (nsplit == 1) {
+          const int i = qr / G, hh = qr % G;
+          a.out[((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
+        } else {
+          const size_t base = ((size_t)pair * nsplit + split) * (RT * 16) + qr;
+          a.part_o[base * kD + d] = acc;
+          if (d == 0) {
+            a.part_ml[base * 2] = mx;
+            a.part_ml[base * 2 + 1] = wsum;
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // Merge KV-split partials in split order: out = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
 // One workgroup per (sequence, KV head, query row), one thread per head dim.
 __global__ __launch_bounds__(kD) void attn_combine_kernel(const float* __restrict__ part_o,
@@ -228,7 +483,8 @@ __global__ __launch_bounds__(kD) void attn_combine_kernel(const float* __restric
   for (int s = 0; s < nsplit; ++s) {
     const size_t base = ((size_t)pair * nsplit + s) * rpad + qr;
     const float m = part_ml[base * 2];
-    const float f = (m == -INFINITY) ? 0.f : exp2f(m - mx);
+    if (m == -INFINITY) continue;  // empty split: only its marker was written
+    const float f = exp2f(m - mx);
     wsum += f * part_ml[base * 2 + 1];
     acc += f * part_o[base * kD + d];
   }
@@ -320,21 +576,26 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnF a) {
 void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, int* blocks_per_split) {
   (void)T;
   (void)G;
+  // Enough workgroups to keep ~2048 chunk streams in flight, and no split
+  // longer than 64 blocks (one workgroup streams its chunks one after the
+  // other, so the longest split sets the kernel's duration); at least 8
+  // blocks per split, and at most pairs + kMaxExtraSplits workgroups, which
+  // bounds the partial buffer whatever the context length.
   const int pairs = B * Hkv;
-  int ns = (kTargetWorkgroups + pairs - 1) / pairs;
-  const int cap = (max_blocks + 7) / 8;  // at least ~8 cached blocks (2 per wave) per split
-  if (ns > cap) ns = cap;
-  if (ns < 1) ns = 1;
+  int ns = std::max((2048 + pairs - 1) / pairs, (max_blocks + 63) / 64);
+  ns = std::min(ns, 1 + kMaxExtraSplits / pairs);
+  ns = std::min(ns, (max_blocks + 7) / 8);
+  ns = std::max(ns, 1);
   int bps = (max_blocks + ns - 1) / ns;
-  ns = (max_blocks + bps - 1) / bps;
-  if (ns < 1) ns = 1;
+  bps = (bps + kCB - 1) / kCB * kCB;
+  ns = std::max(1, (max_blocks + bps - 1) / bps);
   *nsplit = ns;
-  *blocks_per_split = bps < 1 ? 1 : bps;
+  *blocks_per_split = bps;
 }
 
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D) {
   const int rpad = ((T * G + 15) / 16) * 16;
-  return (size_t)(B * Hkv + kTargetWorkgroups) * rpad * (D + 2);
+  return (size_t)(B * Hkv + kMaxExtraSplits) * rpad * (D + 2);
 }
 
 hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
@@ -355,11 +616,19 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
           static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv, x.blocks_per_split,
           (float)(1.4426950408889634 / sqrt((double)kD))};
   dim3 grid(x.B * x.Hkv, x.nsplit);
-  switch (RT) {
-    case 1: hipLaunchKernelGGL(attn_bf16_kernel<1>, grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(256), 0, s, a); break;
-    case 3: hipLaunchKernelGGL(attn_bf16_kernel<3>, grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL(attn_bf16_kernel<4>, grid, dim3(256), 0, s, a); break;
+  if (x.variant == 1) {
+    switch (RT) {
+      case 1: hipLaunchKernelGGL(attn_bf16_kernel<1>, grid, dim3(256), 0, s, a); break;
+      case 2: hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(256), 0, s, a); break;
+      case 3: hipLaunchKernelGGL(attn_bf16_kernel<3>, grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL(attn_bf16_kernel<4>, grid, dim3(256), 0, s, a); break;
+    }
+  } else {
+    switch (RT) {
+      case 1: hipLaunchKernelGGL(attn_lds_kernel<1>, grid, dim3(256), 0, s, a); break;
+      case 2: hipLaunchKernelGGL(attn_lds_kernel<2>, grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL(attn_lds_kernel<4>, grid, dim3(256), 0, s, a); break;
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || x.nsplit == 1) return e;

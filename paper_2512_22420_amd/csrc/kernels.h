@@ -92,6 +92,7 @@ struct AttnArgs {
   int nsplit, blocks_per_split;
   void* out;            // [M][H*D]
   int* err;
+  int variant = 0;      // bf16 path: 0 LDS-staged chunks, 1 direct-to-register blocks
 };
 // Number of KV splits the bf16 path uses, and the partial buffer floats it needs.
 void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, int* blocks_per_split);

@@ -14,7 +14,9 @@ import torch
 from . import binding as nb
 
 
-def _to_dev(a: np.ndarray, device) -> torch.Tensor:
+def _to_dev(a, device) -> torch.Tensor:
+    if isinstance(a, torch.Tensor):  # already resident (bf16 bits as int16, or fp32/int32)
+        return a
     a = np.ascontiguousarray(a)
     if a.dtype == np.uint16:
         a = a.view(np.int16)

@@ -176,6 +176,24 @@ def ctx_lengths(kind: str, B: int, seed: int = 0, **kw) -> np.ndarray:
     raise ValueError(kind)
 
 
+def make_block_table(shape: ModelShape, ctx: Sequence[int], k_max: int, seed: int = 0, spare: float = 0.05):
+    """Block table of the paged cache: sequence b owns ceil((ctx_b + k_max + 1)/16)
+    physical blocks, taken in order from a shuffled pool of sum(need)*(1+spare)+1
+    blocks; unused entries are -1.  Returns (table [B, max_blocks], num_blocks, max_blocks)."""
+    ctx = np.asarray(ctx, dtype=np.int32)
+    B, bs = len(ctx), shape.block_size
+    need = [(int(c) + k_max + 1 + bs - 1) // bs for c in ctx]
+    num_blocks = int(math.ceil(sum(need) * (1.0 + spare))) + 1
+    perm = _rng(seed, _K_PERM, B).permutation(num_blocks).astype(np.int32)
+    max_blocks = max(need)
+    table = np.full((B, max_blocks), -1, dtype=np.int32)
+    off = 0
+    for b in range(B):
+        table[b, : need[b]] = perm[off: off + need[b]]
+        off += need[b]
+    return table, num_blocks, max_blocks
+
+
 def make_context(shape: ModelShape, ctx: Sequence[int], k_max: int, seed: int = 0,
                  spare: float = 0.05, kv_std: float = 0.5) -> Dict:
     """Paged KV cache holding ``ctx[b]`` cached tokens per sequence.
@@ -187,16 +205,7 @@ def make_context(shape: ModelShape, ctx: Sequence[int], k_max: int, seed: int = 
     s = shape
     ctx = np.asarray(ctx, dtype=np.int32)
     B, bs = len(ctx), s.block_size
-    need = [(int(c) + k_max + 1 + bs - 1) // bs for c in ctx]
-    total = sum(need)
-    num_blocks = int(math.ceil(total * (1.0 + spare))) + 1
-    perm = _rng(seed, _K_PERM, B).permutation(num_blocks).astype(np.int32)
-    max_blocks = max(need)
-    table = np.full((B, max_blocks), -1, dtype=np.int32)
-    off = 0
-    for b in range(B):
-        table[b, : need[b]] = perm[off: off + need[b]]
-        off += need[b]
+    table, num_blocks, max_blocks = make_block_table(shape, ctx, k_max, seed, spare)
     k_pages, v_pages = [], []
     for l in range(s.n_layers):
         kshape = (num_blocks, s.n_kv_heads, bs, s.head_dim)
