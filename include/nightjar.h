@@ -80,7 +80,7 @@ typedef struct nj_model_desc {
   int32_t d_model;    /* d                      */
   int32_t n_heads;    /* H query heads          */
   int32_t n_kv_heads; /* Hkv; H % Hkv == 0      */
-  int32_t head_dim;   /* D (even)               */
+  int32_t head_dim;   /* D (multiple of 8)      */
   int32_t ffn_dim;    /* F                      */
   int32_t vocab;      /* V                      */
   int32_t block_size; /* tokens per KV block: 16 */
@@ -173,13 +173,15 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
  * finalised before the next begins; rejected drafts leave no KV behind).
  *
  * For each b, window rows 0..accepted_len[b] (the last committed token plus the
- * accepted drafts) are written to positions context_lens[b] + j of the pages,
- * then context_lens[b] += accepted_len[b] + 1 on the device.  The emitted token
- * is not appended: it is the next step's last token.  Must follow the
- * nightjar_verify_step that filled `workspace`, with the same desc, kv,
- * block_table, max_blocks, B and k, before another verify step reuses it.
+ * accepted drafts) are written to positions c_b + j of the pages, where c_b is
+ * context_lens[b] as the verify step read it (the positions its RoPE used,
+ * kept in the workspace), then context_lens[b] = c_b + accepted_len[b] + 1 on
+ * the device.  The emitted token is not appended: it is the next step's last
+ * token.  Must follow the nightjar_verify_step that filled `workspace`, with
+ * the same desc, kv, block_table, max_blocks, B and k, before another verify
+ * step reuses it.  Page arrays must be 16-byte aligned.
  *
- *   context_lens   device int32 [B], in/out
+ *   context_lens   device int32 [B], out (overwritten as above)
  *   accepted_len   device int32 [B]
  */
 int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const int32_t* block_table,

@@ -6,18 +6,18 @@
 // where the bandwidth goes.  Three kernels:
 //
 //   accept_stats   (rows x 8192-wide chunks): chunk max and sum of exp(l - max).
-//   accept_tiles   (rows x tile blocks): every window row i of every sequence is
-//                  a candidate draw row -- weights max(0, p_i - q_i) for i < k
-//                  (the residual after a rejection at i), p_k for the bonus row
-//                  -- and gets fp64 sums over 256-wide tiles.  Done for all
-//                  rows at once, since n is not known yet.
-//   accept_finalize (one wave per sequence): lanes run the k accept tests in
-//                  parallel (u_i < p_i(x_i) / q_i(x_i), q == 0 accepts), n =
-//                  first failure; then the smallest j whose running sum of
-//                  row n's weights exceeds u_k times their total: a prefix scan
-//                  over lane-contiguous tile sums finds the tile, a prefix scan
-//                  over that tile's 256 weights finds the entry.  All sums are
-//                  fp64 in a fixed order, so the draw is reproducible.
+//   accept_tiles   (sequences x tile blocks): every workgroup first runs the
+//                  k accept tests of its sequence (u_i < p_i(x_i) / q_i(x_i),
+//                  q == 0 accepts; p from the chunk statistics) to find n, the
+//                  first failure, then sums the draw weights of row n only --
+//                  max(0, p_n - q_n) after a rejection, p_k for the bonus -- in
+//                  fp64 over 256-wide tiles.  The tests are cheap and
+//                  identical in every workgroup of a sequence.
+//   accept_finalize (one wave per sequence): the smallest j whose running sum
+//                  of row n's weights exceeds u_k times their total: a prefix
+//                  scan over lane-contiguous tile sums finds the tile, a prefix
+//                  scan over that tile's 256 weights finds the entry.  All sums
+//                  are fp64 in a fixed order, so the draw is reproducible.
 #include "common.h"
 #include "kernels.h"
 
@@ -27,7 +27,7 @@ namespace {
 constexpr int kChunk = 8192;
 constexpr int kStatThreads = 256;
 constexpr int kTile = 256;          // weights per tile (4 per lane of a wave)
-constexpr int kTilesPerBlock = 32;  // tiles per accept_tiles workgroup
+constexpr int kTilesPerBlock = 8;   // tiles per accept_tiles workgroup (two per wave)
 constexpr int kMaxTiles = 2048;     // V <= 524288
 
 // One pass: each thread holds its 32 values of the chunk in registers.
@@ -97,8 +97,9 @@ struct AccK {
   const float* dprobs;    // [B][k][V]
   const float* uniforms;  // [B][T]
   const float* stats;     // [B*T][nch][2]
-  float* rowstat;         // [B*T][2]: max, 1/sum
-  double* tsum;           // [B*T][ntile]
+  float* rowstat;         // [B][2]: max, 1/sum of the draw row
+  double* tsum;           // [B][ntile]: tile sums of the draw row
+  int32_t* nsel;          // [B]: accepted length n
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
@@ -106,17 +107,47 @@ struct AccK {
 };
 
 __global__ __launch_bounds__(256) void accept_tiles_kernel(AccK a) {
-  const int row = blockIdx.x, T = a.k + 1, b = row / T, i = row % T;
+  __shared__ float s_m[kWave], s_inv[kWave];
+  __shared__ int s_n;
+  const int b = blockIdx.x, T = a.k + 1, V = a.V;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float m, inv_s;
-  row_stats(a.stats + (size_t)row * a.nch * 2, a.nch, &m, &inv_s);
-  if (blockIdx.y == 0 && threadIdx.x == 0) {
-    a.rowstat[row * 2] = m;
-    a.rowstat[row * 2 + 1] = inv_s;
+  if (wave == 0) {
+    // row statistics of the window rows (lane i: row i) and the k accept tests
+    float m = 0.f, inv_s = 0.f;
+    if (lane < T) {
+      row_stats(a.stats + (size_t)(b * T + lane) * a.nch * 2, a.nch, &m, &inv_s);
+      s_m[lane] = m;
+      s_inv[lane] = inv_s;
+    }
+    bool ok = true;
+    if (lane < a.k) {
+      const int x = a.drafts[b * a.k + lane];
+      if (x < 0 || x >= V) {
+        if (blockIdx.y == 0) flag_error(a.err, kErrToken);
+        ok = false;
+      } else {
+        const float p = expf(a.logits[(size_t)(b * T + lane) * V + x] - m) * inv_s;
+        const float q = a.dprobs[((size_t)b * a.k + lane) * V + x];
+        ok = (q <= 0.f) || (a.uniforms[b * T + lane] < p / q);
+      }
+    }
+    const unsigned long long fails = __ballot(lane < a.k && !ok);
+    const int n = fails ? __ffsll((long long)fails) - 1 : a.k;
+    if (lane == 0) {
+      s_n = n;
+      if (blockIdx.y == 0) a.nsel[b] = n;
+    }
   }
-  const bool resid = i < a.k;
-  const float* lrow = a.logits + (size_t)row * a.V;
-  const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + i) * a.V : lrow;
+  __syncthreads();
+  const int n = s_n;
+  const float m = s_m[n], inv_s = s_inv[n];
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    a.rowstat[b * 2] = m;
+    a.rowstat[b * 2 + 1] = inv_s;
+  }
+  const bool resid = n < a.k;
+  const float* lrow = a.logits + (size_t)(b * T + n) * V;
+  const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * V : lrow;
   const int t0 = blockIdx.y * kTilesPerBlock, t1 = min(t0 + kTilesPerBlock, a.ntile);
   const bool vec = (a.V & 3) == 0;
   for (int t = t0 + wave; t < t1; t += 4) {
@@ -136,7 +167,7 @@ __global__ __launch_bounds__(256) void accept_tiles_kernel(AccK a) {
         if (j0 + e < a.V) ls += (double)draw_weight(lrow, qrow, m, inv_s, resid, j0 + e);
     }
     ls = wave_sum_d(ls);
-    if (lane == 0) a.tsum[(size_t)row * a.ntile + t] = ls;
+    if (lane == 0) a.tsum[(size_t)b * a.ntile + t] = ls;
   }
 }
 
@@ -154,30 +185,14 @@ __global__ __launch_bounds__(64) void accept_finalize_kernel(AccK a) {
   __shared__ double fb_tsum[kMaxTiles];  // only for an all-zero residual
   const int b = blockIdx.x, T = a.k + 1, V = a.V, lane = threadIdx.x;
 
-  // the k accept tests, one per lane (lanes 0..k-1), then n = first failure
-  bool ok = true;
-  if (lane < a.k) {
-    const int x = a.drafts[b * a.k + lane];
-    if (x < 0 || x >= V) {
-      flag_error(a.err, kErrToken);
-      ok = false;
-    } else {
-      const int r = b * T + lane;
-      const float p = expf(a.logits[(size_t)r * V + x] - a.rowstat[r * 2]) * a.rowstat[r * 2 + 1];
-      const float q = a.dprobs[((size_t)b * a.k + lane) * V + x];
-      ok = (q <= 0.f) || (a.uniforms[b * T + lane] < p / q);
-    }
-  }
-  const unsigned long long fails = __ballot(lane < a.k && !ok);
-  const int n = fails ? __ffsll((long long)fails) - 1 : a.k;
-
+  const int n = a.nsel[b];
   const int row = b * T + n;
   bool resid = n < a.k;
   const float* lrow = a.logits + (size_t)row * V;
   const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * V : lrow;
-  const float m = a.rowstat[row * 2], inv_s = a.rowstat[row * 2 + 1];
+  const float m = a.rowstat[b * 2], inv_s = a.rowstat[b * 2 + 1];
   const int ntile = a.ntile;
-  const double* ts = a.tsum + (size_t)row * ntile;
+  const double* ts = a.tsum + (size_t)b * ntile;
 
   // lane-contiguous tile ranges; the total is the last inclusive prefix, so it
   // is made of exactly the additions the search below walks through
@@ -306,7 +321,7 @@ int accept_chunks(int V) { return (V + kChunk - 1) / kChunk; }
 size_t accept_workspace_bytes(int rows, int V) {
   const int ntile = (V + kTile - 1) / kTile;
   return al256((size_t)rows * accept_chunks(V) * 2 * 4) + al256((size_t)rows * 2 * 4) +
-         al256((size_t)rows * ntile * 8);
+         al256((size_t)rows * ntile * 8) + al256((size_t)rows * 4);
 }
 
 hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
@@ -315,12 +330,14 @@ hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
   float* stats = reinterpret_cast<float*>(ws);
   float* rowstat = reinterpret_cast<float*>(ws + al256((size_t)rows * nch * 2 * 4));
   double* tsum = reinterpret_cast<double*>(ws + al256((size_t)rows * nch * 2 * 4) + al256((size_t)rows * 2 * 4));
+  int32_t* nsel = reinterpret_cast<int32_t*>(ws + al256((size_t)rows * nch * 2 * 4) + al256((size_t)rows * 2 * 4) +
+                                             al256((size_t)rows * ntile * 8));
   hipLaunchKernelGGL(accept_stats_kernel, dim3(rows, nch), dim3(kStatThreads), 0, s, x.logits, x.V, nch, stats);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, stats, rowstat, tsum, x.accepted_len, x.next_tokens, x.err,
-         x.k, x.V, nch, ntile};
-  hipLaunchKernelGGL(accept_tiles_kernel, dim3(rows, (ntile + kTilesPerBlock - 1) / kTilesPerBlock), dim3(256), 0,
+  AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, stats, rowstat, tsum, nsel, x.accepted_len, x.next_tokens,
+         x.err, x.k, x.V, nch, ntile};
+  hipLaunchKernelGGL(accept_tiles_kernel, dim3(x.B, (ntile + kTilesPerBlock - 1) / kTilesPerBlock), dim3(256), 0,
                      s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -39,7 +39,8 @@ size_t al(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
-  size_t err, gemm_cnt, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats, gemm_part, total;
+  size_t err, gemm_cnt, ctx_snap, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats, gemm_part,
+      total;
   size_t win_layer_bytes;
 };
 
@@ -62,7 +63,7 @@ bool desc_ok(const nj_model_desc* d) {
       d->ffn_dim < 1 || d->vocab < 1)
     return !fail(NJ_EINVAL, "model dimensions must be positive");
   if (d->n_heads % d->n_kv_heads) return !fail(NJ_EINVAL, "n_heads %% n_kv_heads != 0");
-  if (d->head_dim % 2) return !fail(NJ_EINVAL, "head_dim must be even");
+  if (d->head_dim % 8) return !fail(NJ_EINVAL, "head_dim must be a multiple of 8");
   if (d->block_size != 16) return !fail(NJ_EINVAL, "block_size must be 16");
   if (d->dtype != NJ_F32 && d->dtype != NJ_BF16) return !fail(NJ_EINVAL, "dtype must be NJ_F32 or NJ_BF16");
   if (d->vocab > kMaxVocab) return !fail(NJ_EINVAL, "vocab > %d", kMaxVocab);
@@ -99,6 +100,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   // workspace never write activations over them.  Zeroed by
   // nightjar_workspace_init and left at zero by every GEMM.
   L.gemm_cnt = take(kGemmCounterBytes);
+  L.ctx_snap = take((size_t)B * 4);  // context lengths read by the verify step, for the KV append
   size_t part = 0;
   if (d.dtype == NJ_BF16) {
     GemmShape gs[5];
@@ -236,7 +238,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     void* wk = ws + L.win_k + l * L.win_layer_bytes;
     void* wv = ws + L.win_v + l * L.win_layer_bytes;
     NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
-                              wk, wv, s),
+                              wk, wv, l == 0 ? reinterpret_cast<int32_t*>(ws + L.ctx_snap) : nullptr, s),
            "rope");
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
@@ -281,9 +283,12 @@ int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const i
   const Layout L = layout(d, B, k);
   if (workspace_bytes < L.total) return fail(NJ_EINVAL, "workspace too small");
   const char* ws = static_cast<const char*>(workspace);
+  for (int l = 0; l < d.n_layers; ++l)
+    if (!aligned16(kv->k_pages[l]) || !aligned16(kv->v_pages[l])) return fail(NJ_EINVAL, "layer %d pages not 16-byte aligned", l);
   KvAppendArgs a{d.dtype == NJ_BF16 ? kBF16 : kF32, kv->k_pages, kv->v_pages, ws + L.win_k, ws + L.win_v,
-                 block_table, max_blocks, kv->num_blocks, context_lens, accepted_len, d.n_layers, B, k,
-                 d.n_kv_heads, d.head_dim, reinterpret_cast<int*>(const_cast<char*>(ws) + L.err)};
+                 block_table, max_blocks, kv->num_blocks, reinterpret_cast<const int32_t*>(ws + L.ctx_snap),
+                 context_lens, accepted_len, d.n_layers, B, k, d.n_kv_heads, d.head_dim,
+                 reinterpret_cast<int*>(const_cast<char*>(ws) + L.err)};
   hipError_t e = launch_kv_append(a, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "kv_append");
 }

@@ -13,11 +13,9 @@
 // so the softmax numerators go straight from the score registers into the
 // second product with no data exchange.  The A operand V^T needs 4
 // consecutive tokens of one dim: V pages are stored dim-major inside a block
-// ([D][16]), which makes that an 8-byte load.  K and V blocks are read
-// straight into MFMA operand registers (64 contiguous bytes per lane for K).
-// Softmax is online in the log2 domain; blocks are dealt round-robin to the 4
-// waves, merged through LDS, and, when the grid splits the KV range, written
-// as partials that a combine kernel merges in split order.
+// ([D][16]), which makes that an 8-byte read.  Softmax is online in the log2
+// domain.  When the grid splits the KV range, each split writes its partial
+// (o, max, sum) and a combine kernel merges the splits in split order.
 #include <algorithm>
 
 #include "common.h"
@@ -49,174 +47,7 @@ struct AttnK {
   float scale_log2;
 };
 
-template <int RT>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnK a) {
-  const int pair = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
-  const int b = pair / a.Hkv, kvh = pair % a.Hkv;
-  const int G = a.H / a.Hkv, R = a.T * G;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, g = lane >> 4;
-
-  int ctx = a.ctx[b];
-  if (ctx < 0 || ctx + a.T > a.max_blocks * kBlock) {
-    if (threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
-    ctx = max(0, min(ctx, a.max_blocks * kBlock - a.T));
-  }
-  const int nb_ctx = (ctx + kBlock - 1) / kBlock;
-  const int c0 = split * a.bps, c1 = min(c0 + a.bps, nb_ctx);
-  const int ncached = max(0, c1 - c0);
-  const int nent = ncached + (split == 0 ? 1 : 0);  // split 0 also takes the window block
-
-  bf16x8 qf[RT][4];
-  int qpos[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int qc = min(rt * 16 + r16, R - 1);  // padding rows repeat the last real row
-    const int i = qc / G, hh = qc % G;
-    const bf16_t* src = a.q + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + 32 * g;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qf[rt][s] = ld8(src + 8 * s);
-    qpos[rt] = i;
-  }
-
-  float m_run[RT], l_run[RT];
-  f32x4 o[RT][8];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    m_run[rt] = -INFINITY;
-    l_run[rt] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  for (int e = wave; e < nent; e += 4) {
-    const bool win = (e == ncached);
-    const bf16_t* kb;
-    const bf16_t* vb;
-    int nvalid;
-    if (!win) {
-      const int j = c0 + e;
-      const int phys = a.table[(size_t)b * a.max_blocks + j];
-      if (phys < 0 || phys >= a.num_blocks) {
-        if (lane == 0) flag_error(a.err, kErrBlock);
-        continue;
-      }
-      kb = a.kp + ((size_t)phys * a.Hkv + kvh) * (kBlock * kD);
-      vb = a.vp + ((size_t)phys * a.Hkv + kvh) * (kBlock * kD);
-      nvalid = min(kBlock, ctx - j * kBlock);
-    } else {
-      kb = a.wk + ((size_t)b * a.Hkv + kvh) * (kBlock * kD);
-      vb = a.wv + ((size_t)b * a.Hkv + kvh) * (kBlock * kD);
-      nvalid = a.T;
-    }
-    bf16x8 kf[4];
-    const bf16_t* krow = kb + r16 * kD + 32 * g;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) kf[s] = ld8(krow + 8 * s);
-    u32x2 vf[8];
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
-      vf[dt] = *reinterpret_cast<const u32x2*>(vb + (16 * dt + r16) * kBlock + 4 * g);
-    if (4 * g + 3 >= nvalid) {  // tokens past the valid ones may hold anything: zero them
-      const int keep = nvalid - 4 * g;  // tokens of this lane kept: 0..3
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        uint32_t lo = vf[dt][0], hi = vf[dt][1];
-        if (keep <= 0) lo = 0u;
-        else if (keep == 1) lo &= 0xffffu;
-        if (keep <= 2) hi = 0u;
-        else if (keep == 3) hi &= 0xffffu;
-        vf[dt][0] = lo;
-        vf[dt][1] = hi;
-      }
-    }
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      f32x4 st = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < 4; ++s) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qf[rt][s], st, 0, 0, 0);
-      float sc[4];
-      float bm = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = 4 * g + i;
-        const bool ok = tok < nvalid && (!win || tok <= qpos[rt]);
-        sc[i] = ok ? st[i] * a.scale_log2 : -INFINITY;
-        bm = fmaxf(bm, sc[i]);
-      }
-      bm = fmaxf(bm, __shfl_xor(bm, 16));
-      bm = fmaxf(bm, __shfl_xor(bm, 32));
-      const float mn = fmaxf(m_run[rt], bm);
-      const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m_run[rt] - mn);
-      float p[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) p[i] = (sc[i] == -INFINITY) ? 0.f : exp2f(sc[i] - mn);
-      l_run[rt] = l_run[rt] * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-      m_run[rt] = mn;
-      u32x2 pp;
-      pp[0] = pack_bf16x2(p[0], p[1]);
-      pp[1] = pack_bf16x2(p[2], p[3]);
-      const bf16x4 pf = __builtin_bit_cast(bf16x4, pp);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        o[rt][dt] *= alpha;
-        o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vf[dt]), pf, o[rt][dt],
-                                                              0, 0, 0);
-      }
-    }
-  }
-
-  // merge the 4 waves, one 16-row tile at a time
-  __shared__ float s_o[4][kD][17];
-  __shared__ float s_m[4][16], s_l[4][16];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    float lsum = l_run[rt];
-    lsum += __shfl_xor(lsum, 16);
-    lsum += __shfl_xor(lsum, 32);
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) s_o[wave][16 * dt + 4 * g + i][r16] = o[rt][dt][i];
-    if (g == 0) {
-      s_m[wave][r16] = m_run[rt];
-      s_l[wave][r16] = lsum;
-    }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < 16 * kD; idx += 256) {
-      const int qr16 = idx / kD, d = idx % kD;
-      const int qr = rt * 16 + qr16;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) mx = fmaxf(mx, s_m[w][qr16]);
-      float acc = 0.f, wsum = 0.f;
-      if (mx != -INFINITY) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float f = (s_m[w][qr16] == -INFINITY) ? 0.f : exp2f(s_m[w][qr16] - mx);
-          wsum += f * s_l[w][qr16];
-          acc += f * s_o[w][d][qr16];
-        }
-      }
-      if (qr < R) {
-        if (nsplit == 1) {
-          const int i = qr / G, hh = qr % G;
-          a.out[((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
-        } else {
-          const size_t base = ((size_t)pair * nsplit + split) * (RT * 16) + qr;
-          a.part_o[base * kD + d] = acc;
-          if (d == 0) {
-            a.part_ml[base * 2] = mx;
-            a.part_ml[base * 2 + 1] = wsum;
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-}
-
-// LDS-staged variant for long contexts and many query rows.  The workgroup
+// The workgroup
 // streams its KV range in chunks of kCB blocks: all 256 threads load the next
 // chunk (coalesced 16-byte pieces) while the current one is multiplied out of
 // LDS, so one chunk per workgroup is always in flight.  Waves are split into
@@ -616,19 +447,10 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
           static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv, x.blocks_per_split,
           (float)(1.4426950408889634 / sqrt((double)kD))};
   dim3 grid(x.B * x.Hkv, x.nsplit);
-  if (x.variant == 1) {
-    switch (RT) {
-      case 1: hipLaunchKernelGGL(attn_bf16_kernel<1>, grid, dim3(256), 0, s, a); break;
-      case 2: hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(256), 0, s, a); break;
-      case 3: hipLaunchKernelGGL(attn_bf16_kernel<3>, grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL(attn_bf16_kernel<4>, grid, dim3(256), 0, s, a); break;
-    }
-  } else {
-    switch (RT) {
-      case 1: hipLaunchKernelGGL(attn_lds_kernel<1>, grid, dim3(256), 0, s, a); break;
-      case 2: hipLaunchKernelGGL(attn_lds_kernel<2>, grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL(attn_lds_kernel<4>, grid, dim3(256), 0, s, a); break;
-    }
+  switch (RT) {
+    case 1: hipLaunchKernelGGL(attn_lds_kernel<1>, grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL(attn_lds_kernel<2>, grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL(attn_lds_kernel<4>, grid, dim3(256), 0, s, a); break;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || x.nsplit == 1) return e;

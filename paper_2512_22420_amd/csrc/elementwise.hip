@@ -111,11 +111,14 @@ template <typename T>
 __global__ __launch_bounds__(256) void rope_window_kernel(const float* __restrict__ qkv,
                                                           const int32_t* __restrict__ ctx, int T_, int H,
                                                           int Hkv, int D, RopeFreq f, T* __restrict__ q_out,
-                                                          T* __restrict__ win_k, T* __restrict__ win_v) {
+                                                          T* __restrict__ win_k, T* __restrict__ win_v,
+                                                          int32_t* __restrict__ ctx_snap) {
   const int half = D / 2;
   const int hpb = blockDim.x / half;  // heads per workgroup
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   const int hd = blockIdx.y * hpb + threadIdx.x / half, j = threadIdx.x % half;
+  // the positions this step uses, for the KV append that follows it
+  if (ctx_snap && i == 0 && blockIdx.y == 0 && threadIdx.x == 0) ctx_snap[b] = ctx[b];
   if (hd >= H + 2 * Hkv) return;
   const float* src = qkv + (size_t)row * (H + 2 * Hkv) * D + (size_t)hd * D;
   if (hd < H + Hkv) {
@@ -160,52 +163,52 @@ struct PagePtrs {
   void* v[kMaxAppendLayers];
 };
 
-// grid (B, layers of this launch): copy window rows 0..n_b of one layer into
-// their slots, one element per thread step.
+// KV append.  grid (pieces, B, layers of this launch): one thread per (window
+// row j, KV head g, 16-byte group of head dims) of one sequence and layer; rows
+// past n_b exit at once.  K is copied as one 16-byte vector (the page row is
+// contiguous), V element by element (pages keep V dim-major inside a block).
+// Positions come from the context lengths the verify step read (its RoPE
+// positions); the last launch also moves context_lens[b] past the new rows.
 template <typename T>
-__global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int layer0, const T* __restrict__ win_k,
-                                                        const T* __restrict__ win_v,
+__global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int layer0, int last_launch,
+                                                        const T* __restrict__ win_k, const T* __restrict__ win_v,
                                                         const int32_t* __restrict__ table, int max_blocks,
-                                                        int num_blocks, const int32_t* __restrict__ ctx,
-                                                        const int32_t* __restrict__ acc, int B, int k, int Hkv,
-                                                        int D, int* __restrict__ err) {
-  const int b = blockIdx.x, lc = blockIdx.y, l = layer0 + lc;
-  const int n = acc[b], c = ctx[b];
+                                                        int num_blocks, const int32_t* __restrict__ ctx_snap,
+                                                        int32_t* __restrict__ ctx, const int32_t* __restrict__ acc,
+                                                        int B, int k, int Hkv, int D, int* __restrict__ err) {
+  constexpr int EV = 16 / sizeof(T);  // elements per 16-byte group
+  const int b = blockIdx.y, lc = blockIdx.z, l = layer0 + lc;
+  const int groups = D / EV, u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= (k + 1) * Hkv * groups) return;
+  const int j = u / (Hkv * groups), rem = u % (Hkv * groups), g = rem / groups, e0 = (rem % groups) * EV;
+  const int n = acc[b], c = ctx_snap[b];
+  const bool lead = u == 0 && lc == 0;
   if (n < 0 || n > k) {
-    if (threadIdx.x == 0 && lc == 0) flag_error(err, kErrAccept);
+    if (lead) flag_error(err, kErrAccept);
     return;
   }
   if (c < 0 || c + k + 1 > max_blocks * kBlock) {
-    if (threadIdx.x == 0 && lc == 0) flag_error(err, kErrContext);
+    if (lead) flag_error(err, kErrContext);
     return;
   }
+  if (u == 0 && last_launch) ctx[b] = c + n + 1;
+  if (j > n) return;
+  const int pos = c + j;
+  const int phys = table[(size_t)b * max_blocks + pos / kBlock];
+  if (phys < 0 || phys >= num_blocks) {
+    flag_error(err, kErrBlock);
+    return;
+  }
+  const int slot = pos % kBlock;
   T* kp = static_cast<T*>(pages.k[lc]);
   T* vp = static_cast<T*>(pages.v[lc]);
-  const size_t wbase = ((size_t)l * B + b) * Hkv;
-  const int per_row = Hkv * D, total = (n + 1) * per_row;
-#pragma unroll 4
-  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
-    const int j = idx / per_row, rem = idx % per_row, g = rem / D, dd = rem % D;
-    const int pos = c + j;
-    const int phys = table[(size_t)b * max_blocks + pos / kBlock];
-    if (phys < 0 || phys >= num_blocks) {
-      flag_error(err, kErrBlock);
-      continue;
-    }
-    const int slot = pos % kBlock;
-    kp[(((size_t)phys * Hkv + g) * kBlock + slot) * D + dd] = win_k[((wbase + g) * kBlock + j) * D + dd];
-    vp[(((size_t)phys * Hkv + g) * D + dd) * kBlock + slot] = win_v[((wbase + g) * D + dd) * kBlock + j];
-  }
-}
-
-// context_lens[b] += n_b + 1, after every layer's append (a separate launch).
-__global__ void ctx_update_kernel(int32_t* __restrict__ ctx, const int32_t* __restrict__ acc, int B, int k,
-                                  int max_blocks) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  const int n = acc[b], c = ctx[b];
-  if (n < 0 || n > k || c < 0 || c + k + 1 > max_blocks * kBlock) return;
-  ctx[b] = c + n + 1;
+  const size_t wb = ((size_t)l * B + b) * Hkv + g;
+  *reinterpret_cast<u32x4*>(kp + (((size_t)phys * Hkv + g) * kBlock + slot) * D + e0) =
+      *reinterpret_cast<const u32x4*>(win_k + (wb * kBlock + j) * D + e0);
+  const T* vs = win_v + (wb * D + e0) * kBlock + j;
+  T* vd = vp + (((size_t)phys * Hkv + g) * D + e0) * kBlock + slot;
+#pragma unroll
+  for (int e = 0; e < EV; ++e) vd[(size_t)e * kBlock] = vs[(size_t)e * kBlock];
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
@@ -241,7 +244,7 @@ hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, 
 }
 
 hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv, int D,
-                              float theta, void* q_out, void* win_k, void* win_v, hipStream_t s) {
+                              float theta, void* q_out, void* win_k, void* win_v, int32_t* ctx_snap, hipStream_t s) {
   RopeFreq f{};
   const int half = D / 2;
   for (int j = 0; j < half && j < kMaxHalfDim; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / D);
@@ -249,35 +252,37 @@ hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, i
   dim3 grid(B * T, (H + 2 * Hkv + hpb - 1) / hpb), block(hpb * half);
   if (dtype == kF32)
     hipLaunchKernelGGL(rope_window_kernel<float>, grid, block, 0, s, qkv, ctx, T, H, Hkv, D, f,
-                       static_cast<float*>(q_out), static_cast<float*>(win_k), static_cast<float*>(win_v));
+                       static_cast<float*>(q_out), static_cast<float*>(win_k), static_cast<float*>(win_v), ctx_snap);
   else
     hipLaunchKernelGGL(rope_window_kernel<bf16_t>, grid, block, 0, s, qkv, ctx, T, H, Hkv, D, f,
-                       static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(win_k), static_cast<bf16_t*>(win_v));
+                       static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(win_k), static_cast<bf16_t*>(win_v), ctx_snap);
   return hipGetLastError();
 }
 
 hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s) {
+  const int ev = a.dtype == kF32 ? 4 : 8;
+  const int pieces = (a.k + 1) * a.Hkv * (a.D / ev);
   for (int l0 = 0; l0 < a.L; l0 += kMaxAppendLayers) {
     const int nl = (a.L - l0 < kMaxAppendLayers) ? a.L - l0 : kMaxAppendLayers;
+    const int last = l0 + nl == a.L;
     PagePtrs p{};
     for (int i = 0; i < nl; ++i) {
       p.k[i] = a.k_pages[l0 + i];
       p.v[i] = a.v_pages[l0 + i];
     }
+    const dim3 grid((pieces + 255) / 256, a.B, nl);
     if (a.dtype == kF32)
-      hipLaunchKernelGGL(kv_append_kernel<float>, dim3(a.B, nl), dim3(256), 0, s, p, l0,
+      hipLaunchKernelGGL(kv_append_kernel<float>, grid, dim3(256), 0, s, p, l0, last,
                          static_cast<const float*>(a.win_k), static_cast<const float*>(a.win_v), a.block_table,
-                         a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
+                         a.max_blocks, a.num_blocks, a.ctx_snap, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
     else
-      hipLaunchKernelGGL(kv_append_kernel<bf16_t>, dim3(a.B, nl), dim3(256), 0, s, p, l0,
+      hipLaunchKernelGGL(kv_append_kernel<bf16_t>, grid, dim3(256), 0, s, p, l0, last,
                          static_cast<const bf16_t*>(a.win_k), static_cast<const bf16_t*>(a.win_v), a.block_table,
-                         a.max_blocks, a.num_blocks, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
+                         a.max_blocks, a.num_blocks, a.ctx_snap, a.ctx, a.accepted_len, a.B, a.k, a.Hkv, a.D, a.err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(ctx_update_kernel, dim3((a.B + 255) / 256), dim3(256), 0, s, a.ctx, a.accepted_len, a.B, a.k,
-                     a.max_blocks);
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s) {

@@ -73,8 +73,10 @@ constexpr int kMaxHalfDim = 256;
 struct RopeFreq {
   double inv_freq[kMaxHalfDim];  // theta^(-2j/D)
 };
+// ctx_snap (nullable): receives ctx[b], the positions the KV append uses.
 hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv,
-                              int D, float theta, void* q_out, void* win_k, void* win_v, hipStream_t s);
+                              int D, float theta, void* q_out, void* win_k, void* win_v, int32_t* ctx_snap,
+                              hipStream_t s);
 
 struct AttnArgs {
   int dtype;
@@ -92,7 +94,6 @@ struct AttnArgs {
   int nsplit, blocks_per_split;
   void* out;            // [M][H*D]
   int* err;
-  int variant = 0;      // bf16 path: 0 LDS-staged chunks, 1 direct-to-register blocks
 };
 // Number of KV splits the bf16 path uses, and the partial buffer floats it needs.
 void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, int* blocks_per_split);
@@ -123,9 +124,10 @@ struct KvAppendArgs {
   const void* win_v;         // [L][B][Hkv][D][16]
   const int32_t* block_table;
   int max_blocks, num_blocks;
-  int32_t* ctx;
+  const int32_t* ctx_snap;   // [B] context lengths the verify step read
+  int32_t* ctx;              // [B] set to ctx_snap + n + 1
   const int32_t* accepted_len;
-  int L, B, k, Hkv, D;
+  int L, B, k, Hkv, D;       // D % 8 == 0
   int* err;
 };
 hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s);
