@@ -89,17 +89,23 @@ typedef struct nj_model_desc {
   int32_t dtype;      /* NJ_F32 or NJ_BF16      */
 } nj_model_desc;
 
+/*
+ * Weight matrices (w_qkv, w_o, w_gate_up, w_down, lm_head) are [N][K] with
+ * y = x . w^T.  fp32 models pass them row-major.  bf16 models pass them in
+ * the packed layout written by nightjar_pack_weight (see there); the
+ * embedding and the norm gains are always plain arrays.
+ */
 typedef struct nj_layer_weights {
   const void* attn_norm; /* [d]                    */
   const void* w_qkv;     /* [(H+2Hkv)*D][d]        */
   const void* w_o;       /* [d][H*D]               */
   const void* ffn_norm;  /* [d]                    */
-  const void* w_gate_up; /* [2F][d]                */
+  const void* w_gate_up; /* [2F][d]: gate rows, then up rows */
   const void* w_down;    /* [d][F]                 */
 } nj_layer_weights;
 
 typedef struct nj_weights {
-  const void* embed;              /* device [V][d]                      */
+  const void* embed;              /* device [V][d] row-major            */
   const void* final_norm;         /* device [d]                         */
   const void* lm_head;            /* device [V][d]                      */
   const nj_layer_weights* layers; /* host array of n_layers; entries are device pointers */
@@ -216,6 +222,25 @@ int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_
                     int32_t* accepted_len, int32_t* next_tokens, void* workspace, size_t workspace_bytes,
                     void* stream);
 
+/*
+ * Packed layout of a bf16 weight matrix w [N][K] (K % 32 == 0), the form in
+ * which the bf16 GEMMs read their weights (a layout choice of this library,
+ * not of the method: every load instruction of the GEMM kernels reads 1 KB of
+ * contiguous memory).  Rows are taken in groups of 128 (the last group padded
+ * with zero rows); a group is K/32 consecutive k-steps; a k-step is 8 tiles of
+ * 16 rows x 32 k; a tile is 1 KB, element (r, c) of the tile at position
+ * ((c / 8) * 16 + r) * 8 + c % 8.  So element (n, k) lands at
+ *   ((((n / 128) * (K / 32) + k / 32) * 8 + (n / 16) % 8) * 64
+ *     + ((k % 32) / 8) * 16 + n % 16) * 8 + k % 8.
+ * nightjar_packed_weight_elems returns the element count of the packed copy
+ * (0 for bad sizes); nightjar_pack_weight writes it (src row-major [N][K],
+ * dst of packed_weight_elems elements, both device memory, 16-byte aligned,
+ * not overlapping), asynchronously on `stream`.  Returns NJ_OK, NJ_EINVAL
+ * (bad sizes, NULL or misaligned pointers) or NJ_EHIP.
+ */
+size_t nightjar_packed_weight_elems(int32_t N, int32_t K);
+int nightjar_pack_weight(const void* src, void* dst, int32_t N, int32_t K, void* stream);
+
 /* Epilogues of nightjar_gemm. */
 enum {
   NJ_GEMM_STORE = 0,    /* y[m][n] = acc (fp32 out)                                  */
@@ -226,7 +251,8 @@ enum {
 
 /*
  * y = x . w^T with the step's GEMM kernels.  x [M][K] and w [N][K] in `dtype`
- * (NJ_BF16 or NJ_F32), device, 16-byte aligned; y as the epilogue says.
+ * (NJ_BF16 or NJ_F32), device, 16-byte aligned, a bf16 w in the packed layout
+ * of nightjar_pack_weight; y as the epilogue says.
  * M >= 1; for bf16 K % 32 == 0 and the output width % 16 == 0.  workspace:
  * device, 256-byte aligned, at least nightjar_gemm_workspace_bytes(...) bytes,
  * prepared once with nightjar_workspace_init (split-K counters start at zero
@@ -249,7 +275,7 @@ enum {
  * nightjar_gemm with the kernel and the number of K chunks chosen by the
  * caller, for parity tests of every kernel shape and for tuning.  split_k = 0
  * lets the kernel's planner choose; split_k >= 1 is capped so that every chunk
- * has work (256 k per chunk at least for NJ_GEMM_STREAM, 64 for the tiled
+ * has work (128 k per chunk at least for NJ_GEMM_STREAM, 64 for the tiled
  * kernels).  The tiled kernels need K % 64 == 0, and a split run may cover at
  * most 1024 output tiles; otherwise NJ_EINVAL.  Operands, epilogues and errors
  * as in nightjar_gemm; the workspace must hold

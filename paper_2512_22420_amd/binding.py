@@ -67,6 +67,8 @@ _SIGS = {
                                                _vp]),
     "nightjar_gemm_plan_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32, _i32]),
     "nightjar_accept_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
+    "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
 
 
@@ -159,6 +161,17 @@ def gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace
                    stream: int = 0) -> None:
     _check(lib().nightjar_gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace,
                                          workspace_nbytes, stream))
+
+
+def packed_weight_elems(N, K) -> int:
+    n = lib().nightjar_packed_weight_elems(N, K)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def pack_weight(src, dst, N, K, stream: int = 0) -> None:
+    _check(lib().nightjar_pack_weight(src, dst, N, K, stream))
 
 
 def header_functions(header_path: str):

@@ -332,6 +332,25 @@ static int gemm_args_ok(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t 
   return NJ_OK;
 }
 
+size_t nightjar_packed_weight_elems(int32_t N, int32_t K) {
+  if (N < 1 || K < 32 || K % 32) {
+    fail(NJ_EINVAL, "packed weights need N >= 1 and K a positive multiple of 32");
+    return 0;
+  }
+  return packed_weight_elems(N, K);
+}
+
+int nightjar_pack_weight(const void* src, void* dst, int32_t N, int32_t K, void* stream) {
+  if (nightjar_packed_weight_elems(N, K) == 0) return NJ_EINVAL;
+  if (!src || !dst) return fail(NJ_EINVAL, "NULL pointer");
+  if (!aligned16(src) || !aligned16(dst)) return fail(NJ_EINVAL, "pointers must be 16-byte aligned");
+  const uintptr_t s0 = (uintptr_t)src, s1 = s0 + (size_t)N * K * 2, d0 = (uintptr_t)dst,
+                  d1 = d0 + packed_weight_elems(N, K) * 2;
+  if (s0 < d1 && d0 < s1) return fail(NJ_EINVAL, "src and dst overlap");
+  const hipError_t e = launch_pack_weight(src, dst, N, K, (hipStream_t)stream);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "pack_weight");
+}
+
 size_t nightjar_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue) {
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return 0;
   if (dtype != NJ_BF16) return kAlign;

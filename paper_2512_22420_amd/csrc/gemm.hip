@@ -4,27 +4,37 @@
 // is 1..~768 while N*K reaches 5e8 (LM head), so below M ~ 300 the work is
 // bound by reading each weight byte once from HBM.
 //
-// - Each wave owns 16 weight rows -- the A operand of v_mfma_f32_16x16x32_bf16
-//   -- and streams them along K with 16-byte loads, eight 32-wide k-steps per
-//   stage, with the next stage's loads in flight while the current one is
-//   multiplied (two register buffers, no copies between them).
+// Weights are read in the packed layout of pack_weight_kernel (below): 128-row
+// groups, each one contiguous run of K/32 k-steps, each k-step 8 row tiles of
+// 16 rows x 32 k, and each tile exactly the 1 KB that the 64 lanes of a wave
+// load as the A operand of v_mfma_f32_16x16x32_bf16 (lane l: row l & 15,
+// k (l >> 4) * 8 .. +8).  So every weight load instruction reads 1 KB
+// contiguous, the 8 waves of a workgroup read 8 KB contiguous per k-step, and
+// each workgroup streams one contiguous region -- the access pattern that
+// gets closest to the HBM read ceiling on this part (a row-major matrix read
+// in 16-row tiles leaves ~10% of the bandwidth unused).
+//
+// - Each wave owns one 16-row weight tile (gate and up tiles are two waves of
+//   one workgroup for SwiGLU) and streams it along K in stages of 4 k-steps,
+//   with the next stage's loads in flight while the current one is
+//   multiplied (two register sets, a branch-free loop: stages past the end of
+//   the K range re-read the last stage and see zero activations).
 // - The activation rows (B operand, M padded to 16) are staged per stage in
-//   LDS, loaded once per workgroup and shared by all its waves (4 or 8), with
-//   a 16-byte row pad against bank conflicts.  Reading them from L2 per wave
-//   instead costs half the bandwidth at M = 48.
-// - When 16-row tiles alone give too few workgroups to fill 256 CUs (small N),
+//   LDS, loaded once per workgroup and shared by its 8 waves.  The x loads of
+//   a stage are issued before its weight loads, so the wait that puts x into
+//   LDS never waits for weight loads issued after it.
+// - When the tiles alone give too few workgroups to fill 256 CUs (small N),
 //   K is split across workgroups: each writes an fp32 partial, and the last
 //   workgroup of a tile to arrive (device-scope counter) adds the partials in
 //   chunk order and applies the epilogue, so results do not depend on arrival
 //   order.  Counters reset themselves for the next launch.
 // - Epilogues: store fp32, add into the fp32 residual stream, or SwiGLU
-//   (gate rows n and up rows Nout + n are two row groups of the same wave)
+//   (the up waves hand their accumulators to the gate waves through LDS),
 //   stored as bf16.
 //
-// Operand layout (16x16x32 bf16): lane l supplies row (l & 15) of A and
-// column (l & 15) of B, eight consecutive k of k-group (l >> 4); the result
-// lane l holds rows 4*(l >> 4) + i, column l & 15.  Any k permutation applied
-// to both operands leaves the product unchanged.
+// Result layout (16x16x32 bf16): lane l holds weight rows 4*(l >> 4) + i,
+// x row l & 15.  Any k permutation applied to both operands leaves the
+// product unchanged.
 #include <algorithm>
 #include <cmath>
 
@@ -34,258 +44,211 @@
 namespace nj {
 namespace {
 
-constexpr int kU = 8;                     // 32-wide k-steps per stage
-constexpr int kStageK = 32 * kU;          // 256
-constexpr int kRowStride = kStageK + 8;   // LDS row stride in elements (+16 bytes)
+constexpr int kSU = 4;                   // 32-wide k-steps per stage
+constexpr int kSK = 32 * kSU;            // 128 k per stage
+constexpr int kXStride = kSK + 8;        // LDS row stride in elements (+16 bytes)
+constexpr int kNW = 8;                   // waves per workgroup
+constexpr int kTileMinRows = 64;         // windows of at least this many rows may use the LDS-tiled kernel
 constexpr int kSplitTargetWorkgroups = 256;
-// windows of at least this many rows may use the LDS-tiled kernel
-constexpr int kTileMinRows = 64;
-
-__device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
-}
 
 __device__ __forceinline__ float silu_mul(float gte, float up) { return gte / (1.0f + expf(-gte)) * up; }
 
 struct GemmK {
   const bf16_t* X;
-  const bf16_t* W;
+  const bf16_t* W;  // packed
   void* Y;
-  float* part;    // [nkc][M][NG][Nout] fp32 partials (split K only)
-  int* counters;  // [mblocks][ntiles] arrival counters (split K only), zero between launches
-  int M, Nout, K, stages_per_chunk;
+  float* part;      // [nkc][M][N] fp32 partials (split K only; column = weight row)
+  int* counters;    // [mblocks][gridDim.x] arrival counters (split K only), zero between launches
+  int M, Nout, K, KS, stages_per_chunk;
   int part_bytes;
 };
 
-// MT: 16-row x tiles per workgroup; NG: weight row groups (2 for SwiGLU);
-// NW: waves per workgroup (each owns 16 weight rows of every group).
-// FULL: K % 256 == 0 and every wave owns 16 real weight rows, so the stage loop
-// needs no guards at all; the prefetch of the stage after the last one simply
-// re-reads the last one (an L1/L2 hit).  Branches inside the loop would make
-// the compiler drain all outstanding loads at every join.
-template <int MT, int NG, int NW, int EPI, int DEPTH, bool FULL>
-__global__ __launch_bounds__(NW * 64) void gemm_bf16_kernel(GemmK a) {
-  constexpr int ROWS = MT * 16, NTH = NW * 64;
-  constexpr int CHUNKS = ROWS * kStageK / 8;  // 16-byte pieces of one x stage
-  constexpr int PER_T = (CHUNKS + NTH - 1) / NTH;
-  __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kRowStride];
+template <int MT, int EPI>
+__global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
+  constexpr int NG = EPI == kEpiSwiglu ? 2 : 1;
+  constexpr int TPW = kNW / NG;                   // output tiles per workgroup
+  constexpr int ROWS = MT * 16, NTH = kNW * 64;
+  constexpr int CH = ROWS * (kSK / 8);            // 16-byte x pieces per stage
+  constexpr int PT = (CH + NTH - 1) / NTH;
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kXStride];
   __shared__ int s_last;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const int tile = blockIdx.x, mb = blockIdx.y, kc = blockIdx.z, nkc = gridDim.z;
-  const int M = a.M, Nout = a.Nout, K = a.K;
-  const int n0 = (tile * NW + wave) * 16;
+  const int M = a.M, Nout = a.Nout, K = a.K, KS = a.KS;
+  const int mb = blockIdx.y, kc = blockIdx.z, nkc = gridDim.z;
   const int m0 = mb * ROWS;
-  const bool active = n0 < Nout;
-  const int S = K / 32;
-  const int nst = (S + kU - 1) / kU;
+  const int nto = Nout / 16;                       // output tiles
+  const int otile = blockIdx.x * TPW + wave % TPW;
+  const bool active = otile < nto;
+  const int half = NG == 1 ? 0 : wave / TPW;       // 0: gate (or plain) tile, 1: up tile
+  const int wtile = half * nto + min(otile, nto - 1);
+  const bf16_t* wp = a.W + ((size_t)(wtile >> 3) * KS * 8 + (wtile & 7)) * 512 + lane * 8;
+
+  const int nst = (KS + kSU - 1) / kSU;
   const int st0 = kc * a.stages_per_chunk, st1 = min(nst, st0 + a.stages_per_chunk);
+  const int last = st1 - 1;
 
-  const int nrow = min(n0 + r, Nout - 1);
-  const bf16_t* wp[NG];
+  // this thread's x pieces: row, 8-element column of the stage
+  const bf16_t* xp[PT];
+  int xo[PT], xc[PT];
 #pragma unroll
-  for (int q = 0; q < NG; ++q) wp[q] = a.W + (size_t)(q * Nout + nrow) * K + g * 8;
+  for (int c = 0; c < PT; ++c) {
+    const int idx = min((int)threadIdx.x + c * NTH, CH - 1);  // surplus threads repeat the last piece
+    const int row = idx / (kSK / 8), col = (idx % (kSK / 8)) * 8;
+    xp[c] = a.X + (size_t)min(m0 + row, M - 1) * K;
+    xc[c] = col;
+    xo[c] = row * kXStride + col;
+  }
 
-  f32x4 acc[MT][NG];
+  f32x4 acc[MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4 xr[2][PT];
+  bf16x8 wb[2][kSU];
+
+  auto loadx = [&](auto setc, int st) {
+    constexpr int set = decltype(setc)::value;
 #pragma unroll
-    for (int q = 0; q < NG; ++q) acc[mt][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  u32x4 xr[PER_T];
-  bf16x8 wbuf[DEPTH + 1][NG][kU];
-
-#define NJ_GLOAD_X(st)                                                                           \
-  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
-    const int idx = threadIdx.x + c * NTH;                                                       \
-    if (idx < CHUNKS) {                                                                          \
-      const int row = idx / (kStageK / 8), kk = (st) * kStageK + (idx % (kStageK / 8)) * 8;      \
-      xr[c] = kk < K ? *reinterpret_cast<const u32x4*>(a.X + (size_t)min(m0 + row, M - 1) * K + kk) \
-                     : u32x4{0u, 0u, 0u, 0u};                                                    \
-    }                                                                                            \
-  }
-#define NJ_SSTORE_X(buf)                                                                         \
-  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
-    const int idx = threadIdx.x + c * NTH;                                                       \
-    if (idx < CHUNKS) {                                                                          \
-      const int row = idx / (kStageK / 8), col = (idx % (kStageK / 8)) * 8;                      \
-      *reinterpret_cast<u32x4*>(&xs[buf][row * kRowStride + col]) = xr[c];                       \
-    }                                                                                            \
-  }
-#define NJ_LOAD_W(B, st)                                                                         \
-  if (active) {                                                                                  \
-    _Pragma("unroll") for (int u = 0; u < kU; ++u) {                                             \
-      if ((st) * kU + u < S) {                                                                   \
-        _Pragma("unroll") for (int q = 0; q < NG; ++q) wbuf[B][q][u] = ld8(wp[q] + ((st) * kU + u) * 32); \
-      }                                                                                          \
-    }                                                                                            \
-  }
-#define NJ_COMPUTE(B, buf, st)                                                                   \
-  if (active) {                                                                                  \
-    _Pragma("unroll") for (int u = 0; u < kU; ++u) {                                             \
-      if ((st) * kU + u < S) {                                                                   \
-        _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                      \
-          const bf16x8 xv = __builtin_bit_cast(                                                  \
-              bf16x8, *reinterpret_cast<const u32x4*>(&xs[buf][(mt * 16 + r) * kRowStride + u * 32 + g * 8])); \
-          _Pragma("unroll") for (int q = 0; q < NG; ++q) acc[mt][q] =                            \
-              __builtin_amdgcn_mfma_f32_16x16x32_bf16(wbuf[B][q][u], xv, acc[mt][q], 0, 0, 0);   \
-        }                                                                                        \
-      }                                                                                          \
-    }                                                                                            \
-  }
-  // One stage: stage st+1's x (global -> registers) and the w loads of stage
-  // st+DEPTH go out, stage st is multiplied, stage st+1's x goes to the other
-  // LDS buffer.  w stage s lives in register buffer s % (DEPTH + 1).
-#define NJ_STAGE(B, BN)                                       \
-  {                                                           \
-    const bool more = st + 1 < st1;                           \
-    if (more) NJ_GLOAD_X(st + 1);                             \
-    if (st + DEPTH < st1) NJ_LOAD_W(BN, st + DEPTH);          \
-    NJ_COMPUTE(B, (st - st0) & 1, st);                        \
-    if (more) NJ_SSTORE_X((st + 1 - st0) & 1);                \
-    __syncthreads();                                          \
-    ++st;                                                     \
-    if (st >= st1) break;                                     \
-  }
-
-  if constexpr (FULL) {
-    // branch-free stage loop (ping-pong over two w register buffers and two x LDS buffers)
-#define NJ_FGLOAD_X(st)                                                                          \
-  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
-    const int idx = threadIdx.x + c * NTH;                                                       \
-    const int row = idx / (kStageK / 8), kk = (st) * kStageK + (idx % (kStageK / 8)) * 8;        \
-    xr[c] = *reinterpret_cast<const u32x4*>(a.X + (size_t)min(m0 + row, M - 1) * K + kk);        \
-  }
-#define NJ_FSSTORE_X(buf)                                                                        \
-  _Pragma("unroll") for (int c = 0; c < PER_T; ++c) {                                            \
-    const int idx = threadIdx.x + c * NTH;                                                       \
-    const int row = idx / (kStageK / 8), col = (idx % (kStageK / 8)) * 8;                        \
-    *reinterpret_cast<u32x4*>(&xs[buf][row * kRowStride + col]) = xr[c];                         \
-  }
-#define NJ_FLOAD_W(B, st)                                                                        \
-  _Pragma("unroll") for (int u = 0; u < kU; ++u)                                                 \
-    _Pragma("unroll") for (int q = 0; q < NG; ++q) wbuf[B][q][u] = ld8(wp[q] + ((st) * kU + u) * 32);
-#define NJ_FCOMPUTE(B, buf)                                                                      \
-  _Pragma("unroll") for (int u = 0; u < kU; ++u) {                                               \
-    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) {                                          \
-      const bf16x8 xv = __builtin_bit_cast(                                                      \
-          bf16x8, *reinterpret_cast<const u32x4*>(&xs[buf][(mt * 16 + r) * kRowStride + u * 32 + g * 8])); \
-      _Pragma("unroll") for (int q = 0; q < NG; ++q) acc[mt][q] =                                \
-          __builtin_amdgcn_mfma_f32_16x16x32_bf16(wbuf[B][q][u], xv, acc[mt][q], 0, 0, 0);       \
-    }                                                                                            \
-  }
-    static_assert(CHUNKS % NTH == 0, "x stage must split evenly over the workgroup");
-    NJ_FGLOAD_X(st0);
-    NJ_FLOAD_W(0, st0);
-    NJ_FSSTORE_X(0);
-    __syncthreads();
-    for (int st = st0; st < st1; st += 2) {
-      const int s1 = min(st + 1, st1 - 1);
-      NJ_FGLOAD_X(s1);
-      NJ_FLOAD_W(1, s1);
-      __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the multiplies
-      NJ_FCOMPUTE(0, 0);
-      NJ_FSSTORE_X(1);
-      __syncthreads();
-      if (st + 1 >= st1) break;
-      const int s2 = min(st + 2, st1 - 1);
-      NJ_FGLOAD_X(s2);
-      NJ_FLOAD_W(0, s2);
-      __builtin_amdgcn_sched_barrier(0);
-      NJ_FCOMPUTE(1, 1);
-      NJ_FSSTORE_X(0);
-      __syncthreads();
+    for (int c = 0; c < PT; ++c)
+      xr[set][c] = *reinterpret_cast<const u32x4*>(xp[c] + min(st * kSK + xc[c], K - 8));
+  };
+  auto loadw = [&](auto setc, int st) {
+    constexpr int set = decltype(setc)::value;
+#pragma unroll
+    for (int u = 0; u < kSU; ++u)
+      wb[set][u] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wp + (size_t)min(st * kSU + u, KS - 1) * 4096));
+  };
+  // x of stage st into LDS buffer buf; zero past the chunk or past K
+  auto storex = [&](auto setc, int buf, int st) {
+    constexpr int set = decltype(setc)::value;
+#pragma unroll
+    for (int c = 0; c < PT; ++c) {
+      const uint32_t keep = 0u - (uint32_t)(st < st1 && st * kSK + xc[c] < K);  // all ones or zero
+      *reinterpret_cast<u32x4*>(&xs[buf][xo[c]]) = xr[set][c] & keep;
     }
-#undef NJ_FGLOAD_X
-#undef NJ_FSSTORE_X
-#undef NJ_FLOAD_W
-#undef NJ_FCOMPUTE
-  } else if (st0 < st1) {
-    NJ_GLOAD_X(st0);
-    NJ_LOAD_W(0, st0);
-    if (DEPTH > 1 && st0 + 1 < st1) NJ_LOAD_W(1 % (DEPTH + 1), st0 + 1);
-    NJ_SSTORE_X(0);
+  };
+  auto compute = [&](auto setc, int buf) {
+    constexpr int set = decltype(setc)::value;
+#pragma unroll
+    for (int u = 0; u < kSU; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const bf16x8 xv = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(&xs[buf][(mt * 16 + r) * kXStride + u * 32 + g * 8]));
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb[set][u], xv, acc[mt], 0, 0, 0);
+      }
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  loadx(S0{}, st0);
+  loadw(S0{}, st0);
+  storex(S0{}, 0, st0);
+  __syncthreads();
+  for (int st = st0; st < st1; st += 2) {
+    loadx(S1{}, min(st + 1, last));
+    loadw(S1{}, min(st + 1, last));
+    __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the multiplies
+    compute(S0{}, 0);
+    storex(S1{}, 1, st + 1);
     __syncthreads();
-    int st = st0;
-    if constexpr (DEPTH == 1) {
-      for (;;) {
-        NJ_STAGE(0, 1)
-        NJ_STAGE(1, 0)
-      }
-    } else {
-      for (;;) {
-        NJ_STAGE(0, 2 % (DEPTH + 1))
-        NJ_STAGE(1, 3 % (DEPTH + 1))
-        NJ_STAGE(2 % (DEPTH + 1), 4 % (DEPTH + 1))
-      }
-    }
+    loadx(S0{}, min(st + 2, last));
+    loadw(S0{}, min(st + 2, last));
+    __builtin_amdgcn_sched_barrier(0);
+    compute(S1{}, 1);
+    storex(S0{}, 0, st + 2);
+    __syncthreads();
   }
-#undef NJ_GLOAD_X
-#undef NJ_SSTORE_X
-#undef NJ_LOAD_W
-#undef NJ_COMPUTE
-#undef NJ_STAGE
 
-  const int n = n0 + 4 * g;
+  const int ncol = wtile * 16 + 4 * g;  // weight rows of this lane's results
   if (nkc > 1) {
     // Split K: publish this chunk's partial, and the last chunk to arrive
     // finishes the tile.  Partials are written and read with device-coherent
     // accesses, so the hand-off needs neither an L2 writeback nor an L2
     // invalidate: each thread waits until its partial stores are acknowledged,
     // then one counter increment publishes them.
+    const int Ntot = Nout * NG;
     const __amdgpu_buffer_rsrc_t prs = coherent_rsrc(a.part, a.part_bytes);
-    auto poff = [&](int j, int m, int q) { return (uint32_t)((((size_t)j * M + m) * NG + q) * Nout + n) * 4u; };
+    auto poff = [&](int j, int m) { return (uint32_t)(((size_t)j * M + m) * Ntot + ncol) * 4u; };
     if (active) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = m0 + mt * 16 + r;
-        if (m < M)
-#pragma unroll
-          for (int q = 0; q < NG; ++q) coherent_store(prs, poff(kc, m, q), acc[mt][q]);
+        if (m < M) coherent_store(prs, poff(kc, m), acc[mt]);
       }
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    int* cnt = a.counters + (size_t)mb * gridDim.x + tile;
+    int* cnt = a.counters + (size_t)mb * gridDim.x + blockIdx.x;
     if (threadIdx.x == 0)
       s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nkc - 1);
     __syncthreads();
     if (!s_last) return;
     if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
-    if (!active) return;
     // sum all nkc partials (this workgroup's own included, read back) in chunk order
     for (int j = 0; j < nkc; ++j) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = min(m0 + mt * 16 + r, M - 1);  // rows past M: read in range, dropped below
-#pragma unroll
-        for (int q = 0; q < NG; ++q) {
-          const f32x4 v = coherent_load(prs, poff(j, m, q));
-          acc[mt][q] = j == 0 ? v : acc[mt][q] + v;
-        }
+        const f32x4 v = coherent_load(prs, poff(j, m));
+        acc[mt] = j == 0 ? v : acc[mt] + v;
       }
     }
-  } else if (!active) {
-    return;
   }
 
+  if constexpr (EPI == kEpiSwiglu) {
+    // up waves hand their accumulators to the gate waves (LDS is free: the
+    // stage loop ended on a barrier)
+    f32x4* ex = reinterpret_cast<f32x4*>(&xs[0][0]);
+    static_assert(sizeof(xs) >= (size_t)TPW * MT * 64 * sizeof(f32x4), "exchange does not fit");
+    if (half == 1) {
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = m0 + mt * 16 + r;
-    if (m >= M) continue;
-    if constexpr (EPI == kEpiStore) {
-      *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) = acc[mt][0];
-    } else if constexpr (EPI == kEpiResidual) {
-      f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
-      *p = *p + acc[mt][0];
-    } else {
-      const f32x4 gt = acc[mt][0], up = acc[mt][1];
+      for (int mt = 0; mt < MT; ++mt) ex[((wave - TPW) * MT + mt) * 64 + lane] = acc[mt];
+    }
+    __syncthreads();
+    if (half == 1 || !active) return;
+    const int n = otile * 16 + 4 * g;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = m0 + mt * 16 + r;
+      if (m >= M) continue;
+      const f32x4 gt = acc[mt], up = ex[(wave * MT + mt) * 64 + lane];
       u32x2 o;
       o[0] = pack_bf16x2(silu_mul(gt[0], up[0]), silu_mul(gt[1], up[1]));
       o[1] = pack_bf16x2(silu_mul(gt[2], up[2]), silu_mul(gt[3], up[3]));
       *reinterpret_cast<u32x2*>(static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n) = o;
     }
+  } else {
+    if (!active) return;
+    const int n = otile * 16 + 4 * g;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = m0 + mt * 16 + r;
+      if (m >= M) continue;
+      f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
+      if constexpr (EPI == kEpiStore) *p = acc[mt];
+      else *p = *p + acc[mt];
+    }
+  }
+}
+
+// Packed weight layout: element (n, k) of a [N][K] row-major matrix goes to
+//   ((((n / 128) * (K / 32) + k / 32) * 8 + (n / 16) % 8) * 64 + ((k % 32) / 8) * 16 + n % 16) * 8 + k % 8
+// Rows past N up to the next multiple of 128 are zero.  One thread per
+// 16-byte destination piece.
+__global__ __launch_bounds__(256) void pack_weight_kernel(const bf16_t* __restrict__ src, bf16_t* __restrict__ dst,
+                                                          int N, int K, size_t pieces) {
+  const int KS = K / 32;
+  for (size_t p = (size_t)blockIdx.x * 256 + threadIdx.x; p < pieces; p += (size_t)gridDim.x * 256) {
+    const int lane = (int)(p & 63), t = (int)((p >> 6) & 7);
+    const size_t q = p >> 9;
+    const int ks = (int)(q % KS);
+    const size_t grp = q / KS;
+    const size_t n = grp * 128 + t * 16 + (lane & 15);
+    const int k = ks * 32 + (lane >> 4) * 8;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (n < (size_t)N) v = *reinterpret_cast<const u32x4*>(src + n * K + k);
+    *reinterpret_cast<u32x4*>(dst + p * 8) = v;
   }
 }
 
@@ -318,35 +281,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
-template <int MT, int NG, int NW, int EPI>
-hipError_t launch_cfg(const GemmK& a, const GemmPlan& p, hipStream_t s) {
-  const dim3 grid(p.ntiles, p.mblocks, p.nkc), block(NW * 64);
-  const bool full = a.K % kStageK == 0 && (a.Nout / 16) % NW == 0 && a.Nout % 16 == 0;
-  if (full)
-    hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI, 1, true>), grid, block, 0, s, a);
-  else if (NG == 1 && p.depth == 2)
-    hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI, 2, false>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((gemm_bf16_kernel<MT, NG, NW, EPI, 1, false>), grid, block, 0, s, a);
-  return hipGetLastError();
-}
-
-template <int NG, int EPI>
-hipError_t launch_epi(const GemmK& a, const GemmPlan& p, hipStream_t s) {
-  if (p.nw == 4) {
-    switch (p.mt) {
-      case 1: return launch_cfg<1, NG, 4, EPI>(a, p, s);
-      case 2: return launch_cfg<2, NG, 4, EPI>(a, p, s);
-      case 3: return launch_cfg<3, NG, 4, EPI>(a, p, s);
-      default: return launch_cfg<4, NG, 4, EPI>(a, p, s);
-    }
-  }
+template <int EPI>
+hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+  const dim3 grid(p.ntiles, p.mblocks, p.nkc), block(kNW * 64);
   switch (p.mt) {
-    case 1: return launch_cfg<1, NG, 8, EPI>(a, p, s);
-    case 2: return launch_cfg<2, NG, 8, EPI>(a, p, s);
-    case 3: return launch_cfg<3, NG, 8, EPI>(a, p, s);
-    default: return launch_cfg<4, NG, 8, EPI>(a, p, s);
+    case 1: hipLaunchKernelGGL((gemm_stream_kernel<1, EPI>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((gemm_stream_kernel<2, EPI>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((gemm_stream_kernel<3, EPI>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((gemm_stream_kernel<4, EPI>), grid, block, 0, s, a); break;
   }
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -413,7 +357,7 @@ GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile) {
 }
 
 bool tile_fits(int M, int N, int K) {
-  return K % 64 == 0 && (long)M * K < (1L << 31) && (long)N * K < (1L << 31);
+  return K % 64 == 0 && (long)M * K < (1L << 31) && (long)packed_weight_elems(N, K) < (1L << 31);
 }
 
 GemmPlan gemm_plan(int M, int N, int K, int epi) {
@@ -431,20 +375,16 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split) {
   const int Nout = N / NG;
   p.mt = M >= 64 ? 4 : (M + 15) / 16;
   p.mblocks = (M + p.mt * 16 - 1) / (p.mt * 16);
-  const int tiles16 = (Nout + 15) / 16;
-  // 8 waves share each staged x tile when it is large and N is wide enough to
-  // keep 512+ workgroups; otherwise 4 waves (more workgroups)
-  p.nw = (p.mt >= 3 && tiles16 / 8 * p.mblocks >= 512) ? 8 : 4;
-  p.ntiles = (tiles16 + p.nw - 1) / p.nw;
-  const int nst = (K / 32 + kU - 1) / kU;
+  p.nw = kNW;
+  p.ntiles = (Nout / 16 + kNW / NG - 1) / (kNW / NG);
+  const int nst = (K / 32 + kSU - 1) / kSU;
   const long base = (long)p.ntiles * p.mblocks;
-  // Split K until ~256 workgroups run (one per CU), keeping >= 4 stages per
-  // chunk so that the x staging and the partial hand-off are amortised (a
-  // measured sweep over the verify step's shapes puts the optimum there).
+  // Split K until ~256 workgroups run, keeping >= 8 stages (1024 k) per chunk
+  // so that the x staging and the partial hand-off are amortised.
   int nkc = 1;
   if (split > 0) nkc = std::min(split, nst);
   else
-    while (base * nkc * 2 <= kSplitTargetWorkgroups && nst / (nkc * 2) >= 4) nkc *= 2;
+    while (base * nkc * 2 <= kSplitTargetWorkgroups && nst / (nkc * 2) >= 8) nkc *= 2;
   if (split <= 0 && (size_t)nkc * M * N * 4 >= kMaxPartBytes) nkc = 1;
   p.stages_per_chunk = (nst + nkc - 1) / nkc;
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
@@ -460,10 +400,20 @@ hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N,
   if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s);
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.stages_per_chunk, (int)p.part_bytes};
-  if (epi == kEpiStore) return launch_epi<1, kEpiStore>(a, p, s);
-  if (epi == kEpiResidual) return launch_epi<1, kEpiResidual>(a, p, s);
-  return launch_epi<2, kEpiSwiglu>(a, p, s);
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes};
+  if (epi == kEpiStore) return launch_stream<kEpiStore>(a, p, s);
+  if (epi == kEpiResidual) return launch_stream<kEpiResidual>(a, p, s);
+  return launch_stream<kEpiSwiglu>(a, p, s);
+}
+
+size_t packed_weight_elems(int N, int K) { return (size_t)((N + 127) / 128) * 128 * (size_t)K; }
+
+hipError_t launch_pack_weight(const void* src, void* dst, int N, int K, hipStream_t s) {
+  const size_t pieces = packed_weight_elems(N, K) / 8;
+  const int grid = (int)std::min<size_t>((pieces + 255) / 256, 65536);
+  hipLaunchKernelGGL(pack_weight_kernel, dim3(grid), dim3(256), 0, s, static_cast<const bf16_t*>(src),
+                     static_cast<bf16_t*>(dst), N, K, pieces);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,

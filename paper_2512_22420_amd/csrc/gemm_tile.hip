@@ -96,14 +96,26 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     const int idx = threadIdx.x + c * NTH, row = idx / PR;
     xo[c] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)K + (idx % PR) * 8;
   }
+  // Weight pieces come from the packed layout (128-row groups, k-step major,
+  // 1 KB per 16-row x 32-k tile in MFMA lane order): thread piece idx is lane
+  // idx % 64 of k-step (idx / 64) % KSS of 16-row tile idx / (64 * KSS), so
+  // each wave reads whole 1 KB tiles.  Tiles past the edge are clamped to the
+  // last one (computed and never stored).
+  constexpr int KSS = kBK / 32;  // k-steps per stage
+  const int KS = K / 32, nto = Nout / 16;
 #pragma unroll
   for (int c = 0; c < WC; ++c) {
-    const int idx = threadIdx.x + c * NTH, row = idx / PR;
-    int gr;
-    if constexpr (NG == 1) gr = min(n0 + row, Nout - 1);
-    else gr = row < HALF ? min(n0 + row, Nout - 1) : Nout + min(n0 + row - HALF, Nout - 1);
-    wo[c] = (uint32_t)gr * (uint32_t)K + (idx % PR) * 8;
+    const int idx = threadIdx.x + c * NTH;
+    const int t16 = idx / (64 * KSS), ksl = (idx / 64) % KSS, ln = idx % 64;
+    int T;
+    if constexpr (NG == 1) T = min(n0 / 16 + t16, nto - 1);
+    else T = t16 < HALF / 16 ? min(n0 / 16 + t16, nto - 1) : nto + min(n0 / 16 + t16 - HALF / 16, nto - 1);
+    wo[c] = ((uint32_t)(T >> 3) * (uint32_t)KS * 8u + (uint32_t)(T & 7)) * 512u + (uint32_t)ksl * 4096u + ln * 8;
   }
+  auto w_lds = [&](int idx) {  // LDS element offset of weight piece idx
+    const int t16 = idx / (64 * KSS), ksl = (idx / 64) % KSS, ln = idx % 64;
+    return lds_off(t16 * 16 + (ln & 15), ksl * 4 + (ln >> 4));
+  };
 
   // LDS row of weight fragment j of this wave
   auto wrow = [&](int j) {
@@ -129,7 +141,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
 #pragma unroll
     for (int c = 0; c < XC; ++c) xr[set][c] = *reinterpret_cast<const u32x4*>(a.X + (xo[c] + k0));
 #pragma unroll
-    for (int c = 0; c < WC; ++c) wr[set][c] = *reinterpret_cast<const u32x4*>(a.W + (wo[c] + k0));
+    for (int c = 0; c < WC; ++c) wr[set][c] = *reinterpret_cast<const u32x4*>(a.W + (wo[c] + (uint32_t)st * (KSS * 4096u)));
   };
   auto sstore = [&](int set, int buf) {
 #pragma unroll
@@ -138,10 +150,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
       *reinterpret_cast<u32x4*>(&xs[buf][lds_off(idx / PR, idx % PR)]) = xr[set][c];
     }
 #pragma unroll
-    for (int c = 0; c < WC; ++c) {
-      const int idx = threadIdx.x + c * NTH;
-      *reinterpret_cast<u32x4*>(&ws[buf][lds_off(idx / PR, idx % PR)]) = wr[set][c];
-    }
+    for (int c = 0; c < WC; ++c) *reinterpret_cast<u32x4*>(&ws[buf][w_lds(threadIdx.x + c * NTH)]) = wr[set][c];
   };
   auto compute = [&](int buf) {
     constexpr int KS = kBK / 32;

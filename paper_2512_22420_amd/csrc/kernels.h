@@ -14,7 +14,7 @@ enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2 };
 enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
 
 // How the bf16 GEMM splits its work.  Weight-streaming kernel (tile ==
-// kTileNone): 16-row x tiles per workgroup (mt), waves per workgroup (nw),
+// kTileNone): 16-row x tiles per workgroup (mt), waves per workgroup (nw, 8),
 // workgroups along N (ntiles) and M (mblocks).  LDS-tiled kernel: tile shape,
 // ntiles / mblocks output tiles along N and M.  Both: K chunks across
 // workgroups (nkc, stages_per_chunk; a stage is 256 k for the streaming kernel,
@@ -44,14 +44,22 @@ constexpr size_t kGemmCounterBytes = 4096;
 // Split-K partials are addressed with 32-bit buffer offsets.
 constexpr size_t kMaxPartBytes = (size_t)1 << 31;
 
-// y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]).  `counters`
+// bf16 GEMM weights live in a packed layout: 128-row groups, each a run of
+// K/32 k-steps of 8 tiles (16 rows x 32 k, 1 KB, MFMA lane order).  Elements
+// of the packed copy of an [N][K] matrix (rows padded to a multiple of 128),
+// and the kernel that writes it.
+size_t packed_weight_elems(int N, int K);
+hipError_t launch_pack_weight(const void* src, void* dst, int N, int K, hipStream_t s);
+
+// y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]); bf16 w
+// packed, fp32 w row-major.  `counters`
 // (plan.counter_bytes, zero on entry and on exit) and `part`
 // (plan.part_bytes) are scratch; GEMMs that run one after another on a stream
 // may share both as long as the counters are never overwritten by anything else.
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
                        int* counters, float* part, hipStream_t s);
-// bf16 GEMM with an explicit plan (either kernel; for the streaming one nw 4
-// or 8, mt 1..4, any nkc/stages_per_chunk).
+// bf16 GEMM with an explicit plan (either kernel; for the streaming one
+// mt 1..4, any nkc/stages_per_chunk).
 hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s);
 // The LDS-tiled kernel alone (K % 64 == 0).

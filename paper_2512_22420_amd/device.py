@@ -27,6 +27,16 @@ def _ptr(t: Optional[torch.Tensor]) -> int:
     return 0 if t is None else t.data_ptr()
 
 
+def pack_weight(w: torch.Tensor, stream: Optional[int] = None) -> torch.Tensor:
+    """Packed copy (the layout of nightjar_pack_weight) of a bf16 [N][K]
+    weight matrix resident on the device as int16 bits."""
+    N, K = w.shape
+    s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+    out = torch.empty(nb.packed_weight_elems(N, K), dtype=torch.int16, device=w.device)
+    nb.pack_weight(w.data_ptr(), out.data_ptr(), N, K, s)
+    return out
+
+
 def model_desc(shape) -> nb.ModelDesc:
     return nb.ModelDesc(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
                         shape.ffn_dim, shape.vocab, shape.block_size, shape.rms_eps, shape.rope_theta,
@@ -39,11 +49,14 @@ class DeviceModel:
     def __init__(self, shape, weights: Dict, device="cuda"):
         self.shape = shape
         self.desc = model_desc(shape)
+        # bf16 GEMM weights go to the packed layout the GEMM kernels read
+        mat = (lambda a: pack_weight(_to_dev(a, device))) if shape.dtype == "bf16" else (lambda a: _to_dev(a, device))
         self.embed = _to_dev(weights["embed"], device)
         self.final_norm = _to_dev(weights["final_norm"], device)
-        self.lm_head = _to_dev(weights["lm_head"], device)
+        self.lm_head = mat(weights["lm_head"])
         names = ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")
-        self.layers = [{n: _to_dev(lw[n], device) for n in names} for lw in weights["layers"]]
+        self.layers = [{n: (mat(lw[n]) if n.startswith("w_") else _to_dev(lw[n], device)) for n in names}
+                       for lw in weights["layers"]]
         self._c_layers = (nb.LayerWeights * shape.n_layers)(
             *[nb.LayerWeights(*[_ptr(l[n]) for n in names]) for l in self.layers])
         self.c = nb.Weights(_ptr(self.embed), _ptr(self.final_norm), _ptr(self.lm_head),

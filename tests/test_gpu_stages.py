@@ -9,7 +9,7 @@ import torch
 import oracle
 from paper_2512_22420_amd import binding as nb
 from paper_2512_22420_amd import workload as W
-from paper_2512_22420_amd.device import model_desc
+from paper_2512_22420_amd.device import model_desc, pack_weight
 
 from parity import compare
 
@@ -19,6 +19,11 @@ pytestmark = pytest.mark.gpu
 def _dev(a):
     a = np.ascontiguousarray(a)
     return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).cuda()
+
+
+def _devw(w):
+    """A bf16 weight matrix on the device in the packed layout the GEMMs read."""
+    return pack_weight(_dev(w))
 
 
 def _stream():
@@ -42,7 +47,7 @@ def test_gemm_bf16_store(M, N, K):
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     y = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    dx, dw = _dev(x), _dev(w)  # keep the device copies alive across the call
+    dx, dw = _dev(x), _devw(w)  # keep the device copies alive across the call
     _gemm(nb.NJ_BF16, dx, dw, y, M, N, K, nb.NJ_GEMM_STORE)
     ref = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     err = np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max()
@@ -56,7 +61,7 @@ def test_gemm_bf16_residual(M, N, K):
     w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     h0 = rng.standard_normal((M, N), dtype=np.float32)
     y = _dev(h0.copy())
-    dx, dw = _dev(x), _dev(w)
+    dx, dw = _dev(x), _devw(w)
     _gemm(nb.NJ_BF16, dx, dw, y, M, N, K, nb.NJ_GEMM_RESIDUAL)
     ref = h0 + oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     assert np.abs(y.cpu().numpy() - ref).max() / np.abs(ref).max() < 2e-5
@@ -68,7 +73,7 @@ def test_gemm_bf16_swiglu(M, F, K):
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((2 * F, K), dtype=np.float32) * 0.05)
     y = torch.empty((M, F), dtype=torch.int16, device="cuda")
-    dx, dw = _dev(x), _dev(w)
+    dx, dw = _dev(x), _devw(w)
     _gemm(nb.NJ_BF16, dx, dw, y, M, 2 * F, K, nb.NJ_GEMM_SWIGLU)
     gu = oracle.widen(x, "bf16") @ oracle.widen(w, "bf16").T
     ref = oracle.silu(gu[:, :F]) * gu[:, F:]
@@ -133,7 +138,7 @@ def test_gemm_every_kernel_shape(kernel, split, M, N, K, epi):
         y = _dev(y0.copy())
     else:
         y = torch.full((M, Nout), float("nan"), dtype=torch.float32, device="cuda")
-    dx, dw = _dev(x), _dev(w)
+    dx, dw = _dev(x), _devw(w)
     nbytes = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, M, N, K, epi, kernel, split)
     ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     nb.workspace_init(ws.data_ptr(), nbytes, _stream())
@@ -157,7 +162,7 @@ def test_gemm_lm_head_large_window_sampled():
     x = W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
-    dx, dw = _dev(x), _dev(w)
+    dx, dw = _dev(x), _devw(w)
     _gemm(nb.NJ_BF16, dx, dw, y, M, N, K, nb.NJ_GEMM_STORE)
     rows = np.sort(rng.choice(M, 12, replace=False))
     rows[-1] = M - 1
@@ -272,7 +277,7 @@ def test_gemm_split_k_is_deterministic_and_reusable():
     M, N, K = 48, 4096, 14336
     rng = np.random.default_rng(99)
     dx = _dev(W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32)))
-    dw = _dev(W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02))
+    dw = _devw(W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02))
     nbytes = nb.gemm_workspace_bytes(nb.NJ_BF16, M, N, K, nb.NJ_GEMM_STORE)
     ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     nb.workspace_init(ws.data_ptr(), nbytes, _stream())
@@ -286,3 +291,22 @@ def test_gemm_split_k_is_deterministic_and_reusable():
     for y in outs[1:]:
         assert torch.equal(y, outs[0])
     assert not torch.isnan(outs[0]).any()
+
+
+@pytest.mark.parametrize("N,K", [(16, 32), (300, 96), (128, 4096), (2 * 688, 256)])
+def test_pack_weight_layout(N, K):
+    """nightjar_pack_weight against the layout formula of the header, bit for
+    bit, including the zero rows that pad N to a multiple of 128."""
+    rng = np.random.default_rng(N + K)
+    w = rng.integers(0, 1 << 16, size=(N, K), dtype=np.uint16)
+    got = pack_weight(_dev(w)).cpu().numpy().view(np.uint16)
+    npad = (N + 127) // 128 * 128
+    assert got.size == npad * K == nb.packed_weight_elems(N, K)
+    full = np.zeros((npad, K), dtype=np.uint16)
+    full[:N] = w
+    n = np.arange(npad)[:, None]
+    k = np.arange(K)[None, :]
+    idx = ((((n // 128) * (K // 32) + k // 32) * 8 + (n // 16) % 8) * 64 + ((k % 32) // 8) * 16 + n % 16) * 8 + k % 8
+    want = np.empty(npad * K, dtype=np.uint16)
+    want[idx.ravel()] = full.ravel()
+    assert np.array_equal(got, want)
