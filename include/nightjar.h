@@ -268,7 +268,8 @@ enum {
   NJ_GEMM_STREAM = 1,       /* weight-streaming kernel (windows up to ~128 rows)     */
   NJ_GEMM_TILE_256x256 = 2, /* LDS-tiled kernel; output tile = x rows x weight rows  */
   NJ_GEMM_TILE_128x256 = 3,
-  NJ_GEMM_TILE_128x128 = 4
+  NJ_GEMM_TILE_128x128 = 4,
+  NJ_GEMM_STREAM_DEEP = 5   /* weight-streaming kernel, 3 stages in flight per wave  */
 };
 
 /*

@@ -20,7 +20,7 @@ ARCH = "gfx950"
 
 SOURCES = ["api.hip", "gemm.hip", "gemm_tile.hip", "attention.hip", "accept.hip", "elementwise.hip"]
 
-FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall", "-Wno-unused-function",
+FLAGS = ["-O3", "-std=c++20", f"--offload-arch={ARCH}", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 

@@ -3,93 +3,36 @@
 // The test for draft i only needs p_i(x_i) and q_i(x_i), so all k tests are
 // independent; the accepted length n is the index of the first failure.  The
 // draw after it needs a running sum over one full vocabulary row, which is
-// where the bandwidth goes.  Three kernels:
+// where the bandwidth goes.
 //
-//   accept_stats   (rows x 8192-wide chunks): chunk max and sum of exp(l - max).
-//   accept_tiles   (sequences x tile blocks): every workgroup first runs the
-//                  k accept tests of its sequence (u_i < p_i(x_i) / q_i(x_i),
-//                  q == 0 accepts; p from the chunk statistics) to find n, the
-//                  first failure, then sums the draw weights of row n only --
-//                  max(0, p_n - q_n) after a rejection, p_k for the bonus -- in
-//                  fp64 over 256-wide tiles.  The tests are cheap and
-//                  identical in every workgroup of a sequence.
-//   accept_finalize (one wave per sequence): the smallest j whose running sum
-//                  of row n's weights exceeds u_k times their total: a prefix
-//                  scan over lane-contiguous tile sums finds the tile, a prefix
-//                  scan over that tile's 256 weights finds the entry.  All sums
-//                  are fp64 in a fixed order, so the draw is reproducible.
+//   chunk statistics  (max, sum of exp(l - max)) of every 128-wide vocabulary
+//                     chunk of every window row.  The LM-head GEMM writes
+//                     them from its output tile (chunk_stats below is shared);
+//                     accept_stats_kernel computes the same values from logits
+//                     in memory when the GEMM did not.
+//   accept_rows       (one workgroup per window row): row max and 1/sum from
+//                     the chunk statistics, and the accept test of the draft
+//                     the row scores (u_i < p_i(x_i) / q_i(x_i); q == 0
+//                     accepts).
+//   accept_draw       (sequences x tile blocks): n, the first failed test, then
+//                     fp64 sums of the draw weights
+//                     of row n over 256-wide tiles -- max(0, p_n - q_n) after
+//                     a rejection, p_k for the bonus -- and the last workgroup
+//                     of a sequence to finish (device-scope counter) draws:
+//                     the smallest j whose running sum of row n's weights
+//                     exceeds u_k times their total, found by a prefix scan
+//                     over lane-contiguous tile sums and one over the chosen
+//                     tile's 256 weights.  All sums are fp64 in a fixed order,
+//                     so the draw is reproducible.
 #include "common.h"
 #include "kernels.h"
 
 namespace nj {
 namespace {
 
-constexpr int kChunk = 8192;
-constexpr int kStatThreads = 256;
 constexpr int kTile = 256;          // weights per tile (4 per lane of a wave)
-constexpr int kTilesPerBlock = 8;   // tiles per accept_tiles workgroup (two per wave)
+constexpr int kTilesPerBlock = 8;   // tiles per accept_draw workgroup (two per wave)
 constexpr int kMaxTiles = 2048;     // V <= 524288
-
-// One pass: each thread holds its 32 values of the chunk in registers.
-__global__ __launch_bounds__(kStatThreads) void accept_stats_kernel(const float* __restrict__ logits, int V, int nch,
-                                                                    float* __restrict__ stats) {
-  constexpr int PER = kChunk / kStatThreads / 4;  // float4 groups per thread
-  __shared__ float sh[kStatThreads / kWave];
-  const int row = blockIdx.x, c = blockIdx.y;
-  const float* x = logits + (size_t)row * V;
-  const int lo = c * kChunk, hi = min(lo + kChunk, V);
-  float v[PER][4];
-  float mx = -INFINITY;
-  if ((V & 3) == 0) {
-#pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int j = lo + (it * kStatThreads + threadIdx.x) * 4;
-      const f32x4 q = j < hi ? *reinterpret_cast<const f32x4*>(x + j) : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[it][e] = q[e];
-    }
-  } else {
-#pragma unroll
-    for (int it = 0; it < PER; ++it)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int j = lo + (it * kStatThreads + threadIdx.x) * 4 + e;
-        v[it][e] = j < hi ? x[j] : -INFINITY;
-      }
-  }
-#pragma unroll
-  for (int it = 0; it < PER; ++it)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, v[it][e]);
-  mx = block_max<kStatThreads>(mx, sh);
-  float s = 0.f;
-#pragma unroll
-  for (int it = 0; it < PER; ++it)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) s += (v[it][e] == -INFINITY) ? 0.f : expf(v[it][e] - mx);
-  s = block_sum<kStatThreads>(s, sh);
-  if (threadIdx.x == 0) {
-    stats[((size_t)row * nch + c) * 2] = mx;
-    stats[((size_t)row * nch + c) * 2 + 1] = s;
-  }
-}
-
-// Row max and 1/sum from the chunk statistics, in chunk order.
-__device__ __forceinline__ void row_stats(const float* __restrict__ st, int nch, float* m, float* inv_s) {
-  float mx = -INFINITY;
-  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, st[2 * c]);
-  float s = 0.f;
-  for (int c = 0; c < nch; ++c) s += st[2 * c + 1] * expf(st[2 * c] - mx);
-  *m = mx;
-  *inv_s = 1.0f / s;
-}
-
-// Weight of vocabulary entry j in a draw row: p_j, or max(0, p_j - q_j).
-__device__ __forceinline__ float draw_weight(const float* __restrict__ lrow, const float* __restrict__ qrow,
-                                             float m, float inv_s, bool resid, int j) {
-  const float p = expf(lrow[j] - m) * inv_s;
-  return resid ? fmaxf(0.f, p - qrow[j]) : p;
-}
 
 struct AccK {
   const float* logits;    // [B*T][V]
@@ -97,78 +40,88 @@ struct AccK {
   const float* dprobs;    // [B][k][V]
   const float* uniforms;  // [B][T]
   const float* stats;     // [B*T][nch][2]
-  float* rowstat;         // [B][2]: max, 1/sum of the draw row
+  float* rowstat;         // [B*T][2]: max, 1/sum of every window row
+  int32_t* okflag;        // [B*T]: accept test of the draft row i scores (rows 0..k-1)
   double* tsum;           // [B][ntile]: tile sums of the draw row
-  int32_t* nsel;          // [B]: accepted length n
+  int* counters;          // [B]: draw arrivals (zeroed by accept_rows)
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
-  int k, V, nch, ntile;
+  int k, V, nch, ntile, tsum_bytes;
 };
 
-__global__ __launch_bounds__(256) void accept_tiles_kernel(AccK a) {
-  __shared__ float s_m[kWave], s_inv[kWave];
-  __shared__ int s_n;
-  const int b = blockIdx.x, T = a.k + 1, V = a.V;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (wave == 0) {
-    // row statistics of the window rows (lane i: row i) and the k accept tests
-    float m = 0.f, inv_s = 0.f;
-    if (lane < T) {
-      row_stats(a.stats + (size_t)(b * T + lane) * a.nch * 2, a.nch, &m, &inv_s);
-      s_m[lane] = m;
-      s_inv[lane] = inv_s;
-    }
-    bool ok = true;
-    if (lane < a.k) {
-      const int x = a.drafts[b * a.k + lane];
-      if (x < 0 || x >= V) {
-        if (blockIdx.y == 0) flag_error(a.err, kErrToken);
-        ok = false;
-      } else {
-        const float p = expf(a.logits[(size_t)(b * T + lane) * V + x] - m) * inv_s;
-        const float q = a.dprobs[((size_t)b * a.k + lane) * V + x];
-        ok = (q <= 0.f) || (a.uniforms[b * T + lane] < p / q);
-      }
-    }
-    const unsigned long long fails = __ballot(lane < a.k && !ok);
-    const int n = fails ? __ffsll((long long)fails) - 1 : a.k;
-    if (lane == 0) {
-      s_n = n;
-      if (blockIdx.y == 0) a.nsel[b] = n;
-    }
-  }
-  __syncthreads();
-  const int n = s_n;
-  const float m = s_m[n], inv_s = s_inv[n];
-  if (blockIdx.y == 0 && threadIdx.x == 0) {
-    a.rowstat[b * 2] = m;
-    a.rowstat[b * 2 + 1] = inv_s;
-  }
-  const bool resid = n < a.k;
-  const float* lrow = a.logits + (size_t)(b * T + n) * V;
-  const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * V : lrow;
-  const int t0 = blockIdx.y * kTilesPerBlock, t1 = min(t0 + kTilesPerBlock, a.ntile);
-  const bool vec = (a.V & 3) == 0;
-  for (int t = t0 + wave; t < t1; t += 4) {
-    const int j0 = t * kTile + lane * 4;
-    double ls = 0.0;
-    if (vec && j0 + 3 < a.V) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lrow + j0);
-      const f32x4 q4 = *reinterpret_cast<const f32x4*>(qrow + j0);
+// 128-wide chunks of the logits, written by 256-thread workgroups (8 lanes per chunk).
+__global__ __launch_bounds__(256) void accept_stats_kernel(const float* __restrict__ logits, int V, int nch,
+                                                           float* __restrict__ stats) {
+  const int row = blockIdx.x;
+  const int chunk = blockIdx.y * 32 + threadIdx.x / kStatLanes, c = threadIdx.x % kStatLanes;
+  const int cc = min(chunk, nch - 1);  // surplus lanes of the last block repeat the last chunk (not stored)
+  const float* x = logits + (size_t)row * V;
+  float v[kStatPer];
+  const int j0 = cc * kStatChunk + c * kStatPer;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p = expf(l4[e] - m) * inv_s;
-        ls += (double)(resid ? fmaxf(0.f, p - q4[e]) : p);
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (j0 + e < a.V) ls += (double)draw_weight(lrow, qrow, m, inv_s, resid, j0 + e);
-    }
-    ls = wave_sum_d(ls);
-    if (lane == 0) a.tsum[(size_t)b * a.ntile + t] = ls;
+  for (int e = 0; e < kStatPer; ++e) v[e] = j0 + e < V ? x[j0 + e] : -INFINITY;
+  float m, sum;
+  chunk_stats(v, m, sum);
+  if (c == 0 && chunk < nch) {
+    stats[((size_t)row * nch + chunk) * 2] = m;
+    stats[((size_t)row * nch + chunk) * 2 + 1] = sum;
   }
+}
+
+// One workgroup per window row: the row max and 1/sum from the chunk
+// statistics (thread t takes chunks t, t+256, ...; all its loads are issued
+// before any is used), and, for rows 0..k-1, the accept test of the draft the
+// row scores.  Row 0 of each sequence also clears the sequence's draw counter.
+constexpr int kRowThreads = 256, kRowLoads = 16;  // chunks per thread (V <= 524288)
+__global__ __launch_bounds__(kRowThreads) void accept_rows_kernel(AccK a) {
+  __shared__ float sh[kRowThreads / kWave];
+  const int row = blockIdx.x, T = a.k + 1, b = row / T, i = row % T, V = a.V, nch = a.nch;
+  const float* st = a.stats + (size_t)row * nch * 2;
+  // the draft this row scores, and its target logit and draft probability
+  float lx = 0.f, qx = 1.f;
+  bool bad = false;
+  if (threadIdx.x == 0 && i < a.k) {
+    const int x = a.drafts[b * a.k + i];
+    bad = x < 0 || x >= V;
+    const int xs = bad ? 0 : x;
+    lx = a.logits[(size_t)row * V + xs];
+    qx = a.dprobs[((size_t)b * a.k + i) * V + xs];
+  }
+  float cm[kRowLoads], cs[kRowLoads];
+#pragma unroll
+  for (int j = 0; j < kRowLoads; ++j) {
+    const int c = threadIdx.x + j * kRowThreads;
+    const int cc = min(c, nch - 1);
+    cm[j] = c < nch ? st[2 * cc] : -INFINITY;
+    cs[j] = c < nch ? st[2 * cc + 1] : 0.f;
+  }
+  float m = cm[0];
+#pragma unroll
+  for (int j = 1; j < kRowLoads; ++j) m = fmaxf(m, cm[j]);
+  m = block_max<kRowThreads>(m, sh);
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < kRowLoads; ++j) s += (cm[j] == -INFINITY) ? 0.f : cs[j] * expf(cm[j] - m);
+  s = block_sum<kRowThreads>(s, sh);
+  if (threadIdx.x == 0) {
+    const float inv_s = 1.0f / s;
+    a.rowstat[row * 2] = m;
+    a.rowstat[row * 2 + 1] = inv_s;
+    if (i < a.k) {
+      if (bad) flag_error(a.err, kErrToken);
+      const float p = expf(lx - m) * inv_s;
+      a.okflag[row] = !bad && ((qx <= 0.f) || (a.uniforms[row] < p / qx));
+    }
+    if (i == 0) a.counters[b] = 0;
+  }
+}
+
+// Weight of vocabulary entry j in a draw row: p_j, or max(0, p_j - q_j).
+__device__ __forceinline__ float draw_weight(const float* __restrict__ lrow, const float* __restrict__ qrow,
+                                             float m, float inv_s, bool resid, int j) {
+  const float p = expf(lrow[j] - m) * inv_s;
+  return resid ? fmaxf(0.f, p - qrow[j]) : p;
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave.
@@ -181,18 +134,15 @@ __device__ __forceinline__ double wave_incl_scan(double v) {
   return v;
 }
 
-__global__ __launch_bounds__(64) void accept_finalize_kernel(AccK a) {
-  __shared__ double fb_tsum[kMaxTiles];  // only for an all-zero residual
-  const int b = blockIdx.x, T = a.k + 1, V = a.V, lane = threadIdx.x;
-
-  const int n = a.nsel[b];
+// The draw of sequence b from its tile sums ts[0..ntile) (LDS), run by one wave.
+// u: the draw's uniform; dft: draft `lane` of the sequence (lanes < k).
+__device__ void draw_token(const AccK& a, int b, int n, bool resid, float m, float inv_s, float u, int dft, double* ts,
+                           double* fb_tsum) {
+  const int T = a.k + 1, V = a.V, lane = threadIdx.x & 63;
   const int row = b * T + n;
-  bool resid = n < a.k;
   const float* lrow = a.logits + (size_t)row * V;
   const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * V : lrow;
-  const float m = a.rowstat[b * 2], inv_s = a.rowstat[b * 2 + 1];
   const int ntile = a.ntile;
-  const double* ts = a.tsum + (size_t)b * ntile;
 
   // lane-contiguous tile ranges; the total is the last inclusive prefix, so it
   // is made of exactly the additions the search below walks through
@@ -216,14 +166,15 @@ __global__ __launch_bounds__(64) void accept_finalize_kernel(AccK a) {
       s = wave_sum_d(s);
       if (lane == 0) fb_tsum[t] = s;
     }
-    __syncthreads();
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     ts = fb_tsum;
     ls = 0.0;
     for (int t = t0; t < t1; ++t) ls += ts[t];
     incl = wave_incl_scan(ls);
     total = __shfl(incl, kWave - 1);
   }
-  const double target = (double)a.uniforms[b * T + a.k] * total;
+  const double target = (double)u * total;
 
   int tile = -1;
   double base = 0.0;
@@ -305,43 +256,118 @@ __global__ __launch_bounds__(64) void accept_finalize_kernel(AccK a) {
 
   if (lane < T) {
     int v = -1;
-    if (lane < n) v = a.drafts[b * a.k + lane];
+    if (lane < n) v = dft;
     else if (lane == n) v = cand;
     a.next_tokens[b * T + lane] = v;
   }
   if (lane == 0) a.accepted_len[b] = n;
 }
 
+__global__ __launch_bounds__(256) void accept_draw_kernel(AccK a) {
+  __shared__ double s_ts[kMaxTiles];
+  __shared__ double s_fb[kMaxTiles];  // only for an all-zero residual
+  __shared__ int s_last;
+  const int b = blockIdx.x, T = a.k + 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // n = index of the first failed test (k if all passed); the test flags, the
+  // statistics of every window row, the draw's uniform and the drafts are
+  // loaded together, before anything depends on n
+  int okv = 1, dft = -1;
+  float rm = 0.f, ri = 0.f;
+  if (lane < a.k) {
+    okv = a.okflag[b * T + lane];
+    dft = a.drafts[b * a.k + lane];
+  }
+  if (lane < T) {
+    rm = a.rowstat[(b * T + lane) * 2];
+    ri = a.rowstat[(b * T + lane) * 2 + 1];
+  }
+  const float u = a.uniforms[b * T + a.k];
+  const unsigned long long fails = __ballot(lane < a.k && !okv);
+  const int n = fails ? __ffsll((long long)fails) - 1 : a.k;
+  const float m = __shfl(rm, n), inv_s = __shfl(ri, n);
+  const bool resid = n < a.k;
+  const float* lrow = a.logits + (size_t)(b * T + n) * a.V;
+  const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * a.V : lrow;
+  const __amdgpu_buffer_rsrc_t trs = coherent_rsrc(a.tsum, a.tsum_bytes);
+  const int t0 = blockIdx.y * kTilesPerBlock, t1 = min(t0 + kTilesPerBlock, a.ntile);
+  const bool vec = (a.V & 3) == 0;
+  for (int t = t0 + wave; t < t1; t += 4) {
+    const int j0 = t * kTile + lane * 4;
+    double ls = 0.0;
+    if (vec && j0 + 3 < a.V) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lrow + j0);
+      const f32x4 q4 = *reinterpret_cast<const f32x4*>(qrow + j0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = expf(l4[e] - m) * inv_s;
+        ls += (double)(resid ? fmaxf(0.f, p - q4[e]) : p);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j0 + e < a.V) ls += (double)draw_weight(lrow, qrow, m, inv_s, resid, j0 + e);
+    }
+    ls = wave_sum_d(ls);
+    if (lane == 0) coherent_store_f64(trs, (uint32_t)(((size_t)b * a.ntile + t) * 8), ls);
+  }
+  // the last workgroup of the sequence to arrive draws (tile sums written and
+  // read with device-coherent accesses, published by the counter increment)
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0)
+    s_last = (__hip_atomic_fetch_add(a.counters + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              (int)gridDim.y - 1);
+  __syncthreads();
+  if (!s_last) return;
+  for (int t = threadIdx.x; t < a.ntile; t += 256)
+    s_ts[t] = coherent_load_f64(trs, (uint32_t)(((size_t)b * a.ntile + t) * 8));
+  __syncthreads();
+  if (wave == 0) draw_token(a, b, n, resid, m, inv_s, u, dft, s_ts, s_fb);
+}
+
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-int accept_chunks(int V) { return (V + kChunk - 1) / kChunk; }
+int accept_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
 
+// [stats][rowstat][tsum][okflag][counters]
 size_t accept_workspace_bytes(int rows, int V) {
   const int ntile = (V + kTile - 1) / kTile;
   return al256((size_t)rows * accept_chunks(V) * 2 * 4) + al256((size_t)rows * 2 * 4) +
-         al256((size_t)rows * ntile * 8) + al256((size_t)rows * 4);
+         al256((size_t)rows * ntile * 8) + al256((size_t)rows * 4) + al256((size_t)rows * 4);
 }
+
+float* accept_stats_ptr(void* scratch) { return static_cast<float*>(scratch); }
 
 hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
   const int T = x.k + 1, rows = x.B * T, nch = accept_chunks(x.V), ntile = (x.V + kTile - 1) / kTile;
   char* ws = static_cast<char*>(x.scratch);
-  float* stats = reinterpret_cast<float*>(ws);
-  float* rowstat = reinterpret_cast<float*>(ws + al256((size_t)rows * nch * 2 * 4));
-  double* tsum = reinterpret_cast<double*>(ws + al256((size_t)rows * nch * 2 * 4) + al256((size_t)rows * 2 * 4));
-  int32_t* nsel = reinterpret_cast<int32_t*>(ws + al256((size_t)rows * nch * 2 * 4) + al256((size_t)rows * 2 * 4) +
-                                             al256((size_t)rows * ntile * 8));
-  hipLaunchKernelGGL(accept_stats_kernel, dim3(rows, nch), dim3(kStatThreads), 0, s, x.logits, x.V, nch, stats);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, stats, rowstat, tsum, nsel, x.accepted_len, x.next_tokens,
-         x.err, x.k, x.V, nch, ntile};
-  hipLaunchKernelGGL(accept_tiles_kernel, dim3(x.B, (ntile + kTilesPerBlock - 1) / kTilesPerBlock), dim3(256), 0,
-                     s, a);
+  size_t off = 0;
+  float* stats = reinterpret_cast<float*>(ws + off);
+  off += al256((size_t)rows * nch * 2 * 4);
+  float* rowstat = reinterpret_cast<float*>(ws + off);
+  off += al256((size_t)rows * 2 * 4);
+  double* tsum = reinterpret_cast<double*>(ws + off);
+  const size_t tsum_bytes = (size_t)x.B * ntile * 8;
+  off += al256((size_t)rows * ntile * 8);
+  int32_t* okflag = reinterpret_cast<int32_t*>(ws + off);
+  off += al256((size_t)rows * 4);
+  int* counters = reinterpret_cast<int*>(ws + off);
+  hipError_t e;
+  if (!x.stats_ready) {
+    hipLaunchKernelGGL(accept_stats_kernel, dim3(rows, (nch + 31) / 32), dim3(256), 0, s, x.logits, x.V, nch, stats);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, stats, rowstat, okflag, tsum, counters, x.accepted_len,
+         x.next_tokens, x.err, x.k, x.V, nch, ntile, (int)tsum_bytes};
+  hipLaunchKernelGGL(accept_rows_kernel, dim3(rows), dim3(kRowThreads), 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_finalize_kernel, dim3(x.B), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(accept_draw_kernel, dim3(x.B, (ntile + kTilesPerBlock - 1) / kTilesPerBlock), dim3(256), 0, s,
+                     a);
   return hipGetLastError();
 }
 

@@ -39,8 +39,8 @@ size_t al(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
-  size_t err, gemm_cnt, ctx_snap, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats, gemm_part,
-      total;
+  size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats,
+      gemm_part, total;
   size_t win_layer_bytes;
 };
 
@@ -101,6 +101,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   // nightjar_workspace_init and left at zero by every GEMM.
   L.gemm_cnt = take(kGemmCounterBytes);
   L.ctx_snap = take((size_t)B * 4);  // context lengths read by the verify step, for the KV append
+  L.attn_cnt = take((size_t)B * d.n_kv_heads * 4);  // attention split arrivals (cleared before each launch)
   size_t part = 0;
   if (d.dtype == NJ_BF16) {
     GemmShape gs[5];
@@ -238,12 +239,13 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     void* wk = ws + L.win_k + l * L.win_layer_bytes;
     void* wv = ws + L.win_v + l * L.win_layer_bytes;
     NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
-                              wk, wv, l == 0 ? reinterpret_cast<int32_t*>(ws + L.ctx_snap) : nullptr, s),
+                              wk, wv, l == 0 ? reinterpret_cast<int32_t*>(ws + L.ctx_snap) : nullptr,
+                              bf ? reinterpret_cast<int*>(ws + L.attn_cnt) : nullptr, s),
            "rope");
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
-                reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml), nsplit, bps,
-                o, err};
+                reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),
+                reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, bps, o, err};
     NJ_TRY(launch_attention(aa, s), "attention");
     NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s), "o gemm");
     NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s), "ffn_norm");
@@ -251,9 +253,15 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s), "down gemm");
   }
   NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s), "final_norm");
-  NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
-  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, accepted_len, next_tokens,
-                err};
+  bool stats_ready = false;
+  if (bf)
+    NJ_TRY(launch_gemm_logits(x, w->lm_head, logits, accept_stats_ptr(ws + L.stats), M, d.vocab, d.d_model, gcnt, gpart,
+                              s, &stats_ready),
+           "lm_head gemm");
+  else
+    NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
+  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, stats_ready, accepted_len,
+                next_tokens, err};
   NJ_TRY(launch_accept(ac, s), "accept");
 #undef NJ_TRY
   {
@@ -313,8 +321,8 @@ int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_
   if (workspace_bytes < need) return fail(NJ_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, need);
   if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
   char* ws = static_cast<char*>(workspace);
-  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, ws + kAlign, accepted_len, next_tokens,
-               reinterpret_cast<int*>(ws)};
+  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, ws + kAlign, false, accepted_len,
+               next_tokens, reinterpret_cast<int*>(ws)};
   hipError_t e = launch_accept(a, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "accept");
 }
@@ -379,7 +387,7 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
                      GemmPlan* out) {
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
   if (split < 0) return fail(NJ_EINVAL, "split_k must be >= 0");
-  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_TILE_128x128) return fail(NJ_EINVAL, "bad kernel choice");
+  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_STREAM_DEEP) return fail(NJ_EINVAL, "bad kernel choice");
   if (dtype != NJ_BF16) {
     if (kernel != NJ_GEMM_AUTO || split) return fail(NJ_EINVAL, "the fp32 GEMM has a single kernel and no split");
     *out = GemmPlan{};
@@ -391,8 +399,9 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
     return NJ_OK;
   }
   GemmPlan p;
-  if (kernel == NJ_GEMM_STREAM) {
+  if (kernel == NJ_GEMM_STREAM || kernel == NJ_GEMM_STREAM_DEEP) {
     p = gemm_stream_plan(M, N, K, epilogue, split);
+    p.depth = kernel == NJ_GEMM_STREAM_DEEP ? 3 : 1;
   } else {
     if (!tile_fits(M, N, K)) return fail(NJ_EINVAL, "the tiled kernels need K %% 64 == 0 and M*K, N*K < 2^31");
     const int tile = kernel == NJ_GEMM_TILE_256x256 ? kTile256x256

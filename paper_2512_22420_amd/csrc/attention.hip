@@ -15,7 +15,7 @@
 // consecutive tokens of one dim: V pages are stored dim-major inside a block
 // ([D][16]), which makes that an 8-byte read.  Softmax is online in the log2
 // domain.  When the grid splits the KV range, each split writes its partial
-// (o, max, sum) and a combine kernel merges the splits in split order.
+// (o, max, sum) and the last split to arrive merges them in split order.
 #include <algorithm>
 
 #include "common.h"
@@ -41,10 +41,12 @@ struct AttnK {
   const int32_t* ctx;
   float* part_o;
   float* part_ml;
+  int* counters;  // [B*Hkv] split arrivals, zero on entry (cleared by the RoPE kernel before each launch)
   bf16_t* out;
   int* err;
   int max_blocks, num_blocks, T, H, Hkv, bps;
   float scale_log2;
+  int part_o_bytes, part_ml_bytes;
 };
 
 // The workgroup
@@ -63,6 +65,100 @@ __device__ __forceinline__ int k_lds(int tok, int chunk16) {  // element offset 
 }
 __device__ __forceinline__ int v_lds(int dim, int unit8) {  // element offset in a V block [128][16]
   return dim * kBlock + ((unit8 ^ (((dim >> 3) & 1) << 1)) & 3) * 4;
+}
+
+// A split has written its partial (o, max, sum) with device-coherent stores;
+// count it in, and let the last split of the (sequence, KV head) to arrive
+// merge all splits in split order:
+//   out = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
+// The per-split (m, l) of every query row go to LDS first and each row's
+// weights 2^(m_s - M) are formed once; then each thread merges 4 head dims of
+// one query row per unit, with the loads of all splits of a unit in flight
+// together.  `lds` is the kernel's staging buffer (free by now).
+constexpr int kMergeSplits = 8;  // split partials loaded per batch
+__device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT, int G, int b, int kvh,
+                             __amdgpu_buffer_rsrc_t ors, __amdgpu_buffer_rsrc_t mrs, float* lds, int lds_floats) {
+  __shared__ int s_last;
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0)
+    s_last = (__hip_atomic_fetch_add(a.counters + pair, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1);
+  __syncthreads();
+  if (!s_last) return;
+  const int rpad = RT * 16;
+  const size_t pbase = (size_t)pair * nsplit * rpad;
+  // s_f[qr][sp]: weight of split sp for row qr (0 for empty splits); s_w[qr]: 1 / sum_s f l_s
+  float* s_f = lds;
+  float* s_w = lds + R * nsplit;
+  const bool staged = R * nsplit + R <= lds_floats;
+  if (staged) {
+    for (int u = threadIdx.x; u < R * nsplit; u += 256) {
+      const int qr = u / nsplit, sp = u % nsplit;
+      s_f[u] = coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)sp * rpad + qr) * 2) * 4));
+    }
+    __syncthreads();
+    for (int qr = threadIdx.x; qr < R; qr += 256) {
+      float mx = -INFINITY;
+      for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, s_f[qr * nsplit + sp]);
+      for (int sp = 0; sp < nsplit; ++sp) {
+        const float m = s_f[qr * nsplit + sp];
+        s_f[qr * nsplit + sp] = (m == -INFINITY) ? 0.f : exp2f(m - mx);
+      }
+    }
+    __syncthreads();
+    // l_s weighted sums (one thread per row; the loads of all splits together)
+    for (int qr = threadIdx.x; qr < R; qr += 256) {
+      float wsum = 0.f;
+      for (int s0 = 0; s0 < nsplit; s0 += kMergeSplits) {
+        float lv[kMergeSplits];
+#pragma unroll
+        for (int j = 0; j < kMergeSplits; ++j)
+          lv[j] = s0 + j < nsplit ? coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)(s0 + j) * rpad + qr) * 2 + 1) * 4)) : 0.f;
+#pragma unroll
+        for (int j = 0; j < kMergeSplits; ++j)
+          if (s0 + j < nsplit) wsum += s_f[qr * nsplit + s0 + j] * lv[j];
+      }
+      s_w[qr] = 1.0f / wsum;
+    }
+    __syncthreads();
+  }
+  for (int u = threadIdx.x; u < R * (kD / 4); u += 256) {
+    const int qr = u / (kD / 4), d = (u % (kD / 4)) * 4;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    float inv;
+    if (staged) {
+      for (int s0 = 0; s0 < nsplit; s0 += kMergeSplits) {
+        f32x4 ov[kMergeSplits];
+#pragma unroll
+        for (int j = 0; j < kMergeSplits; ++j)
+          ov[j] = s0 + j < nsplit ? coherent_load(ors, (uint32_t)(((pbase + (size_t)(s0 + j) * rpad + qr) * kD + d) * 4))
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < kMergeSplits; ++j)
+          if (s0 + j < nsplit) acc += s_f[qr * nsplit + s0 + j] * ov[j];
+      }
+      inv = s_w[qr];
+    } else {  // too many splits to stage: direct loads
+      float mx = -INFINITY;
+      for (int sp = 0; sp < nsplit; ++sp)
+        mx = fmaxf(mx, coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)sp * rpad + qr) * 2) * 4)));
+      float wsum = 0.f;
+      for (int sp = 0; sp < nsplit; ++sp) {
+        const size_t base = pbase + (size_t)sp * rpad + qr;
+        const float m = coherent_load_f32(mrs, (uint32_t)((base * 2) * 4));
+        if (m == -INFINITY) continue;  // empty split: only its marker was written
+        const float f = exp2f(m - mx);
+        wsum += f * coherent_load_f32(mrs, (uint32_t)((base * 2 + 1) * 4));
+        acc += f * coherent_load(ors, (uint32_t)((base * kD + d) * 4));
+      }
+      inv = 1.0f / wsum;
+    }
+    const int i = qr / G, hh = qr % G;
+    u32x2 o;
+    o[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+    o[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+    *reinterpret_cast<u32x2*>(a.out + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d) = o;
+  }
 }
 
 template <int RTW>
@@ -88,9 +184,13 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
   const int ncc = (ncached + kCB - 1) / kCB;      // cached chunks
   const int nchunks = ncc + (split == 0 ? 1 : 0);  // split 0 also takes the window block, as a last chunk
 
+  const __amdgpu_buffer_rsrc_t ors = coherent_rsrc(a.part_o, a.part_o_bytes);
+  const __amdgpu_buffer_rsrc_t mrs = coherent_rsrc(a.part_ml, a.part_ml_bytes);
   if (nchunks == 0) {  // a split past this sequence's context: mark its rows empty for the combine
     for (int qr = threadIdx.x; qr < R; qr += 256)
-      a.part_ml[(((size_t)pair * nsplit + split) * (RT * 16) + qr) * 2] = -INFINITY;
+      coherent_store_f32(mrs, (uint32_t)(((((size_t)pair * nsplit + split) * (RT * 16) + qr) * 2) * 4), -INFINITY);
+    split_arrive(a, pair, nsplit, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
+                 (int)(sizeof(smem) / sizeof(float)));
     return;
   }
   bf16x8 qf[4];
@@ -288,39 +388,19 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
           a.out[((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
         } else {
           const size_t base = ((size_t)pair * nsplit + split) * (RT * 16) + qr;
-          a.part_o[base * kD + d] = acc;
+          coherent_store_f32(ors, (uint32_t)((base * kD + d) * 4), acc);
           if (d == 0) {
-            a.part_ml[base * 2] = mx;
-            a.part_ml[base * 2 + 1] = wsum;
+            coherent_store_f32(mrs, (uint32_t)(base * 2 * 4), mx);
+            coherent_store_f32(mrs, (uint32_t)((base * 2 + 1) * 4), wsum);
           }
         }
       }
     }
     __syncthreads();
   }
-}
-
-// Merge KV-split partials in split order: out = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
-// One workgroup per (sequence, KV head, query row), one thread per head dim.
-__global__ __launch_bounds__(kD) void attn_combine_kernel(const float* __restrict__ part_o,
-                                                          const float* __restrict__ part_ml,
-                                                          bf16_t* __restrict__ out, int nsplit, int rpad, int T,
-                                                          int H, int Hkv) {
-  const int pair = blockIdx.x, qr = blockIdx.y, d = threadIdx.x;
-  const int b = pair / Hkv, kvh = pair % Hkv, G = H / Hkv;
-  float mx = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, part_ml[(((size_t)pair * nsplit + s) * rpad + qr) * 2]);
-  float acc = 0.f, wsum = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const size_t base = ((size_t)pair * nsplit + s) * rpad + qr;
-    const float m = part_ml[base * 2];
-    if (m == -INFINITY) continue;  // empty split: only its marker was written
-    const float f = exp2f(m - mx);
-    wsum += f * part_ml[base * 2 + 1];
-    acc += f * part_o[base * kD + d];
-  }
-  const int i = qr / G, hh = qr % G;
-  out[((size_t)(b * T + i) * H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
+  if (nsplit > 1)
+    split_arrive(a, pair, nsplit, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
+                 (int)(sizeof(smem) / sizeof(float)));
 }
 
 // fp32 path: one workgroup per (sequence, query head, window position); scores
@@ -443,19 +523,17 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
   const int R = x.T * G, RT = (R + 15) / 16;
   AttnK a{static_cast<const bf16_t*>(x.q), static_cast<const bf16_t*>(x.k_pages),
           static_cast<const bf16_t*>(x.v_pages), static_cast<const bf16_t*>(x.win_k),
-          static_cast<const bf16_t*>(x.win_v), x.block_table, x.ctx, x.part_o, x.part_ml,
+          static_cast<const bf16_t*>(x.win_v), x.block_table, x.ctx, x.part_o, x.part_ml, x.counters,
           static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv, x.blocks_per_split,
-          (float)(1.4426950408889634 / sqrt((double)kD))};
+          (float)(1.4426950408889634 / sqrt((double)kD)),
+          (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * kD * 4, INT32_MAX),
+          (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * 2 * 4, INT32_MAX)};
   dim3 grid(x.B * x.Hkv, x.nsplit);
   switch (RT) {
     case 1: hipLaunchKernelGGL(attn_lds_kernel<1>, grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL(attn_lds_kernel<2>, grid, dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL(attn_lds_kernel<4>, grid, dim3(256), 0, s, a); break;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || x.nsplit == 1) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(x.B * x.Hkv, R), dim3(kD), 0, s, x.part_o, x.part_ml,
-                     static_cast<bf16_t*>(x.out), x.nsplit, RT * 16, x.T, x.H, x.Hkv);
   return hipGetLastError();
 }
 

@@ -29,7 +29,42 @@ __device__ __forceinline__ f32x4 coherent_load(__amdgpu_buffer_rsrc_t r, uint32_
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 16 /* sc1 */));
 }
 
+__device__ __forceinline__ void coherent_store_f32(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, byte_off, 0, 16 /* sc1 */);
+}
+__device__ __forceinline__ float coherent_load_f32(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 16 /* sc1 */));
+}
+__device__ __forceinline__ void coherent_store_f64(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, double v) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), r, byte_off, 0, 16 /* sc1 */);
+}
+__device__ __forceinline__ double coherent_load_f64(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, 16 /* sc1 */));
+}
+
 constexpr int kWave = 64;
+
+// Softmax statistics of one 128-wide vocabulary chunk, computed by 8
+// consecutive lanes holding 16 consecutive entries each (lane c of the group:
+// entries 16c .. 16c+15; -inf marks entries past the vocabulary).  Every lane
+// of the group returns the chunk max and the sum of exp(v - max), each formed
+// in a fixed order, so the LM-head GEMM epilogue and the stand-alone
+// statistics kernel produce the same bits.
+constexpr int kStatChunk = 128, kStatLanes = 8, kStatPer = 16;
+__device__ __forceinline__ void chunk_stats(const float (&v)[kStatPer], float& m, float& s) {
+  m = v[0];
+#pragma unroll
+  for (int e = 1; e < kStatPer; ++e) m = fmaxf(m, v[e]);
+  m = fmaxf(m, __shfl_xor(m, 1));
+  m = fmaxf(m, __shfl_xor(m, 2));
+  m = fmaxf(m, __shfl_xor(m, 4));
+  s = 0.f;
+#pragma unroll
+  for (int e = 0; e < kStatPer; ++e) s += (v[e] == -INFINITY) ? 0.f : expf(v[e] - m);
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 4);
+}
 constexpr int kBlock = 16;  // tokens per KV block
 
 // Device error bits (mirror NJ_DEV_* of the public header).

@@ -112,13 +112,16 @@ __global__ __launch_bounds__(256) void rope_window_kernel(const float* __restric
                                                           const int32_t* __restrict__ ctx, int T_, int H,
                                                           int Hkv, int D, RopeFreq f, T* __restrict__ q_out,
                                                           T* __restrict__ win_k, T* __restrict__ win_v,
-                                                          int32_t* __restrict__ ctx_snap) {
+                                                          int32_t* __restrict__ ctx_snap, int* __restrict__ attn_cnt) {
   const int half = D / 2;
   const int hpb = blockDim.x / half;  // heads per workgroup
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   const int hd = blockIdx.y * hpb + threadIdx.x / half, j = threadIdx.x % half;
   // the positions this step uses, for the KV append that follows it
   if (ctx_snap && i == 0 && blockIdx.y == 0 && threadIdx.x == 0) ctx_snap[b] = ctx[b];
+  // the split counters of the attention launch that follows start at zero
+  if (attn_cnt && i == 0 && blockIdx.y == 0)
+    for (int g = threadIdx.x; g < Hkv; g += blockDim.x) attn_cnt[b * Hkv + g] = 0;
   if (hd >= H + 2 * Hkv) return;
   const float* src = qkv + (size_t)row * (H + 2 * Hkv) * D + (size_t)hd * D;
   if (hd < H + Hkv) {
@@ -244,7 +247,8 @@ hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, 
 }
 
 hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv, int D,
-                              float theta, void* q_out, void* win_k, void* win_v, int32_t* ctx_snap, hipStream_t s) {
+                              float theta, void* q_out, void* win_k, void* win_v, int32_t* ctx_snap, int* attn_counters,
+                              hipStream_t s) {
   RopeFreq f{};
   const int half = D / 2;
   for (int j = 0; j < half && j < kMaxHalfDim; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / D);
@@ -252,10 +256,10 @@ hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, i
   dim3 grid(B * T, (H + 2 * Hkv + hpb - 1) / hpb), block(hpb * half);
   if (dtype == kF32)
     hipLaunchKernelGGL(rope_window_kernel<float>, grid, block, 0, s, qkv, ctx, T, H, Hkv, D, f,
-                       static_cast<float*>(q_out), static_cast<float*>(win_k), static_cast<float*>(win_v), ctx_snap);
+                       static_cast<float*>(q_out), static_cast<float*>(win_k), static_cast<float*>(win_v), ctx_snap, attn_counters);
   else
     hipLaunchKernelGGL(rope_window_kernel<bf16_t>, grid, block, 0, s, qkv, ctx, T, H, Hkv, D, f,
-                       static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(win_k), static_cast<bf16_t*>(win_v), ctx_snap);
+                       static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(win_k), static_cast<bf16_t*>(win_v), ctx_snap, attn_counters);
   return hipGetLastError();
 }
 

@@ -37,6 +37,7 @@
 // product unchanged.
 #include <algorithm>
 #include <cmath>
+#include <utility>
 
 #include "common.h"
 #include "kernels.h"
@@ -61,12 +62,15 @@ struct GemmK {
   int* counters;    // [mblocks][gridDim.x] arrival counters (split K only), zero between launches
   int M, Nout, K, KS, stages_per_chunk;
   int part_bytes;
+  float* stats;     // kEpiLogits: [M][nch][2] chunk max and sum of exp (chunk = this kernel's 128 columns)
+  int nch;
 };
 
-template <int MT, int EPI>
+template <int MT, int EPI, int NB>
 __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   constexpr int NG = EPI == kEpiSwiglu ? 2 : 1;
   constexpr int TPW = kNW / NG;                   // output tiles per workgroup
+  static_assert(EPI != kEpiLogits || TPW * 16 == kStatChunk, "a workgroup's columns are one statistics chunk");
   constexpr int ROWS = MT * 16, NTH = kNW * 64;
   constexpr int CH = ROWS * (kSK / 8);            // 16-byte x pieces per stage
   constexpr int PT = (CH + NTH - 1) / NTH;
@@ -104,8 +108,10 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   f32x4 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  u32x4 xr[2][PT];
-  bf16x8 wb[2][kSU];
+  // NB register sets: the loads of stages st+1 .. st+NB-1 are in flight while
+  // stage st is multiplied
+  u32x4 xr[NB][PT];
+  bf16x8 wb[NB][kSU];
 
   auto loadx = [&](auto setc, int st) {
     constexpr int set = decltype(setc)::value;
@@ -139,25 +145,29 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
         acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb[set][u], xv, acc[mt], 0, 0, 0);
       }
   };
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
-  loadx(S0{}, st0);
-  loadw(S0{}, st0);
-  storex(S0{}, 0, st0);
+  // prologue: stages st0 .. st0+NB-2 in flight, stage st0's x in LDS buffer 0
+  [&]<int... I>(std::integer_sequence<int, I...>) {
+    ((loadx(std::integral_constant<int, I>{}, min(st0 + I, last)),
+      loadw(std::integral_constant<int, I>{}, min(st0 + I, last))), ...);
+  }(std::make_integer_sequence<int, NB - 1>{});
+  storex(std::integral_constant<int, 0>{}, 0, st0);
   __syncthreads();
-  for (int st = st0; st < st1; st += 2) {
-    loadx(S1{}, min(st + 1, last));
-    loadw(S1{}, min(st + 1, last));
-    __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the multiplies
-    compute(S0{}, 0);
-    storex(S1{}, 1, st + 1);
-    __syncthreads();
-    loadx(S0{}, min(st + 2, last));
-    loadw(S0{}, min(st + 2, last));
-    __builtin_amdgcn_sched_barrier(0);
-    compute(S1{}, 1);
-    storex(S0{}, 0, st + 2);
-    __syncthreads();
+  // stage t = st + J uses register set J and LDS buffer J & 1 (NB is even);
+  // it issues the loads of stage t + NB - 1 into set (J + NB - 1) % NB, which
+  // stage t - 1 has finished with
+  for (int st = st0; st < st1; st += NB) {
+    [&]<int... J>(std::integer_sequence<int, J...>) {
+      ([&] {
+        constexpr int nxt = (J + NB - 1) % NB;
+        const int t = st + J;
+        loadx(std::integral_constant<int, nxt>{}, min(t + NB - 1, last));
+        loadw(std::integral_constant<int, nxt>{}, min(t + NB - 1, last));
+        __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the multiplies
+        compute(std::integral_constant<int, J>{}, J & 1);
+        storex(std::integral_constant<int, (J + 1) % NB>{}, (J + 1) & 1, t + 1);
+        __syncthreads();
+      }(), ...);
+    }(std::make_integer_sequence<int, NB>{});
   }
 
   const int ncol = wtile * 16 + 4 * g;  // weight rows of this lane's results
@@ -218,6 +228,45 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       o[1] = pack_bf16x2(silu_mul(gt[2], up[2]), silu_mul(gt[3], up[3]));
       *reinterpret_cast<u32x2*>(static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n) = o;
     }
+  } else if constexpr (EPI == kEpiStore || EPI == kEpiLogits) {
+    // The MFMA result layout puts 16 rows x 64 bytes in one store
+    // instruction; staged through LDS, each wave instead writes two 512-byte
+    // row segments per instruction (full cache lines).  LDS is free: the stage
+    // loop (or the split-K hand-off) ended on a barrier.
+    constexpr int OS = TPW * 16 + 4;  // row stride in floats
+    static_assert(sizeof(xs) >= (size_t)ROWS * OS * sizeof(float), "output tile does not fit");
+    float* ot = reinterpret_cast<float*>(&xs[0][0]);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = acc[mt][i];
+    __syncthreads();
+    const int n0 = blockIdx.x * TPW * 16;
+    if constexpr (EPI == kEpiLogits) {
+      // softmax statistics of this 128-column chunk, 8 lanes per row
+      const int row = min((int)threadIdx.x / kStatLanes, ROWS - 1), c = threadIdx.x % kStatLanes;
+      float v[kStatPer];
+#pragma unroll
+      for (int e = 0; e < kStatPer; ++e)
+        v[e] = n0 + c * kStatPer + e < Nout ? ot[row * OS + c * kStatPer + e] : -INFINITY;
+      float cm, cs;
+      chunk_stats(v, cm, cs);
+      const int m = m0 + row;
+      if (c == 0 && (int)threadIdx.x / kStatLanes < ROWS && m < M) {
+        a.stats[((size_t)m * a.nch + blockIdx.x) * 2] = cm;
+        a.stats[((size_t)m * a.nch + blockIdx.x) * 2 + 1] = cs;
+      }
+    }
+    constexpr int PIECES = ROWS * TPW * 4;  // 16-byte pieces of the tile
+#pragma unroll
+    for (int it = 0; it < (PIECES + NTH - 1) / NTH; ++it) {
+      const int idx = threadIdx.x + it * NTH;
+      const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
+      const int m = m0 + row, n = n0 + c4;
+      if (idx < PIECES && m < M && n < Nout)
+        *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) =
+            *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
+    }
   } else {
     if (!active) return;
     const int n = otile * 16 + 4 * g;
@@ -226,8 +275,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       const int m = m0 + mt * 16 + r;
       if (m >= M) continue;
       f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
-      if constexpr (EPI == kEpiStore) *p = acc[mt];
-      else *p = *p + acc[mt];
+      *p = *p + acc[mt];
     }
   }
 }
@@ -281,16 +329,21 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
-template <int EPI>
-hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+template <int EPI, int NB>
+hipError_t launch_stream_nb(const GemmK& a, const GemmPlan& p, hipStream_t s) {
   const dim3 grid(p.ntiles, p.mblocks, p.nkc), block(kNW * 64);
   switch (p.mt) {
-    case 1: hipLaunchKernelGGL((gemm_stream_kernel<1, EPI>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((gemm_stream_kernel<2, EPI>), grid, block, 0, s, a); break;
-    case 3: hipLaunchKernelGGL((gemm_stream_kernel<3, EPI>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((gemm_stream_kernel<4, EPI>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((gemm_stream_kernel<1, EPI, NB>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((gemm_stream_kernel<2, EPI, NB>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((gemm_stream_kernel<3, EPI, NB>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((gemm_stream_kernel<4, EPI, NB>), grid, block, 0, s, a); break;
   }
   return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+  return p.depth >= 3 ? launch_stream_nb<EPI, 4>(a, p, s) : launch_stream_nb<EPI, 2>(a, p, s);
 }
 
 }  // namespace
@@ -400,10 +453,21 @@ hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N,
   if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s);
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes};
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0};
   if (epi == kEpiStore) return launch_stream<kEpiStore>(a, p, s);
   if (epi == kEpiResidual) return launch_stream<kEpiResidual>(a, p, s);
   return launch_stream<kEpiSwiglu>(a, p, s);
+}
+
+hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* stats, int M, int N, int K,
+                              int* counters, float* part, hipStream_t s, bool* stats_written) {
+  const GemmPlan p = gemm_plan(M, N, K, kEpiStore);
+  *stats_written = p.tile == kTileNone;
+  if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s);
+  GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
+          p.nkc > 1 ? counters : nullptr, M, N, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, stats,
+          (N + kStatChunk - 1) / kStatChunk};
+  return launch_stream<kEpiLogits>(a, p, s);
 }
 
 size_t packed_weight_elems(int N, int K) { return (size_t)((N + 127) / 128) * 128 * (size_t)K; }

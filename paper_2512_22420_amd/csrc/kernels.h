@@ -8,7 +8,9 @@
 namespace nj {
 
 enum { kF32 = 0, kBF16 = 1 };
-enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2 };
+// kEpiLogits (internal): fp32 store plus the softmax statistics of every
+// 128-wide output chunk, for the acceptance kernels.
+enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3 };
 
 // Output tiles of the LDS-tiled kernel for large windows: x rows x weight rows.
 enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
@@ -23,7 +25,7 @@ enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
 struct GemmPlan {
   int tile;
   int mt, nw, ntiles, mblocks, nkc, stages_per_chunk;
-  int depth;  // weight stages in flight ahead of the one being multiplied (1 or 2)
+  int depth;  // streaming kernel: weight stages in flight ahead of the one being multiplied (1 or 3)
   size_t part_bytes, counter_bytes;
 };
 GemmPlan gemm_plan(int M, int N, int K, int epi);
@@ -62,6 +64,11 @@ hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, 
 // mt 1..4, any nkc/stages_per_chunk).
 hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s);
+// LM head: y = x . w^T stored fp32, plus the chunk statistics of the
+// acceptance kernels (stats [M][accept_chunks(N)][2]) when the plan uses the
+// weight-streaming kernel; *stats_written says whether it did.
+hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* stats, int M, int N, int K,
+                              int* counters, float* part, hipStream_t s, bool* stats_written);
 // The LDS-tiled kernel alone (K % 64 == 0).
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s);
@@ -82,9 +89,10 @@ struct RopeFreq {
   double inv_freq[kMaxHalfDim];  // theta^(-2j/D)
 };
 // ctx_snap (nullable): receives ctx[b], the positions the KV append uses.
+// attn_counters (nullable): [B*Hkv] cleared for the attention launch that follows.
 hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, int B, int T, int H, int Hkv,
                               int D, float theta, void* q_out, void* win_k, void* win_v, int32_t* ctx_snap,
-                              hipStream_t s);
+                              int* attn_counters, hipStream_t s);
 
 struct AttnArgs {
   int dtype;
@@ -99,6 +107,7 @@ struct AttnArgs {
   int num_blocks, B, T, H, Hkv, D;
   float* part_o;        // split partials (bf16 path)
   float* part_ml;
+  int* counters;         // [B*Hkv] split arrivals, zero on entry (bf16 path)
   int nsplit, blocks_per_split;
   void* out;            // [M][H*D]
   int* err;
@@ -116,11 +125,13 @@ struct AcceptArgs {
   const float* uniforms;    // [B][k+1]
   int B, k, V;
   void* scratch;            // accept_workspace_bytes(B*T, V) bytes
+  bool stats_ready;         // the chunk statistics at accept_stats_ptr(scratch) are already written
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
 };
 int accept_chunks(int V);
+float* accept_stats_ptr(void* scratch);  // [B*T][accept_chunks(V)][2] chunk max, sum of exp
 size_t accept_workspace_bytes(int rows, int V);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
