@@ -39,8 +39,8 @@ size_t al(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
-  size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits, stats,
-      gemm_part, total;
+  size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, ssq, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits,
+      stats, gemm_part, total;
   size_t win_layer_bytes;
 };
 
@@ -110,6 +110,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   }
   L.h = take(M * d.d_model * 4);
   L.x = take(M * d.d_model * e);
+  L.ssq = take(M * ((d.d_model + 127) / 128) * 4);  // per-row sums of h^2 over 128-column tiles (folded norm)
   L.qkv = take(M * qkv * 4);
   L.q = take(M * HD * e);
   L.win_layer_bytes = (size_t)B * d.n_kv_heads * 16 * d.head_dim * e;
@@ -229,13 +230,35 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     if (e != hipSuccess) return hip_fail(e, what); \
   } while (0)
 
-  NJ_TRY(launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
-                           d.vocab, d.rms_eps, err, s),
-         "embed");
+  // bf16 with every GEMM on the weight-streaming kernel: the RMSNorms are
+  // folded into the GEMMs (the residual GEMMs and the embedding write h * gain
+  // and per-tile sums of h^2; the next GEMM scales its rows by 1/rms)
+  const int F2 = 2 * d.ffn_dim;
+  bool fused = bf && gemm_streams(M, QKV, d.d_model, kEpiStore) && gemm_streams(M, d.d_model, HD, kEpiResidual) &&
+               gemm_streams(M, F2, d.d_model, kEpiSwiglu) && gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual) &&
+               gemm_streams(M, d.vocab, d.d_model, kEpiStore) && aligned16(w->final_norm);
+  for (int l = 0; l < d.n_layers && fused; ++l)
+    fused = aligned16(w->layers[l].attn_norm) && aligned16(w->layers[l].ffn_norm);
+  float* ssq = reinterpret_cast<float*>(ws + L.ssq);
+  const int nt = (d.d_model + 127) / 128;
+  const GemmNorm scale_in{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, nullptr};
+
+  if (fused)
+    NJ_TRY(launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
+                               d.vocab, err, s),
+           "embed");
+  else
+    NJ_TRY(launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
+                             d.vocab, d.rms_eps, err, s),
+           "embed");
   for (int l = 0; l < d.n_layers; ++l) {
     const nj_layer_weights& lw = w->layers[l];
-    if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s), "attn_norm");
-    NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s), "qkv gemm");
+    if (fused) {
+      NJ_TRY(launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, scale_in, gcnt, gpart, s), "qkv gemm");
+    } else {
+      if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s), "attn_norm");
+      NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s), "qkv gemm");
+    }
     void* wk = ws + L.win_k + l * L.win_layer_bytes;
     void* wv = ws + L.win_v + l * L.win_layer_bytes;
     NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
@@ -247,19 +270,37 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),
                 reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, bps, o, err};
     NJ_TRY(launch_attention(aa, s), "attention");
-    NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s), "o gemm");
-    NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s), "ffn_norm");
-    NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu, gcnt, gpart, s), "gate_up gemm");
-    NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s), "down gemm");
+    const void* g_next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : w->final_norm;
+    if (fused) {
+      const GemmNorm to_ffn{nullptr, 0, 0.f, lw.ffn_norm, x, ssq, nullptr};
+      NJ_TRY(launch_gemm_norm(o, lw.w_o, h, M, d.d_model, HD, kEpiResidualNorm, to_ffn, gcnt, gpart, s), "o gemm");
+      NJ_TRY(launch_gemm_norm(x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, scale_in, gcnt, gpart, s),
+             "gate_up gemm");
+      const GemmNorm to_next{nullptr, 0, 0.f, g_next, x, ssq, nullptr};
+      NJ_TRY(launch_gemm_norm(act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidualNorm, to_next, gcnt, gpart, s),
+             "down gemm");
+    } else {
+      NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s), "o gemm");
+      NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s), "ffn_norm");
+      NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, gcnt, gpart, s), "gate_up gemm");
+      NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s), "down gemm");
+    }
   }
-  NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s), "final_norm");
   bool stats_ready = false;
-  if (bf)
-    NJ_TRY(launch_gemm_logits(x, w->lm_head, logits, accept_stats_ptr(ws + L.stats), M, d.vocab, d.d_model, gcnt, gpart,
-                              s, &stats_ready),
+  float* stats = accept_stats_ptr(ws + L.stats);
+  if (fused) {
+    const GemmNorm lm{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, stats};
+    NJ_TRY(launch_gemm_norm(x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiLogits, lm, gcnt, gpart, s),
            "lm_head gemm");
-  else
-    NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
+    stats_ready = true;
+  } else {
+    NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s), "final_norm");
+    if (bf)
+      NJ_TRY(launch_gemm_logits(x, w->lm_head, logits, stats, M, d.vocab, d.d_model, gcnt, gpart, s, &stats_ready),
+             "lm_head gemm");
+    else
+      NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
+  }
   AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, stats_ready, accepted_len,
                 next_tokens, err};
   NJ_TRY(launch_accept(ac, s), "accept");

@@ -83,6 +83,50 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
   norm_row<T>(hv, gain, x + (size_t)row * d, d, eps, sh);
 }
 
+// bf16 path with the RMSNorm folded into the GEMMs: h = E[id], x = bf16(h *
+// gain) and ssq[row][t] = sum of h^2 over columns 128t .. 128t+127 (the 32
+// threads of a 128-column tile: lane order, then a 5-step butterfly), which
+// the first GEMM turns into its row scale.
+__global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
+    const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const bf16_t* __restrict__ embed,
+    const bf16_t* __restrict__ gain, float* __restrict__ h, bf16_t* __restrict__ x, float* __restrict__ ssq, int d,
+    int V, int* __restrict__ err) {
+  const int row = blockIdx.x, b = row / T_, i = row % T_;
+  int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
+  if (tok < 0 || tok >= V) {
+    if (threadIdx.x == 0) flag_error(err, kErrToken);
+    tok = 0;
+  }
+  const bf16_t* e = embed + (size_t)tok * d;
+  const int nt = (d + 127) / 128;
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+    if (j >= ((d + 127) / 128) * 128) break;  // uniform per 32-lane tile
+    float hv[4] = {0.f, 0.f, 0.f, 0.f};
+    float part = 0.f;
+    if (j < d) {
+      float gv[4], o[4];
+      load4(e + j, hv);
+      store4(h + (size_t)row * d + j, hv);
+      load4(gain + j, gv);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = hv[q] * gv[q];
+      store4(x + (size_t)row * d + j, o);
+      part = hv[0] * hv[0];
+      part = fmaf(hv[1], hv[1], part);
+      part = fmaf(hv[2], hv[2], part);
+      part = fmaf(hv[3], hv[3], part);
+    }
+    part += __shfl_xor(part, 1);
+    part += __shfl_xor(part, 2);
+    part += __shfl_xor(part, 4);
+    part += __shfl_xor(part, 8);
+    part += __shfl_xor(part, 16);
+    if ((threadIdx.x & 31) == 0) ssq[(size_t)row * nt + j / 128] = part;
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __restrict__ h,
                                                                const T* __restrict__ gain, T* __restrict__ x,
@@ -232,6 +276,14 @@ hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* draf
     hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h,
                        static_cast<bf16_t*>(x), d, V, eps, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
+                               const void* gain, float* h, void* x, float* ssq, int d, int V, int* err, hipStream_t s) {
+  hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
+                     static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h, static_cast<bf16_t*>(x),
+                     ssq, d, V, err);
   return hipGetLastError();
 }
 

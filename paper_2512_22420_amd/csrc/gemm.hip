@@ -64,6 +64,17 @@ struct GemmK {
   int part_bytes;
   float* stats;     // kEpiLogits: [M][nch][2] chunk max and sum of exp (chunk = this kernel's 128 columns)
   int nch;
+  // RMSNorm folded into the GEMMs.  Input side (any epilogue but the
+  // residual ones): x holds h * gain, and row m of the product is scaled by
+  // 1 / sqrt(sum_t ssq_in[m][t] / K + eps).  Output side (kEpiResidualNorm):
+  // besides h += acc, write xg = bf16(h * gain) and ssq_out[m][tile] = sum of
+  // h^2 over the workgroup's 128 columns, the next GEMM's input side.
+  const float* ssq_in;
+  int nt_in;
+  float eps;
+  const bf16_t* gain;
+  bf16_t* xg;
+  float* ssq_out;
 };
 
 template <int MT, int EPI, int NB>
@@ -71,6 +82,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   constexpr int NG = EPI == kEpiSwiglu ? 2 : 1;
   constexpr int TPW = kNW / NG;                   // output tiles per workgroup
   static_assert(EPI != kEpiLogits || TPW * 16 == kStatChunk, "a workgroup's columns are one statistics chunk");
+  static_assert(EPI != kEpiResidualNorm || TPW * 4 == 32, "a row segment is 32 lanes");
   constexpr int ROWS = MT * 16, NTH = kNW * 64;
   constexpr int CH = ROWS * (kSK / 8);            // 16-byte x pieces per stage
   constexpr int PT = (CH + NTH - 1) / NTH;
@@ -103,6 +115,36 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     xp[c] = a.X + (size_t)min(m0 + row, M - 1) * K;
     xc[c] = col;
     xo[c] = row * kXStride + col;
+  }
+
+  // Loads only the epilogue needs are issued first, so that they complete
+  // under the weight stream instead of adding a round trip at either end.
+  // Input-side norm: this thread's 8 sums-of-squares partials (8 lanes per
+  // row; lane c takes partials c, c+8, ...).
+  __shared__ float s_rinv[ROWS];
+  const bool scaled = a.ssq_in != nullptr;
+  float ssq_v[8];
+  if (scaled) {
+    const int row = min((int)threadIdx.x / 8, ROWS - 1), c = threadIdx.x % 8;
+    const float* sp = a.ssq_in + (size_t)min(m0 + row, M - 1) * a.nt_in;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ssq_v[j] = c + 8 * j < a.nt_in ? sp[c + 8 * j] : 0.f;
+  }
+  // Residual-norm epilogue: the residual rows and gains of this thread's
+  // output pieces (see the epilogue for the piece layout).
+  constexpr int RN_PIECES = ROWS * TPW * 4, RN_IT = (RN_PIECES + NTH - 1) / NTH;
+  f32x4 h_pre[EPI == kEpiResidualNorm ? RN_IT : 1];
+  u32x2 g_pre[EPI == kEpiResidualNorm ? RN_IT : 1];
+  if constexpr (EPI == kEpiResidualNorm) {
+    const int n0 = blockIdx.x * TPW * 16;
+#pragma unroll
+    for (int it = 0; it < RN_IT; ++it) {
+      const int idx = threadIdx.x + it * NTH;
+      const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
+      const int m = min(m0 + row, M - 1), n = min(n0 + c4, Nout - 4);
+      h_pre[it] = *reinterpret_cast<const f32x4*>(static_cast<const float*>(a.Y) + (size_t)m * Nout + n);
+      g_pre[it] = *reinterpret_cast<const u32x2*>(a.gain + n);
+    }
   }
 
   f32x4 acc[MT];
@@ -206,6 +248,21 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     }
   }
 
+  if (scaled) {
+    // 1/rms of this workgroup's rows: lane sums in order, a 3-step butterfly
+    // over the row's 8 lanes (LDS is free: the loop ended on a barrier)
+    float t = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) t += ssq_v[j];
+    t += __shfl_xor(t, 1);
+    t += __shfl_xor(t, 2);
+    t += __shfl_xor(t, 4);
+    if (threadIdx.x % 8 == 0 && (int)threadIdx.x / 8 < ROWS) s_rinv[threadIdx.x / 8] = 1.0f / sqrtf(t / (float)K + a.eps);
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] *= s_rinv[mt * 16 + r];
+  }
+
   if constexpr (EPI == kEpiSwiglu) {
     // up waves hand their accumulators to the gate waves (LDS is free: the
     // stage loop ended on a barrier)
@@ -266,6 +323,49 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       if (idx < PIECES && m < M && n < Nout)
         *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) =
             *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
+    }
+  } else if constexpr (EPI == kEpiResidualNorm) {
+    // h += acc through an LDS-staged tile, 32 lanes per 512-byte row segment;
+    // each row segment also yields bf16(h * gain) and its sum of h^2 (lane
+    // order, then a 5-step butterfly over the 32 lanes)
+    constexpr int OS = TPW * 16 + 4;
+    static_assert(sizeof(xs) >= (size_t)ROWS * OS * sizeof(float), "output tile does not fit");
+    float* ot = reinterpret_cast<float*>(&xs[0][0]);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = acc[mt][i];
+    __syncthreads();
+    const int n0 = blockIdx.x * TPW * 16;
+    constexpr int PIECES = RN_PIECES;
+    static_assert(PIECES % NTH == 0 || PIECES < NTH, "row segments must not straddle passes");
+#pragma unroll
+    for (int it = 0; it < RN_IT; ++it) {
+      const int idx = threadIdx.x + it * NTH;
+      const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
+      const int m = m0 + row, n = n0 + c4;
+      float part = 0.f;
+      const bool ok = idx < PIECES && m < M && n < Nout;
+      if (ok) {
+        f32x4* hp = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
+        const f32x4 hv = h_pre[it] + *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
+        *hp = hv;
+        const u32x2 gw = g_pre[it];
+        u32x2 o;
+        o[0] = pack_bf16x2(hv[0] * bf2f((bf16_t)(gw[0] & 0xffffu)), hv[1] * bf2f((bf16_t)(gw[0] >> 16)));
+        o[1] = pack_bf16x2(hv[2] * bf2f((bf16_t)(gw[1] & 0xffffu)), hv[3] * bf2f((bf16_t)(gw[1] >> 16)));
+        *reinterpret_cast<u32x2*>(a.xg + (size_t)m * Nout + n) = o;
+        part = hv[0] * hv[0];
+        part = fmaf(hv[1], hv[1], part);
+        part = fmaf(hv[2], hv[2], part);
+        part = fmaf(hv[3], hv[3], part);
+      }
+      part += __shfl_xor(part, 1);
+      part += __shfl_xor(part, 2);
+      part += __shfl_xor(part, 4);
+      part += __shfl_xor(part, 8);
+      part += __shfl_xor(part, 16);
+      if ((idx % (TPW * 4)) == 0 && idx < PIECES && m < M) a.ssq_out[(size_t)m * a.nch + blockIdx.x] = part;
     }
   } else {
     if (!active) return;
@@ -453,7 +553,7 @@ hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N,
   if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s);
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0};
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0, nullptr, 0, 0.f, nullptr, nullptr, nullptr};
   if (epi == kEpiStore) return launch_stream<kEpiStore>(a, p, s);
   if (epi == kEpiResidual) return launch_stream<kEpiResidual>(a, p, s);
   return launch_stream<kEpiSwiglu>(a, p, s);
@@ -466,8 +566,28 @@ hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* sta
   if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s);
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, N, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, stats,
-          (N + kStatChunk - 1) / kStatChunk};
+          (N + kStatChunk - 1) / kStatChunk, nullptr, 0, 0.f, nullptr, nullptr, nullptr};
   return launch_stream<kEpiLogits>(a, p, s);
+}
+
+bool gemm_streams(int M, int N, int K, int epi) { return gemm_plan(M, N, K, epi).tile == kTileNone; }
+
+hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
+                            int* counters, float* part, hipStream_t s) {
+  const GemmPlan p = gemm_plan(M, N, K, epi == kEpiResidualNorm ? kEpiResidual : epi == kEpiLogits ? kEpiStore : epi);
+  if (p.tile != kTileNone) return hipErrorInvalidValue;  // the caller checks gemm_streams first
+  const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
+  GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nm.stats,
+          (Nout + kStatChunk - 1) / kStatChunk, nm.ssq_in, nm.nt_in, nm.eps,
+          static_cast<const bf16_t*>(nm.gain), static_cast<bf16_t*>(nm.xg), nm.ssq_out};
+  switch (epi) {
+    case kEpiStore: return launch_stream<kEpiStore>(a, p, s);
+    case kEpiSwiglu: return launch_stream<kEpiSwiglu>(a, p, s);
+    case kEpiLogits: return launch_stream<kEpiLogits>(a, p, s);
+    case kEpiResidualNorm: return launch_stream<kEpiResidualNorm>(a, p, s);
+    default: return launch_stream<kEpiResidual>(a, p, s);
+  }
 }
 
 size_t packed_weight_elems(int N, int K) { return (size_t)((N + 127) / 128) * 128 * (size_t)K; }

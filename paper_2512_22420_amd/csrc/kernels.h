@@ -10,7 +10,9 @@ namespace nj {
 enum { kF32 = 0, kBF16 = 1 };
 // kEpiLogits (internal): fp32 store plus the softmax statistics of every
 // 128-wide output chunk, for the acceptance kernels.
-enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3 };
+// kEpiResidualNorm (internal): residual add that also writes the next
+// RMSNorm's input (see GemmNorm).
+enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3, kEpiResidualNorm = 4 };
 
 // Output tiles of the LDS-tiled kernel for large windows: x rows x weight rows.
 enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
@@ -69,6 +71,26 @@ hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N,
 // weight-streaming kernel; *stats_written says whether it did.
 hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* stats, int M, int N, int K,
                               int* counters, float* part, hipStream_t s, bool* stats_written);
+// RMSNorm folded into the weight-streaming GEMMs.  A producer (residual
+// epilogue kEpiResidualNorm) adds into h and writes xg = bf16(h * gain) and
+// ssq_out[m][t], the sum of h^2 over output columns 128t .. 128t+127; a
+// consumer (x = xg) scales row m of its product by
+// 1 / sqrt(sum_t ssq_in[m][t] / K + eps) before its epilogue.  stats: the
+// kEpiLogits chunk statistics.
+struct GemmNorm {
+  const float* ssq_in;  // consumer side (nullable)
+  int nt_in;            // partials per row (<= 64)
+  float eps;
+  const void* gain;     // producer side: bf16 [N]
+  void* xg;             // bf16 [M][N]
+  float* ssq_out;       // [M][ceil(N / 128)]
+  float* stats;         // kEpiLogits only
+};
+// Whether gemm_plan picks the weight-streaming kernel for this shape (the
+// only one with the folded norm).
+bool gemm_streams(int M, int N, int K, int epi);
+hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
+                            int* counters, float* part, hipStream_t s);
 // The LDS-tiled kernel alone (K % 64 == 0).
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s);
@@ -77,6 +99,11 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
                              const void* embed, const void* gain, float* h, void* x, int d, int V,
                              float eps, int* err, hipStream_t s);
+
+// bf16, norm folded into the GEMMs: h[r] = E[id(r)], x[r] = bf16(h[r] * gain),
+// ssq[r][t] = sum of h[r]^2 over columns 128t .. 128t+127.
+hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
+                               const void* gain, float* h, void* x, float* ssq, int d, int V, int* err, hipStream_t s);
 
 // x[r] = rmsnorm(h[r]) * gain
 hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, int M, int d, float eps,
