@@ -39,8 +39,8 @@ size_t al(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
-  size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, ssq, qkv, q, win_k, win_v, part_o, part_ml, o, act, logits,
-      stats, gemm_part, total;
+  size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, ssq, rope_cs, qkv, q, win_k, win_v, part_o, part_ml, o, act,
+      logits, stats, gemm_part, total;
   size_t win_layer_bytes;
 };
 
@@ -111,6 +111,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   L.h = take(M * d.d_model * 4);
   L.x = take(M * d.d_model * e);
   L.ssq = take(M * ((d.d_model + 127) / 128) * 4);  // per-row sums of h^2 over 128-column tiles (folded norm)
+  L.rope_cs = take(M * 64 * 2 * 4);                  // the step's RoPE (cos, sin) table (bf16 path)
   L.qkv = take(M * qkv * 4);
   L.q = take(M * HD * e);
   L.win_layer_bytes = (size_t)B * d.n_kv_heads * 16 * d.head_dim * e;
@@ -245,7 +246,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
 
   if (fused)
     NJ_TRY(launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
-                               d.vocab, err, s),
+                               d.vocab, err, context_lens, d.rope_theta, reinterpret_cast<float*>(ws + L.rope_cs), s),
            "embed");
   else
     NJ_TRY(launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
@@ -253,18 +254,22 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
            "embed");
   for (int l = 0; l < d.n_layers; ++l) {
     const nj_layer_weights& lw = w->layers[l];
-    if (fused) {
-      NJ_TRY(launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, scale_in, gcnt, gpart, s), "qkv gemm");
+    void* wk = ws + L.win_k + l * L.win_layer_bytes;
+    void* wv = ws + L.win_v + l * L.win_layer_bytes;
+    int32_t* snap = l == 0 ? reinterpret_cast<int32_t*>(ws + L.ctx_snap) : nullptr;
+    int* acnt = bf ? reinterpret_cast<int*>(ws + L.attn_cnt) : nullptr;
+    if (fused) {  // RoPE and the window store in the QKV GEMM's epilogue
+      const QkvRope rope{context_lens, T, d.n_heads, d.n_kv_heads, reinterpret_cast<const float*>(ws + L.rope_cs), q,
+                         wk, wv, snap, acnt};
+      NJ_TRY(launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiQkvRope, scale_in, gcnt, gpart, s, &rope),
+             "qkv gemm");
     } else {
       if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s), "attn_norm");
       NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s), "qkv gemm");
+      NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
+                                wk, wv, snap, acnt, s),
+             "rope");
     }
-    void* wk = ws + L.win_k + l * L.win_layer_bytes;
-    void* wv = ws + L.win_v + l * L.win_layer_bytes;
-    NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
-                              wk, wv, l == 0 ? reinterpret_cast<int32_t*>(ws + L.ctx_snap) : nullptr,
-                              bf ? reinterpret_cast<int*>(ws + L.attn_cnt) : nullptr, s),
-           "rope");
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),

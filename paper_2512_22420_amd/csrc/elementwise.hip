@@ -87,11 +87,25 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
 // gain) and ssq[row][t] = sum of h^2 over columns 128t .. 128t+127 (the 32
 // threads of a 128-column tile: lane order, then a 5-step butterfly), which
 // the first GEMM turns into its row scale.
+// It also writes the RoPE table of the step, rope_cs[row][j] = (cos, sin) of
+// pos * theta^(-j/64), pos = ctx[b] + i, for the 64 rotation pairs of a
+// 128-dim head (angle formed and reduced to [-pi, pi] in fp64, then fp32
+// sin/cos, as in rope_window_kernel); every head and layer of the step uses it.
 __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const bf16_t* __restrict__ embed,
     const bf16_t* __restrict__ gain, float* __restrict__ h, bf16_t* __restrict__ x, float* __restrict__ ssq, int d,
-    int V, int* __restrict__ err) {
+    int V, int* __restrict__ err, const int32_t* __restrict__ ctx, float theta, float* __restrict__ rope_cs) {
   const int row = blockIdx.x, b = row / T_, i = row % T_;
+  if (rope_cs && threadIdx.x < 64) {
+    const int j = threadIdx.x;
+    const double ang = (double)(max(ctx[b], 0) + i) * pow((double)theta, -(double)j / 64.0);
+    const double kq = rint(ang * 0.15915494309189535);
+    const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
+    float sn, cs;
+    sincosf((float)red, &sn, &cs);
+    rope_cs[((size_t)row * 64 + j) * 2] = cs;
+    rope_cs[((size_t)row * 64 + j) * 2 + 1] = sn;
+  }
   int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
   if (tok < 0 || tok >= V) {
     if (threadIdx.x == 0) flag_error(err, kErrToken);
@@ -280,10 +294,11 @@ hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* draf
 }
 
 hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
-                               const void* gain, float* h, void* x, float* ssq, int d, int V, int* err, hipStream_t s) {
+                               const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
+                               const int32_t* ctx, float theta, float* rope_cs, hipStream_t s) {
   hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
                      static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h, static_cast<bf16_t*>(x),
-                     ssq, d, V, err);
+                     ssq, d, V, err, ctx, theta, rope_cs);
   return hipGetLastError();
 }
 

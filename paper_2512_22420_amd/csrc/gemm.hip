@@ -78,6 +78,7 @@ struct GemmK {
   const bf16_t* gain;
   bf16_t* xg;
   float* ssq_out;
+  QkvRope rope;     // kEpiQkvRope
 };
 
 // The weight stream of one 16-row weight tile (wp: this lane's piece of k-step
@@ -161,6 +162,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   constexpr int TPW = kNW / NG;                   // output tiles per workgroup
   static_assert(EPI != kEpiLogits || TPW * 16 == kStatChunk, "a workgroup's columns are one statistics chunk");
   static_assert(EPI != kEpiResidualNorm || TPW * 4 == 32, "a row segment is 32 lanes");
+  static_assert(EPI != kEpiQkvRope || TPW * 16 == 128, "a workgroup's columns are one head");
   constexpr int ROWS = MT * 16, NTH = kNW * 64;
   constexpr int CH = ROWS * (kSK / 8);            // 16-byte x pieces per stage
   constexpr int PT = (CH + NTH - 1) / NTH;
@@ -206,6 +208,18 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     const float* sp = a.ssq_in + (size_t)min(m0 + row, M - 1) * a.nt_in;
 #pragma unroll
     for (int j = 0; j < 8; ++j) ssq_v[j] = c + 8 * j < a.nt_in ? sp[c + 8 * j] : 0.f;
+  }
+  // QKV + RoPE epilogue: the (cos, sin) of this thread's rotation units
+  // (unit u = thread + it * NTH: row u / 64, pair u % 64).
+  constexpr int RP_IT = (ROWS * 64 + NTH - 1) / NTH;
+  u32x2 cs_pre[EPI == kEpiQkvRope ? RP_IT : 1];
+  if constexpr (EPI == kEpiQkvRope) {
+#pragma unroll
+    for (int it = 0; it < RP_IT; ++it) {
+      const int u = threadIdx.x + it * NTH;
+      const int m = min(m0 + u / 64, M - 1), j = u % 64;
+      cs_pre[it] = *reinterpret_cast<const u32x2*>(a.rope.cs + ((size_t)m * 64 + j) * 2);
+    }
   }
   // Residual-norm epilogue: the residual rows and gains of this thread's
   // output pieces (see the epilogue for the piece layout).
@@ -340,6 +354,79 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       if (idx < PIECES && m < M && n < Nout)
         *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) =
             *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
+    }
+  } else if constexpr (EPI == kEpiQkvRope) {
+    // this workgroup's 128 columns are head hd; rows m0 .. m0+ROWS-1
+    constexpr int OS = TPW * 16 + 4;
+    static_assert(sizeof(xs) >= (size_t)ROWS * OS * sizeof(float), "output tile does not fit");
+    float* ot = reinterpret_cast<float*>(&xs[0][0]);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = acc[mt][i];
+    __syncthreads();
+    const QkvRope& rp = a.rope;
+    const int hd = blockIdx.x, T = rp.T, H = rp.H, Hkv = rp.Hkv;
+    const int rows = min(ROWS, M - m0);
+    if (hd < H + Hkv) {
+      bf16_t* base = static_cast<bf16_t*>(hd < H ? rp.q_out : rp.win_k);
+#pragma unroll
+      for (int it = 0; it < RP_IT; ++it) {
+        const int u = threadIdx.x + it * NTH, row = u / 64, j = u % 64, m = m0 + row;
+        if (row >= rows) break;
+        const int b = m / T, i = m % T;
+        const float cs = __uint_as_float(cs_pre[it][0]), sn = __uint_as_float(cs_pre[it][1]);
+        const float x1 = ot[row * OS + j], x2 = ot[row * OS + j + 64];
+        bf16_t* dst = hd < H ? base + ((size_t)m * H + hd) * 128
+                             : base + (((size_t)b * Hkv + (hd - H)) * kBlock + i) * 128;
+        dst[j] = f2bf(x1 * cs - x2 * sn);
+        dst[j + 64] = f2bf(x2 * cs + x1 * sn);
+      }
+      // unused slots T..15 of the K window blocks of the sequences that start here
+      if (hd >= H) {
+        bf16_t* wb0 = static_cast<bf16_t*>(rp.win_k);
+        const int nz = (kBlock - T) * 128 / 8;  // 16-byte pieces
+        for (int b = (m0 + T - 1) / T; b * T < m0 + rows; ++b)
+          for (int u = threadIdx.x; u < nz; u += NTH)
+            *reinterpret_cast<u32x4*>(wb0 + (((size_t)b * Hkv + (hd - H)) * kBlock + T) * 128 + u * 8) =
+                u32x4{0u, 0u, 0u, 0u};
+      }
+    } else {
+      // V: one thread per (sequence, head dim) writes the dim's whole 16-slot
+      // window row (its T values, then zeros) as two 16-byte stores, for the
+      // sequences whose rows all lie in this workgroup (the others' rows are
+      // written one value at a time)
+      bf16_t* vb = static_cast<bf16_t*>(rp.win_v);
+      const int gv = hd - H - Hkv;
+      const int b0 = (m0 + T - 1) / T, b1 = (m0 + rows) / T;  // whole sequences [b0, b1)
+      for (int u = threadIdx.x; u < (b1 - b0) * 128; u += NTH) {
+        const int b = b0 + u / 128, dd = u % 128;
+        uint32_t w[8];
+#pragma unroll
+        for (int p2 = 0; p2 < 8; ++p2) {
+          const int i0 = 2 * p2, i1 = 2 * p2 + 1;
+          const float v0 = i0 < T ? ot[(b * T + i0 - m0) * OS + dd] : 0.f;
+          const float v1 = i1 < T ? ot[(b * T + i1 - m0) * OS + dd] : 0.f;
+          w[p2] = pack_bf16x2(v0, v1);
+        }
+        u32x4* dst = reinterpret_cast<u32x4*>(vb + (((size_t)b * Hkv + gv) * 128 + dd) * kBlock);
+        dst[0] = u32x4{w[0], w[1], w[2], w[3]};
+        dst[1] = u32x4{w[4], w[5], w[6], w[7]};
+      }
+      for (int u = threadIdx.x; u < rows * 128; u += NTH) {  // rows of sequences cut by the block edge
+        const int row = u / 128, dd = u % 128, m = m0 + row, b = m / T, i = m % T;
+        if (b >= b0 && b < b1) continue;
+        vb[(((size_t)b * Hkv + gv) * 128 + dd) * kBlock + i] = f2bf(ot[row * OS + dd]);
+        if (i == 0)
+          for (int sl = T; sl < kBlock; ++sl) vb[(((size_t)b * Hkv + gv) * 128 + dd) * kBlock + sl] = 0;
+      }
+    }
+    if (hd == 0 && m0 == 0) {
+      const int B = M / T;
+      for (int u = threadIdx.x; u < B; u += NTH)
+        if (rp.ctx_snap) rp.ctx_snap[u] = rp.ctx[u];
+      for (int u = threadIdx.x; u < B * Hkv; u += NTH)
+        if (rp.attn_cnt) rp.attn_cnt[u] = 0;
     }
   } else if constexpr (EPI == kEpiResidualNorm) {
     // h += acc through an LDS-staged tile, 32 lanes per 512-byte row segment;
@@ -693,7 +780,7 @@ hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N,
   if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s);
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0, nullptr, 0, 0.f, nullptr, nullptr, nullptr};
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0, nullptr, 0, 0.f, nullptr, nullptr, nullptr, {}};
   if (epi == kEpiStore) return launch_logits(a, p, s);  // stats == nullptr: plain store
   if (epi == kEpiResidual) return launch_stream<kEpiResidual>(a, p, s);
   return launch_stream<kEpiSwiglu>(a, p, s);
@@ -706,22 +793,24 @@ hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* sta
   if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s);
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, N, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, stats,
-          (N + kStatChunk - 1) / kStatChunk, nullptr, 0, 0.f, nullptr, nullptr, nullptr};
+          (N + kStatChunk - 1) / kStatChunk, nullptr, 0, 0.f, nullptr, nullptr, nullptr, {}};
   return launch_logits(a, p, s);
 }
 
 bool gemm_streams(int M, int N, int K, int epi) { return gemm_plan(M, N, K, epi).tile == kTileNone; }
 
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
-                            int* counters, float* part, hipStream_t s) {
-  const GemmPlan p = gemm_plan(M, N, K, epi == kEpiResidualNorm ? kEpiResidual : epi == kEpiLogits ? kEpiStore : epi);
+                            int* counters, float* part, hipStream_t s, const QkvRope* rope) {
+  const int pe = epi == kEpiResidualNorm ? kEpiResidual : (epi == kEpiLogits || epi == kEpiQkvRope) ? kEpiStore : epi;
+  const GemmPlan p = gemm_plan(M, N, K, pe);
   if (p.tile != kTileNone) return hipErrorInvalidValue;  // the caller checks gemm_streams first
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nm.stats,
           (Nout + kStatChunk - 1) / kStatChunk, nm.ssq_in, nm.nt_in, nm.eps,
-          static_cast<const bf16_t*>(nm.gain), static_cast<bf16_t*>(nm.xg), nm.ssq_out};
+          static_cast<const bf16_t*>(nm.gain), static_cast<bf16_t*>(nm.xg), nm.ssq_out, rope ? *rope : QkvRope{}};
   switch (epi) {
+    case kEpiQkvRope: return launch_stream<kEpiQkvRope>(a, p, s);
     case kEpiStore: return launch_stream<kEpiStore>(a, p, s);
     case kEpiSwiglu: return launch_stream<kEpiSwiglu>(a, p, s);
     case kEpiLogits: return launch_logits(a, p, s);

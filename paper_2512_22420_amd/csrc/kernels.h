@@ -12,7 +12,9 @@ enum { kF32 = 0, kBF16 = 1 };
 // 128-wide output chunk, for the acceptance kernels.
 // kEpiResidualNorm (internal): residual add that also writes the next
 // RMSNorm's input (see GemmNorm).
-enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3, kEpiResidualNorm = 4 };
+// kEpiQkvRope (internal): QKV projection whose epilogue applies RoPE and
+// stores q and the window K/V blocks (see QkvRope).
+enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3, kEpiResidualNorm = 4, kEpiQkvRope = 5 };
 
 // Output tiles of the LDS-tiled kernel for large windows: x rows x weight rows.
 enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
@@ -86,11 +88,29 @@ struct GemmNorm {
   float* ssq_out;       // [M][ceil(N / 128)]
   float* stats;         // kEpiLogits only
 };
+// kEpiQkvRope: the QKV GEMM's 128-column groups are its heads (head_dim 128):
+// q heads are rotated and stored to q_out [M][H][128], k heads rotated into
+// the window blocks win_k [B][Hkv][16][128], v heads into win_v
+// [B][Hkv][128][16]; slots T..15 of the window blocks are zeroed.  Rotate-half
+// pairs (j, j+64) turn by the step's RoPE table cs [M][64] of (cos, sin)
+// (written by launch_embed_gather).  Workgroup 0 also stores ctx_snap
+// (nullable) and clears the attention split counters attn_cnt [B*Hkv]
+// (nullable).
+struct QkvRope {
+  const int32_t* ctx;
+  int T, H, Hkv;
+  const float* cs;
+  void* q_out;
+  void* win_k;
+  void* win_v;
+  int32_t* ctx_snap;
+  int* attn_cnt;
+};
 // Whether gemm_plan picks the weight-streaming kernel for this shape (the
 // only one with the folded norm).
 bool gemm_streams(int M, int N, int K, int epi);
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
-                            int* counters, float* part, hipStream_t s);
+                            int* counters, float* part, hipStream_t s, const QkvRope* rope = nullptr);
 // The LDS-tiled kernel alone (K % 64 == 0).
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s);
@@ -101,9 +121,11 @@ hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* draf
                              float eps, int* err, hipStream_t s);
 
 // bf16, norm folded into the GEMMs: h[r] = E[id(r)], x[r] = bf16(h[r] * gain),
-// ssq[r][t] = sum of h[r]^2 over columns 128t .. 128t+127.
+// ssq[r][t] = sum of h[r]^2 over columns 128t .. 128t+127; and the step's RoPE
+// table rope_cs[r][j] = (cos, sin) of (ctx[b] + i) * theta^(-j/64) (nullable).
 hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
-                               const void* gain, float* h, void* x, float* ssq, int d, int V, int* err, hipStream_t s);
+                               const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
+                               const int32_t* ctx, float theta, float* rope_cs, hipStream_t s);
 
 // x[r] = rmsnorm(h[r]) * gain
 hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, int M, int d, float eps,
