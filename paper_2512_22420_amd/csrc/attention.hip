@@ -26,6 +26,7 @@ namespace {
 
 constexpr int kD = 128;  // head dim of the bf16 path
 constexpr int kMaxExtraSplits = 4096;  // KV-split workgroups beyond one per (sequence, KV head)
+constexpr int kResidentWorkgroups = 512;  // 256 CUs x 2 attention workgroups
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -75,7 +76,8 @@ __device__ __forceinline__ int v_lds(int dim, int unit8) {  // element offset in
 // weights 2^(m_s - M) are formed once; then each thread merges 4 head dims of
 // one query row per unit, with the loads of all splits of a unit in flight
 // together.  `lds` is the kernel's staging buffer (free by now).
-constexpr int kMergeSplits = 8;  // split partials loaded per batch
+constexpr int kMergeSplits = 8;   // split partials loaded together per unit
+constexpr int kMergeUnits = 4;    // units merged together per thread
 __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT, int G, int b, int kvh,
                              __amdgpu_buffer_rsrc_t ors, __amdgpu_buffer_rsrc_t mrs, float* lds, int lds_floats) {
   __shared__ int s_last;
@@ -87,72 +89,93 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
   if (!s_last) return;
   const int rpad = RT * 16;
   const size_t pbase = (size_t)pair * nsplit * rpad;
-  // s_f[qr][sp]: weight of split sp for row qr (0 for empty splits); s_w[qr]: 1 / sum_s f l_s
+  // s_f[qr][sp]: weight 2^(m_sp - M) of split sp for row qr (0 for empty
+  // splits); s_w[qr]: 1 / sum_sp weight * l_sp.  The (m, l) of every row and
+  // split are loaded in one pass.
   float* s_f = lds;
-  float* s_w = lds + R * nsplit;
-  const bool staged = R * nsplit + R <= lds_floats;
-  if (staged) {
+  float* s_l = lds + R * nsplit;
+  float* s_w = lds + 2 * R * nsplit;
+  if (2 * R * nsplit + R <= lds_floats) {
     for (int u = threadIdx.x; u < R * nsplit; u += 256) {
       const int qr = u / nsplit, sp = u % nsplit;
-      s_f[u] = coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)sp * rpad + qr) * 2) * 4));
+      const uint32_t off = (uint32_t)(((pbase + (size_t)sp * rpad + qr) * 2) * 4);
+      s_f[u] = coherent_load_f32(mrs, off);
+      s_l[u] = coherent_load_f32(mrs, off + 4);
     }
     __syncthreads();
     for (int qr = threadIdx.x; qr < R; qr += 256) {
       float mx = -INFINITY;
       for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, s_f[qr * nsplit + sp]);
+      float wsum = 0.f;
       for (int sp = 0; sp < nsplit; ++sp) {
         const float m = s_f[qr * nsplit + sp];
-        s_f[qr * nsplit + sp] = (m == -INFINITY) ? 0.f : exp2f(m - mx);
-      }
-    }
-    __syncthreads();
-    // l_s weighted sums (one thread per row; the loads of all splits together)
-    for (int qr = threadIdx.x; qr < R; qr += 256) {
-      float wsum = 0.f;
-      for (int s0 = 0; s0 < nsplit; s0 += kMergeSplits) {
-        float lv[kMergeSplits];
-#pragma unroll
-        for (int j = 0; j < kMergeSplits; ++j)
-          lv[j] = s0 + j < nsplit ? coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)(s0 + j) * rpad + qr) * 2 + 1) * 4)) : 0.f;
-#pragma unroll
-        for (int j = 0; j < kMergeSplits; ++j)
-          if (s0 + j < nsplit) wsum += s_f[qr * nsplit + s0 + j] * lv[j];
+        const float f = (m == -INFINITY) ? 0.f : exp2f(m - mx);
+        s_f[qr * nsplit + sp] = f;
+        wsum += f * s_l[qr * nsplit + sp];
       }
       s_w[qr] = 1.0f / wsum;
     }
     __syncthreads();
+    // each unit: 4 head dims of one row.  A thread takes up to kMergeUnits
+    // units at a time and issues the loads of all their splits (kMergeSplits
+    // at a time) together.
+    const int nunits = R * (kD / 4);
+    for (int ub = 0; ub < nunits; ub += 256 * kMergeUnits) {
+      f32x4 acc[kMergeUnits];
+#pragma unroll
+      for (int q = 0; q < kMergeUnits; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s0 = 0; s0 < nsplit; s0 += kMergeSplits) {
+        f32x4 ov[kMergeUnits][kMergeSplits];
+#pragma unroll
+        for (int q = 0; q < kMergeUnits; ++q) {
+          const int u = min(ub + (int)threadIdx.x + q * 256, nunits - 1);
+          const int qr = u / (kD / 4), d = (u % (kD / 4)) * 4;
+#pragma unroll
+          for (int j = 0; j < kMergeSplits; ++j) {
+            const int sp = min(s0 + j, nsplit - 1);
+            ov[q][j] = coherent_load(ors, (uint32_t)(((pbase + (size_t)sp * rpad + qr) * kD + d) * 4));
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < kMergeUnits; ++q) {
+          const int qr = min(ub + (int)threadIdx.x + q * 256, nunits - 1) / (kD / 4);
+#pragma unroll
+          for (int j = 0; j < kMergeSplits; ++j)
+            if (s0 + j < nsplit) acc[q] += s_f[qr * nsplit + s0 + j] * ov[q][j];
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kMergeUnits; ++q) {
+        const int u = ub + (int)threadIdx.x + q * 256;
+        if (u >= nunits) break;
+        const int qr = u / (kD / 4), d = (u % (kD / 4)) * 4;
+        const float inv = s_w[qr];
+        const int i = qr / G, hh = qr % G;
+        u32x2 o;
+        o[0] = pack_bf16x2(acc[q][0] * inv, acc[q][1] * inv);
+        o[1] = pack_bf16x2(acc[q][2] * inv, acc[q][3] * inv);
+        *reinterpret_cast<u32x2*>(a.out + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d) = o;
+      }
+    }
+    return;
   }
+  // too many splits to stage (not reached by attention_plan's splits): direct loads
   for (int u = threadIdx.x; u < R * (kD / 4); u += 256) {
     const int qr = u / (kD / 4), d = (u % (kD / 4)) * 4;
+    float mx = -INFINITY;
+    for (int sp = 0; sp < nsplit; ++sp)
+      mx = fmaxf(mx, coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)sp * rpad + qr) * 2) * 4)));
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    float inv;
-    if (staged) {
-      for (int s0 = 0; s0 < nsplit; s0 += kMergeSplits) {
-        f32x4 ov[kMergeSplits];
-#pragma unroll
-        for (int j = 0; j < kMergeSplits; ++j)
-          ov[j] = s0 + j < nsplit ? coherent_load(ors, (uint32_t)(((pbase + (size_t)(s0 + j) * rpad + qr) * kD + d) * 4))
-                                  : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < kMergeSplits; ++j)
-          if (s0 + j < nsplit) acc += s_f[qr * nsplit + s0 + j] * ov[j];
-      }
-      inv = s_w[qr];
-    } else {  // too many splits to stage: direct loads
-      float mx = -INFINITY;
-      for (int sp = 0; sp < nsplit; ++sp)
-        mx = fmaxf(mx, coherent_load_f32(mrs, (uint32_t)(((pbase + (size_t)sp * rpad + qr) * 2) * 4)));
-      float wsum = 0.f;
-      for (int sp = 0; sp < nsplit; ++sp) {
-        const size_t base = pbase + (size_t)sp * rpad + qr;
-        const float m = coherent_load_f32(mrs, (uint32_t)((base * 2) * 4));
-        if (m == -INFINITY) continue;  // empty split: only its marker was written
-        const float f = exp2f(m - mx);
-        wsum += f * coherent_load_f32(mrs, (uint32_t)((base * 2 + 1) * 4));
-        acc += f * coherent_load(ors, (uint32_t)((base * kD + d) * 4));
-      }
-      inv = 1.0f / wsum;
+    float wsum = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const size_t base = pbase + (size_t)sp * rpad + qr;
+      const float m = coherent_load_f32(mrs, (uint32_t)((base * 2) * 4));
+      if (m == -INFINITY) continue;  // empty split: only its marker was written
+      const float f = exp2f(m - mx);
+      wsum += f * coherent_load_f32(mrs, (uint32_t)((base * 2 + 1) * 4));
+      acc += f * coherent_load(ors, (uint32_t)((base * kD + d) * 4));
     }
+    const float inv = 1.0f / wsum;
     const int i = qr / G, hh = qr % G;
     u32x2 o;
     o[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
@@ -367,28 +390,34 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
       }
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < 16 * kD; idx += 256) {
-      const int qr16 = idx / kD, d = idx % kD;
+    // thread: 4 consecutive head dims of one query row per unit (2 units)
+    for (int u = threadIdx.x; u < 16 * (kD / 4); u += 256) {
+      const int qr16 = u / (kD / 4), d = (u % (kD / 4)) * 4;
       const int qr = t * 16 + qr16;
       float mx = -INFINITY;
 #pragma unroll
       for (int w = 0; w < NTP; ++w) mx = fmaxf(mx, s_m[w * 16 + qr16]);
-      float acc = 0.f, wsum = 0.f;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      float wsum = 0.f;
       if (mx != -INFINITY) {
 #pragma unroll
         for (int w = 0; w < NTP; ++w) {
           const float f = (s_m[w * 16 + qr16] == -INFINITY) ? 0.f : exp2f(s_m[w * 16 + qr16] - mx);
           wsum += f * s_l[w * 16 + qr16];
-          acc += f * s_o[(w * kD + d) * 17 + qr16];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += f * s_o[(w * kD + d + e) * 17 + qr16];
         }
       }
       if (qr < R) {
         if (nsplit == 1) {
           const int i = qr / G, hh = qr % G;
-          a.out[((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d] = f2bf(acc / wsum);
+          u32x2 ov;
+          ov[0] = pack_bf16x2(acc[0] / wsum, acc[1] / wsum);
+          ov[1] = pack_bf16x2(acc[2] / wsum, acc[3] / wsum);
+          *reinterpret_cast<u32x2*>(a.out + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d) = ov;
         } else {
           const size_t base = ((size_t)pair * nsplit + split) * (RT * 16) + qr;
-          coherent_store_f32(ors, (uint32_t)((base * kD + d) * 4), acc);
+          coherent_store(ors, (uint32_t)((base * kD + d) * 4), acc);
           if (d == 0) {
             coherent_store_f32(mrs, (uint32_t)(base * 2 * 4), mx);
             coherent_store_f32(mrs, (uint32_t)((base * 2 + 1) * 4), wsum);
@@ -493,7 +522,12 @@ void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, i
   // blocks per split, and at most pairs + kMaxExtraSplits workgroups, which
   // bounds the partial buffer whatever the context length.
   const int pairs = B * Hkv;
-  int ns = std::max((2048 + pairs - 1) / pairs, (max_blocks + 63) / 64);
+  const int ns_len = (max_blocks + 63) / 64;
+  int ns = std::max((2048 + pairs - 1) / pairs, ns_len);
+  // keep every workgroup resident at once (2 per CU) when the split-length
+  // bound allows: a split that starts late holds up the merge of its
+  // (sequence, KV head)
+  if (pairs * ns > kResidentWorkgroups) ns = std::max(ns_len, kResidentWorkgroups / pairs);
   ns = std::min(ns, 1 + kMaxExtraSplits / pairs);
   ns = std::min(ns, (max_blocks + 7) / 8);
   ns = std::max(ns, 1);
