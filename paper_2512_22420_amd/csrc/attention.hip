@@ -106,12 +106,14 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
     for (int qr = threadIdx.x; qr < R; qr += 256) {
       float mx = -INFINITY;
       for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, s_f[qr * nsplit + sp]);
+      // an empty split wrote only its -inf marker: its l and o slots hold
+      // whatever the workspace held before, so it is masked out, not weighted 0
       float wsum = 0.f;
       for (int sp = 0; sp < nsplit; ++sp) {
         const float m = s_f[qr * nsplit + sp];
         const float f = (m == -INFINITY) ? 0.f : exp2f(m - mx);
         s_f[qr * nsplit + sp] = f;
-        wsum += f * s_l[qr * nsplit + sp];
+        if (m != -INFINITY) wsum += f * s_l[qr * nsplit + sp];
       }
       s_w[qr] = 1.0f / wsum;
     }
@@ -141,7 +143,7 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
           const int qr = min(ub + (int)threadIdx.x + q * 256, nunits - 1) / (kD / 4);
 #pragma unroll
           for (int j = 0; j < kMergeSplits; ++j)
-            if (s0 + j < nsplit) acc[q] += s_f[qr * nsplit + s0 + j] * ov[q][j];
+            if (s0 + j < nsplit && s_f[qr * nsplit + s0 + j] != 0.f) acc[q] += s_f[qr * nsplit + s0 + j] * ov[q][j];
         }
       }
 #pragma unroll

@@ -285,3 +285,23 @@ def test_steps_of_different_sizes_share_one_workspace():
         assert err_s == 0 and err_f == 0
         assert torch.equal(io_s.logits, io_f.logits), (B, k)
         assert torch.equal(io_s.next_tokens, io_f.next_tokens), (B, k)
+
+
+@pytest.mark.parametrize("k", [3, 12])
+def test_stale_workspace_contents_never_reach_the_outputs(k):
+    """A step reads no workspace memory that it has not written first (beyond
+    the error word and the split-K counters, which workspace_init zeroes and
+    every kernel leaves at zero): with the rest of the workspace filled with
+    0xFF bytes (NaN bit patterns), outputs equal those of a fresh workspace,
+    bitwise.  The contexts leave some KV splits of the attention empty."""
+    ctx = np.array([0, 5, 37, 100, 16, 250], dtype=np.int32)
+    x = _inputs(SMALL_BF16, ctx, k, seed=21)
+    model, _, io_f, _, err_f = _run(SMALL_BF16, x)
+    ws = Workspace(SMALL_BF16, len(ctx), k)
+    zero_prefix = 256 + 4096  # error word, split-K arrival counters
+    ws.buf[zero_prefix:].fill_(255)
+    _, _, io_s, _, err_s = _run(SMALL_BF16, x, model=model, ws=ws)
+    assert err_f == 0 and err_s == 0
+    assert torch.equal(io_s.logits, io_f.logits)
+    assert torch.equal(io_s.next_tokens, io_f.next_tokens)
+    assert torch.equal(io_s.accepted_len, io_f.accepted_len)
