@@ -320,7 +320,7 @@ def main():
     lm_bytes = R.lm_head_bytes(shape, M)
     lm_gbs = lm_bytes / (lm_us * 1e-6) / 1e9
     log(f"lm_head gemm M={M}: {lm_us:.1f} us, {lm_gbs:.0f} GB/s")
-    roofline = {"kernel": "gemm_bf16 (LM head, M=%d, N=%d, K=%d)" % (M, shape.vocab, shape.d_model),
+    roofline = {"kernel": "gemm_logits_kernel (LM head, M=%d, N=%d, K=%d)" % (M, shape.vocab, shape.d_model),
                 "bound": "hbm", "achieved": round(lm_gbs, 1), "peak": R.HBM_BYTES_PER_S / 1e9, "unit": "GB/s",
                 "frac": round(lm_gbs / (R.HBM_BYTES_PER_S / 1e9), 4),
                 "traffic": measured_traffic(M),
