@@ -43,7 +43,7 @@ struct AccK {
   float* rowstat;         // [B*T][2]: max, 1/sum of every window row
   int32_t* okflag;        // [B*T]: accept test of the draft row i scores (rows 0..k-1)
   double* tsum;           // [B][ntile]: tile sums of the draw row
-  int* counters;          // [B]: draw arrivals (zeroed by accept_rows)
+  int* counters;          // [B][kCounterStride]: draw arrivals (zeroed by accept_rows)
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
@@ -113,7 +113,7 @@ __global__ __launch_bounds__(kRowThreads) void accept_rows_kernel(AccK a) {
       const float p = expf(lx - m) * inv_s;
       a.okflag[row] = !bad && ((qx <= 0.f) || (a.uniforms[row] < p / qx));
     }
-    if (i == 0) a.counters[b] = 0;
+    if (i == 0) a.counters[b * kCounterStride] = 0;
   }
 }
 
@@ -316,7 +316,7 @@ __global__ __launch_bounds__(256) void accept_draw_kernel(AccK a) {
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0)
-    s_last = (__hip_atomic_fetch_add(a.counters + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+    s_last = (__hip_atomic_fetch_add(a.counters + b * kCounterStride, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
               (int)gridDim.y - 1);
   __syncthreads();
   if (!s_last) return;
@@ -336,7 +336,7 @@ int accept_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
 size_t accept_workspace_bytes(int rows, int V) {
   const int ntile = (V + kTile - 1) / kTile;
   return al256((size_t)rows * accept_chunks(V) * 2 * 4) + al256((size_t)rows * 2 * 4) +
-         al256((size_t)rows * ntile * 8) + al256((size_t)rows * 4) + al256((size_t)rows * 4);
+         al256((size_t)rows * ntile * 8) + al256((size_t)rows * 4) + al256((size_t)rows * kCounterStride * 4);
 }
 
 float* accept_stats_ptr(void* scratch) { return static_cast<float*>(scratch); }

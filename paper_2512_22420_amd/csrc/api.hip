@@ -101,7 +101,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   // nightjar_workspace_init and left at zero by every GEMM.
   L.gemm_cnt = take(kGemmCounterBytes);
   L.ctx_snap = take((size_t)B * 4);  // context lengths read by the verify step, for the KV append
-  L.attn_cnt = take((size_t)B * d.n_kv_heads * 4);  // attention split arrivals (cleared before each launch)
+  L.attn_cnt = take((size_t)B * d.n_kv_heads * kCounterStride * 4);  // attention split arrivals (cleared before each launch)
   size_t part = 0;
   if (d.dtype == NJ_BF16) {
     GemmShape gs[5];
@@ -221,8 +221,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   const int dt = bf ? kBF16 : kF32;
   const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
 
-  int nsplit = 1, bps = max_blocks;
-  if (bf) attention_plan(B, d.n_kv_heads, T, G, max_blocks, &nsplit, &bps);
+  const int nsplit = bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1;
 
   hipError_t e;
 #define NJ_TRY(call, what)                   \
@@ -273,7 +272,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),
-                reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, bps, o, err};
+                reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, o, err};
     NJ_TRY(launch_attention(aa, s), "attention");
     const void* g_next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : w->final_norm;
     if (fused) {
@@ -456,7 +455,7 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
               : gemm_tile_choose(M, N, K, epilogue, tile);
   }
   if (p.nkc > 1 && p.counter_bytes > kGemmCounterBytes)
-    return fail(NJ_EINVAL, "a split-K run may cover at most %zu output tiles", kGemmCounterBytes / 4);
+    return fail(NJ_EINVAL, "a split-K run may cover at most %zu output tiles", kGemmCounterBytes / (kCounterStride * 4));
   if (p.part_bytes >= kMaxPartBytes) return fail(NJ_EINVAL, "split-K partials would take 2 GiB or more");
   *out = p;
   return NJ_OK;

@@ -42,10 +42,10 @@ struct AttnK {
   const int32_t* ctx;
   float* part_o;
   float* part_ml;
-  int* counters;  // [B*Hkv] split arrivals, zero on entry (cleared by the RoPE kernel before each launch)
+  int* counters;  // [B*Hkv][kCounterStride] split arrivals, zero on entry (cleared before each launch)
   bf16_t* out;
   int* err;
-  int max_blocks, num_blocks, T, H, Hkv, bps;
+  int max_blocks, num_blocks, T, H, Hkv;
   float scale_log2;
   int part_o_bytes, part_ml_bytes;
 };
@@ -84,7 +84,7 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0)
-    s_last = (__hip_atomic_fetch_add(a.counters + pair, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1);
+    s_last = (__hip_atomic_fetch_add(a.counters + pair * kCounterStride, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1);
   __syncthreads();
   if (!s_last) return;
   const int rpad = RT * 16;
@@ -203,15 +203,19 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
     if (threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
     ctx = max(0, min(ctx, a.max_blocks * kBlock - a.T));
   }
+  // this split's share of the cached blocks, from the actual context length
+  // (shares differ by at most one block); split 0 also takes the window block,
+  // as its first chunk: it is in L2 (just written), so its compute overlaps
+  // the first cached chunk's loads
   const int nb_ctx = (ctx + kBlock - 1) / kBlock;
-  const int c0 = split * a.bps, c1 = min(c0 + a.bps, nb_ctx);
-  const int ncached = max(0, c1 - c0);
-  const int ncc = (ncached + kCB - 1) / kCB;      // cached chunks
-  const int nchunks = ncc + (split == 0 ? 1 : 0);  // split 0 also takes the window block, as a last chunk
+  const int c0 = (int)((long)split * nb_ctx / nsplit), c1 = (int)((long)(split + 1) * nb_ctx / nsplit);
+  const int ncc = (c1 - c0 + kCB - 1) / kCB;  // cached chunks
+  const int wch = split == 0 ? 1 : 0;         // window chunks
+  const int nchunks = ncc + wch;
 
   const __amdgpu_buffer_rsrc_t ors = coherent_rsrc(a.part_o, a.part_o_bytes);
   const __amdgpu_buffer_rsrc_t mrs = coherent_rsrc(a.part_ml, a.part_ml_bytes);
-  if (nchunks == 0) {  // a split past this sequence's context: mark its rows empty for the combine
+  if (nchunks == 0) {  // no blocks of this sequence for this split: mark its rows empty for the merge
     for (int qr = threadIdx.x; qr < R; qr += 256)
       coherent_store_f32(mrs, (uint32_t)(((((size_t)pair * nsplit + split) * (RT * 16) + qr) * 2) * 4), -INFINITY);
     split_arrive(a, pair, nsplit, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
@@ -235,8 +239,8 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
 
   // chunk ch: blocks [j0, j0 + nblk) of the cached range, or the window block
   auto chunk_blocks = [&](int ch, int& j0, int& nblk) {
-    if (ch < ncc) {
-      j0 = c0 + ch * kCB;
+    if (ch >= wch) {
+      j0 = c0 + (ch - wch) * kCB;
       nblk = min(kCB, c1 - j0);
     } else {
       j0 = -1;
@@ -515,14 +519,13 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnF a) {
 
 }  // namespace
 
-void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, int* blocks_per_split) {
-  (void)T;
-  (void)G;
+int attention_plan(int B, int Hkv, int max_blocks) {
   // Enough workgroups to keep ~2048 chunk streams in flight, and no split
   // longer than 64 blocks (one workgroup streams its chunks one after the
   // other, so the longest split sets the kernel's duration); at least 8
   // blocks per split, and at most pairs + kMaxExtraSplits workgroups, which
-  // bounds the partial buffer whatever the context length.
+  // bounds the partial buffer whatever the context length.  The kernel divides
+  // each sequence's actual blocks evenly over the splits.
   const int pairs = B * Hkv;
   const int ns_len = (max_blocks + 63) / 64;
   int ns = std::max((2048 + pairs - 1) / pairs, ns_len);
@@ -532,12 +535,7 @@ void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, i
   if (pairs * ns > kResidentWorkgroups) ns = std::max(ns_len, kResidentWorkgroups / pairs);
   ns = std::min(ns, 1 + kMaxExtraSplits / pairs);
   ns = std::min(ns, (max_blocks + 7) / 8);
-  ns = std::max(ns, 1);
-  int bps = (max_blocks + ns - 1) / ns;
-  bps = (bps + kCB - 1) / kCB * kCB;
-  ns = std::max(1, (max_blocks + bps - 1) / bps);
-  *nsplit = ns;
-  *blocks_per_split = bps;
+  return std::max(ns, 1);
 }
 
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D) {
@@ -560,7 +558,7 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
   AttnK a{static_cast<const bf16_t*>(x.q), static_cast<const bf16_t*>(x.k_pages),
           static_cast<const bf16_t*>(x.v_pages), static_cast<const bf16_t*>(x.win_k),
           static_cast<const bf16_t*>(x.win_v), x.block_table, x.ctx, x.part_o, x.part_ml, x.counters,
-          static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv, x.blocks_per_split,
+          static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv,
           (float)(1.4426950408889634 / sqrt((double)kD)),
           (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * kD * 4, INT32_MAX),
           (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * 2 * 4, INT32_MAX)};

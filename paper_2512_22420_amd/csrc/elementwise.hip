@@ -91,14 +91,18 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
 // pos * theta^(-j/64), pos = ctx[b] + i, for the 64 rotation pairs of a
 // 128-dim head (angle formed and reduced to [-pi, pi] in fp64, then fp32
 // sin/cos, as in rope_window_kernel); every head and layer of the step uses it.
+struct RopeFreqHead {  // theta^(-2j/128) for the 64 rotation pairs of a 128-dim head, from the host in fp64
+  double inv_freq[64];
+};
+
 __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const bf16_t* __restrict__ embed,
     const bf16_t* __restrict__ gain, float* __restrict__ h, bf16_t* __restrict__ x, float* __restrict__ ssq, int d,
-    int V, int* __restrict__ err, const int32_t* __restrict__ ctx, float theta, float* __restrict__ rope_cs) {
+    int V, int* __restrict__ err, const int32_t* __restrict__ ctx, RopeFreqHead f, float* __restrict__ rope_cs) {
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   if (rope_cs && threadIdx.x < 64) {
     const int j = threadIdx.x;
-    const double ang = (double)(max(ctx[b], 0) + i) * pow((double)theta, -(double)j / 64.0);
+    const double ang = (double)(max(ctx[b], 0) + i) * f.inv_freq[j];
     const double kq = rint(ang * 0.15915494309189535);
     const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
     float sn, cs;
@@ -179,7 +183,7 @@ __global__ __launch_bounds__(256) void rope_window_kernel(const float* __restric
   if (ctx_snap && i == 0 && blockIdx.y == 0 && threadIdx.x == 0) ctx_snap[b] = ctx[b];
   // the split counters of the attention launch that follows start at zero
   if (attn_cnt && i == 0 && blockIdx.y == 0)
-    for (int g = threadIdx.x; g < Hkv; g += blockDim.x) attn_cnt[b * Hkv + g] = 0;
+    for (int g = threadIdx.x; g < Hkv; g += blockDim.x) attn_cnt[(b * Hkv + g) * kCounterStride] = 0;
   if (hd >= H + 2 * Hkv) return;
   const float* src = qkv + (size_t)row * (H + 2 * Hkv) * D + (size_t)hd * D;
   if (hd < H + Hkv) {
@@ -296,9 +300,11 @@ hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* draf
 hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
                                const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
                                const int32_t* ctx, float theta, float* rope_cs, hipStream_t s) {
+  RopeFreqHead f{};
+  for (int j = 0; j < 64; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / 128);
   hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
                      static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h, static_cast<bf16_t*>(x),
-                     ssq, d, V, err, ctx, theta, rope_cs);
+                     ssq, d, V, err, ctx, f, rope_cs);
   return hipGetLastError();
 }
 

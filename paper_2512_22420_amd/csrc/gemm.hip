@@ -54,6 +54,7 @@ constexpr int kXStride = kSK + 8;        // LDS row stride in elements (+16 byte
 constexpr int kNW = 8;                   // waves per workgroup
 constexpr int kTileMinRows = 64;         // windows of at least this many rows may use the LDS-tiled kernel
 constexpr int kSplitTargetWorkgroups = 256;
+constexpr int kRedBatch = 4;             // split-K partials loaded together by the reducing workgroup
 
 __device__ __forceinline__ float silu_mul(float gte, float up) { return gte / (1.0f + expf(-gte)) * up; }
 
@@ -62,7 +63,7 @@ struct GemmK {
   const bf16_t* W;  // packed
   void* Y;
   float* part;      // [nkc][M][N] fp32 partials (split K only; column = weight row)
-  int* counters;    // [mblocks][gridDim.x] arrival counters (split K only), zero between launches
+  int* counters;    // [mblocks][gridDim.x][kCounterStride] arrival counters (split K only), zero between launches
   int M, Nout, K, KS, stages_per_chunk;
   int part_bytes;
   float* stats;     // kEpiLogits: [M][nch][2] chunk max and sum of exp (chunk = this kernel's 128 columns)
@@ -119,16 +120,29 @@ __device__ __forceinline__ void stream_tile(f32x4 (&acc)[MT], const bf16_t* wp, 
       *reinterpret_cast<u32x4*>(&xs[buf * XB + xo[c]]) = xr[set][c] & keep;
     }
   };
+  // The x fragments of k-step u+1 are read from LDS while k-step u is
+  // multiplied (two register sets): left to itself the scheduler waits for
+  // each LDS read right before its MFMA, which serialises the read latencies.
   auto compute = [&](auto setc, int buf) {
     constexpr int set = decltype(setc)::value;
+    bf16x8 xv[2][MT];
+    auto rd = [&](int slot, int u) {
 #pragma unroll
-    for (int u = 0; u < kSU; ++u)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const bf16x8 xv = __builtin_bit_cast(
+      for (int mt = 0; mt < MT; ++mt)
+        xv[slot][mt] = __builtin_bit_cast(
             bf16x8, *reinterpret_cast<const u32x4*>(&xs[buf * XB + (mt * 16 + r) * kXStride + u * 32 + g * 8]));
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb[set][u], xv, acc[mt], 0, 0, 0);
-      }
+    };
+    rd(0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, MT, 0);
+#pragma unroll
+    for (int u = 0; u < kSU; ++u) {
+      if (u + 1 < kSU) rd((u + 1) & 1, u + 1);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb[set][u], xv[u & 1][mt], acc[mt], 0, 0, 0);
+      if (u + 1 < kSU) __builtin_amdgcn_sched_group_barrier(0x100, MT, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, MT, 0);
+    }
   };
   // prologue: stages st0 .. st0+NB-2 in flight, stage st0's x in LDS buffer 0
   [&]<int... I>(std::integer_sequence<int, I...>) {
@@ -145,9 +159,14 @@ __device__ __forceinline__ void stream_tile(f32x4 (&acc)[MT], const bf16_t* wp, 
       ([&] {
         constexpr int nxt = (J + NB - 1) % NB;
         const int t = st + J;
+        // issue order pinned: x before the weights (the in-order load counter
+        // then lets the x wait leave the weight loads in flight), both ahead
+        // of the multiplies
+        __builtin_amdgcn_sched_barrier(0);
         loadx(std::integral_constant<int, nxt>{}, min(t + NB - 1, last));
+        __builtin_amdgcn_sched_barrier(0);
         loadw(std::integral_constant<int, nxt>{}, min(t + NB - 1, last));
-        __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the multiplies
+        __builtin_amdgcn_sched_barrier(0);
         compute(std::integral_constant<int, J>{}, J & 1);
         storex(std::integral_constant<int, (J + 1) % NB>{}, (J + 1) & 1, t + 1);
         __syncthreads();
@@ -262,20 +281,30 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    int* cnt = a.counters + (size_t)mb * gridDim.x + blockIdx.x;
+    int* cnt = a.counters + ((size_t)mb * gridDim.x + blockIdx.x) * kCounterStride;
     if (threadIdx.x == 0)
       s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nkc - 1);
     __syncthreads();
     if (!s_last) return;
     if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
-    // sum all nkc partials (this workgroup's own included, read back) in chunk order
-    for (int j = 0; j < nkc; ++j) {
+    // sum all nkc partials (this workgroup's own included, read back) in
+    // chunk order; the loads of kRedBatch chunks are issued together (one at
+    // a time, each chunk cost a full memory round trip)
+    for (int j0 = 0; j0 < nkc; j0 += kRedBatch) {
+      f32x4 v[kRedBatch][MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = min(m0 + mt * 16 + r, M - 1);  // rows past M: read in range, dropped below
-        const f32x4 v = coherent_load(prs, poff(j, m));
-        acc[mt] = j == 0 ? v : acc[mt] + v;
-      }
+      for (int q = 0; q < kRedBatch; ++q)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = min(m0 + mt * 16 + r, M - 1);  // rows past M: read in range, dropped below
+          v[q][mt] = coherent_load(prs, poff(min(j0 + q, nkc - 1), m));
+        }
+#pragma unroll
+      for (int q = 0; q < kRedBatch; ++q)
+        if (j0 + q < nkc) {
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[mt] = j0 + q == 0 ? v[q][mt] : acc[mt] + v[q][mt];
+        }
     }
   }
 
@@ -426,7 +455,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       for (int u = threadIdx.x; u < B; u += NTH)
         if (rp.ctx_snap) rp.ctx_snap[u] = rp.ctx[u];
       for (int u = threadIdx.x; u < B * Hkv; u += NTH)
-        if (rp.attn_cnt) rp.attn_cnt[u] = 0;
+        if (rp.attn_cnt) rp.attn_cnt[u * kCounterStride] = 0;
     }
   } else if constexpr (EPI == kEpiResidualNorm) {
     // h += acc through an LDS-staged tile, 32 lanes per 512-byte row segment;
@@ -485,20 +514,28 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
 }
 
 // LM head (and other wide fp32-store GEMMs) for windows of up to 48 rows: a
-// persistent form of the streaming kernel.  Logits stores issued while the weight stream runs cost far more
-// than their bytes (the HBM keeps turning the bus around between reads and
-// writes), so each workgroup streams kLogitsTiles 128-row weight groups one
-// after another, keeps each finished 48 x 128 logits tile in LDS, and writes
-// them all after its last group.  The chunk statistics of a tile are written
-// as soon as it is done (a few hundred bytes; skipped when stats is null).
+// persistent form of the streaming kernel.  Logits stores issued while the
+// weight stream runs cost far more than their bytes (the HBM keeps turning the
+// bus around between reads and writes), so each workgroup streams
+// kLogitsTiles groups of NW * 16 weight rows (one row tile per wave) one after
+// another, keeps each finished logits tile in LDS, and writes them all after
+// its last group.  The chunk statistics of a tile are written as soon as it is
+// done (a few hundred bytes; skipped when stats is null).
 // Row scale (folded RMSNorm) and statistics as in the kEpiLogits epilogue of
 // gemm_stream_kernel.
 constexpr int kLogitsTiles = 2;
-template <int MT>
-__global__ __launch_bounds__(kNW * 64) void gemm_logits_kernel(GemmK a) {
-  constexpr int TPW = kNW;  // 16-column output tiles per group: one 128-column statistics chunk
-  static_assert(TPW * 16 == kStatChunk, "a group's columns are one statistics chunk");
-  constexpr int ROWS = MT * 16, NTH = kNW * 64;
+// Waves per workgroup for windows of more than 16 rows: 256 weight rows per
+// group, so each staged x stage feeds 16 waves (with 8, the x traffic of a
+// 48-row window is 37% of the weight traffic and holds the kernel ~4% below
+// the read rate it reaches at 16 rows).
+constexpr int kLogitsWaves = 16;
+template <int MT, int NW>
+__global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
+  constexpr int TPW = NW;                // 16-column output tiles per group
+  constexpr int CPG = TPW * 16 / kStatChunk;  // statistics chunks per group
+  static_assert(CPG * kStatChunk == TPW * 16, "a group's columns are whole statistics chunks");
+  constexpr int ROWS = MT * 16, NTH = NW * 64;
+  static_assert(ROWS * CPG * kStatLanes <= NTH && ROWS * 8 <= NTH, "one pass of statistics lanes");
   constexpr int CH = ROWS * (kSK / 8), PT = (CH + NTH - 1) / NTH;
   constexpr int OS = TPW * 16 + 4;  // LDS row stride of an output tile, in floats
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kXStride];
@@ -560,23 +597,24 @@ __global__ __launch_bounds__(kNW * 64) void gemm_logits_kernel(GemmK a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) ot[tt][(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = acc[mt][i];
     __syncthreads();
-    if (a.stats) {  // softmax statistics of this chunk, 8 lanes per row
-      const int n0 = grp * TPW * 16;
-      const int row = min((int)threadIdx.x / kStatLanes, ROWS - 1), c = threadIdx.x % kStatLanes;
+    if (a.stats) {  // softmax statistics of the group's chunks, 8 lanes per (row, chunk)
+      const int unit = threadIdx.x / kStatLanes, c = threadIdx.x % kStatLanes;
+      const int row = min(unit / CPG, ROWS - 1), ch = unit % CPG;
+      const int n0 = grp * TPW * 16 + ch * kStatChunk;
       float v[kStatPer];
 #pragma unroll
       for (int e = 0; e < kStatPer; ++e)
-        v[e] = n0 + c * kStatPer + e < Nout ? ot[tt][row * OS + c * kStatPer + e] : -INFINITY;
+        v[e] = n0 + c * kStatPer + e < Nout ? ot[tt][row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
       float cm, cs;
       chunk_stats(v, cm, cs);
-      if (c == 0 && (int)threadIdx.x / kStatLanes < ROWS && row < M) {
-        a.stats[((size_t)row * a.nch + grp) * 2] = cm;
-        a.stats[((size_t)row * a.nch + grp) * 2 + 1] = cs;
+      if (c == 0 && unit < ROWS * CPG && row < M && n0 < Nout) {
+        a.stats[((size_t)row * a.nch + grp * CPG + ch) * 2] = cm;
+        a.stats[((size_t)row * a.nch + grp * CPG + ch) * 2 + 1] = cs;
       }
     }
     done = tt + 1;
   }
-  // the finished tiles, 512-byte row segments per half wave
+  // the finished tiles, full 512-byte row segments
   constexpr int PIECES = ROWS * TPW * 4;
   for (int tt = 0; tt < done; ++tt) {
     const int n0 = (blockIdx.x + tt * gridDim.x) * TPW * 16;
@@ -663,12 +701,14 @@ hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
 hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
   if (p.nkc > 1 || p.mblocks > 1 || p.mt > 3 || p.depth >= 3)
     return a.stats ? launch_stream<kEpiLogits>(a, p, s) : launch_stream<kEpiStore>(a, p, s);
-  const int groups = (a.Nout / 16 + kNW - 1) / kNW;
-  const dim3 grid((groups + kLogitsTiles - 1) / kLogitsTiles), block(kNW * 64);
+  // 16-row windows stage little x per weight byte: 8 waves per workgroup
+  const int NW = p.mt == 1 ? kNW : kLogitsWaves;
+  const int groups = (a.Nout / 16 + NW - 1) / NW;
+  const dim3 grid((groups + kLogitsTiles - 1) / kLogitsTiles), block(NW * 64);
   switch (p.mt) {
-    case 1: hipLaunchKernelGGL(gemm_logits_kernel<1>, grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL(gemm_logits_kernel<2>, grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL(gemm_logits_kernel<3>, grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((gemm_logits_kernel<1, kNW>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((gemm_logits_kernel<2, kLogitsWaves>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((gemm_logits_kernel<3, kLogitsWaves>), grid, block, 0, s, a); break;
   }
   return hipGetLastError();
 }
@@ -690,7 +730,7 @@ GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc) {
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
   p.depth = 1;
   p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
-  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * 4) : 0;
+  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * kCounterStride * 4) : 0;
   return p;
 }
 
@@ -770,8 +810,8 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split) {
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
   p.depth = 1;
   p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
-  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * 4) : 0;
-  static_assert(kSplitTargetWorkgroups / 2 * 4 <= kGemmCounterBytes, "counter region too small");
+  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * kCounterStride * 4) : 0;
+  static_assert(kSplitTargetWorkgroups / 2 * kCounterStride * 4 <= kGemmCounterBytes, "counter region too small");
   return p;
 }
 

@@ -34,7 +34,7 @@ struct TileK {
   const bf16_t* W;
   void* Y;
   float* part;    // [nkc][M][NG][Nout] fp32 partials (split K only)
-  int* counters;  // [tiles_n * tiles_m] arrival counters (split K only), zero between launches
+  int* counters;  // [tiles_n * tiles_m][kCounterStride] arrival counters (split K only), zero between launches
   int M, Nout, K, tiles_m, tiles_n, nkc, stages_per_chunk;
   int part_bytes;
 };
@@ -308,7 +308,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    int* cnt = a.counters + (size_t)tn * a.tiles_m + tm;
+    int* cnt = a.counters + ((size_t)tn * a.tiles_m + tm) * kCounterStride;
     if (threadIdx.x == 0)
       s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.nkc - 1);
     __syncthreads();

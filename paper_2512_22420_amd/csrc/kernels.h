@@ -46,7 +46,11 @@ int tile_bm(int tile);
 int tile_bn(int tile);
 // Split K only happens when ntiles * mblocks <= 256, so every GEMM's arrival
 // counters fit in this many bytes (a fixed region, whatever M, N, K).
-constexpr size_t kGemmCounterBytes = 4096;
+// Arrival counters that many workgroups increment are kept 256 bytes apart:
+// device-scope atomics on one cache line are serialised, so counters that
+// share a line make every workgroup of a launch wait for all the others'.
+constexpr int kCounterStride = 64;  // ints
+constexpr size_t kGemmCounterBytes = 128 * kCounterStride * 4;  // split-K counters of up to 128 output tiles
 // Split-K partials are addressed with 32-bit buffer offsets.
 constexpr size_t kMaxPartBytes = (size_t)1 << 31;
 
@@ -157,12 +161,12 @@ struct AttnArgs {
   float* part_o;        // split partials (bf16 path)
   float* part_ml;
   int* counters;         // [B*Hkv] split arrivals, zero on entry (bf16 path)
-  int nsplit, blocks_per_split;
+  int nsplit;  // KV splits per (sequence, KV head); a split's blocks come from the actual context length
   void* out;            // [M][H*D]
   int* err;
 };
 // Number of KV splits the bf16 path uses, and the partial buffer floats it needs.
-void attention_plan(int B, int Hkv, int T, int G, int max_blocks, int* nsplit, int* blocks_per_split);
+int attention_plan(int B, int Hkv, int max_blocks);
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
