@@ -5,13 +5,14 @@
 // draw after it needs a running sum over one full vocabulary row, which is
 // where the bandwidth goes.
 //
-//   chunk statistics  (max, sum of exp(l - max)) of every 128-wide vocabulary
-//                     chunk of every window row.  The LM-head GEMM writes
-//                     them from its output tile (chunk_stats below is shared);
-//                     accept_stats_kernel computes the same values from logits
-//                     in memory when the GEMM did not.
+//   statistics        (max, sum of exp(l - max)) pairs of every window row
+//                     over disjoint column sets.  The LM-head GEMM writes them
+//                     from its output tiles (one pair per workgroup and row,
+//                     its 128-wide chunks merged; chunk_stats is shared);
+//                     accept_stats_kernel computes one pair per 128-wide
+//                     chunk from logits in memory when the GEMM did not.
 //   accept_rows       (one workgroup per window row): row max and 1/sum from
-//                     the chunk statistics, and the accept test of the draft
+//                     the statistics pairs, and the accept test of the draft
 //                     the row scores (u_i < p_i(x_i) / q_i(x_i); q == 0
 //                     accepts).
 //   accept_draw       (sequences x tile blocks): n, the first failed test, then
@@ -39,7 +40,7 @@ struct AccK {
   const int32_t* drafts;  // [B][k]
   const float* dprobs;    // [B][k][V]
   const float* uniforms;  // [B][T]
-  const float* stats;     // [B*T][nch][2]
+  const float* stats;     // [B*T][nch][2]; entries 0 .. nst-1 of each row are used
   float* rowstat;         // [B*T][2]: max, 1/sum of every window row
   int32_t* okflag;        // [B*T]: accept test of the draft row i scores (rows 0..k-1)
   double* tsum;           // [B][ntile]: tile sums of the draw row
@@ -47,7 +48,7 @@ struct AccK {
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
-  int k, V, nch, ntile, tsum_bytes;
+  int k, V, nch, nst, ntile, tsum_bytes;
 };
 
 // 128-wide chunks of the logits, written by 256-thread workgroups (8 lanes per chunk).
@@ -76,8 +77,8 @@ __global__ __launch_bounds__(256) void accept_stats_kernel(const float* __restri
 constexpr int kRowThreads = 256, kRowLoads = 16;  // chunks per thread (V <= 524288)
 __global__ __launch_bounds__(kRowThreads) void accept_rows_kernel(AccK a) {
   __shared__ float sh[kRowThreads / kWave];
-  const int row = blockIdx.x, T = a.k + 1, b = row / T, i = row % T, V = a.V, nch = a.nch;
-  const float* st = a.stats + (size_t)row * nch * 2;
+  const int row = blockIdx.x, T = a.k + 1, b = row / T, i = row % T, V = a.V, nst = a.nst;
+  const float* st = a.stats + (size_t)row * a.nch * 2;
   // the draft this row scores, and its target logit and draft probability
   float lx = 0.f, qx = 1.f;
   bool bad = false;
@@ -92,9 +93,9 @@ __global__ __launch_bounds__(kRowThreads) void accept_rows_kernel(AccK a) {
 #pragma unroll
   for (int j = 0; j < kRowLoads; ++j) {
     const int c = threadIdx.x + j * kRowThreads;
-    const int cc = min(c, nch - 1);
-    cm[j] = c < nch ? st[2 * cc] : -INFINITY;
-    cs[j] = c < nch ? st[2 * cc + 1] : 0.f;
+    const int cc = min(c, nst - 1);
+    cm[j] = c < nst ? st[2 * cc] : -INFINITY;
+    cs[j] = c < nst ? st[2 * cc + 1] : 0.f;
   }
   float m = cm[0];
 #pragma unroll
@@ -361,8 +362,10 @@ hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  const int nst = x.stats_ready ? x.stat_entries : nch;
+  if (nst < 1 || nst > nch || nst > kRowThreads * kRowLoads) return hipErrorInvalidValue;
   AccK a{x.logits, x.drafts, x.dprobs, x.uniforms, stats, rowstat, okflag, tsum, counters, x.accepted_len,
-         x.next_tokens, x.err, x.k, x.V, nch, ntile, (int)tsum_bytes};
+         x.next_tokens, x.err, x.k, x.V, nch, nst, ntile, (int)tsum_bytes};
   hipLaunchKernelGGL(accept_rows_kernel, dim3(rows), dim3(kRowThreads), 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

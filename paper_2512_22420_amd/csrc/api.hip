@@ -305,8 +305,8 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     else
       NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
   }
-  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, stats_ready, accepted_len,
-                next_tokens, err};
+  AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, stats_ready,
+                stats_ready ? logits_stat_entries(M, d.vocab, d.d_model) : 0, accepted_len, next_tokens, err};
   NJ_TRY(launch_accept(ac, s), "accept");
 #undef NJ_TRY
   {
@@ -366,7 +366,7 @@ int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_
   if (workspace_bytes < need) return fail(NJ_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, need);
   if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
   char* ws = static_cast<char*>(workspace);
-  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, ws + kAlign, false, accepted_len,
+  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, ws + kAlign, false, 0, accepted_len,
                next_tokens, reinterpret_cast<int*>(ws)};
   hipError_t e = launch_accept(a, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "accept");

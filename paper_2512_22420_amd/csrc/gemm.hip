@@ -519,8 +519,10 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
 // bus around between reads and writes), so each workgroup streams
 // kLogitsTiles groups of NW * 16 weight rows (one row tile per wave) one after
 // another, keeps each finished logits tile in LDS, and writes them all after
-// its last group.  The chunk statistics of a tile are written as soon as it is
-// done (a few hundred bytes; skipped when stats is null).
+// its last group.  Softmax statistics (skipped when stats is null): the
+// (max, sum of exp) of each 128-column chunk of its groups, merged per row in
+// a fixed order into one pair per workgroup, stats[row][blockIdx.x] -- so the
+// acceptance reads one pair per workgroup and row, not one per chunk.
 // Row scale (folded RMSNorm) and statistics as in the kEpiLogits epilogue of
 // gemm_stream_kernel.
 constexpr int kLogitsTiles = 2;
@@ -541,6 +543,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kXStride];
   __shared__ __attribute__((aligned(16))) float ot[kLogitsTiles][ROWS * OS];
   __shared__ float s_rinv[ROWS];
+  __shared__ float2 s_cst[kLogitsTiles][ROWS * CPG];  // chunk statistics of each group
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
@@ -607,12 +610,32 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
         v[e] = n0 + c * kStatPer + e < Nout ? ot[tt][row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
       float cm, cs;
       chunk_stats(v, cm, cs);
-      if (c == 0 && unit < ROWS * CPG && row < M && n0 < Nout) {
-        a.stats[((size_t)row * a.nch + grp * CPG + ch) * 2] = cm;
-        a.stats[((size_t)row * a.nch + grp * CPG + ch) * 2 + 1] = cs;
-      }
+      if (c == 0 && unit < ROWS * CPG) s_cst[tt][unit] = float2{cm, cs};
     }
     done = tt + 1;
+  }
+  if (a.stats) {  // one (max, sum) per row: the chunks merged in (group, chunk) order
+    __syncthreads();
+    const int row = threadIdx.x;
+    if (row < ROWS && row < M) {
+      float m = -INFINITY, sum = 0.f;
+      for (int tt = 0; tt < done; ++tt)
+#pragma unroll
+        for (int ch = 0; ch < CPG; ++ch) {
+          const float2 c2 = s_cst[tt][row * CPG + ch];
+          if (c2.x == -INFINITY) continue;
+          if (m == -INFINITY) {
+            m = c2.x;
+            sum = c2.y;
+          } else if (c2.x > m) {
+            sum = sum * expf(m - c2.x) + c2.y;
+            m = c2.x;
+          } else {
+            sum += c2.y * expf(c2.x - m);
+          }
+        }
+      *reinterpret_cast<float2*>(a.stats + ((size_t)row * a.nch + blockIdx.x) * 2) = float2{m, sum};
+    }
   }
   // the finished tiles, full 512-byte row segments
   constexpr int PIECES = ROWS * TPW * 4;
@@ -697,14 +720,21 @@ hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
 }
 
 // The LM head: the persistent kernel when the window fits one 48-row block and
-// K is not split, else the streaming kernel's kEpiLogits epilogue.
-hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
-  if (p.nkc > 1 || p.mblocks > 1 || p.mt > 3 || p.depth >= 3)
-    return a.stats ? launch_stream<kEpiLogits>(a, p, s) : launch_stream<kEpiStore>(a, p, s);
+// K is not split (its grid size: the statistics pairs per row), else 0 and the
+// streaming kernel's kEpiLogits epilogue.
+int logits_persistent_grid(const GemmPlan& p, int Nout) {
+  if (p.nkc > 1 || p.mblocks > 1 || p.mt > 3 || p.depth >= 3) return 0;
   // 16-row windows stage little x per weight byte: 8 waves per workgroup
   const int NW = p.mt == 1 ? kNW : kLogitsWaves;
-  const int groups = (a.Nout / 16 + NW - 1) / NW;
-  const dim3 grid((groups + kLogitsTiles - 1) / kLogitsTiles), block(NW * 64);
+  const int groups = (Nout / 16 + NW - 1) / NW;
+  return (groups + kLogitsTiles - 1) / kLogitsTiles;
+}
+
+hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+  const int pg = logits_persistent_grid(p, a.Nout);
+  if (pg == 0) return a.stats ? launch_stream<kEpiLogits>(a, p, s) : launch_stream<kEpiStore>(a, p, s);
+  const int NW = p.mt == 1 ? kNW : kLogitsWaves;
+  const dim3 grid(pg), block(NW * 64);
   switch (p.mt) {
     case 1: hipLaunchKernelGGL((gemm_logits_kernel<1, kNW>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((gemm_logits_kernel<2, kLogitsWaves>), grid, block, 0, s, a); break;
@@ -838,6 +868,13 @@ hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* sta
 }
 
 bool gemm_streams(int M, int N, int K, int epi) { return gemm_plan(M, N, K, epi).tile == kTileNone; }
+
+int logits_stat_entries(int M, int N, int K) {
+  const GemmPlan p = gemm_plan(M, N, K, kEpiStore);
+  if (p.tile != kTileNone) return 0;
+  const int pg = logits_persistent_grid(p, N);
+  return pg > 0 ? pg : (N + kStatChunk - 1) / kStatChunk;
+}
 
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
                             int* counters, float* part, hipStream_t s, const QkvRope* rope) {

@@ -113,6 +113,9 @@ struct QkvRope {
 // Whether gemm_plan picks the weight-streaming kernel for this shape (the
 // only one with the folded norm).
 bool gemm_streams(int M, int N, int K, int epi);
+// (max, sum of exp) pairs per row that the LM-head GEMM's statistics epilogue
+// writes (0: its plan writes none)
+int logits_stat_entries(int M, int N, int K);
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
                             int* counters, float* part, hipStream_t s, const QkvRope* rope = nullptr);
 // The LDS-tiled kernel alone (K % 64 == 0).
@@ -179,6 +182,7 @@ struct AcceptArgs {
   int B, k, V;
   void* scratch;            // accept_workspace_bytes(B*T, V) bytes
   bool stats_ready;         // the chunk statistics at accept_stats_ptr(scratch) are already written
+  int stat_entries;         // stats_ready: (max, sum) pairs per row written (row stride accept_chunks(V))
   int32_t* accepted_len;
   int32_t* next_tokens;
   int* err;
