@@ -246,6 +246,14 @@ __global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int laye
   const int groups = D / EV, u = blockIdx.x * blockDim.x + threadIdx.x;
   if (u >= (k + 1) * Hkv * groups) return;
   const int j = u / (Hkv * groups), rem = u % (Hkv * groups), g = rem / groups, e0 = (rem % groups) * EV;
+  // the window row's values do not depend on n or the position: their loads
+  // go out together with those of n and the context length
+  const size_t wb = ((size_t)l * B + b) * Hkv + g;
+  const u32x4 kv = *reinterpret_cast<const u32x4*>(win_k + (wb * kBlock + j) * D + e0);
+  const T* vs = win_v + (wb * D + e0) * kBlock + j;
+  T vv[EV];
+#pragma unroll
+  for (int e = 0; e < EV; ++e) vv[e] = vs[(size_t)e * kBlock];
   const int n = acc[b], c = ctx_snap[b];
   const bool lead = u == 0 && lc == 0;
   if (n < 0 || n > k) {
@@ -267,13 +275,10 @@ __global__ __launch_bounds__(256) void kv_append_kernel(PagePtrs pages, int laye
   const int slot = pos % kBlock;
   T* kp = static_cast<T*>(pages.k[lc]);
   T* vp = static_cast<T*>(pages.v[lc]);
-  const size_t wb = ((size_t)l * B + b) * Hkv + g;
-  *reinterpret_cast<u32x4*>(kp + (((size_t)phys * Hkv + g) * kBlock + slot) * D + e0) =
-      *reinterpret_cast<const u32x4*>(win_k + (wb * kBlock + j) * D + e0);
-  const T* vs = win_v + (wb * D + e0) * kBlock + j;
+  *reinterpret_cast<u32x4*>(kp + (((size_t)phys * Hkv + g) * kBlock + slot) * D + e0) = kv;
   T* vd = vp + (((size_t)phys * Hkv + g) * D + e0) * kBlock + slot;
 #pragma unroll
-  for (int e = 0; e < EV; ++e) vd[(size_t)e * kBlock] = vs[(size_t)e * kBlock];
+  for (int e = 0; e < EV; ++e) vd[(size_t)e * kBlock] = vv[e];
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
