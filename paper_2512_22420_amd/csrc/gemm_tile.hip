@@ -5,11 +5,17 @@
 // (2*M FLOP per weight byte against a 312 FLOP/byte ridge), so the
 // weight-streaming kernel, which re-reads the weights once per 64 window rows
 // and feeds every MFMA with one LDS read, is the wrong shape.  Here a
-// workgroup owns a BM x BN output tile (x rows x weight rows), stages 64-wide
-// K slices of both operands in LDS (double-buffered, 16-byte row pad), and
-// each wave multiplies a (BM/WM) x (BN/WN) sub-tile with 16x16x32 bf16 MFMAs,
-// so every LDS fragment read feeds TN (or TM) MFMAs.
+// workgroup owns a BM x BN output tile (x rows x weight rows) and each wave
+// multiplies a (BM/WM) x (BN/WN) sub-tile with 16x16x32 bf16 MFMAs, so every
+// LDS fragment read feeds TN (or TM) MFMAs.
 //
+// - Operands go from memory straight into LDS (global_load_lds_dwordx4: no
+//   staging registers, no LDS write instructions), one 32-wide k-step per
+//   stage, NBUF stage buffers, NBUF-1 stages in flight.  Each stage holds
+//   1 KB units of 16 rows x 32 k in MFMA operand order (lane l: row l % 16,
+//   k 8 (l / 16) .. +8): a unit is one load instruction (lane l's 16 bytes land
+//   at byte 16 l) and one conflict-free fragment read.  Weight units are the
+//   packed layout's tiles copied as they are; x units gather 16 row segments.
 // - Tile order is XCD-aware: workgroup IDs go round-robin over the 8 XCDs, so
 //   the linear ID is remapped to give each XCD a contiguous run of tiles, with
 //   the M tiles of one weight tile adjacent.  The weight tile is then fetched
@@ -39,34 +45,22 @@ struct TileK {
   int part_bytes;
 };
 
-// BK: K per stage (32 or 64); LDS rows are padded by 16 bytes, which keeps
-// the 16-byte fragment reads of 8 consecutive rows on distinct banks.  DIST:
-// stages loaded ahead of the one being multiplied (1 or 2).
-template <int BM, int BN, int WM, int WN, int BK, int DIST, int LAYOUT, int PIPE, int NG, int EPI>
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int BM, int BN, int WM, int WN, int NBUF, int NG, int EPI>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
-  constexpr int kBK = BK;
-  constexpr int PR = BK / 8;                       // 16-byte pieces per row and stage
-  constexpr int kLdsStride = LAYOUT == 0 ? BK + 8 : BK;
-  constexpr int NTH = WM * WN * 64;
+  constexpr int NW = WM * WN;
   constexpr int TM = BM / WM / 16;                 // x fragments per wave
   constexpr int TN = BN / WN / 16;                 // weight fragments per wave
-  constexpr int XC = BM * PR / NTH;                // 16-byte x pieces per thread per stage
-  constexpr int WC = BN * PR / NTH;
+  constexpr int XU = BM / 16, WU = BN / 16;        // 1 KB units per stage
+  constexpr int UPW = (XU + WU) / NW;              // units each wave loads per stage
+  constexpr int STAGE = (XU + WU) * 512;           // bf16 elements per stage buffer
+  constexpr int DIST = NBUF - 1;                   // stages in flight ahead of the one multiplied
   constexpr int HALF = BN / 2;                     // SwiGLU: gate rows, then up rows
-  static_assert(XC * NTH == BM * PR && WC * NTH == BN * PR, "stage must split evenly");
+  static_assert(UPW * NW == XU + WU, "a stage's units must split evenly over the waves");
   static_assert(NG == 1 || (TN % 2 == 0), "SwiGLU waves hold gate and up fragments in pairs");
-  // LDS element offset of 16-byte piece `ch` of tile row `row`
-  auto lds_off = [](int row, int ch) {
-    if constexpr (LAYOUT == 0) return row * kLdsStride + ch * 8;
-    else if constexpr (LAYOUT == 1) {
-      const int f = PR == 8 ? ((row >> 1) ^ ((row & 1) << 2)) : ((row >> 1) ^ (row >> 3));
-      return row * kLdsStride + ((ch ^ f) & (PR - 1)) * 8;
-    } else {
-      return row * kLdsStride + ((ch ^ row) & (PR - 1)) * 8;
-    }
-  };
-  __shared__ __attribute__((aligned(16))) bf16_t xs[2][BM * kLdsStride];
-  __shared__ __attribute__((aligned(16))) bf16_t ws[2][BN * kLdsStride];
+  static_assert(DIST * UPW <= 63, "load counter range");
+  __shared__ __attribute__((aligned(16))) bf16_t lds[NBUF * STAGE];
   __shared__ int s_last;
 
   // XCD-aware tile order: workgroup b runs on XCD b % 8; XCD x takes the
@@ -86,41 +80,52 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   const int r = lane & 15, g = lane >> 4;
   const int m0 = tm * BM;
   const int n0 = tn * (NG == 1 ? BN : HALF);
-
-  // element offsets of this thread's 16-byte pieces (row clamped into range;
-  // rows past the end are computed and never stored).  Both operands hold
-  // fewer than 2^31 elements (checked by the host).
-  uint32_t xo[XC], wo[WC];
-#pragma unroll
-  for (int c = 0; c < XC; ++c) {
-    const int idx = threadIdx.x + c * NTH, row = idx / PR;
-    xo[c] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)K + (idx % PR) * 8;
-  }
-  // Weight pieces come from the packed layout (128-row groups, k-step major,
-  // 1 KB per 16-row x 32-k tile in MFMA lane order): thread piece idx is lane
-  // idx % 64 of k-step (idx / 64) % KSS of 16-row tile idx / (64 * KSS), so
-  // each wave reads whole 1 KB tiles.  Tiles past the edge are clamped to the
-  // last one (computed and never stored).
-  constexpr int KSS = kBK / 32;  // k-steps per stage
   const int KS = K / 32, nto = Nout / 16;
-#pragma unroll
-  for (int c = 0; c < WC; ++c) {
-    const int idx = threadIdx.x + c * NTH;
-    const int t16 = idx / (64 * KSS), ksl = (idx / 64) % KSS, ln = idx % 64;
-    int T;
-    if constexpr (NG == 1) T = min(n0 / 16 + t16, nto - 1);
-    else T = t16 < HALF / 16 ? min(n0 / 16 + t16, nto - 1) : nto + min(n0 / 16 + t16 - HALF / 16, nto - 1);
-    wo[c] = ((uint32_t)(T >> 3) * (uint32_t)KS * 8u + (uint32_t)(T & 7)) * 512u + (uint32_t)ksl * 4096u + ln * 8;
-  }
-  auto w_lds = [&](int idx) {  // LDS element offset of weight piece idx
-    const int t16 = idx / (64 * KSS), ksl = (idx / 64) % KSS, ln = idx % 64;
-    return lds_off(t16 * 16 + (ln & 15), ksl * 4 + (ln >> 4));
-  };
 
-  // LDS row of weight fragment j of this wave
-  auto wrow = [&](int j) {
-    if constexpr (NG == 1) return wn * (BN / WN) + j * 16;
-    else return (j < TN / 2) ? wn * (HALF / WN) + j * 16 : HALF + wn * (HALF / WN) + (j - TN / 2) * 16;
+  // The units this wave loads: u = wave * UPW + q; u < XU is x row tile u
+  // (rows clamped into range: rows past the end are computed and never
+  // stored), else weight tile u - XU (SwiGLU: gate tiles, then up tiles;
+  // tiles past the edge clamped to the last one).  Address of stage st: the
+  // uniform base ubase[q] + st * ustep[q] bytes plus the lane's 32-bit
+  // offset vofs[q].
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const char* ubase[UPW];
+  uint32_t ustep[UPW], vofs[UPW];
+#pragma unroll
+  for (int q = 0; q < UPW; ++q) {
+    const int u = wv * UPW + q;
+    if (u < XU) {
+      ubase[q] = reinterpret_cast<const char*>(a.X);
+      ustep[q] = 64;
+      vofs[q] = ((uint32_t)min(m0 + u * 16 + r, M - 1) * (uint32_t)K + g * 8) * 2u;
+    } else {
+      const int t16 = u - XU;
+      int T;
+      if constexpr (NG == 1) T = min(n0 / 16 + t16, nto - 1);
+      else T = t16 < HALF / 16 ? min(n0 / 16 + t16, nto - 1) : nto + min(n0 / 16 + t16 - HALF / 16, nto - 1);
+      ubase[q] = reinterpret_cast<const char*>(a.W + ((size_t)(T >> 3) * KS * 8 + (T & 7)) * 512);
+      ustep[q] = 8192;
+      vofs[q] = lane * 16;
+    }
+  }
+  // Unit q of stage st into buffer buf.  Written as assembly so that the
+  // compiler, which cannot tell the stage buffers apart, does not wait for
+  // these loads before every LDS read; the waits are explicit below.
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void*)lds;
+  auto issue1 = [&](int q, int st, int buf) {
+    const char* sb = ubase[q] + (size_t)st * ustep[q];
+    const uint32_t dst = lds_base + (uint32_t)(buf * STAGE + (wv * UPW + q) * 512) * 2u;
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(vofs[q]), "s"(sb), "s"(dst)
+                 : "memory", "m0");
+  };
+  auto issue = [&](int st, int buf) {
+#pragma unroll
+    for (int q = 0; q < UPW; ++q) issue1(q, st, buf);
+  };
+  // LDS unit of weight fragment j of this wave
+  auto wunit = [&](int j) {
+    if constexpr (NG == 1) return XU + wn * TN + j;
+    else return (j < TN / 2) ? XU + wn * (TN / 2) + j : XU + WU / 2 + wn * (TN / 2) + (j - TN / 2);
   };
 
   f32x4 acc[TM][TN];
@@ -129,159 +134,77 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // the plan counts K in 64-wide stages
-  const int nst = K / kBK, spc = a.stages_per_chunk * (64 / kBK);
-  const int st0 = kc * spc, st1 = min(nst, st0 + spc);
-
-  // DIST register sets: with two, the loads of stage s+2 are in flight while
-  // stage s is multiplied and stage s+1 is copied into LDS.
-  u32x4 xr[DIST][XC], wr[DIST][WC];
-  auto gload = [&](int set, int st) {
-    const int k0 = st * kBK;
+  // Fragments go through two register sets: those of stage st+1 are read
+  // from LDS while stage st is multiplied.
+  bf16x8 xf[2][TM], wf[2][TN];
+  auto rd = [&](auto setc, int buf) {
+    constexpr int set = decltype(setc)::value;
+    const bf16_t* base = lds + buf * STAGE + lane * 8;
 #pragma unroll
-    for (int c = 0; c < XC; ++c) xr[set][c] = *reinterpret_cast<const u32x4*>(a.X + (xo[c] + k0));
+    for (int j = 0; j < TN; ++j)
+      wf[set][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + wunit(j) * 512));
 #pragma unroll
-    for (int c = 0; c < WC; ++c) wr[set][c] = *reinterpret_cast<const u32x4*>(a.W + (wo[c] + (uint32_t)st * (KSS * 4096u)));
+    for (int i = 0; i < TM; ++i)
+      xf[set][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + (wm * TM + i) * 512));
   };
-  auto sstore = [&](int set, int buf) {
+  auto mm = [&](auto setc) {
+    constexpr int set = decltype(setc)::value;
 #pragma unroll
-    for (int c = 0; c < XC; ++c) {
-      const int idx = threadIdx.x + c * NTH;
-      *reinterpret_cast<u32x4*>(&xs[buf][lds_off(idx / PR, idx % PR)]) = xr[set][c];
-    }
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int c = 0; c < WC; ++c) *reinterpret_cast<u32x4*>(&ws[buf][w_lds(threadIdx.x + c * NTH)]) = wr[set][c];
-  };
-  auto compute = [&](int buf) {
-    constexpr int KS = kBK / 32;
-    if constexpr (PIPE == 2) {
-      // per k-step: TN+2 reads ahead, then two more reads per group of TN multiplies
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 xf[TM], wf[TN];
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          wf[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                 &ws[buf][lds_off(wrow(j) + r, ks * 4 + g)]));
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          xf[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                 &xs[buf][lds_off(wm * (BM / WM) + i * 16 + r, ks * 4 + g)]));
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], xf[i], acc[i][j], 0, 0, 0);
-        constexpr int REM = TM - 2, N2 = REM / 2;
-        __builtin_amdgcn_sched_group_barrier(0x100, TN + 2, 0);
-#pragma unroll
-        for (int q = 0; q < N2; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        }
-        if constexpr (REM & 1) {
-          __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-#pragma unroll
-        for (int q = N2 + (REM & 1); q < TM; ++q) __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-      }
-    } else if constexpr (PIPE == 0) {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 xf[TM], wf[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          xf[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                 &xs[buf][lds_off(wm * (BM / WM) + i * 16 + r, ks * 4 + g)]));
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          wf[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                 &ws[buf][lds_off(wrow(j) + r, ks * 4 + g)]));
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], xf[i], acc[i][j], 0, 0, 0);
-      }
-    } else {
-      // Fragment reads run ahead of the multiplies: the stage's reads are
-      // issued in use order (per k-step: weight fragments, then x fragments),
-      // and the scheduler is held to "TN+2 reads, then per group of TN
-      // multiplies two more reads", so each LDS read has at least one MFMA
-      // group (and the other wave on the SIMD) to hide its latency.
-      bf16x8 xf[KS][TM], wf[KS][TN];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          wf[ks][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                     &ws[buf][lds_off(wrow(j) + r, ks * 4 + g)]));
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          xf[ks][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                     &xs[buf][lds_off(wm * (BM / WM) + i * 16 + r, ks * 4 + g)]));
-      }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[ks][j], xf[ks][i], acc[i][j], 0, 0, 0);
-      constexpr int R = KS * (TM + TN), INIT = TN + 2, REM = R - INIT, G = KS * TM, N2 = REM / 2;
-      static_assert(N2 + (REM & 1) <= G, "read schedule longer than the multiplies");
-      __builtin_amdgcn_sched_group_barrier(0x100, INIT, 0);
-#pragma unroll
-      for (int q = 0; q < N2; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
-      if constexpr (REM & 1) {
-        __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-#pragma unroll
-      for (int q = N2 + (REM & 1); q < G; ++q) __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-    }
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[set][j], xf[set][i], acc[i][j], 0, 0, 0);
   };
 
-  // Branch-free double-buffered stage loops (the last iterations re-load the
-  // last stage into buffers nobody reads, an L2 hit; branches inside the loop
-  // would make the compiler drain the loads in flight at every join).
-  if constexpr (DIST == 1) {
-    gload(0, st0);
-    sstore(0, 0);
-    __syncthreads();
-    for (int st = st0; st < st1; ++st) {
-      const int buf = (st - st0) & 1;
-      gload(0, min(st + 1, st1 - 1));
+  // the plan counts K in 64-wide stages; here a stage is one 32-wide k-step
+  const int spc = a.stages_per_chunk * 2;
+  const int st0 = kc * spc, st1 = min(KS, st0 + spc);
+  // Prologue: stages st0 .. st0+NBUF-1 in flight, stage st0 read.  Stages
+  // past the chunk re-load its last stage into a buffer nobody reads, so
+  // every iteration issues the same number of loads and the wait counts
+  // below are exact.
+#pragma unroll
+  for (int d = 0; d < NBUF; ++d) issue(min(st0 + d, st1 - 1), d);
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NBUF - 1) * UPW) : "memory");
+  rd(std::integral_constant<int, 0>{}, 0);
+  // Iteration st: stage st+1 has landed in this wave's units once at most
+  // the NBUF-2 later stages' loads are outstanding, and in every wave's after
+  // the barrier -- by which time every wave has also read stage st into
+  // registers, so its buffer takes stage st+NBUF.  Then stage st+1 is read
+  // while stage st is multiplied.
+  // Each MFMA row i (TN multiplies) is preceded by this stage's share of the
+  // loads for stage st+NBUF and of the fragment reads for stage st+1, so the
+  // wave never stops issuing MFMAs for long (one wave per SIMD in the
+  // 4-wave shape hides nothing behind another wave).
+  constexpr int NRD = TM + TN;
+  auto step = [&](auto pc, int st) {
+    constexpr int P = decltype(pc)::value;
+    constexpr int Q = 1 - P;
+    const int i0 = st - st0;
+    const int nst = min(st + NBUF, st1 - 1), nbuf = i0 % NBUF, rbuf = (i0 + 1) % NBUF;
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NBUF - 2) * UPW) : "memory");
+    const bf16_t* rbase = lds + rbuf * STAGE + lane * 8;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
       __builtin_amdgcn_sched_barrier(0);
-      compute(buf);
-      sstore(0, buf ^ 1);
-      __syncthreads();
+#pragma unroll
+      for (int q = i * UPW / TM; q < (i + 1) * UPW / TM; ++q) issue1(q, nst, nbuf);
+#pragma unroll
+      for (int e = i * NRD / TM; e < (i + 1) * NRD / TM; ++e) {
+        if (e < TN) wf[Q][e] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rbase + wunit(e) * 512));
+        else xf[Q][e - TN] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rbase + (wm * TM + e - TN) * 512));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[P][j], xf[P][i], acc[i][j], 0, 0, 0);
     }
-  } else {
-    // register set q and LDS buffer q alternate; stage st + 2 is loaded while
-    // stage st is multiplied and stage st + 1 goes from registers to LDS
-    gload(0, st0);
-    gload(1, min(st0 + 1, st1 - 1));
-    sstore(0, 0);
-    __syncthreads();
-    for (int st = st0; st < st1; st += 2) {
-      gload(0, min(st + 2, st1 - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(0);
-      sstore(1, 1);
-      __syncthreads();
-      if (st + 1 >= st1) break;
-      gload(1, min(st + 3, st1 - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(1);
-      sstore(0, 0);
-      __syncthreads();
-    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int st = st0; st < st1; st += 2) {
+    step(std::integral_constant<int, 0>{}, st);
+    if (st + 1 < st1) step(std::integral_constant<int, 1>{}, st + 1);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the surplus loads, before LDS is reused or the workgroup exits
 
   // output coordinates of fragment (i, j): row m(i), columns n(j)..n(j)+3 of group q(j)
   auto out_m = [&](int i) { return m0 + wm * (BM / WM) + i * 16 + r; };
@@ -358,13 +281,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int BK, int DIST, int LAYOUT, int PIPE>
+template <int BM, int BN, int WM, int WN, int NBUF>
 hipError_t launch_shape(const TileK& a, int epi, hipStream_t s) {
   const dim3 grid(a.tiles_m * a.tiles_n * a.nkc), block(WM * WN * 64);
-  if (epi == kEpiStore) hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, BK, DIST, LAYOUT, PIPE, 1, kEpiStore>), grid, block, 0, s, a);
+  if (epi == kEpiStore) hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 1, kEpiStore>), grid, block, 0, s, a);
   else if (epi == kEpiResidual)
-    hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, BK, DIST, LAYOUT, PIPE, 1, kEpiResidual>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, BK, DIST, LAYOUT, PIPE, 2, kEpiSwiglu>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 1, kEpiResidual>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 2, kEpiSwiglu>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
@@ -380,9 +303,13 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
           p.nkc > 1 ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles, p.nkc, p.stages_per_chunk,
           (int)p.part_bytes};
   switch (p.tile) {
-    case kTile256x256: return launch_shape<256, 256, 2, 4, 64, 2, 1, 2>(a, epi, s);
-    case kTile128x256: return launch_shape<128, 256, 2, 4, 64, 2, 1, 1>(a, epi, s);
-    default: return launch_shape<128, 128, 2, 2, 64, 1, 1, 0>(a, epi, s);
+    // 4 waves of 128 x 128 (a quarter fewer LDS reads per MFMA; all 512
+    // registers per lane), 8 waves of 128 x 64 for SwiGLU, whose epilogue
+    // would not fit beside the larger accumulators
+    case kTile256x256:
+      return epi == kEpiSwiglu ? launch_shape<256, 256, 2, 4, 4>(a, epi, s) : launch_shape<256, 256, 2, 2, 4>(a, epi, s);
+    case kTile128x256: return launch_shape<128, 256, 2, 4, 4>(a, epi, s);
+    default: return launch_shape<128, 128, 2, 2, 4>(a, epi, s);
   }
 }
 
