@@ -269,7 +269,8 @@ enum {
   NJ_GEMM_TILE_256x256 = 2, /* LDS-tiled kernel; output tile = x rows x weight rows  */
   NJ_GEMM_TILE_128x256 = 3,
   NJ_GEMM_TILE_128x128 = 4,
-  NJ_GEMM_STREAM_DEEP = 5   /* weight-streaming kernel, 3 stages in flight per wave  */
+  NJ_GEMM_STREAM_DEEP = 5,  /* weight-streaming kernel, 3 stages in flight per wave  */
+  NJ_GEMM_TILE_192x256 = 6  /* LDS-tiled kernel, 192-row x tiles (windows of 3 x 64 rows)    */
 };
 
 /*

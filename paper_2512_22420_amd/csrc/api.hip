@@ -432,7 +432,7 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
                      GemmPlan* out) {
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
   if (split < 0) return fail(NJ_EINVAL, "split_k must be >= 0");
-  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_STREAM_DEEP) return fail(NJ_EINVAL, "bad kernel choice");
+  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_TILE_192x256) return fail(NJ_EINVAL, "bad kernel choice");
   if (dtype != NJ_BF16) {
     if (kernel != NJ_GEMM_AUTO || split) return fail(NJ_EINVAL, "the fp32 GEMM has a single kernel and no split");
     *out = GemmPlan{};
@@ -449,8 +449,10 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
     p.depth = kernel == NJ_GEMM_STREAM_DEEP ? 3 : 1;
   } else {
     if (!tile_fits(M, N, K)) return fail(NJ_EINVAL, "the tiled kernels need K %% 64 == 0 and M*K, N*K < 2^31");
-    const int tile = kernel == NJ_GEMM_TILE_256x256 ? kTile256x256
-                     : kernel == NJ_GEMM_TILE_128x256 ? kTile128x256 : kTile128x128;
+    const int tile = kernel == NJ_GEMM_TILE_256x256   ? kTile256x256
+                     : kernel == NJ_GEMM_TILE_192x256 ? kTile192x256
+                     : kernel == NJ_GEMM_TILE_128x256 ? kTile128x256
+                                                      : kTile128x128;
     p = split ? gemm_tile_plan(M, N, K, epilogue, tile, std::min(split, K / 64))
               : gemm_tile_choose(M, N, K, epilogue, tile);
   }

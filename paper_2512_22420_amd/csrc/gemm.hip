@@ -776,7 +776,7 @@ constexpr double kLaunch = 5e-6;
 double tile_cost(const GemmPlan& p, int M, int N, int K) {
   const int bm = tile_bm(p.tile), bn = tile_bn(p.tile);
   const double slots = p.tile == kTile128x128 ? 512.0 : 256.0;  // resident workgroups
-  const double eff = p.tile == kTile256x256 ? 0.47 : p.tile == kTile128x256 ? 0.37 : 0.28;
+  const double eff = p.tile == kTile256x256 ? 0.47 : p.tile == kTile192x256 ? 0.45 : p.tile == kTile128x256 ? 0.37 : 0.28;
   const double rounds = std::ceil((double)p.ntiles * p.mblocks * p.nkc / slots);
   double t = rounds * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (2.5e15 / slots * eff);
   if (p.nkc > 1) t += 2.0 * p.nkc * bm * bn * 4 / 1e11 + 2.0 * p.nkc * (double)M * N * 4 / 5e12;
@@ -793,7 +793,7 @@ double stream_cost(int M, int N, int K) {
 GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile) {
   GemmPlan best{};
   double bc = 1e30;
-  for (int tile : {kTile256x256, kTile128x256, kTile128x128}) {
+  for (int tile : {kTile256x256, kTile192x256, kTile128x256, kTile128x128}) {
     if (only_tile != kTileNone && tile != only_tile) continue;
     for (int nkc = 1; nkc <= 8; nkc *= 2) {
       if (nkc > 1 && K / 64 / nkc < 8) break;

@@ -293,7 +293,7 @@ hipError_t launch_shape(const TileK& a, int epi, hipStream_t s) {
 
 }  // namespace
 
-int tile_bm(int cfg) { return cfg == kTile256x256 ? 256 : 128; }
+int tile_bm(int cfg) { return cfg == kTile256x256 ? 256 : cfg == kTile192x256 ? 192 : 128; }
 int tile_bn(int cfg) { return cfg == kTile128x128 ? 128 : 256; }
 
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
@@ -308,6 +308,8 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
     // would not fit beside the larger accumulators
     case kTile256x256:
       return epi == kEpiSwiglu ? launch_shape<256, 256, 2, 4, 4>(a, epi, s) : launch_shape<256, 256, 2, 2, 4>(a, epi, s);
+    // 4 waves of 96 x 128: windows of 3 x 128 (or 6 x 64) rows without a padded tile
+    case kTile192x256: return launch_shape<192, 256, 2, 2, 4>(a, epi, s);
     case kTile128x256: return launch_shape<128, 256, 2, 4, 4>(a, epi, s);
     default: return launch_shape<128, 128, 2, 2, 4>(a, epi, s);
   }

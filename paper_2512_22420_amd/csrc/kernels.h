@@ -17,7 +17,7 @@ enum { kF32 = 0, kBF16 = 1 };
 enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3, kEpiResidualNorm = 4, kEpiQkvRope = 5 };
 
 // Output tiles of the LDS-tiled kernel for large windows: x rows x weight rows.
-enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3 };
+enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3, kTile192x256 = 4 };
 
 // How the bf16 GEMM splits its work.  Weight-streaming kernel (tile ==
 // kTileNone): 16-row x tiles per workgroup (mt), waves per workgroup (nw, 8),
