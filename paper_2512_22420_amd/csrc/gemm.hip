@@ -859,8 +859,8 @@ hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N,
 hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* stats, int M, int N, int K,
                               int* counters, float* part, hipStream_t s, bool* stats_written) {
   const GemmPlan p = gemm_plan(M, N, K, kEpiStore);
-  *stats_written = p.tile == kTileNone;
-  if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s);
+  *stats_written = true;
+  if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s, stats);
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, N, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, stats,
           (N + kStatChunk - 1) / kStatChunk, nullptr, 0, 0.f, nullptr, nullptr, nullptr, {}};
@@ -871,7 +871,7 @@ bool gemm_streams(int M, int N, int K, int epi) { return gemm_plan(M, N, K, epi)
 
 int logits_stat_entries(int M, int N, int K) {
   const GemmPlan p = gemm_plan(M, N, K, kEpiStore);
-  if (p.tile != kTileNone) return 0;
+  if (p.tile != kTileNone) return p.ntiles;  // one pair per column tile
   const int pg = logits_persistent_grid(p, N);
   return pg > 0 ? pg : (N + kStatChunk - 1) / kStatChunk;
 }

@@ -43,6 +43,8 @@ struct TileK {
   int* counters;  // [tiles_n * tiles_m][kCounterStride] arrival counters (split K only), zero between launches
   int M, Nout, K, tiles_m, tiles_n, nkc, stages_per_chunk;
   int part_bytes;
+  float* stats;   // kEpiStore, nullable: [M][nch][2] (max, sum of exp) of each row over this tile's columns, entry tn
+  int nch;
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -257,6 +259,62 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     }
   }
 
+  if constexpr (EPI == kEpiStore) {
+    if (a.stats) {
+      // Softmax statistics of each row over the tile's BN columns: a wave's
+      // row (i, r) spans its TN fragments in the 4 lanes r + 16 g (max, then
+      // the sum of exp in lane order and a 2-step butterfly -- a + b == b + a,
+      // so the 4 lanes agree), then the WN waves of a row block merge in wave
+      // order through LDS (the stage buffers are free).
+      float* sst = reinterpret_cast<float*>(lds);  // [WM][WN][BM / WM][2]
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (out_n(j) + e < Nout) mx = fmaxf(mx, acc[i][j][e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (out_n(j) + e < Nout) sum += expf(acc[i][j][e] - mx);
+        sum += __shfl_xor(sum, 16);
+        sum += __shfl_xor(sum, 32);
+        if (g == 0) {
+          const int rr = i * 16 + r;
+          sst[((wm * WN + wn) * (BM / WM) + rr) * 2] = mx;
+          sst[((wm * WN + wn) * (BM / WM) + rr) * 2 + 1] = sum;
+        }
+      }
+      __syncthreads();
+      for (int row = threadIdx.x; row < BM; row += NW * 64) {
+        const int bm = row / (BM / WM), rr = row % (BM / WM), mrow = m0 + row;
+        if (mrow >= M) continue;
+        float m = -INFINITY, sum = 0.f;
+        for (int w = 0; w < WN; ++w) {
+          const float m2 = sst[((bm * WN + w) * (BM / WM) + rr) * 2], s2 = sst[((bm * WN + w) * (BM / WM) + rr) * 2 + 1];
+          if (m2 == -INFINITY) continue;
+          if (m == -INFINITY) {
+            m = m2;
+            sum = s2;
+          } else if (m2 > m) {
+            sum = sum * expf(m - m2) + s2;
+            m = m2;
+          } else {
+            sum += s2 * expf(m2 - m);
+          }
+        }
+        *reinterpret_cast<float2*>(a.stats + ((size_t)mrow * a.nch + tn) * 2) = float2{m, sum};
+      }
+    }
+  }
+
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int m = out_m(i);
@@ -297,11 +355,11 @@ int tile_bm(int cfg) { return cfg == kTile256x256 ? 256 : cfg == kTile192x256 ? 
 int tile_bn(int cfg) { return cfg == kTile128x128 ? 128 : 256; }
 
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
-                            int* counters, float* part, hipStream_t s) {
+                            int* counters, float* part, hipStream_t s, float* stats) {
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles, p.nkc, p.stages_per_chunk,
-          (int)p.part_bytes};
+          (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk};
   switch (p.tile) {
     // 4 waves of 128 x 128 (a quarter fewer LDS reads per MFMA; all 512
     // registers per lane), 8 waves of 128 x 64 for SwiGLU, whose epilogue

@@ -114,13 +114,14 @@ struct QkvRope {
 // only one with the folded norm).
 bool gemm_streams(int M, int N, int K, int epi);
 // (max, sum of exp) pairs per row that the LM-head GEMM's statistics epilogue
-// writes (0: its plan writes none)
+// writes: one per 128-column chunk, per persistent workgroup, or per column tile
 int logits_stat_entries(int M, int N, int K);
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
                             int* counters, float* part, hipStream_t s, const QkvRope* rope = nullptr);
 // The LDS-tiled kernel alone (K % 64 == 0).
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
-                            int* counters, float* part, hipStream_t s);
+                            int* counters, float* part, hipStream_t s,
+                            float* stats = nullptr);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
