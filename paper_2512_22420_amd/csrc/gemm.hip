@@ -52,7 +52,7 @@ constexpr int kSU = 4;                   // 32-wide k-steps per stage
 constexpr int kSK = 32 * kSU;            // 128 k per stage
 constexpr int kXStride = kSK + 8;        // LDS row stride in elements (+16 bytes)
 constexpr int kNW = 8;                   // waves per workgroup
-constexpr int kTileMinRows = 64;         // windows of at least this many rows may use the LDS-tiled kernel
+constexpr int kTileMinRows = 65;         // windows of more than 64 rows may use the LDS-tiled kernel
 constexpr int kSplitTargetWorkgroups = 256;
 constexpr int kRedBatch = 4;             // split-K partials loaded together by the reducing workgroup
 
@@ -513,13 +513,13 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   }
 }
 
-// LM head (and other wide fp32-store GEMMs) for windows of up to 48 rows: a
+// LM head (and other wide fp32-store GEMMs) for windows of up to 64 rows: a
 // persistent form of the streaming kernel.  Logits stores issued while the
 // weight stream runs cost far more than their bytes (the HBM keeps turning the
 // bus around between reads and writes), so each workgroup streams
 // kLogitsTiles groups of NW * 16 weight rows (one row tile per wave) one after
-// another, keeps each finished logits tile in LDS, and writes them all after
-// its last group.  Softmax statistics (skipped when stats is null): the
+// another, keeps each finished logits tile in registers, and writes them all
+// after its last group (through one LDS tile, as full row segments).  Softmax statistics (skipped when stats is null): the
 // (max, sum of exp) of each 128-column chunk of its groups, merged per row in
 // a fixed order into one pair per workgroup, stats[row][blockIdx.x] -- so the
 // acceptance reads one pair per workgroup and row, not one per chunk.
@@ -541,7 +541,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
   constexpr int CH = ROWS * (kSK / 8), PT = (CH + NTH - 1) / NTH;
   constexpr int OS = TPW * 16 + 4;  // LDS row stride of an output tile, in floats
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kXStride];
-  __shared__ __attribute__((aligned(16))) float ot[kLogitsTiles][ROWS * OS];
+  __shared__ __attribute__((aligned(16))) float ot[ROWS * OS];
   __shared__ float s_rinv[ROWS];
   __shared__ float2 s_cst[kLogitsTiles][ROWS * CPG];  // chunk statistics of each group
 
@@ -570,6 +570,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
     for (int j = 0; j < 8; ++j) ssq_v[j] = c + 8 * j < a.nt_in ? sp[c + 8 * j] : 0.f;
   }
 
+  // The finished tiles stay in registers (tile tt in fin[tt]) until the last
+  // group's weights have been streamed; then each passes through the one LDS
+  // output tile for its statistics and its row-segment stores.
+  static_assert(kLogitsTiles == 2, "finished tiles are held in two register sets");
+  f32x4 fin0[MT], fin1[MT];
   int done = 0;
   for (int tt = 0; tt < kLogitsTiles; ++tt) {
     const int grp = blockIdx.x + tt * gridDim.x;
@@ -596,9 +601,20 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
       for (int mt = 0; mt < MT; ++mt) acc[mt] *= s_rinv[mt * 16 + r];
     }
 #pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      if (tt == 0) fin0[mt] = acc[mt];
+      else fin1[mt] = acc[mt];
+    }
+    done = tt + 1;
+  }
+  constexpr int PIECES = ROWS * TPW * 4;
+  for (int tt = 0; tt < done; ++tt) {
+    const int grp = blockIdx.x + tt * gridDim.x;
+    __syncthreads();  // the previous tile's stores have read the LDS tile
+#pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) ot[tt][(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = acc[mt][i];
+      for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = tt == 0 ? fin0[mt][i] : fin1[mt][i];
     __syncthreads();
     if (a.stats) {  // softmax statistics of the group's chunks, 8 lanes per (row, chunk)
       const int unit = threadIdx.x / kStatLanes, c = threadIdx.x % kStatLanes;
@@ -607,12 +623,22 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
       float v[kStatPer];
 #pragma unroll
       for (int e = 0; e < kStatPer; ++e)
-        v[e] = n0 + c * kStatPer + e < Nout ? ot[tt][row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
+        v[e] = n0 + c * kStatPer + e < Nout ? ot[row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
       float cm, cs;
       chunk_stats(v, cm, cs);
       if (c == 0 && unit < ROWS * CPG) s_cst[tt][unit] = float2{cm, cs};
     }
-    done = tt + 1;
+    // the finished tile, full 512-byte row segments
+    const int n0 = grp * TPW * 16;
+#pragma unroll
+    for (int it = 0; it < (PIECES + NTH - 1) / NTH; ++it) {
+      const int idx = threadIdx.x + it * NTH;
+      const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
+      const int n = n0 + c4;
+      if (idx < PIECES && row < M && n < Nout)
+        *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)row * Nout + n) =
+            *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
+    }
   }
   if (a.stats) {  // one (max, sum) per row: the chunks merged in (group, chunk) order
     __syncthreads();
@@ -635,20 +661,6 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
           }
         }
       *reinterpret_cast<float2*>(a.stats + ((size_t)row * a.nch + blockIdx.x) * 2) = float2{m, sum};
-    }
-  }
-  // the finished tiles, full 512-byte row segments
-  constexpr int PIECES = ROWS * TPW * 4;
-  for (int tt = 0; tt < done; ++tt) {
-    const int n0 = (blockIdx.x + tt * gridDim.x) * TPW * 16;
-#pragma unroll
-    for (int it = 0; it < (PIECES + NTH - 1) / NTH; ++it) {
-      const int idx = threadIdx.x + it * NTH;
-      const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
-      const int n = n0 + c4;
-      if (idx < PIECES && row < M && n < Nout)
-        *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)row * Nout + n) =
-            *reinterpret_cast<const f32x4*>(&ot[tt][row * OS + c4]);
     }
   }
 }
@@ -723,7 +735,7 @@ hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
 // K is not split (its grid size: the statistics pairs per row), else 0 and the
 // streaming kernel's kEpiLogits epilogue.
 int logits_persistent_grid(const GemmPlan& p, int Nout) {
-  if (p.nkc > 1 || p.mblocks > 1 || p.mt > 3 || p.depth >= 3) return 0;
+  if (p.nkc > 1 || p.mblocks > 1 || p.mt > 4 || p.depth >= 3) return 0;
   // 16-row windows stage little x per weight byte: 8 waves per workgroup
   const int NW = p.mt == 1 ? kNW : kLogitsWaves;
   const int groups = (Nout / 16 + NW - 1) / NW;
@@ -738,7 +750,8 @@ hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
   switch (p.mt) {
     case 1: hipLaunchKernelGGL((gemm_logits_kernel<1, kNW>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((gemm_logits_kernel<2, kLogitsWaves>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((gemm_logits_kernel<3, kLogitsWaves>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((gemm_logits_kernel<3, kLogitsWaves>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((gemm_logits_kernel<4, kLogitsWaves>), grid, block, 0, s, a); break;
   }
   return hipGetLastError();
 }

@@ -28,6 +28,7 @@
 //   rows and the second half the matching up rows.
 #include "common.h"
 #include "kernels.h"
+#include <utility>
 
 namespace nj {
 namespace {
@@ -124,11 +125,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
 #pragma unroll
     for (int q = 0; q < UPW; ++q) issue1(q, st, buf);
   };
-  // LDS unit of weight fragment j of this wave
-  auto wunit = [&](int j) {
-    if constexpr (NG == 1) return XU + wn * TN + j;
-    else return (j < TN / 2) ? XU + wn * (TN / 2) + j : XU + WU / 2 + wn * (TN / 2) + (j - TN / 2);
-  };
+  // LDS unit of weight fragment j of this wave: wave base + a constant
+  const int wub = XU + wn * (NG == 1 ? TN : TN / 2), xub = wm * TM;
+  auto wofs = [](int j) { return NG == 1 ? j : (j < TN / 2 ? j : WU / 2 + j - TN / 2); };
 
   f32x4 acc[TM][TN];
 #pragma unroll
@@ -136,27 +135,21 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Per-buffer fragment read addresses, fixed for the whole loop: every read
+  // below is one of these plus a compile-time offset (a ds_read immediate),
+  // so the loop computes no LDS addresses.
+  const bf16_t* wrd[NBUF];
+  const bf16_t* xrd[NBUF];
+#pragma unroll
+  for (int b = 0; b < NBUF; ++b) {
+    wrd[b] = lds + b * STAGE + wub * 512 + lane * 8;
+    xrd[b] = lds + b * STAGE + xub * 512 + lane * 8;
+  }
+  auto ld16 = [](const bf16_t* p) { return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p)); };
+
   // Fragments go through two register sets: those of stage st+1 are read
   // from LDS while stage st is multiplied.
   bf16x8 xf[2][TM], wf[2][TN];
-  auto rd = [&](auto setc, int buf) {
-    constexpr int set = decltype(setc)::value;
-    const bf16_t* base = lds + buf * STAGE + lane * 8;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      wf[set][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + wunit(j) * 512));
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-      xf[set][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(base + (wm * TM + i) * 512));
-  };
-  auto mm = [&](auto setc) {
-    constexpr int set = decltype(setc)::value;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[set][j], xf[set][i], acc[i][j], 0, 0, 0);
-  };
 
   // the plan counts K in 64-wide stages; here a stage is one 32-wide k-step
   const int spc = a.stages_per_chunk * 2;
@@ -168,33 +161,38 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
 #pragma unroll
   for (int d = 0; d < NBUF; ++d) issue(min(st0 + d, st1 - 1), d);
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NBUF - 1) * UPW) : "memory");
-  rd(std::integral_constant<int, 0>{}, 0);
-  // Iteration st: stage st+1 has landed in this wave's units once at most
-  // the NBUF-2 later stages' loads are outstanding, and in every wave's after
-  // the barrier -- by which time every wave has also read stage st into
-  // registers, so its buffer takes stage st+NBUF.  Then stage st+1 is read
-  // while stage st is multiplied.
+#pragma unroll
+  for (int j = 0; j < TN; ++j) wf[0][j] = ld16(wrd[0] + wofs(j) * 512);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) xf[0][i] = ld16(xrd[0] + i * 512);
+  // Step st (stage st sits in buffer (st - st0) % NBUF): stage st+1 has
+  // landed in this wave's units once at most the NBUF-2 later stages' loads
+  // are outstanding, and in every wave's after the barrier -- by which time
+  // every wave's reads of stage st (issued during step st-1, completed before
+  // the barrier) are done, so its buffer takes stage st+NBUF.  Then stage
+  // st+1 is read while stage st is multiplied.
   // Each MFMA row i (TN multiplies) is preceded by this stage's share of the
   // loads for stage st+NBUF and of the fragment reads for stage st+1, so the
   // wave never stops issuing MFMAs for long (one wave per SIMD in the
   // 4-wave shape hides nothing behind another wave).
   constexpr int NRD = TM + TN;
-  auto step = [&](auto pc, int st) {
-    constexpr int P = decltype(pc)::value;
-    constexpr int Q = 1 - P;
-    const int i0 = st - st0;
-    const int nst = min(st + NBUF, st1 - 1), nbuf = i0 % NBUF, rbuf = (i0 + 1) % NBUF;
+  auto step = [&](auto pc, auto bc, int st) {
+    constexpr int P = decltype(pc)::value, Q = 1 - P;
+    constexpr int BUF = decltype(bc)::value, RBUF = (BUF + 1) % NBUF;
+    const int nst = min(st + NBUF, st1 - 1);
+    // LDS reads first, as a wait the compiler sees (so it knows every
+    // fragment register has landed), then the loads and the barrier
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NBUF - 2) * UPW) : "memory");
-    const bf16_t* rbase = lds + rbuf * STAGE + lane * 8;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int q = i * UPW / TM; q < (i + 1) * UPW / TM; ++q) issue1(q, nst, nbuf);
+      for (int q = i * UPW / TM; q < (i + 1) * UPW / TM; ++q) issue1(q, nst, BUF);
 #pragma unroll
       for (int e = i * NRD / TM; e < (i + 1) * NRD / TM; ++e) {
-        if (e < TN) wf[Q][e] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rbase + wunit(e) * 512));
-        else xf[Q][e - TN] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rbase + (wm * TM + e - TN) * 512));
+        if (e < TN) wf[Q][e] = ld16(wrd[RBUF] + wofs(e) * 512);
+        else xf[Q][e - TN] = ld16(xrd[RBUF] + (e - TN) * 512);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j)
@@ -202,9 +200,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     }
     __builtin_amdgcn_sched_barrier(0);
   };
-  for (int st = st0; st < st1; st += 2) {
-    step(std::integral_constant<int, 0>{}, st);
-    if (st + 1 < st1) step(std::integral_constant<int, 1>{}, st + 1);
+  // Unrolled so that the buffer and the register set of every step are
+  // compile-time constants.
+  constexpr int UNR = NBUF % 2 == 0 ? NBUF : 2 * NBUF;
+  for (int st = st0; st < st1; st += UNR) {
+    [&]<int... S>(std::integer_sequence<int, S...>) {
+      ((st + S < st1 ? (step(std::integral_constant<int, S % 2>{}, std::integral_constant<int, S % NBUF>{}, st + S), 0) : 0), ...);
+    }(std::make_integer_sequence<int, UNR>{});
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the surplus loads, before LDS is reused or the workgroup exits
 
