@@ -26,7 +26,11 @@ namespace {
 
 constexpr int kD = 128;  // head dim of the bf16 path
 constexpr int kMaxExtraSplits = 4096;  // KV-split workgroups beyond one per (sequence, KV head)
-constexpr int kResidentWorkgroups = 512;  // 256 CUs x 2 attention workgroups
+constexpr int kAttnBuf = 2;    // chunk buffers per workgroup (kAttnBuf - 1 chunks in flight)
+constexpr int kAttnChunk = 4;  // cached blocks per chunk
+// workgroups per CU that the chunk buffers leave room for (160 KB of LDS)
+constexpr int attn_wgs_per_cu(int nbuf, int cb) { return (160 * 1024 - 1024) / (nbuf * cb * 8 * 1024); }
+constexpr int kResidentWorkgroups = 256 * attn_wgs_per_cu(kAttnBuf, kAttnChunk);
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
@@ -51,14 +55,13 @@ struct AttnK {
 };
 
 // The workgroup
-// streams its KV range in chunks of kCB blocks: all 256 threads load the next
-// chunk (coalesced 16-byte pieces) while the current one is multiplied out of
-// LDS, so one chunk per workgroup is always in flight.  Waves are split into
+// streams its KV range in chunks of kCB blocks, loaded straight into LDS
+// while earlier ones are multiplied out of LDS (NBUF buffers, NBUF-1 chunks in
+// flight).  Waves are split into
 // RTW row tiles x (4 / RTW) token phases: a wave multiplies its row tile
 // against every (4/RTW)-th block of the chunk, and the phases of a tile are
 // merged at the end.  LDS rows are XOR-swizzled in 16-byte (K) and 8-byte (V)
 // units so that the fragment reads of 16 consecutive rows hit distinct banks.
-constexpr int kCB = 4;  // cached blocks per chunk
 constexpr int kKPieces = kBlock * kD / 8;  // 16-byte pieces per K (or V) block: 256
 
 __device__ __forceinline__ int k_lds(int tok, int chunk16) {  // element offset in a K block [16][128]
@@ -186,11 +189,14 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
   }
 }
 
-template <int RTW>
-__global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
+template <int RTW, int NBUF, int kCB>
+__global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kernel(AttnK a) {
   constexpr int NTP = 4 / RTW;  // token phases per row tile
   constexpr int KV_ELEMS = kCB * kBlock * kD;  // one chunk of K (or V)
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * 2 * KV_ELEMS];  // [buf][K|V][chunk], 64 KB
+  constexpr int WPB = 4 / kCB;  // waves loading one block (its K and V halves when 2)
+  constexpr int UPW = 8 / WPB;  // 1 KB load instructions per wave and chunk
+  static_assert(kCB == 2 || kCB == 4, "a chunk's blocks split evenly over the 4 waves");
+  __shared__ __attribute__((aligned(16))) bf16_t smem[NBUF * 2 * KV_ELEMS];  // [buf][K|V][chunk], 32 KB per buffer
   const int pair = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
   const int b = pair / a.Hkv, kvh = pair % a.Hkv;
   const int G = a.H / a.Hkv, R = a.T * G, RT = (R + 15) / 16;
@@ -224,14 +230,6 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
   }
   bf16x8 qf[4];
   int qpos;
-  {
-    const int qc = min(rt * 16 + r16, R - 1);  // padding rows repeat the last real row
-    const int i = qc / G, hh = qc % G;
-    const bf16_t* src = a.q + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + 32 * g;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qf[s] = ld8(src + 8 * s);
-    qpos = i;
-  }
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 o[8];
 #pragma unroll
@@ -247,73 +245,94 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
       nblk = 1;
     }
   };
-  // Thread t loads piece t of each block of the chunk (K: token t/16, 16-byte
-  // column t%16; V: dim t/2, tokens 8*(t%2)..+7).  Branch-free: every piece is
-  // loaded from a valid address (blocks past the chunk or with a bad id read
-  // the window block) and zeroed when stored.  The block ids of a chunk are
-  // read one chunk ahead of its pages.
+  // Chunk loads go from memory straight into LDS (global_load_lds_dwordx4):
+  // a block is 4 K and 4 V instructions of 1 KB, loaded by one wave (chunks
+  // of 4 blocks) or by two (K and V; chunks of 2), and
+  // lane i's 16 bytes land at byte 16 i of the instruction's KB -- so each lane
+  // fetches the global piece that the swizzled layout keeps there.  NBUF
+  // buffers, NBUF-1 chunks in flight.  A block's page id is read with a scalar
+  // load one chunk before its pages; blocks past the chunk, or with a bad id,
+  // load the window block (valid memory, never read as cache).  Every chunk
+  // issues the same UPW loads per wave, so the wait counts below are exact.
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t kofs[4], vofs[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int tok = 4 * j + (lane >> 4), slot = lane & 15;
+    kofs[j] = (uint32_t)(tok * kD + ((slot ^ tok) & 15) * 8) * 2u;
+    const int dim = 32 * j + (lane >> 1), hv = (lane & 1) ^ ((dim >> 3) & 1);
+    vofs[j] = (uint32_t)(dim * kBlock + hv * 8) * 2u;
+  }
   const bf16_t* win_k = a.wk + ((size_t)b * a.Hkv + kvh) * (kBlock * kD);
   const bf16_t* win_v = a.wv + ((size_t)b * a.Hkv + kvh) * (kBlock * kD);
-  const int32_t* trow = a.table + (size_t)b * a.max_blocks;
-  u32x4 kr[kCB], vr[kCB];
-  bool okb[kCB];
-  int ph[kCB];
-  auto tload = [&](int ch, int (&dst)[kCB]) {
-    int j0, nblk;
-    chunk_blocks(ch, j0, nblk);
-#pragma unroll
-    for (int bi = 0; bi < kCB; ++bi) dst[bi] = trow[max(0, min(j0 + bi, c1 - 1))];
-  };
-  auto gload = [&](int ch) {
-    int j0, nblk;
-    chunk_blocks(ch, j0, nblk);
-    bool bad = false;
-#pragma unroll
-    for (int bi = 0; bi < kCB; ++bi) {
-      const bool used = j0 >= 0 && bi < nblk;
-      const bool valid = ph[bi] >= 0 && ph[bi] < a.num_blocks;
-      bad |= used && !valid;
-      okb[bi] = (used && valid) || (j0 < 0 && bi == 0);
-      const size_t off = ((size_t)(used && valid ? ph[bi] : 0) * a.Hkv + kvh) * (kBlock * kD);
-      const bf16_t* kb = (used && valid) ? a.kp + off : win_k;
-      const bf16_t* vb = (used && valid) ? a.vp + off : win_v;
-      kr[bi] = *reinterpret_cast<const u32x4*>(kb + threadIdx.x * 8);
-      vr[bi] = *reinterpret_cast<const u32x4*>(vb + threadIdx.x * 8);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
+  bool bad = false;
+  // Page ids: lane l of wave w holds the id of block w of cached chunk
+  // idbase + l, read 64 chunks at a time (a split longer than 64 chunks
+  // reloads, waiting for its loads in flight); a chunk's id is then a lane
+  // read, with no memory access in the loop.  -1: load the window block.
+  int idv = -1, idbase = -64;
+  auto block_id = [&](int ch) {
+    if (ch < wch || ch >= nchunks) return -1;
+    const int cc = ch - wch;
+    if (cc - idbase >= 64) {
+      idbase = cc;
+      const int blk = c0 + (cc + lane) * kCB + wv / WPB;
+      idv = (cc + lane < ncc && blk < c1) ? a.table[(size_t)b * a.max_blocks + blk] : -1;
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
-    if (bad && threadIdx.x == 0) flag_error(a.err, kErrBlock);
+    return __builtin_amdgcn_readlane(idv, cc - idbase);
   };
-  auto sstore = [&](int buf) {
-    bf16_t* ks = smem + buf * 2 * KV_ELEMS;
-    bf16_t* vs = ks + KV_ELEMS;
-    const int t = threadIdx.x;
-    const u32x4 z = u32x4{0u, 0u, 0u, 0u};
+  auto issue = [&](int ch, int id) {
+    const int buf = ch % NBUF;
+    int ph = __builtin_amdgcn_readfirstlane(id);
+    if (ph != -1 && (ph < 0 || ph >= a.num_blocks)) {
+      bad = true;
+      ph = -1;
+    }
+    const size_t off = ((size_t)max(ph, 0) * a.Hkv + kvh) * (kBlock * kD);
+    const bf16_t* kb = ph >= 0 ? a.kp + off : win_k;
+    const bf16_t* vb = ph >= 0 ? a.vp + off : win_v;
+    const uint32_t kd = lds0 + (uint32_t)(buf * 2 * KV_ELEMS + (wv / WPB) * kBlock * kD) * 2u;
+    const uint32_t vd = kd + (uint32_t)KV_ELEMS * 2u;
+    if (WPB == 1 || wv % 2 == 0) {
 #pragma unroll
-    for (int bi = 0; bi < kCB; ++bi) {
-      *reinterpret_cast<u32x4*>(ks + bi * kBlock * kD + k_lds(t >> 4, t & 15)) = okb[bi] ? kr[bi] : z;
-      *reinterpret_cast<u32x4*>(vs + bi * kBlock * kD + v_lds(t >> 1, (t & 1) * 2)) = okb[bi] ? vr[bi] : z;
+      for (int j = 0; j < 4; ++j)
+        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(kofs[j]), "s"(kb), "s"(kd + j * 1024)
+                     : "memory", "m0");
+    }
+    if (WPB == 1 || wv % 2 == 1) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(vofs[j]), "s"(vb), "s"(vd + j * 1024)
+                     : "memory", "m0");
     }
   };
-
-  if (nchunks > 0) {
-    tload(0, ph);
-    gload(0);
-    tload(min(1, nchunks - 1), ph);
-    sstore(0);
+  for (int d = 0; d < NBUF - 1; ++d) issue(d, block_id(d));
+  int ph_pre = block_id(NBUF - 1);
+  // q after the prologue's chunks, and a wait the compiler sees: from here on
+  // no load of its own is outstanding, so it adds no load waits in the loop
+  // (which would also wait for the chunks in flight)
+  {
+    const int qc = min(rt * 16 + r16, R - 1);  // padding rows repeat the last real row
+    const int i = qc / G, hh = qc % G;
+    const bf16_t* src = a.q + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + 32 * g;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = ld8(src + 8 * s);
+    qpos = i;
   }
-  __syncthreads();
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   for (int ch = 0; ch < nchunks; ++ch) {
-    const int buf = ch & 1;
-    // ids of chunk ch+2 first (older in the load queue, so waiting for them
-    // never waits for the pages), then the pages of chunk ch+1; the chunk
-    // after the last re-loads the last one into the idle buffer (unread),
-    // which keeps the loop free of branches around the loads
-    int ph2[kCB];
-    tload(min(ch + 2, nchunks - 1), ph2);
-    gload(min(ch + 1, nchunks - 1));
+    // this wave's loads of chunk ch have landed once at most the later
+    // NBUF-2 chunks' are outstanding; after the barrier every wave's have, and
+    // every wave is done with chunk ch-1, whose buffer takes chunk ch+NBUF-1
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NBUF - 2) * UPW) : "memory");
+    issue(ch + NBUF - 1, ph_pre);
+    ph_pre = block_id(ch + NBUF);
     int j0, nblk;
     chunk_blocks(ch, j0, nblk);
     const bool win = j0 < 0;
-    const bf16_t* ks = smem + buf * 2 * KV_ELEMS;
+    const bf16_t* ks = smem + (ch % NBUF) * 2 * KV_ELEMS;
     const bf16_t* vs = ks + KV_ELEMS;
     if (rt < RT) {
       for (int bi = tp; bi < nblk; bi += NTP) {
@@ -371,11 +390,10 @@ __global__ __launch_bounds__(256, 2) void attn_lds_kernel(AttnK a) {
         }
       }
     }
-    sstore(buf ^ 1);
-    __syncthreads();
-#pragma unroll
-    for (int bi = 0; bi < kCB; ++bi) ph[bi] = ph2[bi];
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the surplus loads, before LDS is reused
+  __syncthreads();
+  if (bad && lane == 0) flag_error(a.err, kErrBlock);  // bad is per wave
 
   // merge the token phases of each row tile (LDS reused), then store or write partials
   float* s_o = reinterpret_cast<float*>(smem);  // [NTP][kD][17]
@@ -564,9 +582,9 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
           (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * 2 * 4, INT32_MAX)};
   dim3 grid(x.B * x.Hkv, x.nsplit);
   switch (RT) {
-    case 1: hipLaunchKernelGGL(attn_lds_kernel<1>, grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL(attn_lds_kernel<2>, grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL(attn_lds_kernel<4>, grid, dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((attn_lds_kernel<1, kAttnBuf, kAttnChunk>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((attn_lds_kernel<2, kAttnBuf, kAttnChunk>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((attn_lds_kernel<4, kAttnBuf, kAttnChunk>), grid, dim3(256), 0, s, a); break;
   }
   return hipGetLastError();
 }
