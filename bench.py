@@ -175,9 +175,15 @@ def report(args):
                 n = nb.gemm_workspace_bytes(nb.NJ_BF16, M, N, K, epi)
                 gws = torch.empty(n, dtype=torch.uint8, device="cuda")
                 nb.workspace_init(gws.data_ptr(), n, s)
-                call = lambda: nb.gemm(nb.NJ_BF16, x.data_ptr(), wt.data_ptr(), y.data_ptr(), M, N, K, epi,
+                # the tiled kernel's inputs in the k-blocked layout, as the step writes them
+                flag = nb.NJ_GEMM_KBLOCKED
+                call = lambda: nb.gemm(nb.NJ_BF16, x.data_ptr(), wt.data_ptr(), y.data_ptr(), M, N, K, epi | flag,
                                        gws.data_ptr(), n, s)
-                call()
+                try:
+                    call()
+                except nb.NightjarError:  # a streaming-kernel plan: row-major x
+                    flag = 0
+                    call()
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
                 for _ in range(5):

@@ -245,8 +245,14 @@ int nightjar_pack_weight(const void* src, void* dst, int32_t N, int32_t K, void*
 enum {
   NJ_GEMM_STORE = 0,    /* y[m][n] = acc (fp32 out)                                  */
   NJ_GEMM_RESIDUAL = 1, /* y[m][n] += acc (fp32 in/out)                              */
-  NJ_GEMM_SWIGLU = 2    /* N = 2F weight rows; y[m][f] = silu(acc_f) * acc_{F+f}, y in
+  NJ_GEMM_SWIGLU = 2,   /* N = 2F weight rows; y[m][f] = silu(acc_f) * acc_{F+f}, y in
                            the weight dtype, [M][F]                                 */
+  /* Flag OR-ed into the epilogue: x (and a SWIGLU y) in the k-blocked layout
+     the verify step gives the tiled kernel's inputs, [K/32][M][32]: element
+     (m, k) at ((k / 32) * M + m) * 32 + k % 32 (for y, F in place of K; F % 32
+     == 0).  bf16 and the tiled kernel only (nightjar_gemm: when its planner picks that
+     kernel); otherwise NJ_EINVAL. */
+  NJ_GEMM_KBLOCKED = 16
 };
 
 /*

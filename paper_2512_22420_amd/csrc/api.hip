@@ -239,6 +239,14 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
                gemm_streams(M, d.vocab, d.d_model, kEpiStore) && aligned16(w->final_norm);
   for (int l = 0; l < d.n_layers && fused; ++l)
     fused = aligned16(w->layers[l].attn_norm) && aligned16(w->layers[l].ffn_norm);
+  // Without the folded norm, the input of each GEMM that runs on the
+  // LDS-tiled kernel is written k-blocked by its producer (norm, attention,
+  // SwiGLU epilogue), so the tile loads read 1 KB contiguous units.
+  const bool kb_qkv = bf && !fused && !gemm_streams(M, QKV, d.d_model, kEpiStore);
+  const bool kb_o = bf && !fused && !gemm_streams(M, d.d_model, HD, kEpiResidual);
+  const bool kb_gu = bf && !fused && !gemm_streams(M, F2, d.d_model, kEpiSwiglu);
+  const bool kb_dn = bf && !fused && d.ffn_dim % 32 == 0 && !gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual);
+  const bool kb_lm = bf && !fused && !gemm_streams(M, d.vocab, d.d_model, kEpiStore);
   float* ssq = reinterpret_cast<float*>(ws + L.ssq);
   const int nt = (d.d_model + 127) / 128;
   const GemmNorm scale_in{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, nullptr};
@@ -249,7 +257,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
            "embed");
   else
     NJ_TRY(launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
-                             d.vocab, d.rms_eps, err, s),
+                             d.vocab, d.rms_eps, err, s, kb_qkv),
            "embed");
   for (int l = 0; l < d.n_layers; ++l) {
     const nj_layer_weights& lw = w->layers[l];
@@ -263,8 +271,8 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
       NJ_TRY(launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiQkvRope, scale_in, gcnt, gpart, s, &rope),
              "qkv gemm");
     } else {
-      if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s), "attn_norm");
-      NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s), "qkv gemm");
+      if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s, kb_qkv), "attn_norm");
+      NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb_qkv), "qkv gemm");
       NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
                                 wk, wv, snap, acnt, s),
              "rope");
@@ -272,7 +280,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),
-                reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, o, err};
+                reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, o, err, kb_o};
     NJ_TRY(launch_attention(aa, s), "attention");
     const void* g_next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : w->final_norm;
     if (fused) {
@@ -284,10 +292,12 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
       NJ_TRY(launch_gemm_norm(act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidualNorm, to_next, gcnt, gpart, s),
              "down gemm");
     } else {
-      NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s), "o gemm");
-      NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s), "ffn_norm");
-      NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, gcnt, gpart, s), "gate_up gemm");
-      NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s), "down gemm");
+      NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s, kb_o), "o gemm");
+      NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s, kb_gu), "ffn_norm");
+      NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, gcnt, gpart, s, kb_gu, kb_dn),
+             "gate_up gemm");
+      NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s, kb_dn),
+             "down gemm");
     }
   }
   bool stats_ready = false;
@@ -298,9 +308,10 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
            "lm_head gemm");
     stats_ready = true;
   } else {
-    NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s), "final_norm");
+    NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s, kb_lm), "final_norm");
     if (bf)
-      NJ_TRY(launch_gemm_logits(x, w->lm_head, logits, stats, M, d.vocab, d.d_model, gcnt, gpart, s, &stats_ready),
+      NJ_TRY(launch_gemm_logits(x, w->lm_head, logits, stats, M, d.vocab, d.d_model, gcnt, gpart, s, &stats_ready,
+                                kb_lm),
              "lm_head gemm");
     else
       NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
@@ -405,6 +416,7 @@ int nightjar_pack_weight(const void* src, void* dst, int32_t N, int32_t K, void*
 }
 
 size_t nightjar_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue) {
+  epilogue &= ~NJ_GEMM_KBLOCKED;
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return 0;
   if (dtype != NJ_BF16) return kAlign;
   const GemmPlan p = gemm_plan(M, N, K, epilogue);
@@ -413,7 +425,12 @@ size_t nightjar_gemm_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_
 
 int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
                   int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream) {
+  const bool kb = (epilogue & NJ_GEMM_KBLOCKED) != 0;
+  epilogue &= ~NJ_GEMM_KBLOCKED;
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
+  if (kb && (dtype != NJ_BF16 || gemm_plan(M, N, K, epilogue).tile == kTileNone))
+    return fail(NJ_EINVAL, "k-blocked operands need the tiled kernel");
+  if (kb && epilogue == NJ_GEMM_SWIGLU && (N / 2) % 32) return fail(NJ_EINVAL, "k-blocked SwiGLU output needs F %% 32 == 0");
   if (!x || !w || !y) return fail(NJ_EINVAL, "NULL operand");
   if (dtype == NJ_BF16 && (!aligned16(x) || !aligned16(w) || !aligned16(y)))
     return fail(NJ_EINVAL, "operands must be 16-byte aligned");
@@ -424,7 +441,8 @@ int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t 
   size_t cnt_bytes = 0;
   if (dtype == NJ_BF16) cnt_bytes = gemm_plan(M, N, K, epilogue).counter_bytes;
   hipError_t e = launch_gemm(dtype == NJ_BF16 ? kBF16 : kF32, x, w, y, M, N, K, epilogue, reinterpret_cast<int*>(ws),
-                             reinterpret_cast<float*>(ws + cnt_bytes), (hipStream_t)stream);
+                             reinterpret_cast<float*>(ws + cnt_bytes), (hipStream_t)stream, kb,
+                             kb && epilogue == NJ_GEMM_SWIGLU);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "gemm");
 }
 
@@ -465,6 +483,7 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
 
 size_t nightjar_gemm_plan_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue,
                                           int32_t kernel, int32_t split_k) {
+  epilogue &= ~NJ_GEMM_KBLOCKED;
   GemmPlan p;
   if (plan_with(dtype, M, N, K, epilogue, kernel, split_k, &p) != NJ_OK) return 0;
   return dtype == NJ_BF16 ? kAlign + p.counter_bytes + p.part_bytes : kAlign;
@@ -473,8 +492,12 @@ size_t nightjar_gemm_plan_workspace_bytes(int32_t dtype, int32_t M, int32_t N, i
 int nightjar_gemm_with_plan(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N, int32_t K,
                             int32_t epilogue, int32_t kernel, int32_t split_k, void* workspace,
                             size_t workspace_bytes, void* stream) {
+  const bool kb = (epilogue & NJ_GEMM_KBLOCKED) != 0;
+  epilogue &= ~NJ_GEMM_KBLOCKED;
   GemmPlan p;
   if (plan_with(dtype, M, N, K, epilogue, kernel, split_k, &p) != NJ_OK) return NJ_EINVAL;
+  if (kb && (dtype != NJ_BF16 || p.tile == kTileNone)) return fail(NJ_EINVAL, "k-blocked operands need the tiled kernel");
+  if (kb && epilogue == NJ_GEMM_SWIGLU && (N / 2) % 32) return fail(NJ_EINVAL, "k-blocked SwiGLU output needs F %% 32 == 0");
   if (!x || !w || !y) return fail(NJ_EINVAL, "NULL operand");
   if (dtype == NJ_BF16 && (!aligned16(x) || !aligned16(w) || !aligned16(y)))
     return fail(NJ_EINVAL, "operands must be 16-byte aligned");
@@ -485,7 +508,8 @@ int nightjar_gemm_with_plan(int32_t dtype, const void* x, const void* w, void* y
   hipError_t e;
   if (dtype == NJ_BF16)
     e = launch_gemm_plan(x, w, y, M, N, K, epilogue, p, reinterpret_cast<int*>(ws),
-                         reinterpret_cast<float*>(ws + p.counter_bytes), (hipStream_t)stream);
+                         reinterpret_cast<float*>(ws + p.counter_bytes), (hipStream_t)stream, kb,
+                         kb && epilogue == NJ_GEMM_SWIGLU);
   else
     e = launch_gemm(kF32, x, w, y, M, N, K, epilogue, nullptr, nullptr, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "gemm");

@@ -52,7 +52,14 @@ struct AttnK {
   int max_blocks, num_blocks, T, H, Hkv;
   float scale_log2;
   int part_o_bytes, part_ml_bytes;
+  int okbM;  // nonzero: out stored k-blocked, [H*kD/32][okbM][32] (okbM = B*T rows)
 };
+
+// output row m = b*T + i, column c = head * kD + d (4 consecutive columns)
+__device__ __forceinline__ u32x2* out_at(const AttnK& a, int m, int c) {
+  return reinterpret_cast<u32x2*>(a.okbM ? a.out + ((size_t)(c >> 5) * a.okbM + m) * 32 + (c & 31)
+                                         : a.out + (size_t)m * a.H * kD + c);
+}
 
 // The workgroup
 // streams its KV range in chunks of kCB blocks, loaded straight into LDS
@@ -159,7 +166,7 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
         u32x2 o;
         o[0] = pack_bf16x2(acc[q][0] * inv, acc[q][1] * inv);
         o[1] = pack_bf16x2(acc[q][2] * inv, acc[q][3] * inv);
-        *reinterpret_cast<u32x2*>(a.out + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d) = o;
+        *out_at(a, b * a.T + i, (kvh * G + hh) * kD + d) = o;
       }
     }
     return;
@@ -185,7 +192,7 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
     u32x2 o;
     o[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     o[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
-    *reinterpret_cast<u32x2*>(a.out + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d) = o;
+    *out_at(a, b * a.T + i, (kvh * G + hh) * kD + d) = o;
   }
 }
 
@@ -438,7 +445,7 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
           u32x2 ov;
           ov[0] = pack_bf16x2(acc[0] / wsum, acc[1] / wsum);
           ov[1] = pack_bf16x2(acc[2] / wsum, acc[3] / wsum);
-          *reinterpret_cast<u32x2*>(a.out + ((size_t)(b * a.T + i) * a.H + kvh * G + hh) * kD + d) = ov;
+          *out_at(a, b * a.T + i, (kvh * G + hh) * kD + d) = ov;
         } else {
           const size_t base = ((size_t)pair * nsplit + split) * (RT * 16) + qr;
           coherent_store(ors, (uint32_t)((base * kD + d) * 4), acc);
@@ -539,13 +546,14 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnF a) {
 
 int attention_plan(int B, int Hkv, int max_blocks) {
   // Enough workgroups to keep ~2048 chunk streams in flight, and no split
-  // longer than 64 blocks (one workgroup streams its chunks one after the
-  // other, so the longest split sets the kernel's duration); at least 8
-  // blocks per split, and at most pairs + kMaxExtraSplits workgroups, which
-  // bounds the partial buffer whatever the context length.  The kernel divides
-  // each sequence's actual blocks evenly over the splits.
+  // longer than 256 blocks (one workgroup streams its chunks one after the
+  // other, so the longest split sets the kernel's duration; shorter splits
+  // cost more in per-split start-up and merging than they win in balance); at
+  // least 8 blocks per split, and at most pairs + kMaxExtraSplits
+  // workgroups, which bounds the partial buffer whatever the context length.
+  // The kernel divides each sequence's actual blocks evenly over the splits.
   const int pairs = B * Hkv;
-  const int ns_len = (max_blocks + 63) / 64;
+  const int ns_len = (max_blocks + 255) / 256;
   int ns = std::max((2048 + pairs - 1) / pairs, ns_len);
   // keep every workgroup resident at once (2 per CU) when the split-length
   // bound allows: a split that starts late holds up the merge of its
@@ -579,7 +587,8 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
           static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv,
           (float)(1.4426950408889634 / sqrt((double)kD)),
           (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * kD * 4, INT32_MAX),
-          (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * 2 * 4, INT32_MAX)};
+          (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * 2 * 4, INT32_MAX),
+          x.out_kblocked ? x.B * x.T : 0};
   dim3 grid(x.B * x.Hkv, x.nsplit);
   switch (RT) {
     case 1: hipLaunchKernelGGL((attn_lds_kernel<1, kAttnBuf, kAttnChunk>), grid, dim3(256), 0, s, a); break;

@@ -33,7 +33,7 @@ __device__ __forceinline__ void store4(bf16_t* p, const float* v) {
 // (d % 4 == 0, d <= 4 * kNormThreads * kNormMaxPer).
 template <typename T>
 __device__ __forceinline__ void norm_row(const float (&hv)[kNormMaxPer][4], const T* __restrict__ gain,
-                                         T* __restrict__ x, int d, float eps, float* sh) {
+                                         T* __restrict__ X, int row, int kbM, int d, float eps, float* sh) {
   float ss = 0.f;
 #pragma unroll
   for (int it = 0; it < kNormMaxPer; ++it) {
@@ -52,7 +52,8 @@ __device__ __forceinline__ void norm_row(const float (&hv)[kNormMaxPer][4], cons
       load4(gain + j, gv);
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = hv[it][e] * r * gv[e];
-      store4(x + j, o);
+      // row-major [M][d], or k-blocked [d/32][M][32] for the LDS-tiled GEMM
+      store4(kbM ? X + ((size_t)(j >> 5) * kbM + row) * 32 + (j & 31) : X + (size_t)row * d + j, o);
     }
   }
 }
@@ -61,7 +62,7 @@ template <typename T>
 __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const T* __restrict__ embed,
     const T* __restrict__ gain, float* __restrict__ h, T* __restrict__ x, int d, int V, float eps,
-    int* __restrict__ err) {
+    int* __restrict__ err, int kbM) {
   __shared__ float sh[kNormThreads / kWave];
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
       store4(hr + j, hv[it]);
     }
   }
-  norm_row<T>(hv, gain, x + (size_t)row * d, d, eps, sh);
+  norm_row<T>(hv, gain, x, row, kbM, d, eps, sh);
 }
 
 // bf16 path with the RMSNorm folded into the GEMMs: h = E[id], x = bf16(h *
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
 template <typename T>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __restrict__ h,
                                                                const T* __restrict__ gain, T* __restrict__ x,
-                                                               int d, float eps) {
+                                                               int d, float eps, int kbM) {
   __shared__ float sh[kNormThreads / kWave];
   const float* hr = h + (size_t)blockIdx.x * d;
   float hv[kNormMaxPer][4];
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
     const int j = (it * kNormThreads + threadIdx.x) * 4;
     if (j < d) load4(hr + j, hv[it]);
   }
-  norm_row<T>(hv, gain, x + (size_t)blockIdx.x * d, d, eps, sh);
+  norm_row<T>(hv, gain, x, blockIdx.x, kbM, d, eps, sh);
 }
 
 // RoPE and the window K/V store.  One thread per rotation pair (j, j + D/2) of
@@ -290,15 +291,16 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
 
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
                              const void* gain, float* h, void* x, int d, int V, float eps, int* err,
-                             hipStream_t s) {
+                             hipStream_t s, bool x_kblocked) {
+  const int kbM = x_kblocked ? B * T : 0;
   if (dtype == kF32)
     hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const float*>(embed), static_cast<const float*>(gain), h,
-                       static_cast<float*>(x), d, V, eps, err);
+                       static_cast<float*>(x), d, V, eps, err, kbM);
   else
     hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h,
-                       static_cast<bf16_t*>(x), d, V, eps, err);
+                       static_cast<bf16_t*>(x), d, V, eps, err, kbM);
   return hipGetLastError();
 }
 
@@ -314,13 +316,14 @@ hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B
 }
 
 hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, int M, int d, float eps,
-                          hipStream_t s) {
+                          hipStream_t s, bool x_kblocked) {
+  const int kbM = x_kblocked ? M : 0;
   if (dtype == kF32)
     hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(M), dim3(kNormThreads), 0, s, h,
-                       static_cast<const float*>(gain), static_cast<float*>(x), d, eps);
+                       static_cast<const float*>(gain), static_cast<float*>(x), d, eps, kbM);
   else
     hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(M), dim3(kNormThreads), 0, s, h,
-                       static_cast<const bf16_t*>(gain), static_cast<bf16_t*>(x), d, eps);
+                       static_cast<const bf16_t*>(gain), static_cast<bf16_t*>(x), d, eps, kbM);
   return hipGetLastError();
 }
 

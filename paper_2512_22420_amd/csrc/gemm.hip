@@ -80,6 +80,7 @@ struct GemmK {
   bf16_t* xg;
   float* ssq_out;
   QkvRope rope;     // kEpiQkvRope
+  int ykbM;         // kEpiSwiglu: nonzero = y stored k-blocked, [Nout/32][M][32] (M = ykbM)
 };
 
 // The weight stream of one 16-row weight tile (wp: this lane's piece of k-step
@@ -343,7 +344,9 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       u32x2 o;
       o[0] = pack_bf16x2(silu_mul(gt[0], up[0]), silu_mul(gt[1], up[1]));
       o[1] = pack_bf16x2(silu_mul(gt[2], up[2]), silu_mul(gt[3], up[3]));
-      *reinterpret_cast<u32x2*>(static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n) = o;
+      bf16_t* yp = a.ykbM ? static_cast<bf16_t*>(a.Y) + ((size_t)(n >> 5) * a.ykbM + m) * 32 + (n & 31)
+                          : static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n;
+      *reinterpret_cast<u32x2*>(yp) = o;
     }
   } else if constexpr (EPI == kEpiStore || EPI == kEpiLogits) {
     // The MFMA result layout puts 16 rows x 64 bytes in one store
@@ -859,21 +862,26 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split) {
 }
 
 hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
-                            int* counters, float* part, hipStream_t s) {
-  if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s);
+                            int* counters, float* part, hipStream_t s, bool x_kblocked, bool y_kblocked) {
+  if (p.tile != kTileNone)
+    return launch_gemm_tile(x, w, y, M, N, K, epi, p, counters, part, s, nullptr, x_kblocked, y_kblocked);
+  if (x_kblocked) return hipErrorInvalidValue;  // the streaming kernel reads row-major x
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0, nullptr, 0, 0.f, nullptr, nullptr, nullptr, {}};
+          p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nullptr, 0, nullptr, 0, 0.f, nullptr, nullptr, nullptr, {},
+          y_kblocked ? M : 0};
   if (epi == kEpiStore) return launch_logits(a, p, s);  // stats == nullptr: plain store
   if (epi == kEpiResidual) return launch_stream<kEpiResidual>(a, p, s);
   return launch_stream<kEpiSwiglu>(a, p, s);
 }
 
 hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* stats, int M, int N, int K,
-                              int* counters, float* part, hipStream_t s, bool* stats_written) {
+                              int* counters, float* part, hipStream_t s, bool* stats_written, bool x_kblocked) {
   const GemmPlan p = gemm_plan(M, N, K, kEpiStore);
   *stats_written = true;
-  if (p.tile != kTileNone) return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s, stats);
+  if (p.tile != kTileNone)
+    return launch_gemm_tile(x, w, y, M, N, K, kEpiStore, p, counters, part, s, stats, x_kblocked);
+  if (x_kblocked) return hipErrorInvalidValue;  // the streaming kernel reads row-major x
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, N, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, stats,
           (N + kStatChunk - 1) / kStatChunk, nullptr, 0, 0.f, nullptr, nullptr, nullptr, {}};
@@ -920,7 +928,7 @@ hipError_t launch_pack_weight(const void* src, void* dst, int N, int K, hipStrea
 }
 
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
-                       int* counters, float* part, hipStream_t s) {
+                       int* counters, float* part, hipStream_t s, bool x_kblocked, bool y_kblocked) {
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   if (dtype == kF32) {
     dim3 grid((Nout + 3) / 4);
@@ -931,7 +939,7 @@ hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, 
     else hipLaunchKernelGGL(gemm_f32_kernel<kEpiSwiglu>, grid, dim3(256), 0, s, xf, wf, y, M, Nout, K);
     return hipGetLastError();
   }
-  return launch_gemm_plan(x, w, y, M, N, K, epi, gemm_plan(M, N, K, epi), counters, part, s);
+  return launch_gemm_plan(x, w, y, M, N, K, epi, gemm_plan(M, N, K, epi), counters, part, s, x_kblocked, y_kblocked);
 }
 
 }  // namespace nj

@@ -46,6 +46,7 @@ struct TileK {
   int part_bytes;
   float* stats;   // kEpiStore, nullable: [M][nch][2] (max, sum of exp) of each row over this tile's columns, entry tn
   int nch;
+  int xkb, ykb;   // x (SwiGLU: y) stored k-blocked, [K/32][M][32]
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -98,9 +99,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   for (int q = 0; q < UPW; ++q) {
     const int u = wv * UPW + q;
     if (u < XU) {
+      // row-major x: 64 bytes of each of 16 rows; k-blocked x: one 1 KB run
+      const uint32_t row = (uint32_t)min(m0 + u * 16 + r, M - 1);
       ubase[q] = reinterpret_cast<const char*>(a.X);
-      ustep[q] = 64;
-      vofs[q] = ((uint32_t)min(m0 + u * 16 + r, M - 1) * (uint32_t)K + g * 8) * 2u;
+      ustep[q] = a.xkb ? (uint32_t)M * 64u : 64u;
+      vofs[q] = a.xkb ? (row * 32u + g * 8) * 2u : (row * (uint32_t)K + g * 8) * 2u;
     } else {
       const int t16 = u - XU;
       int T;
@@ -335,7 +338,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
         u32x2 o;
         o[0] = pack_bf16x2(silu_mul(gt[0], up[0]), silu_mul(gt[1], up[1]));
         o[1] = pack_bf16x2(silu_mul(gt[2], up[2]), silu_mul(gt[3], up[3]));
-        *reinterpret_cast<u32x2*>(static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n) = o;
+        bf16_t* yp = a.ykb ? static_cast<bf16_t*>(a.Y) + ((size_t)(n >> 5) * M + m) * 32 + (n & 31)
+                           : static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n;
+        *reinterpret_cast<u32x2*>(yp) = o;
       }
     }
   }
@@ -357,11 +362,13 @@ int tile_bm(int cfg) { return cfg == kTile256x256 ? 256 : cfg == kTile192x256 ? 
 int tile_bn(int cfg) { return cfg == kTile128x128 ? 128 : 256; }
 
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
-                            int* counters, float* part, hipStream_t s, float* stats) {
+                            int* counters, float* part, hipStream_t s, float* stats, bool x_kblocked,
+                            bool y_kblocked) {
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles, p.nkc, p.stages_per_chunk,
-          (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk};
+          (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk,
+          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0};
   switch (p.tile) {
     // 4 waves of 128 x 128 (a quarter fewer LDS reads per MFMA; all 512
     // registers per lane), 8 waves of 128 x 64 for SwiGLU, whose epilogue

@@ -67,16 +67,17 @@ hipError_t launch_pack_weight(const void* src, void* dst, int N, int K, hipStrea
 // (plan.part_bytes) are scratch; GEMMs that run one after another on a stream
 // may share both as long as the counters are never overwritten by anything else.
 hipError_t launch_gemm(int dtype, const void* x, const void* w, void* y, int M, int N, int K, int epi,
-                       int* counters, float* part, hipStream_t s);
+                       int* counters, float* part, hipStream_t s, bool x_kblocked = false, bool y_kblocked = false);
 // bf16 GEMM with an explicit plan (either kernel; for the streaming one
 // mt 1..4, any nkc/stages_per_chunk).
 hipError_t launch_gemm_plan(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
-                            int* counters, float* part, hipStream_t s);
+                            int* counters, float* part, hipStream_t s, bool x_kblocked = false,
+                            bool y_kblocked = false);
 // LM head: y = x . w^T stored fp32, plus the chunk statistics of the
 // acceptance kernels (stats [M][accept_chunks(N)][2]) when the plan uses the
 // weight-streaming kernel; *stats_written says whether it did.
 hipError_t launch_gemm_logits(const void* x, const void* w, float* y, float* stats, int M, int N, int K,
-                              int* counters, float* part, hipStream_t s, bool* stats_written);
+                              int* counters, float* part, hipStream_t s, bool* stats_written, bool x_kblocked = false);
 // RMSNorm folded into the weight-streaming GEMMs.  A producer (residual
 // epilogue kEpiResidualNorm) adds into h and writes xg = bf16(h * gain) and
 // ssq_out[m][t], the sum of h^2 over output columns 128t .. 128t+127; a
@@ -118,15 +119,19 @@ bool gemm_streams(int M, int N, int K, int epi);
 int logits_stat_entries(int M, int N, int K);
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
                             int* counters, float* part, hipStream_t s, const QkvRope* rope = nullptr);
-// The LDS-tiled kernel alone (K % 64 == 0).
+// The LDS-tiled kernel alone (K % 64 == 0).  x_kblocked: x is stored
+// k-blocked, [K/32][M][32] (element (m, k) at ((k / 32) * M + m) * 32 + k % 32),
+// so that each 16-row x 32-column operand unit is 1 KB of contiguous memory;
+// y_kblocked: the SwiGLU output [M][F] is written that way too (as the next
+// tiled GEMM's input).
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s,
-                            float* stats = nullptr);
+                            float* stats = nullptr, bool x_kblocked = false, bool y_kblocked = false);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
                              const void* embed, const void* gain, float* h, void* x, int d, int V,
-                             float eps, int* err, hipStream_t s);
+                             float eps, int* err, hipStream_t s, bool x_kblocked = false);
 
 // bf16, norm folded into the GEMMs: h[r] = E[id(r)], x[r] = bf16(h[r] * gain),
 // ssq[r][t] = sum of h[r]^2 over columns 128t .. 128t+127; and the step's RoPE
@@ -135,9 +140,9 @@ hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B
                                const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
                                const int32_t* ctx, float theta, float* rope_cs, hipStream_t s);
 
-// x[r] = rmsnorm(h[r]) * gain
+// x[r] = rmsnorm(h[r]) * gain; x row-major, or k-blocked (as launch_gemm_tile reads it)
 hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, int M, int d, float eps,
-                          hipStream_t s);
+                          hipStream_t s, bool x_kblocked = false);
 
 // RoPE on q and k rows of qkv at positions ctx[b] + i; q -> q_out [M][H][D];
 // k, v -> one 16-slot window block per (b, kv head).  D <= 2 * kMaxHalfDim.
@@ -166,8 +171,9 @@ struct AttnArgs {
   float* part_ml;
   int* counters;         // [B*Hkv] split arrivals, zero on entry (bf16 path)
   int nsplit;  // KV splits per (sequence, KV head); a split's blocks come from the actual context length
-  void* out;            // [M][H*D]
+  void* out;            // [M][H*D]; k-blocked [H*D/32][M][32] when out_kblocked (bf16 path)
   int* err;
+  bool out_kblocked;
 };
 // Number of KV splits the bf16 path uses, and the partial buffer floats it needs.
 int attention_plan(int B, int Hkv, int max_blocks);

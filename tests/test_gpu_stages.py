@@ -154,6 +154,53 @@ def test_gemm_every_kernel_shape(kernel, split, M, N, K, epi):
         assert np.abs(got - ref).max() <= _gemm_tol(ref, epi), (rep, np.abs(got - ref).max())
 
 
+def _kblock(a, M, K):
+    """[M][K] -> the k-blocked layout [K/32][M][32] (flattened)."""
+    return np.ascontiguousarray(a.reshape(M, K // 32, 32).transpose(1, 0, 2)).reshape(-1)
+
+
+@pytest.mark.parametrize("kernel,split,M,N,K,epi", [
+    (nb.NJ_GEMM_TILE_256x256, 0, 300, 1040, 512, nb.NJ_GEMM_STORE),       # ragged M and N
+    (nb.NJ_GEMM_TILE_192x256, 0, 384, 4096, 1024, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_TILE_128x256, 2, 130, 2 * 704, 1024, nb.NJ_GEMM_SWIGLU),   # split, ragged M
+    (nb.NJ_GEMM_TILE_128x128, 3, 257, 1024, 2048, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_256x256, 0, 512, 2 * 512, 1024, nb.NJ_GEMM_SWIGLU),
+])
+def test_gemm_kblocked_operands_match_row_major(kernel, split, M, N, K, epi):
+    """The k-blocked x (and SwiGLU y) layout of the verify step's tiled GEMMs:
+    the same products as with row-major operands, bit for bit (only the
+    addressing differs), and a stream-kernel plan refuses the flag."""
+    x, w, y0 = _gemm_case(M, N, K, epi, seed=M + N + K + 7 * kernel)
+    Nout = N // 2 if epi == nb.NJ_GEMM_SWIGLU else N
+    dw = _devw(w)
+    nbytes = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, M, N, K, epi, kernel, split)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(ws.data_ptr(), nbytes, _stream())
+    outs = []
+    for kb in (False, True):
+        dx = _dev(_kblock(x, M, K).reshape(M, K) if kb else x)
+        if epi == nb.NJ_GEMM_SWIGLU:
+            y = torch.empty((M, Nout), dtype=torch.int16, device="cuda")
+        elif epi == nb.NJ_GEMM_RESIDUAL:
+            y = _dev(y0.copy())
+        else:
+            y = torch.full((M, Nout), float("nan"), dtype=torch.float32, device="cuda")
+        flag = nb.NJ_GEMM_KBLOCKED if kb else 0
+        nb.gemm_with_plan(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, epi | flag, kernel, split,
+                          ws.data_ptr(), nbytes, _stream())
+        torch.cuda.synchronize()
+        got = y.cpu().numpy()
+        if kb and epi == nb.NJ_GEMM_SWIGLU:  # back to row-major
+            got = got.reshape(-1).reshape(Nout // 32, M, 32).transpose(1, 0, 2).reshape(M, Nout)
+        outs.append(got)
+    assert np.array_equal(outs[0].view(np.uint8), outs[1].view(np.uint8))
+    ref = _gemm_ref(x, w, epi, y0)
+    assert np.abs(_gemm_out(torch.from_numpy(outs[1]), epi) - ref).max() <= _gemm_tol(ref, epi)
+    with pytest.raises(RuntimeError):  # the streaming kernel reads row-major x only
+        nb.gemm_with_plan(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), 48, N, K,
+                          epi | nb.NJ_GEMM_KBLOCKED, nb.NJ_GEMM_STREAM, 0, ws.data_ptr(), nbytes, _stream())
+
+
 def test_gemm_lm_head_large_window_sampled():
     """The LM-head shape at the largest window of the large-batch grid (768 rows
     x 128256 x 4096, auto plan), checked on sampled rows and a column band."""
