@@ -287,6 +287,81 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
   if (i < n) p[i] = v;
 }
 
+// RoPE and the window K/V store for bf16 heads of 128 dims: one workgroup
+// per (sequence, head) covers the window's T rows, so the window blocks are
+// written whole (slots T..15 zero) with 8- and 16-byte stores.  Thread t:
+// row t / 16, rotation pairs (j, j + 64) for j = 4 (t % 16) .. +3.  V goes
+// through LDS to come out dim-major ([128][16], 32 bytes per dim).  Angles as
+// in rope_window_kernel.
+__global__ __launch_bounds__(256) void rope_window_d128_kernel(const float* __restrict__ qkv,
+                                                               const int32_t* __restrict__ ctx, int T_, int H,
+                                                               int Hkv, RopeFreq f, bf16_t* __restrict__ q_out,
+                                                               bf16_t* __restrict__ win_k, bf16_t* __restrict__ win_v,
+                                                               int32_t* __restrict__ ctx_snap,
+                                                               int* __restrict__ attn_cnt) {
+  __shared__ float sv[kBlock][132];
+  const int b = blockIdx.x, hd = blockIdx.y, t = threadIdx.x;
+  const int i = t >> 4, j0 = 4 * (t & 15);
+  const int nh = H + 2 * Hkv;
+  if (hd == 0) {
+    // the positions this step uses, for the KV append that follows it; and
+    // the split counters of the attention launch that follows start at zero
+    if (ctx_snap && t == 0) ctx_snap[b] = ctx[b];
+    if (attn_cnt && t < Hkv) attn_cnt[(b * Hkv + t) * kCounterStride] = 0;
+  }
+  const float* src = qkv + ((size_t)(b * T_ + min(i, T_ - 1)) * nh + hd) * 128;
+  if (hd < H + Hkv) {
+    float ro[4], rh[4];
+    if (i < T_) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(src + j0), c = *reinterpret_cast<const f32x4*>(src + 64 + j0);
+      const double pos = (double)(max(ctx[b], 0) + i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double ang = pos * f.inv_freq[j0 + e];
+        const double kq = rint(ang * 0.15915494309189535);
+        const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
+        float sn, cs;
+        sincosf((float)red, &sn, &cs);
+        ro[e] = a[e] * cs - c[e] * sn;
+        rh[e] = c[e] * cs + a[e] * sn;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ro[e] = rh[e] = 0.f;
+    }
+    bf16_t* dst;
+    if (hd < H) {
+      if (i >= T_) return;
+      dst = q_out + ((size_t)(b * T_ + i) * H + hd) * 128;
+    } else {
+      dst = win_k + (((size_t)b * Hkv + (hd - H)) * kBlock + i) * 128;  // rows T..15 zero
+    }
+    u32x2 lo, hi;
+    lo[0] = pack_bf16x2(ro[0], ro[1]);
+    lo[1] = pack_bf16x2(ro[2], ro[3]);
+    hi[0] = pack_bf16x2(rh[0], rh[1]);
+    hi[1] = pack_bf16x2(rh[2], rh[3]);
+    *reinterpret_cast<u32x2*>(dst + j0) = lo;
+    *reinterpret_cast<u32x2*>(dst + 64 + j0) = hi;
+  } else {
+    const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+    const f32x4 a = i < T_ ? *reinterpret_cast<const f32x4*>(src + j0) : z;
+    const f32x4 c = i < T_ ? *reinterpret_cast<const f32x4*>(src + 64 + j0) : z;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sv[i][j0 + e] = a[e];
+      sv[i][64 + j0 + e] = c[e];
+    }
+    __syncthreads();
+    const int d = t >> 1, h8 = (t & 1) * 8;  // dim d, slots h8 .. h8+7
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(sv[h8 + 2 * e][d], sv[h8 + 2 * e + 1][d]);
+    bf16_t* vb = win_v + ((size_t)b * Hkv + (hd - H - Hkv)) * 128 * kBlock;
+    *reinterpret_cast<u32x4*>(vb + d * kBlock + h8) = o;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
@@ -333,6 +408,12 @@ hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, i
   RopeFreq f{};
   const int half = D / 2;
   for (int j = 0; j < half && j < kMaxHalfDim; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / D);
+  if (dtype != kF32 && D == 128 && T <= kBlock) {
+    hipLaunchKernelGGL(rope_window_d128_kernel, dim3(B, H + 2 * Hkv), dim3(256), 0, s, qkv, ctx, T, H, Hkv, f,
+                       static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(win_k), static_cast<bf16_t*>(win_v), ctx_snap,
+                       attn_counters);
+    return hipGetLastError();
+  }
   const int hpb = half >= 256 ? 1 : 256 / half;
   dim3 grid(B * T, (H + 2 * Hkv + hpb - 1) / hpb), block(hpb * half);
   if (dtype == kF32)
