@@ -35,6 +35,8 @@ namespace {
 
 
 __device__ __forceinline__ float silu_mul(float gte, float up) { return gte / (1.0f + expf(-gte)) * up; }
+// exp(x) = 2^(x log2 e): the statistics sum one hardware exp2 per logit
+constexpr float kLog2e = 1.4426950408889634f;
 
 struct TileK {
   const bf16_t* X;
@@ -268,7 +270,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     if (a.stats) {
       // Softmax statistics of each row over the tile's BN columns: a wave's
       // row (i, r) spans its TN fragments in the 4 lanes r + 16 g (max, then
-      // the sum of exp in lane order and a 2-step butterfly -- a + b == b + a,
+      // the sum of exp (as 2^((v - max) log2 e)) in lane order and a 2-step butterfly -- a + b == b + a,
       // so the 4 lanes agree), then the WN waves of a row block merge in wave
       // order through LDS (the stage buffers are free).
       float* sst = reinterpret_cast<float*>(lds);  // [WM][WN][BM / WM][2]
@@ -288,7 +290,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (out_n(j) + e < Nout) sum += expf(acc[i][j][e] - mx);
+            if (out_n(j) + e < Nout) sum += __builtin_amdgcn_exp2f((acc[i][j][e] - mx) * kLog2e);
         sum += __shfl_xor(sum, 16);
         sum += __shfl_xor(sum, 32);
         if (g == 0) {
