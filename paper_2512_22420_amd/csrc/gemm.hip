@@ -791,10 +791,13 @@ namespace {
 constexpr double kLaunch = 5e-6;
 double tile_cost(const GemmPlan& p, int M, int N, int K) {
   const int bm = tile_bm(p.tile), bn = tile_bn(p.tile);
-  const double slots = p.tile == kTile128x128 ? 512.0 : 256.0;  // resident workgroups
-  const double eff = p.tile == kTile256x256 ? 0.47 : p.tile == kTile192x256 ? 0.45 : p.tile == kTile128x256 ? 0.37 : 0.28;
-  const double rounds = std::ceil((double)p.ntiles * p.mblocks * p.nkc / slots);
-  double t = rounds * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (2.5e15 / slots * eff);
+  // sustained fraction of a CU's MFMA peak with k-blocked x; 128x128 tiles
+  // reach about the same with one or two workgroups on a CU
+  const double eff = p.tile == kTile256x256 ? 0.49 : p.tile == kTile192x256 ? 0.44 : p.tile == kTile128x256 ? 0.37 : 0.31;
+  const double wgs = (double)p.ntiles * p.mblocks * p.nkc;
+  const double per_cu = p.tile == kTile128x128 && wgs > 256.0 ? 2.0 : 1.0;  // resident workgroups per CU
+  const double rounds = std::ceil(wgs / (256.0 * per_cu));
+  double t = rounds * per_cu * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (2.5e15 / 256.0 * eff);
   if (p.nkc > 1) t += 2.0 * p.nkc * bm * bn * 4 / 1e11 + 2.0 * p.nkc * (double)M * N * 4 / 5e12;
   return t + kLaunch;
 }
@@ -829,7 +832,8 @@ bool tile_fits(int M, int N, int K) {
 GemmPlan gemm_plan(int M, int N, int K, int epi) {
   if (M >= kTileMinRows && tile_fits(M, N, K)) {
     const GemmPlan t = gemm_tile_choose(M, N, K, epi, kTileNone);
-    if (tile_cost(t, M, N, K) < stream_cost(M, N, K)) return t;
+    // the tiled kernel only when clearly ahead: the two models err by ~15%
+    if (tile_cost(t, M, N, K) < 0.85 * stream_cost(M, N, K)) return t;
   }
   return gemm_stream_plan(M, N, K, epi, 0);
 }
