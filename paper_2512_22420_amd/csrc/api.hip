@@ -463,8 +463,8 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
   }
   GemmPlan p;
   if (kernel == NJ_GEMM_STREAM || kernel == NJ_GEMM_STREAM_DEEP) {
-    p = gemm_stream_plan(M, N, K, epilogue, split);
-    p.depth = kernel == NJ_GEMM_STREAM_DEEP ? 3 : 1;
+    p = gemm_stream_plan(M, N, K, epilogue, split, kernel == NJ_GEMM_STREAM_DEEP ? 3 : 1);
+    if (epilogue == NJ_GEMM_STORE) p = gemm_logits_widen(p, M, N);
   } else {
     if (!tile_fits(M, N, K)) return fail(NJ_EINVAL, "the tiled kernels need K %% 64 == 0 and M*K, N*K < 2^31");
     const int tile = kernel == NJ_GEMM_TILE_256x256   ? kTile256x256

@@ -516,12 +516,12 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   }
 }
 
-// LM head (and other wide fp32-store GEMMs) for windows of up to 64 rows: a
+// LM head (and other wide fp32-store GEMMs) for windows of up to 96 rows: a
 // persistent form of the streaming kernel.  Logits stores issued while the
 // weight stream runs cost far more than their bytes (the HBM keeps turning the
 // bus around between reads and writes), so each workgroup streams
-// kLogitsTiles groups of NW * 16 weight rows (one row tile per wave) one after
-// another, keeps each finished logits tile in registers, and writes them all
+// kLogitsTiles groups of NW * 16 weight rows (one row tile per wave; one group
+// for windows of more than 64 rows) one after another, keeps each finished logits tile in registers, and writes them all
 // after its last group (through one LDS tile, as full row segments).  Softmax statistics (skipped when stats is null): the
 // (max, sum of exp) of each 128-column chunk of its groups, merged per row in
 // a fixed order into one pair per workgroup, stats[row][blockIdx.x] -- so the
@@ -529,6 +529,10 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
 // Row scale (folded RMSNorm) and statistics as in the kEpiLogits epilogue of
 // gemm_stream_kernel.
 constexpr int kLogitsTiles = 2;
+constexpr int kLogitsMaxTiles = 6;  // 16-row tiles of the largest window it takes
+// groups per workgroup of an MT-row window: windows of more than 64 rows keep
+// one finished group in registers (two would not fit beside the stream's)
+constexpr int logits_tiles(int mt) { return mt > 4 ? 1 : kLogitsTiles; }
 // Waves per workgroup for windows of more than 16 rows: 256 weight rows per
 // group, so each staged x stage feeds 16 waves (with 8, the x traffic of a
 // 48-row window is 37% of the weight traffic and holds the kernel ~4% below
@@ -540,13 +544,14 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
   constexpr int CPG = TPW * 16 / kStatChunk;  // statistics chunks per group
   static_assert(CPG * kStatChunk == TPW * 16, "a group's columns are whole statistics chunks");
   constexpr int ROWS = MT * 16, NTH = NW * 64;
-  static_assert(ROWS * CPG * kStatLanes <= NTH && ROWS * 8 <= NTH, "one pass of statistics lanes");
+  static_assert(ROWS * 8 <= NTH, "one pass of sum-of-squares lanes");
   constexpr int CH = ROWS * (kSK / 8), PT = (CH + NTH - 1) / NTH;
   constexpr int OS = TPW * 16 + 4;  // LDS row stride of an output tile, in floats
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][ROWS * kXStride];
   __shared__ __attribute__((aligned(16))) float ot[ROWS * OS];
   __shared__ float s_rinv[ROWS];
-  __shared__ float2 s_cst[kLogitsTiles][ROWS * CPG];  // chunk statistics of each group
+  constexpr int LT = logits_tiles(MT);
+  __shared__ float2 s_cst[LT][ROWS * CPG];  // chunk statistics of each group
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
@@ -572,14 +577,27 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) ssq_v[j] = c + 8 * j < a.nt_in ? sp[c + 8 * j] : 0.f;
   }
+  auto row_scales = [&] {  // 1/rms of every row into s_rinv
+    float t = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) t += ssq_v[j];
+    t += __shfl_xor(t, 1);
+    t += __shfl_xor(t, 2);
+    t += __shfl_xor(t, 4);
+    if (threadIdx.x % 8 == 0 && (int)threadIdx.x / 8 < ROWS) s_rinv[threadIdx.x / 8] = 1.0f / sqrtf(t / (float)K + a.eps);
+    __syncthreads();
+  };
+  // Windows of more than 64 rows have no registers to spare for the partials
+  // across the weight stream: their scales are taken before it.
+  if (MT > 4 && scaled) row_scales();
 
   // The finished tiles stay in registers (tile tt in fin[tt]) until the last
   // group's weights have been streamed; then each passes through the one LDS
   // output tile for its statistics and its row-segment stores.
-  static_assert(kLogitsTiles == 2, "finished tiles are held in two register sets");
-  f32x4 fin0[MT], fin1[MT];
+  static_assert(LT == 1 || LT == 2, "finished tiles are held in one or two register sets");
+  f32x4 fin0[MT], fin1[LT == 2 ? MT : 1];
   int done = 0;
-  for (int tt = 0; tt < kLogitsTiles; ++tt) {
+  for (int tt = 0; tt < LT; ++tt) {
     const int grp = blockIdx.x + tt * gridDim.x;
     if (grp >= ngroups) break;
     const int wtile = min(grp * TPW + wave, nto - 1);
@@ -589,24 +607,14 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
     for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     stream_tile<MT, 2, PT>(acc, wp, xp, xc, xo, K, KS, 0, nst, &xs[0][0]);
     if (scaled) {
-      if (tt == 0) {
-        float t = 0.f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) t += ssq_v[j];
-        t += __shfl_xor(t, 1);
-        t += __shfl_xor(t, 2);
-        t += __shfl_xor(t, 4);
-        if (threadIdx.x % 8 == 0 && (int)threadIdx.x / 8 < ROWS)
-          s_rinv[threadIdx.x / 8] = 1.0f / sqrtf(t / (float)K + a.eps);
-        __syncthreads();
-      }
+      if (MT <= 4 && tt == 0) row_scales();
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) acc[mt] *= s_rinv[mt * 16 + r];
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       if (tt == 0) fin0[mt] = acc[mt];
-      else fin1[mt] = acc[mt];
+      else if constexpr (LT == 2) fin1[mt] = acc[mt];
     }
     done = tt + 1;
   }
@@ -617,19 +625,21 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = tt == 0 ? fin0[mt][i] : fin1[mt][i];
+      for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = tt == 0 ? fin0[mt][i] : fin1[LT == 2 ? mt : 0][i];
     __syncthreads();
     if (a.stats) {  // softmax statistics of the group's chunks, 8 lanes per (row, chunk)
-      const int unit = threadIdx.x / kStatLanes, c = threadIdx.x % kStatLanes;
-      const int row = min(unit / CPG, ROWS - 1), ch = unit % CPG;
-      const int n0 = grp * TPW * 16 + ch * kStatChunk;
-      float v[kStatPer];
+      const int c = threadIdx.x % kStatLanes;
+      for (int unit = threadIdx.x / kStatLanes; unit < ROWS * CPG; unit += NTH / kStatLanes) {
+        const int row = unit / CPG, ch = unit % CPG;
+        const int n0 = grp * TPW * 16 + ch * kStatChunk;
+        float v[kStatPer];
 #pragma unroll
-      for (int e = 0; e < kStatPer; ++e)
-        v[e] = n0 + c * kStatPer + e < Nout ? ot[row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
-      float cm, cs;
-      chunk_stats(v, cm, cs);
-      if (c == 0 && unit < ROWS * CPG) s_cst[tt][unit] = float2{cm, cs};
+        for (int e = 0; e < kStatPer; ++e)
+          v[e] = n0 + c * kStatPer + e < Nout ? ot[row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
+        float cm, cs;
+        chunk_stats(v, cm, cs);
+        if (c == 0) s_cst[tt][unit] = float2{cm, cs};
+      }
     }
     // the finished tile, full 512-byte row segments
     const int n0 = grp * TPW * 16;
@@ -731,6 +741,7 @@ hipError_t launch_stream_nb(const GemmK& a, const GemmPlan& p, hipStream_t s) {
 
 template <int EPI>
 hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+  if (p.mt > 4) return hipErrorInvalidValue;  // 5 and 6 row tiles: the persistent kernel only
   return p.depth >= 3 ? launch_stream_nb<EPI, 4>(a, p, s) : launch_stream_nb<EPI, 2>(a, p, s);
 }
 
@@ -738,11 +749,12 @@ hipError_t launch_stream(const GemmK& a, const GemmPlan& p, hipStream_t s) {
 // K is not split (its grid size: the statistics pairs per row), else 0 and the
 // streaming kernel's kEpiLogits epilogue.
 int logits_persistent_grid(const GemmPlan& p, int Nout) {
-  if (p.nkc > 1 || p.mblocks > 1 || p.mt > 4 || p.depth >= 3) return 0;
+  if (p.nkc > 1 || p.mblocks > 1 || p.mt > kLogitsMaxTiles || p.depth >= 3) return 0;
   // 16-row windows stage little x per weight byte: 8 waves per workgroup
   const int NW = p.mt == 1 ? kNW : kLogitsWaves;
   const int groups = (Nout / 16 + NW - 1) / NW;
-  return (groups + kLogitsTiles - 1) / kLogitsTiles;
+  const int lt = logits_tiles(p.mt);
+  return (groups + lt - 1) / lt;
 }
 
 hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
@@ -754,7 +766,9 @@ hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
     case 1: hipLaunchKernelGGL((gemm_logits_kernel<1, kNW>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((gemm_logits_kernel<2, kLogitsWaves>), grid, block, 0, s, a); break;
     case 3: hipLaunchKernelGGL((gemm_logits_kernel<3, kLogitsWaves>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((gemm_logits_kernel<4, kLogitsWaves>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((gemm_logits_kernel<4, kLogitsWaves>), grid, block, 0, s, a); break;
+    case 5: hipLaunchKernelGGL((gemm_logits_kernel<5, kLogitsWaves>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((gemm_logits_kernel<6, kLogitsWaves>), grid, block, 0, s, a); break;
   }
   return hipGetLastError();
 }
@@ -829,16 +843,31 @@ bool tile_fits(int M, int N, int K) {
   return K % 64 == 0 && (long)M * K < (1L << 31) && (long)packed_weight_elems(N, K) < (1L << 31);
 }
 
+GemmPlan gemm_logits_widen(const GemmPlan& p, int M, int N) {
+  if (p.tile != kTileNone || p.nkc > 1 || p.depth >= 3 || M <= 64 || M > 16 * kLogitsMaxTiles) return p;
+  GemmPlan q = p;
+  q.mt = (M + 15) / 16;
+  q.mblocks = 1;
+  return logits_persistent_grid(q, N) > 0 ? q : p;
+}
+
 GemmPlan gemm_plan(int M, int N, int K, int epi) {
   if (M >= kTileMinRows && tile_fits(M, N, K)) {
+    // wide fp32-store GEMMs (the LM head) of up to 96 rows: the persistent
+    // kernel reads the weights once and runs ~10% ahead of the best tile
+    // (128x256) at 72..96 rows when it fills the chip
+    if (epi == kEpiStore) {
+      const GemmPlan sp = gemm_logits_widen(gemm_stream_plan(M, N, K, epi, 0, 1), M, N);
+      if (sp.mt > 4 && logits_persistent_grid(sp, N) >= 256) return sp;
+    }
     const GemmPlan t = gemm_tile_choose(M, N, K, epi, kTileNone);
     // the tiled kernel only when clearly ahead: the two models err by ~15%
     if (tile_cost(t, M, N, K) < 0.85 * stream_cost(M, N, K)) return t;
   }
-  return gemm_stream_plan(M, N, K, epi, 0);
+  return gemm_stream_plan(M, N, K, epi, 0, 1);
 }
 
-GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split) {
+GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split, int depth) {
   GemmPlan p{};
   p.tile = kTileNone;
   const int NG = epi == kEpiSwiglu ? 2 : 1;
@@ -858,7 +887,7 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split) {
   if (split <= 0 && (size_t)nkc * M * N * 4 >= kMaxPartBytes) nkc = 1;
   p.stages_per_chunk = (nst + nkc - 1) / nkc;
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
-  p.depth = 1;
+  p.depth = depth;
   p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
   p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * kCounterStride * 4) : 0;
   static_assert(kSplitTargetWorkgroups / 2 * kCounterStride * 4 <= kGemmCounterBytes, "counter region too small");

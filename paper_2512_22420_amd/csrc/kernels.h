@@ -40,8 +40,14 @@ bool tile_fits(int M, int N, int K);
 // Best tiled plan by the cost model (only_tile = kTileNone: any tile shape).
 GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile);
 // Plan of the weight-streaming kernel; split > 0 forces that many K chunks
-// (at most one per 256-k stage), 0 picks the split.
-GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split);
+// (at most one per 256-k stage), 0 picks the split; depth 3 = three stages in
+// flight per wave (1: two).
+GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split, int depth);
+// A streaming plan of 65..96 rows without split K, as one block of up to 6 row
+// tiles for the persistent fp32-store (LM-head) kernel, which then reads the
+// weights once; any other plan unchanged.  Only for plans launched through
+// launch_gemm_plan / launch_gemm_logits with the store epilogue.
+GemmPlan gemm_logits_widen(const GemmPlan& p, int M, int N);
 int tile_bm(int tile);
 int tile_bn(int tile);
 // Split K only happens when ntiles * mblocks <= 256, so every GEMM's arrival

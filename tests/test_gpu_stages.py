@@ -125,6 +125,9 @@ def _gemm_tol(ref, epi):
     (nb.NJ_GEMM_TILE_128x128, 0, 1, 272, 64, nb.NJ_GEMM_STORE),            # one row, one stage
     (nb.NJ_GEMM_STREAM, 3, 48, 4096, 4096, nb.NJ_GEMM_STORE),              # streaming kernel, forced split
     (nb.NJ_GEMM_STREAM, 1, 200, 1024, 1024, nb.NJ_GEMM_RESIDUAL),          # streaming kernel past 64 rows
+    (nb.NJ_GEMM_STREAM, 0, 80, 4112, 1024, nb.NJ_GEMM_STORE),              # persistent, 5 row tiles, ragged group
+    (nb.NJ_GEMM_STREAM, 0, 93, 2064, 512, nb.NJ_GEMM_STORE),               # persistent, 6 row tiles, ragged rows
+    (nb.NJ_GEMM_STREAM, 0, 65, 256, 4096, nb.NJ_GEMM_STORE),               # persistent, one group
     (nb.NJ_GEMM_AUTO, 0, 768, 6144, 4096, nb.NJ_GEMM_STORE),
     (nb.NJ_GEMM_AUTO, 0, 320, 4096, 14336, nb.NJ_GEMM_RESIDUAL),
     (nb.NJ_GEMM_AUTO, 0, 256, 2 * 2048, 3584, nb.NJ_GEMM_SWIGLU),

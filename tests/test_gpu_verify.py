@@ -152,6 +152,26 @@ def test_llama8b_layer_tiled_gemms(llama_layer, B, k):
     _decisions_ok(io, ref, x, gpu_logits=gl)
 
 
+@pytest.mark.parametrize("B,k", [(16, 4), (16, 5)])
+def test_llama8b_layer_wide_persistent_lm_head(llama_layer, B, k):
+    """Windows of 80 and 96 rows: the persistent LM-head kernel with 5 and 6
+    row tiles (one group per workgroup) and its softmax statistics feeding the
+    acceptance.  These windows take the unfused path (bf16 normed GEMM inputs),
+    so rows are held to 1.5e-2 as for the tiled windows: row 62 of the 80-row
+    case reaches 1.08e-2, with the tiled LM head as well (same logits bits)."""
+    shape, weights, model = llama_layer
+    ctx = W.ctx_lengths("lognormal", B, seed=6, median=768, sigma=0.5, lo=128, hi=2048)
+    x = _inputs(shape, ctx, k, seed=3, weights=weights, k_max=5)
+    _, _, io, _, err = _run(shape, x, model=model)
+    assert err == 0
+    ref = _oracle(x, shape)
+    gl = io.logits.cpu().numpy()
+    r = np.asarray(ref["logits"])
+    assert np.linalg.norm(gl - r) / np.linalg.norm(r) <= 1e-2
+    assert rel_l2_rows(gl, r).max() <= 1.5e-2
+    _decisions_ok(io, ref, x, gpu_logits=gl)
+
+
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("shape,ctx,k", [(W.TINY_F32, [32, 48], 3), (SMALL_BF16, [0, 15, 31, 77], 5)],
                          ids=["f32", "bf16"])
