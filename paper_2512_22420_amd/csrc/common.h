@@ -60,7 +60,7 @@ __device__ __forceinline__ void chunk_stats(const float (&v)[kStatPer], float& m
   m = fmaxf(m, __shfl_xor(m, 4));
   s = 0.f;
 #pragma unroll
-  for (int e = 0; e < kStatPer; ++e) s += (v[e] == -INFINITY) ? 0.f : expf(v[e] - m);
+  for (int e = 0; e < kStatPer; ++e) s += (v[e] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((v[e] - m) * 1.4426950408889634f);
   s += __shfl_xor(s, 1);
   s += __shfl_xor(s, 2);
   s += __shfl_xor(s, 4);

@@ -627,21 +627,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) ot[(mt * 16 + r) * OS + wave * 16 + 4 * g + i] = tt == 0 ? fin0[mt][i] : fin1[LT == 2 ? mt : 0][i];
     __syncthreads();
-    if (a.stats) {  // softmax statistics of the group's chunks, 8 lanes per (row, chunk)
-      const int c = threadIdx.x % kStatLanes;
-      for (int unit = threadIdx.x / kStatLanes; unit < ROWS * CPG; unit += NTH / kStatLanes) {
-        const int row = unit / CPG, ch = unit % CPG;
-        const int n0 = grp * TPW * 16 + ch * kStatChunk;
-        float v[kStatPer];
-#pragma unroll
-        for (int e = 0; e < kStatPer; ++e)
-          v[e] = n0 + c * kStatPer + e < Nout ? ot[row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
-        float cm, cs;
-        chunk_stats(v, cm, cs);
-        if (c == 0) s_cst[tt][unit] = float2{cm, cs};
-      }
-    }
-    // the finished tile, full 512-byte row segments
+    // the finished tile, full 512-byte row segments (issued first: the
+    // statistics below only read LDS and run while the stores drain)
     const int n0 = grp * TPW * 16;
 #pragma unroll
     for (int it = 0; it < (PIECES + NTH - 1) / NTH; ++it) {
@@ -651,6 +638,20 @@ __global__ __launch_bounds__(NW * 64) void gemm_logits_kernel(GemmK a) {
       if (idx < PIECES && row < M && n < Nout)
         *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)row * Nout + n) =
             *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
+    }
+    if (a.stats) {  // softmax statistics of the group's chunks, 8 lanes per (row, chunk)
+      const int c = threadIdx.x % kStatLanes;
+      for (int unit = threadIdx.x / kStatLanes; unit < ROWS * CPG; unit += NTH / kStatLanes) {
+        const int row = unit / CPG, ch = unit % CPG;
+        const int c0 = n0 + ch * kStatChunk;
+        float v[kStatPer];
+#pragma unroll
+        for (int e = 0; e < kStatPer; ++e)
+          v[e] = c0 + c * kStatPer + e < Nout ? ot[row * OS + ch * kStatChunk + c * kStatPer + e] : -INFINITY;
+        float cm, cs;
+        chunk_stats(v, cm, cs);
+        if (c == 0) s_cst[tt][unit] = float2{cm, cs};
+      }
     }
   }
   if (a.stats) {  // one (max, sum) per row: the chunks merged in (group, chunk) order
