@@ -395,11 +395,18 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
+        cores = len(os.sched_getaffinity(0))
+        blas = "unknown BLAS"
+        threads = cores
         try:
             from threadpoolctl import threadpool_info
-            threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-        except Exception:  # pragma: no cover
-            threads = len(os.sched_getaffinity(0))
+            libs = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+            if libs:
+                threads = max(p.get("num_threads", 1) for p in libs)
+                blas = ", ".join(sorted({f"{p.get('internal_api', '?')} {p.get('version') or ''}".strip()
+                                         for p in libs}))
+        except ImportError:  # pragma: no cover
+            pass
         # the headline configuration, repeated until at least 10 s of host work
         cB, ck = B, k
         c = W.make_context(shape, wl.ctx(cB, seed=0), k_max, seed=0)
@@ -411,10 +418,10 @@ def main():
                                d["last_tokens"], d["draft_tokens"], d["draft_probs"], d["uniforms"])
             tc += time.perf_counter() - t1
             n_steps += 1
-        cpu = {"value": round(n_steps * cB * (ck + 1) / tc, 3), "unit": "verified tokens/s", "cores": threads,
-               "kind": "oracle",
+        cpu = {"value": round(n_steps * cB * (ck + 1) / tc, 3), "unit": "verified tokens/s", "cores": cores,
+               "kind": "oracle", "blas": blas, "blas_threads": threads,
                "sample": f"{n_steps} fp64 oracle verify steps at B={cB} k={ck} ctx 1024 (the headline workload), "
-                         f"{tc:.1f} s, NumPy/OpenBLAS on {threads} threads"}
+                         f"{tc:.1f} s; NumPy with {blas} on {threads} BLAS threads, {cores} cores in the affinity mask"}
         log(f"cpu oracle: {n_steps} steps in {tc:.1f} s at B={cB} k={ck} on {threads} threads")
 
     out = {

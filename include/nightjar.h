@@ -223,6 +223,61 @@ int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_
                     void* stream);
 
 /*
+ * nightjar_rmsnorm_rope -- the inputs of one layer's attention (a stage of the
+ * verify step, with the kernels the step uses for a window of B*(k+1) rows):
+ * x = RMSNorm(h) * attn_norm (x / sqrt(mean(x^2) + eps), the Llama-style
+ * decoder's pre-attention norm), [q | k | v] = x . w_qkv^T, then rotate-half
+ * RoPE on q and k at position context_lens[b] + i for window row i of
+ * sequence b (pair (j, j + D/2) turns by pos * rope_theta^(-2j/D)).  Window K
+ * and V go to one 16-slot block per (sequence, KV head), in the layout of a
+ * page block, ready for nightjar_attn_verify (Sec. 2.2: all drafts are scored
+ * in one forward; Sec. 2.1: paged K/V blocks).
+ *
+ *   h             device fp32 [B*(k+1)][d]   residual rows (row b*(k+1)+i)
+ *   attn_norm     device [d] (desc dtype)
+ *   w_qkv         device [(H+2Hkv)*D][d]: bf16 packed (nightjar_pack_weight), fp32 row-major
+ *   context_lens  device int32 [B]
+ *   q_out         device [B*(k+1)][H][D] (desc dtype), rotated queries
+ *   win_k         device [B][Hkv][16][D]: rotated keys in slots 0..k, slots k+1..15 zero
+ *   win_v         device [B][Hkv][D][16]: values in slots 0..k, slots k+1..15 zero
+ *   workspace     device, 256-byte aligned, >= nightjar_rmsnorm_rope_workspace_bytes(desc, B, k),
+ *                 zero-filled once by nightjar_workspace_init
+ * Every pointer 16-byte aligned.  Only the descriptor's d_model, heads,
+ * head_dim, rms_eps, rope_theta and dtype are used (plus ffn_dim and vocab,
+ * which decide, as in the step, whether the norm is folded into the GEMM).
+ */
+size_t nightjar_rmsnorm_rope_workspace_bytes(const nj_model_desc* desc, int32_t B, int32_t k);
+int nightjar_rmsnorm_rope(const nj_model_desc* desc, const float* h, const void* attn_norm, const void* w_qkv,
+                          const int32_t* context_lens, int32_t B, int32_t k, void* q_out, void* win_k, void* win_v,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * nightjar_attn_verify -- paged verify attention of one layer (Sec. 2.1:
+ * PagedAttention, cached K/V in 16-token blocks reached through a block table;
+ * Sec. 2.2: the k+1 window tokens of each sequence are scored together).
+ * Window query i of sequence b attends to the context_lens[b] cached tokens of
+ * b and to window tokens 0..i; query head h reads KV head h / (H / Hkv);
+ * scores q.k / sqrt(D), softmax, weighted sum of values.
+ *
+ *   q              device [B*(k+1)][H][D] (desc dtype)
+ *   k_pages        device [num_blocks][Hkv][16][D]    one layer's pages
+ *   v_pages        device [num_blocks][Hkv][D][16]
+ *   win_k, win_v   device, the window blocks as nightjar_rmsnorm_rope writes them
+ *   block_table    device int32 [B][max_blocks]; context_lens device int32 [B]
+ *   out            device [B*(k+1)][H*D] (desc dtype)
+ *   workspace      device, 256-byte aligned, >= nightjar_attn_workspace_bytes(desc, B, k),
+ *                  zero-filled once by nightjar_workspace_init; device errors
+ *                  (NJ_DEV_BAD_BLOCK, NJ_DEV_BAD_CONTEXT) are read from it with
+ *                  nightjar_device_error
+ * bf16: (k+1) * (H/Hkv) <= 64 and 16-byte aligned pointers; fp32: max_blocks <= 1024.
+ */
+size_t nightjar_attn_workspace_bytes(const nj_model_desc* desc, int32_t B, int32_t k);
+int nightjar_attn_verify(const nj_model_desc* desc, const void* q, const void* k_pages, const void* v_pages,
+                         int32_t num_blocks, const void* win_k, const void* win_v, const int32_t* block_table,
+                         int32_t max_blocks, const int32_t* context_lens, int32_t B, int32_t k, void* out,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Packed layout of a bf16 weight matrix w [N][K] (K % 32 == 0), the form in
  * which the bf16 GEMMs read their weights (a layout choice of this library,
  * not of the method: every load instruction of the GEMM kernels reads 1 KB of

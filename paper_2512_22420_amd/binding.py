@@ -70,6 +70,12 @@ _SIGS = {
                                                _vp]),
     "nightjar_gemm_plan_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32, _i32]),
     "nightjar_accept_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "nightjar_rmsnorm_rope_workspace_bytes": (_sz, [ctypes.POINTER(ModelDesc), _i32, _i32]),
+    "nightjar_rmsnorm_rope": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                             _vp, _vp, _sz, _vp]),
+    "nightjar_attn_workspace_bytes": (_sz, [ctypes.POINTER(ModelDesc), _i32, _i32]),
+    "nightjar_attn_verify": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _i32, _vp, _vp, _vp, _i32,
+                                            _vp, _i32, _i32, _vp, _vp, _sz, _vp]),
     "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
     "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
@@ -164,6 +170,33 @@ def gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace
                    stream: int = 0) -> None:
     _check(lib().nightjar_gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace,
                                          workspace_nbytes, stream))
+
+
+def rmsnorm_rope_workspace_bytes(desc, B, k) -> int:
+    n = lib().nightjar_rmsnorm_rope_workspace_bytes(ctypes.byref(desc), B, k)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def rmsnorm_rope(desc, h, attn_norm, w_qkv, context_lens, B, k, q_out, win_k, win_v, workspace, workspace_nbytes,
+                 stream: int = 0) -> None:
+    _check(lib().nightjar_rmsnorm_rope(ctypes.byref(desc), h, attn_norm, w_qkv, context_lens, B, k, q_out, win_k,
+                                       win_v, workspace, workspace_nbytes, stream))
+
+
+def attn_workspace_bytes(desc, B, k) -> int:
+    n = lib().nightjar_attn_workspace_bytes(ctypes.byref(desc), B, k)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def attn_verify(desc, q, k_pages, v_pages, num_blocks, win_k, win_v, block_table, max_blocks, context_lens, B, k,
+                out, workspace, workspace_nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_attn_verify(ctypes.byref(desc), q, k_pages, v_pages, num_blocks, win_k, win_v,
+                                      block_table, max_blocks, context_lens, B, k, out, workspace, workspace_nbytes,
+                                      stream))
 
 
 def packed_weight_elems(N, K) -> int:

@@ -81,6 +81,16 @@ bool desc_ok(const nj_model_desc* d) {
   return true;
 }
 
+// Whether a window of M rows runs with the RMSNorms folded into the GEMMs:
+// bf16 with every GEMM of the step on the weight-streaming kernel.
+bool fold_norms(const nj_model_desc& d, int M) {
+  if (d.dtype != NJ_BF16) return false;
+  const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
+  return gemm_streams(M, QKV, d.d_model, kEpiStore) && gemm_streams(M, d.d_model, HD, kEpiResidual) &&
+         gemm_streams(M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu) &&
+         gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual) && gemm_streams(M, d.vocab, d.d_model, kEpiStore);
+}
+
 Layout layout(const nj_model_desc& d, int B, int k) {
   const size_t e = d.dtype == NJ_BF16 ? 2 : 4;
   const size_t T = k + 1, M = (size_t)B * T;
@@ -126,6 +136,55 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   L.logits = take(M * d.vocab * 4);
   L.stats = take(accept_workspace_bytes((int)M, d.vocab));
   L.gemm_part = take(part);  // split-K partials (GEMMs run one after another)
+  L.total = off;
+  return L;
+}
+
+// Workspace of nightjar_rmsnorm_rope: [error word][split-K counters][x][ssq][rope table][qkv][split-K partials]
+struct PreLayout {
+  size_t err, gemm_cnt, x, ssq, rope_cs, qkv, gemm_part, total;
+};
+PreLayout pre_layout(const nj_model_desc& d, int B, int k) {
+  const size_t e = d.dtype == NJ_BF16 ? 2 : 4;
+  const size_t M = (size_t)B * (k + 1);
+  const int QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
+  PreLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += al(bytes);
+    return o;
+  };
+  L.err = take(kAlign);
+  L.gemm_cnt = take(kGemmCounterBytes);
+  L.x = take(M * d.d_model * e);
+  L.ssq = take(M * ((d.d_model + 127) / 128) * 4);
+  L.rope_cs = take(M * 64 * 2 * 4);
+  L.qkv = take(M * QKV * 4);
+  L.gemm_part = take(d.dtype == NJ_BF16 ? gemm_plan((int)M, QKV, d.d_model, kEpiStore).part_bytes : 0);
+  L.total = off;
+  return L;
+}
+
+// Workspace of nightjar_attn_verify: [error word][split arrival counters][partial o][partial (m, l)]
+struct AttnLayout {
+  size_t err, cnt, part_o, part_ml, total;
+};
+AttnLayout attn_layout(const nj_model_desc& d, int B, int k) {
+  AttnLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += al(bytes);
+    return o;
+  };
+  L.err = take(kAlign);
+  L.cnt = take((size_t)B * d.n_kv_heads * kCounterStride * 4);
+  const size_t pf = d.dtype == NJ_BF16
+                        ? attention_partial_floats(B, d.n_kv_heads, k + 1, d.n_heads / d.n_kv_heads, d.head_dim)
+                        : 0;
+  L.part_o = take(pf * 4);
+  L.part_ml = take((pf ? pf / (d.head_dim + 2) * 2 : 0) * 4);
   L.total = off;
   return L;
 }
@@ -234,9 +293,7 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   // folded into the GEMMs (the residual GEMMs and the embedding write h * gain
   // and per-tile sums of h^2; the next GEMM scales its rows by 1/rms)
   const int F2 = 2 * d.ffn_dim;
-  bool fused = bf && gemm_streams(M, QKV, d.d_model, kEpiStore) && gemm_streams(M, d.d_model, HD, kEpiResidual) &&
-               gemm_streams(M, F2, d.d_model, kEpiSwiglu) && gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual) &&
-               gemm_streams(M, d.vocab, d.d_model, kEpiStore) && aligned16(w->final_norm);
+  bool fused = fold_norms(d, M) && aligned16(w->final_norm);
   for (int l = 0; l < d.n_layers && fused; ++l)
     fused = aligned16(w->layers[l].attn_norm) && aligned16(w->layers[l].ffn_norm);
   // Without the folded norm, the input of each GEMM that runs on the
@@ -355,6 +412,100 @@ int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const i
                  reinterpret_cast<int*>(const_cast<char*>(ws) + L.err)};
   hipError_t e = launch_kv_append(a, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "kv_append");
+}
+
+size_t nightjar_rmsnorm_rope_workspace_bytes(const nj_model_desc* desc, int32_t B, int32_t k) {
+  if (!desc_ok(desc)) return 0;
+  if (B < 1 || k < 0 || k > kMaxK) {
+    fail(NJ_EINVAL, "bad B or k");
+    return 0;
+  }
+  return pre_layout(*desc, B, k).total;
+}
+
+int nightjar_rmsnorm_rope(const nj_model_desc* desc, const float* h, const void* attn_norm, const void* w_qkv,
+                          const int32_t* context_lens, int32_t B, int32_t k, void* q_out, void* win_k, void* win_v,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc)) return NJ_EINVAL;
+  const nj_model_desc& d = *desc;
+  if (B < 1 || k < 0 || k > kMaxK) return fail(NJ_EINVAL, "bad B or k");
+  if (!h || !attn_norm || !w_qkv || !context_lens || !q_out || !win_k || !win_v || !workspace)
+    return fail(NJ_EINVAL, "a required pointer is NULL");
+  const bool bf = d.dtype == NJ_BF16;
+  if (!(aligned16(h) && aligned16(attn_norm) && aligned16(w_qkv) && aligned16(q_out) && aligned16(win_k) &&
+        aligned16(win_v)))
+    return fail(NJ_EINVAL, "h, attn_norm, w_qkv, q_out, win_k and win_v must be 16-byte aligned");
+  const PreLayout L = pre_layout(d, B, k);
+  if (workspace_bytes < L.total) return fail(NJ_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, L.total);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+  const int T = k + 1, M = B * T, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
+  const int dt = bf ? kBF16 : kF32;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = static_cast<char*>(workspace);
+  int* gcnt = reinterpret_cast<int*>(ws + L.gemm_cnt);
+  float* gpart = reinterpret_cast<float*>(ws + L.gemm_part);
+  float* ssq = reinterpret_cast<float*>(ws + L.ssq);
+  float* cs = reinterpret_cast<float*>(ws + L.rope_cs);
+  hipError_t e;
+  if (fold_norms(d, M)) {  // the step's kernels for this window: norm folded into the QKV GEMM, RoPE in its epilogue
+    e = launch_norm_inputs(h, B, T, attn_norm, ws + L.x, ssq, d.d_model, context_lens, d.rope_theta, cs, s);
+    if (e != hipSuccess) return hip_fail(e, "rmsnorm_rope: norm inputs");
+    const GemmNorm scale_in{ssq, (d.d_model + 127) / 128, d.rms_eps, nullptr, nullptr, nullptr, nullptr};
+    const QkvRope rope{context_lens, T, d.n_heads, d.n_kv_heads, cs, q_out, win_k, win_v, nullptr, nullptr};
+    e = launch_gemm_norm(ws + L.x, w_qkv, ws + L.qkv, M, QKV, d.d_model, kEpiQkvRope, scale_in, gcnt, gpart, s, &rope);
+    return e == hipSuccess ? NJ_OK : hip_fail(e, "rmsnorm_rope: qkv gemm");
+  }
+  const bool kb = bf && !gemm_streams(M, QKV, d.d_model, kEpiStore);
+  e = launch_rmsnorm(dt, h, attn_norm, ws + L.x, M, d.d_model, d.rms_eps, s, kb);
+  if (e == hipSuccess)
+    e = launch_gemm(dt, ws + L.x, w_qkv, ws + L.qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb);
+  if (e == hipSuccess)
+    e = launch_rope_window(dt, reinterpret_cast<const float*>(ws + L.qkv), context_lens, B, T, d.n_heads,
+                           d.n_kv_heads, d.head_dim, d.rope_theta, q_out, win_k, win_v, nullptr, nullptr, s);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "rmsnorm_rope");
+}
+
+size_t nightjar_attn_workspace_bytes(const nj_model_desc* desc, int32_t B, int32_t k) {
+  if (!desc_ok(desc)) return 0;
+  if (B < 1 || k < 0 || k > kMaxK) {
+    fail(NJ_EINVAL, "bad B or k");
+    return 0;
+  }
+  return attn_layout(*desc, B, k).total;
+}
+
+int nightjar_attn_verify(const nj_model_desc* desc, const void* q, const void* k_pages, const void* v_pages,
+                         int32_t num_blocks, const void* win_k, const void* win_v, const int32_t* block_table,
+                         int32_t max_blocks, const int32_t* context_lens, int32_t B, int32_t k, void* out,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc)) return NJ_EINVAL;
+  const nj_model_desc& d = *desc;
+  if (B < 1 || k < 0 || k > kMaxK) return fail(NJ_EINVAL, "bad B or k");
+  if (max_blocks < 1 || num_blocks < 1) return fail(NJ_EINVAL, "max_blocks and num_blocks must be >= 1");
+  if (!q || !k_pages || !v_pages || !win_k || !win_v || !block_table || !context_lens || !out || !workspace)
+    return fail(NJ_EINVAL, "a required pointer is NULL");
+  const bool bf = d.dtype == NJ_BF16;
+  const int T = k + 1, G = d.n_heads / d.n_kv_heads;
+  if (bf && !(aligned16(q) && aligned16(k_pages) && aligned16(v_pages) && aligned16(win_k) && aligned16(win_v) &&
+              aligned16(out)))
+    return fail(NJ_EINVAL, "q, pages, window blocks and out must be 16-byte aligned");
+  if (bf && T * G > 64) return fail(NJ_EINVAL, "(k+1) * (H/Hkv) = %d exceeds 64 query rows per KV head", T * G);
+  if (!bf && (size_t)max_blocks * 16 * 4 > 65536) return fail(NJ_EINVAL, "fp32 path supports max_blocks <= 1024");
+  const AttnLayout L = attn_layout(d, B, k);
+  if (workspace_bytes < L.total) return fail(NJ_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, L.total);
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = static_cast<char*>(workspace);
+  int* cnt = reinterpret_cast<int*>(ws + L.cnt);
+  hipError_t e = hipSuccess;
+  if (bf) e = launch_fill_i32(cnt, 0, (int)(L.part_o - L.cnt) / 4, s);  // split arrivals start at zero
+  if (e != hipSuccess) return hip_fail(e, "attn_verify: clear counters");
+  AttnArgs aa{bf ? kBF16 : kF32, q, k_pages, v_pages, win_k, win_v, block_table, max_blocks, context_lens,
+              num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
+              reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml), cnt,
+              bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1, out, reinterpret_cast<int*>(ws + L.err), false};
+  e = launch_attention(aa, s);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "attn_verify");
 }
 
 size_t nightjar_accept_workspace_bytes(int32_t vocab, int32_t B, int32_t k) {

@@ -17,6 +17,7 @@
 // domain.  When the grid splits the KV range, each split writes its partial
 // (o, max, sum) and the last split to arrive merges them in split order.
 #include <algorithm>
+#include <climits>
 
 #include "common.h"
 #include "kernels.h"
@@ -277,15 +278,18 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
   // Page ids: lane l of wave w holds the id of block w of cached chunk
   // idbase + l, read 64 chunks at a time (a split longer than 64 chunks
   // reloads, waiting for its loads in flight); a chunk's id is then a lane
-  // read, with no memory access in the loop.  -1: load the window block.
-  int idv = -1, idbase = -64;
+  // read, with no memory access in the loop.  kNoBlock (not a table value):
+  // load the window block.  Any table entry outside [0, num_blocks) of a block
+  // inside the context, -1 included, is a bad block.
+  constexpr int kNoBlock = INT_MIN;
+  int idv = kNoBlock, idbase = -64;
   auto block_id = [&](int ch) {
-    if (ch < wch || ch >= nchunks) return -1;
+    if (ch < wch || ch >= nchunks) return kNoBlock;
     const int cc = ch - wch;
     if (cc - idbase >= 64) {
       idbase = cc;
       const int blk = c0 + (cc + lane) * kCB + wv / WPB;
-      idv = (cc + lane < ncc && blk < c1) ? a.table[(size_t)b * a.max_blocks + blk] : -1;
+      idv = (cc + lane < ncc && blk < c1) ? a.table[(size_t)b * a.max_blocks + blk] : kNoBlock;
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
     return __builtin_amdgcn_readlane(idv, cc - idbase);
@@ -293,9 +297,9 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
   auto issue = [&](int ch, int id) {
     const int buf = ch % NBUF;
     int ph = __builtin_amdgcn_readfirstlane(id);
-    if (ph != -1 && (ph < 0 || ph >= a.num_blocks)) {
+    if (ph != kNoBlock && (ph < 0 || ph >= a.num_blocks)) {
       bad = true;
-      ph = -1;
+      ph = kNoBlock;
     }
     const size_t off = ((size_t)max(ph, 0) * a.Hkv + kvh) * (kBlock * kD);
     const bf16_t* kb = ph >= 0 ? a.kp + off : win_k;

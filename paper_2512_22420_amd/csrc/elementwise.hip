@@ -96,10 +96,14 @@ struct RopeFreqHead {  // theta^(-2j/128) for the 64 rotation pairs of a 128-dim
   double inv_freq[64];
 };
 
+// With hin (fp32 [rows][d]) the rows are read from there instead of the
+// embedding and h is not written: the same inputs for a given residual stream
+// (the pre-attention stage entry point).
 __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const bf16_t* __restrict__ embed,
     const bf16_t* __restrict__ gain, float* __restrict__ h, bf16_t* __restrict__ x, float* __restrict__ ssq, int d,
-    int V, int* __restrict__ err, const int32_t* __restrict__ ctx, RopeFreqHead f, float* __restrict__ rope_cs) {
+    int V, int* __restrict__ err, const int32_t* __restrict__ ctx, RopeFreqHead f, float* __restrict__ rope_cs,
+    const float* __restrict__ hin) {
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   if (rope_cs && threadIdx.x < 64) {
     const int j = threadIdx.x;
@@ -111,12 +115,15 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     rope_cs[((size_t)row * 64 + j) * 2] = cs;
     rope_cs[((size_t)row * 64 + j) * 2 + 1] = sn;
   }
-  int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
-  if (tok < 0 || tok >= V) {
-    if (threadIdx.x == 0) flag_error(err, kErrToken);
-    tok = 0;
+  const bf16_t* e = nullptr;
+  if (!hin) {
+    int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
+    if (tok < 0 || tok >= V) {
+      if (threadIdx.x == 0) flag_error(err, kErrToken);
+      tok = 0;
+    }
+    e = embed + (size_t)tok * d;
   }
-  const bf16_t* e = embed + (size_t)tok * d;
   const int nt = (d + 127) / 128;
 #pragma unroll
   for (int it = 0; it < kNormMaxPer; ++it) {
@@ -126,8 +133,12 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     float part = 0.f;
     if (j < d) {
       float gv[4], o[4];
-      load4(e + j, hv);
-      store4(h + (size_t)row * d + j, hv);
+      if (hin) {
+        load4(hin + (size_t)row * d + j, hv);
+      } else {
+        load4(e + j, hv);
+        store4(h + (size_t)row * d + j, hv);
+      }
       load4(gain + j, gv);
 #pragma unroll
       for (int q = 0; q < 4; ++q) o[q] = hv[q] * gv[q];
@@ -386,7 +397,17 @@ hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B
   for (int j = 0; j < 64; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / 128);
   hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
                      static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h, static_cast<bf16_t*>(x),
-                     ssq, d, V, err, ctx, f, rope_cs);
+                     ssq, d, V, err, ctx, f, rope_cs, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_inputs(const float* h, int B, int T, const void* gain, void* x, float* ssq, int d,
+                              const int32_t* ctx, float theta, float* rope_cs, hipStream_t s) {
+  RopeFreqHead f{};
+  for (int j = 0; j < 64; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / 128);
+  hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, nullptr, nullptr, T, nullptr,
+                     static_cast<const bf16_t*>(gain), nullptr, static_cast<bf16_t*>(x), ssq, d, 0, nullptr, ctx, f,
+                     rope_cs, h);
   return hipGetLastError();
 }
 

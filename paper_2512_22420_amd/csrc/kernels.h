@@ -146,6 +146,11 @@ hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B
                                const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
                                const int32_t* ctx, float theta, float* rope_cs, hipStream_t s);
 
+// The same outputs (x, ssq, rope_cs) for given residual rows h [B*T][d] fp32
+// instead of embedding rows (h is only read).
+hipError_t launch_norm_inputs(const float* h, int B, int T, const void* gain, void* x, float* ssq, int d,
+                              const int32_t* ctx, float theta, float* rope_cs, hipStream_t s);
+
 // x[r] = rmsnorm(h[r]) * gain; x row-major, or k-blocked (as launch_gemm_tile reads it)
 hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, void* x, int M, int d, float eps,
                           hipStream_t s, bool x_kblocked = false);

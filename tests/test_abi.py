@@ -109,3 +109,21 @@ def test_gemm_with_plan_rejects_impossible_plans_on_host():
     # a workspace one byte short is refused before any launch
     assert L.nightjar_gemm_with_plan(nb.NJ_BF16, 16, 16, 16, 384, 4096, 4096, st, nb.NJ_GEMM_TILE_256x256, 4, 256,
                                      b - 1, 0) == nb.NJ_EINVAL
+
+
+def test_stage_entries_reject_bad_arguments_on_host():
+    desc = model_desc(W.QWEN7B)  # G = 7: k = 9 gives 70 query rows per KV head
+    n = nb.attn_workspace_bytes(desc, 1, 9)
+    rc = nb.lib().nightjar_attn_verify(ctypes.byref(desc), 16, 16, 16, 4, 16, 16, 16, 4, 16, 1, 9, 16, 256, n, 0)
+    assert rc == nb.NJ_EINVAL and "64 query rows" in nb.last_error()
+    rc = nb.lib().nightjar_attn_verify(ctypes.byref(desc), 16, 16, 16, 4, 16, 16, 16, 4, 16, 1, 2, 16, 256, 255, 0)
+    assert rc == nb.NJ_EINVAL and "workspace" in nb.last_error()
+    rc = nb.lib().nightjar_attn_verify(ctypes.byref(desc), 0, 16, 16, 4, 16, 16, 16, 4, 16, 1, 2, 16, 256, n, 0)
+    assert rc == nb.NJ_EINVAL and "NULL" in nb.last_error()
+    d8 = model_desc(W.LLAMA8B_LAYER)
+    m = nb.rmsnorm_rope_workspace_bytes(d8, 2, 3)
+    assert m > nb.rmsnorm_rope_workspace_bytes(d8, 1, 3) > 0
+    rc = nb.lib().nightjar_rmsnorm_rope(ctypes.byref(d8), 16, 16, 16, 16, 2, 3, 16, 16, 8, 256, m, 0)
+    assert rc == nb.NJ_EINVAL and "aligned" in nb.last_error()
+    rc = nb.lib().nightjar_rmsnorm_rope(ctypes.byref(d8), 16, 16, 16, 16, 2, 16, 16, 16, 16, 256, m, 0)
+    assert rc == nb.NJ_EINVAL

@@ -360,3 +360,50 @@ def test_pack_weight_layout(N, K):
     want = np.empty(npad * K, dtype=np.uint16)
     want[idx.ravel()] = full.ravel()
     assert np.array_equal(got, want)
+
+
+def test_accept_empty_residual_falls_back_to_target():
+    """q = 1.001 p makes max(0, p - q) zero everywhere: a rejection then draws
+    from p_n itself (the oracle's reading for an empty residual).  Accept
+    uniforms in [0.9995, 1) reject at ratio 1/1.001."""
+    B, k, V = 12, 3, 4096
+    rng = np.random.default_rng(17)
+    logits = (rng.standard_normal((B, k + 1, V)) * 2).astype(np.float32)
+    p = oracle.softmax(logits.astype(np.float64))
+    q = (1.001 * p[:, :k]).astype(np.float32)
+    drafts = np.stack([[oracle.invcdf(p[b, i], rng.random()) for i in range(k)] for b in range(B)]).astype(np.int32)
+    u = rng.random((B, k + 1), dtype=np.float32)
+    u[:, :k] = 0.9995 + 0.0004 * rng.random((B, k), dtype=np.float32)
+    acc, nxt = _run_accept(V, logits, drafts, q, u)
+    assert np.all(acc == 0)
+    for b in range(B):
+        n, toks = oracle.accept(p[b], q[b], drafts[b], u[b])
+        assert n == 0
+        resid = np.maximum(0.0, p[b, 0] - q[b, 0].astype(np.float64))
+        assert not np.any(resid > 0)  # the fallback branch is the one taken
+        assert nxt[b, 0] == toks[0], b
+        assert np.all(nxt[b, 1:] == -1)
+    # every accept test sits within the 1e-3 ratio margin of its uniform, so the
+    # generic comparison flags them all; the loop above compared them exactly
+    res = compare(acc, nxt, logits, drafts, q, u)
+    assert not res["mismatches"]
+
+
+def test_accept_zero_draft_probability_counts_as_accepted():
+    """q_i(x) = 0 for the draft token: the ratio is +inf, so the draft is kept
+    whatever its uniform (here u close to 1 and p(x) tiny)."""
+    B, k, V = 8, 3, 2048
+    rng = np.random.default_rng(23)
+    logits = (rng.standard_normal((B, k + 1, V)) * 2).astype(np.float32)
+    q = oracle.softmax(rng.standard_normal((B, k, V)) * 2).astype(np.float32)
+    drafts = rng.integers(0, V, size=(B, k)).astype(np.int32)
+    for b in range(B):
+        for i in range(k):
+            q[b, i, drafts[b, i]] = 0.0
+    u = rng.random((B, k + 1), dtype=np.float32)
+    u[:, :k] = 0.999
+    acc, nxt = _run_accept(V, logits, drafts, q, u)
+    assert np.all(acc == k)
+    assert np.array_equal(nxt[:, :k], drafts)
+    res = compare(acc, nxt, logits, drafts, q, u)
+    assert not res["mismatches"]

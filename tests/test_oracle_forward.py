@@ -295,3 +295,119 @@ def test_widen_bf16_bit_patterns():
     assert list(vals[:5]) == [1.0, -2.0, 0.25, 0.0, -0.0]
     assert vals[5] == 1.0 + 2.0 ** -7
     assert vals[6] == (2.0 - 2.0 ** -7) * 2.0 ** 127
+
+
+# --------------------------------------------------------------------------
+# the composed step at gamma > 0 (which target row scores which draft)
+# --------------------------------------------------------------------------
+def _self_draft_case(shape, weights, m, ctx, k, seed):
+    """Prefixes cached from the library model's prefill, and k drafts sampled
+    from the library model itself token by token (q_i = its own p_i), so every
+    draft must be accepted (Sec. 2.2: a draft the target agrees with is kept)
+    and the extra token is the target's own next sample (Sec. 3.1: n accepted
+    plus one).  Returns the inputs and, per sequence, the library model's
+    sample at window position k drawn with the step's last uniform."""
+    rng = np.random.default_rng(seed)
+    cd = W.make_context(shape, ctx, k, seed=seed)
+    cd["k_pages"] = [np.asarray(a, dtype=np.float64).copy() for a in cd["k_pages"]]
+    cd["v_pages"] = [np.asarray(a, dtype=np.float64).copy() for a in cd["v_pages"]]
+    B = len(ctx)
+    last = np.zeros(B, np.int32)
+    drafts = np.zeros((B, k), np.int32)
+    dprobs = np.zeros((B, k, shape.vocab), np.float32)
+    unif = np.zeros((B, k + 1), np.float32)
+    bonus = []
+    for b in range(B):
+        ids = list(rng.integers(0, shape.vocab, size=int(ctx[b]) + 1))
+        if ctx[b] > 0:
+            _write_prefix(cd, shape, b, _hf_prefill(m, ids[: ctx[b]]))
+        last[b] = ids[-1]
+        unif[b, :k] = rng.random(k) * 0.9  # accept tests, away from ratio 1
+        unif[b, k] = rng.random()
+        for i in range(k + 1):
+            lg = _hf_logits(m, ids)[-1]
+            p = np.exp(lg - lg.max())
+            c = np.cumsum(p)
+            v = rng.random() if i < k else float(unif[b, k])
+            y = int(np.searchsorted(c, v * c[-1], side="right"))
+            if i < k:
+                dprobs[b, i] = (p / c[-1]).astype(np.float32)
+                drafts[b, i] = y
+                ids.append(y)
+            else:
+                bonus.append(y)
+    return cd, last, drafts, dprobs, unif, bonus
+
+
+@pytest.mark.parametrize("k", [1, 4])
+def test_self_drafts_are_all_accepted_and_bonus_is_library_sample(k):
+    """With q_i equal to the target's own p_i every draft passes (u < p/q = 1),
+    and the bonus token is the library model's autoregressive sample at window
+    position k with the last uniform.  This pins that window row i scores draft
+    i+1 and that the bonus comes from row k."""
+    shape = SHAPES[1]
+    weights = W.make_weights(shape, seed=6, std=0.05)
+    m = _hf_model(shape, weights)
+    ctx = np.array([13, 30, 0], dtype=np.int32)
+    cd, last, drafts, dprobs, unif, bonus = _self_draft_case(shape, weights, m, ctx, k, seed=10 + k)
+    r = oracle.verify_step(weights, shape, cd["k_pages"], cd["v_pages"], cd["block_table"], ctx, last, drafts,
+                           dprobs, unif)
+    assert list(r["accepted_len"]) == [k] * len(ctx)
+    for b in range(len(ctx)):
+        assert list(r["next_tokens"][b]) == list(drafts[b]) + [bonus[b]]
+
+
+def test_misaligned_rows_fail_the_self_draft_pin():
+    """Planted mistake: scoring draft i with target row i+1 (an off-by-one
+    between rows and drafts) must break the self-draft property above."""
+    shape = SHAPES[1]
+    weights = W.make_weights(shape, seed=6, std=0.05)
+    m = _hf_model(shape, weights)
+    ctx = np.array([13, 30, 0], dtype=np.int32)
+    k = 4
+    cd, last, drafts, dprobs, unif, bonus = _self_draft_case(shape, weights, m, ctx, k, seed=14)
+    vs = __import__("sys").modules["oracle.verify_step"]
+    orig = vs.accept
+
+    def shifted(p, q, d, u):
+        return orig(np.concatenate([p[1:], p[-1:]], axis=0), q, d, u)
+    try:
+        vs.accept = shifted
+        r = oracle.verify_step(weights, shape, cd["k_pages"], cd["v_pages"], cd["block_table"], ctx, last, drafts,
+                               dprobs, unif)
+    finally:
+        vs.accept = orig
+    ok = all(r["accepted_len"][b] == k and list(r["next_tokens"][b]) == list(drafts[b]) + [bonus[b]]
+             for b in range(len(ctx)))
+    assert not ok
+
+
+def test_window_rows_equal_a_chain_of_gamma0_steps():
+    """A gamma = k window equals k+1 chained gamma = 0 steps fed the same tokens
+    (each followed by the KV append of its one row): row i of the window is the
+    gamma = 0 step at position ctx + i, and when every draft is accepted the
+    bonus equals the gamma = 0 step's draw with the same uniform (Sec. 4:
+    gamma = 0 is plain decoding)."""
+    x = W.tiny_inputs(seed=7, k=4)
+    s = x["shape"]
+    k = 4
+    # drafts the step must accept: q_i = the window's own p_i, accept uniforms 0
+    toks = oracle.window_tokens(x["last_tokens"], x["draft_tokens"])
+    logits, _, _ = oracle.forward_window(x["weights"], s, x["k_pages"], x["v_pages"], x["block_table"],
+                                         x["context_lens"], toks)
+    q = oracle.softmax(logits[:, :k]).astype(np.float32)
+    u = x["uniforms"].copy()
+    u[:, :k] = 0.0
+    r = oracle.verify_step(x["weights"], s, x["k_pages"], x["v_pages"], x["block_table"], x["context_lens"],
+                           x["last_tokens"], x["draft_tokens"], q, u)
+    assert list(r["accepted_len"]) == [k, k]
+    kp, vp, ctx = x["k_pages"], x["v_pages"], x["context_lens"].copy()
+    for i in range(k + 1):
+        ui = u[:, k:k + 1] if i == k else np.full((2, 1), 0.5, np.float32)
+        ri = oracle.verify_step(x["weights"], s, kp, vp, x["block_table"], ctx, toks[:, i].astype(np.int32),
+                                np.zeros((2, 0), np.int32), np.zeros((2, 0, s.vocab), np.float32), ui)
+        np.testing.assert_allclose(ri["logits"][:, 0], r["logits"][:, i], rtol=0, atol=1e-10)
+        if i == k:
+            assert list(ri["next_tokens"][:, 0]) == list(r["next_tokens"][:, k])
+        kp, vp, ctx = oracle.kv_append(kp, vp, x["block_table"], ctx, ri["accepted_len"], ri["win_k"], ri["win_v"],
+                                       s.block_size, s.dtype)
