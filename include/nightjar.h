@@ -278,6 +278,28 @@ int nightjar_attn_verify(const nj_model_desc* desc, const void* q, const void* k
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nightjar_accept_noalloc -- nightjar_accept with no workspace, for callers
+ * that cannot allocate device memory (code under HIP graph capture, serving
+ * loops and harnesses that forbid hipMalloc).  Same rule, same kernels, same
+ * outputs bit for bit as nightjar_accept.  Its scratch is a fixed array of
+ * 32 MiB of device memory, one per GPU, that the library holds until the
+ * process ends; a call whose
+ * B * (k+1) rows and vocabulary need more (about rows * vocab * 3/32 bytes)
+ * fails with NJ_EINVAL before anything is enqueued.  The call allocates
+ * nothing (its first call on a device looks up that device's copy of the
+ * array).  Every call on one GPU shares that GPU's array: calls that overlap
+ * in time on one GPU (other streams, other threads) race and give undefined
+ * outputs; calls in order on one stream are safe.
+ *
+ *   device_error   device int32, out: the NJ_DEV_* bits this call found (0 if none);
+ *                  read it after the stream has finished
+ * The other arguments as in nightjar_accept.
+ */
+int nightjar_accept_noalloc(const nj_model_desc* desc, const float* logits, const int32_t* draft_tokens,
+                            const float* draft_probs, const float* uniforms, int32_t B, int32_t k,
+                            int32_t* accepted_len, int32_t* next_tokens, int32_t* device_error, void* stream);
+
+/*
  * Packed layout of a bf16 weight matrix w [N][K] (K % 32 == 0), the form in
  * which the bf16 GEMMs read their weights (a layout choice of this library,
  * not of the method: every load instruction of the GEMM kernels reads 1 KB of

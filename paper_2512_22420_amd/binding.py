@@ -76,6 +76,8 @@ _SIGS = {
     "nightjar_attn_workspace_bytes": (_sz, [ctypes.POINTER(ModelDesc), _i32, _i32]),
     "nightjar_attn_verify": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _i32, _vp, _vp, _vp, _i32,
                                             _vp, _i32, _i32, _vp, _vp, _sz, _vp]),
+    "nightjar_accept_noalloc": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                               _vp, _vp]),
     "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
     "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
@@ -170,6 +172,12 @@ def gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace
                    stream: int = 0) -> None:
     _check(lib().nightjar_gemm_with_plan(dtype, x, w, y, M, N, K, epilogue, kernel, split_k, workspace,
                                          workspace_nbytes, stream))
+
+
+def accept_noalloc(desc, logits, draft_tokens, draft_probs, uniforms, B, k, accepted_len, next_tokens, device_error,
+                   stream: int = 0) -> None:
+    _check(lib().nightjar_accept_noalloc(ctypes.byref(desc), logits, draft_tokens, draft_probs, uniforms, B, k,
+                                         accepted_len, next_tokens, device_error, stream))
 
 
 def rmsnorm_rope_workspace_bytes(desc, B, k) -> int:

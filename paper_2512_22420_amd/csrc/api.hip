@@ -13,6 +13,14 @@
 
 using namespace nj;
 
+// Scratch of nightjar_accept_noalloc: a fixed array in device memory, one copy
+// per GPU the library runs on, held until the process ends.  In host code this
+// name is only a stand-in for the symbol: its device address comes from
+// hipGetSymbolAddress (accept_noalloc_scratch below), and only that address is
+// ever passed to a kernel.
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
 
 thread_local std::string g_err;
@@ -189,11 +197,35 @@ AttnLayout attn_layout(const nj_model_desc& d, int B, int k) {
   return L;
 }
 
+// Device address of `scratch` on each device, taken once per device with
+// that device current (the first nightjar_accept_noalloc call on it).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int accept_noalloc_scratch(void** out);
+
 struct StepRecord {
   int B, k, n_layers;
 };
 std::mutex g_mu;
 std::unordered_map<const void*, StepRecord> g_steps;
+
+int accept_noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "accept_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(NJ_EINVAL, "accept_noalloc: device id %d out of range", dev);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "accept_noalloc: hipGetSymbolAddress");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return NJ_OK;
+}
 
 }  // namespace
 
@@ -532,6 +564,32 @@ int nightjar_accept(const nj_model_desc* desc, const float* logits, const int32_
                next_tokens, reinterpret_cast<int*>(ws)};
   hipError_t e = launch_accept(a, (hipStream_t)stream);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "accept");
+}
+
+int nightjar_accept_noalloc(const nj_model_desc* desc, const float* logits, const int32_t* draft_tokens,
+                            const float* draft_probs, const float* uniforms, int32_t B, int32_t k,
+                            int32_t* accepted_len, int32_t* next_tokens, int32_t* device_error, void* stream) {
+  if (!desc || desc->vocab < 1 || desc->vocab > kMaxVocab) return fail(NJ_EINVAL, "bad desc or vocab");
+  if (B < 1 || k < 0 || k > kMaxK) return fail(NJ_EINVAL, "bad B or k");
+  if (!logits || !uniforms || !accepted_len || !next_tokens || !device_error)
+    return fail(NJ_EINVAL, "a required pointer is NULL");
+  if (k > 0 && (!draft_tokens || !draft_probs)) return fail(NJ_EINVAL, "k > 0 needs draft_tokens and draft_probs");
+  const size_t need = accept_workspace_bytes(B * (k + 1), desc->vocab);
+  if (need > kNoAllocScratchBytes)
+    return fail(NJ_EINVAL, "accept_noalloc: B=%d, k=%d, vocab=%d needs %zu bytes of scratch, more than its %zu",
+                B, k, desc->vocab, need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  const int rc = accept_noalloc_scratch(&ws);
+  if (rc != NJ_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  // the error word is the caller's output: it starts at zero on every call
+  // (a fill kernel, not a memset, so the call can be captured in a graph)
+  hipError_t e = launch_fill_i32(device_error, 0, 1, s);
+  if (e != hipSuccess) return hip_fail(e, "accept_noalloc: clear error word");
+  AcceptArgs a{logits, draft_tokens, draft_probs, uniforms, B, k, desc->vocab, ws, false, 0, accepted_len,
+               next_tokens, device_error};
+  e = launch_accept(a, s);
+  return e == hipSuccess ? NJ_OK : hip_fail(e, "accept_noalloc");
 }
 
 static int gemm_args_ok(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue) {
