@@ -1,4 +1,4 @@
-"""CPU oracle of the batched speculative verify step (test infrastructure only).
+"""CPU oracle of the batched speculative verify step and of the planner (test infrastructure only).
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg use it;
 the HIP library never does.
@@ -6,3 +6,4 @@ the HIP library never does.
 from .verify_step import (accept, attention, forward_window, gather_cache, invcdf,  # noqa: F401
                           kv_append, linear, rms_norm, rope, silu, softmax, verify_step, widen,
                           window_tokens)
+from . import planner  # noqa: F401

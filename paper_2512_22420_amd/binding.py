@@ -44,6 +44,17 @@ class KvCache(ctypes.Structure):
     _fields_ = [("k_pages", ctypes.POINTER(_vp)), ("v_pages", ctypes.POINTER(_vp)), ("num_blocks", _i32)]
 
 
+class PlannerConfig(ctypes.Structure):
+    _fields_ = [("max_batch", _i32), ("max_gamma", _i32), ("seed", ctypes.c_uint64), ("prev_per_batch", _i32),
+                ("unplayed_latency", ctypes.c_double)]
+
+
+class PlannerBState(ctypes.Structure):
+    _fields_ = [("block", _i32), ("block_len", ctypes.c_int64), ("bin", ctypes.c_int64), ("round", ctypes.c_int64),
+                ("gamma", _i32), ("steps", ctypes.c_int64), ("bins", ctypes.c_int64),
+                ("explore_bins", ctypes.c_int64)]
+
+
 class NightjarError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"nightjar error {code}: {msg}")
@@ -78,6 +89,15 @@ _SIGS = {
                                             _vp, _i32, _i32, _vp, _vp, _sz, _vp]),
     "nightjar_accept_noalloc": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                                _vp, _vp]),
+    "nightjar_planner_create": (_vp, [ctypes.POINTER(PlannerConfig)]),
+    "nightjar_planner_destroy": (None, [_vp]),
+    "nightjar_planner_set_switch_cost": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i32, _vp]),
+    "nightjar_planner_switch_cost": (ctypes.c_double, [_vp, _i32, _i32]),
+    "nightjar_planner_select": (ctypes.c_int, [_vp, _i32, _i32, _i32, ctypes.POINTER(_i32)]),
+    "nightjar_planner_observe": (ctypes.c_int, [_vp, _i32, _i32, ctypes.c_double, _i32]),
+    "nightjar_planner_bstate": (ctypes.c_int, [_vp, _i32, ctypes.POINTER(PlannerBState)]),
+    "nightjar_planner_arm": (ctypes.c_int, [_vp, _i32, _i32, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_int64)]),
     "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
     "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
@@ -216,6 +236,56 @@ def packed_weight_elems(N, K) -> int:
 
 def pack_weight(src, dst, N, K, stream: int = 0) -> None:
     _check(lib().nightjar_pack_weight(src, dst, N, K, stream))
+
+
+class Planner:
+    """The planner of include/nightjar_planner.h (Algorithm 1), one object per
+    decision loop; marshalling only."""
+
+    def __init__(self, max_batch: int, max_gamma: int, seed: int = 0, prev_per_batch: bool = False,
+                 unplayed_latency: float = 0.0):
+        cfg = PlannerConfig(max_batch, max_gamma, seed, int(prev_per_batch), unplayed_latency)
+        self._p = lib().nightjar_planner_create(ctypes.byref(cfg))
+        if not self._p:
+            raise NightjarError(NJ_EINVAL, last_error())
+
+    def __del__(self):
+        if getattr(self, "_p", None) and _LIB is not None:
+            _LIB.nightjar_planner_destroy(self._p)
+            self._p = None
+
+    def set_switch_cost(self, lengths, batches, seconds) -> None:
+        nl, nbt = len(lengths), len(batches)
+        la = (_i32 * nl)(*lengths)
+        ba = (_i32 * nbt)(*batches)
+        flat = [float(v) for row in seconds for v in row]
+        sa = (ctypes.c_double * len(flat))(*flat)
+        _check(lib().nightjar_planner_set_switch_cost(self._p, ctypes.cast(la, _vp), nl, ctypes.cast(ba, _vp), nbt,
+                                                      ctypes.cast(sa, _vp)))
+
+    def switch_cost(self, delta_max: int, B: int) -> float:
+        v = lib().nightjar_planner_switch_cost(self._p, delta_max, B)
+        if v < 0:
+            raise NightjarError(NJ_EINVAL, last_error())
+        return v
+
+    def select(self, B: int, delta_max: int = 0, gamma_limit: int = 15) -> int:
+        g = _i32(-1)
+        _check(lib().nightjar_planner_select(self._p, B, delta_max, gamma_limit, ctypes.byref(g)))
+        return g.value
+
+    def observe(self, B: int, gamma: int, step_seconds: float, committed_tokens: int) -> None:
+        _check(lib().nightjar_planner_observe(self._p, B, gamma, step_seconds, committed_tokens))
+
+    def bstate(self, B: int) -> PlannerBState:
+        st = PlannerBState()
+        _check(lib().nightjar_planner_bstate(self._p, B, ctypes.byref(st)))
+        return st
+
+    def arm(self, B: int, gamma: int):
+        m, n = ctypes.c_double(), ctypes.c_int64()
+        _check(lib().nightjar_planner_arm(self._p, B, gamma, ctypes.byref(m), ctypes.byref(n)))
+        return m.value, n.value
 
 
 def header_functions(header_path: str):

@@ -725,3 +725,15 @@ int nightjar_gemm_with_plan(int32_t dtype, const void* x, const void* w, void* y
 }
 
 }  // extern "C"
+
+namespace nj {
+int set_last_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+}  // namespace nj

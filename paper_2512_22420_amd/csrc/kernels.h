@@ -228,4 +228,7 @@ hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s);
 
+// Sets the message nightjar_last_error() returns on this thread; returns code.
+int set_last_error(int code, const char* fmt, ...);
+
 }  // namespace nj

@@ -16,11 +16,16 @@ pytestmark = pytest.mark.skipif(not os.path.exists(nb.LIB_PATH), reason="libnigh
 
 
 def test_exports_every_declared_function():
+    import glob
     names = nb.header_functions(HEADER)
     assert "nightjar_verify_step" in names and "nightjar_kv_append" in names
+    headers = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
+    assert len(headers) >= 2
     L = nb.lib()
-    for n in names:
-        assert hasattr(L, n), n
+    for h in headers:
+        for n in nb.header_functions(h):
+            assert hasattr(L, n), (h, n)
+            assert n in nb._SIGS, (h, n)  # the binding declares it too
 
 
 def test_struct_sizes_match_header_layout():
