@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libnightjar.so")
 
 NJ_F32, NJ_BF16 = 0, 1
-NJ_OK, NJ_EINVAL, NJ_EDEVICE, NJ_EHIP = 0, -1, -2, -3
+NJ_OK, NJ_EINVAL, NJ_EDEVICE, NJ_EHIP, NJ_EAGAIN = 0, -1, -2, -3, -4
 NJ_DEV_BAD_TOKEN, NJ_DEV_BAD_BLOCK, NJ_DEV_BAD_CONTEXT, NJ_DEV_BAD_ACCEPT = 1, 2, 4, 8
 NJ_GEMM_STORE, NJ_GEMM_RESIDUAL, NJ_GEMM_SWIGLU = 0, 1, 2
 NJ_GEMM_KBLOCKED = 16  # flag: x (and a SwiGLU y) k-blocked, [K/32][M][32]
@@ -98,6 +98,10 @@ _SIGS = {
     "nightjar_planner_bstate": (ctypes.c_int, [_vp, _i32, ctypes.POINTER(PlannerBState)]),
     "nightjar_planner_arm": (ctypes.c_int, [_vp, _i32, _i32, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int64)]),
+    "nightjar_contraction_plan": (ctypes.c_int, [_vp, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _vp, _i32,
+                                                 ctypes.POINTER(_i32), _vp, ctypes.POINTER(_i32)]),
+    "nightjar_kv_migrate": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(KvCache), _vp, _vp, _i32, _vp,
+                                           _vp]),
     "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
     "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
@@ -236,6 +240,29 @@ def packed_weight_elems(N, K) -> int:
 
 def pack_weight(src, dst, N, K, stream: int = 0) -> None:
     _check(lib().nightjar_pack_weight(src, dst, N, K, stream))
+
+
+def contraction_plan(block_table, free_list, k_boundary: int, k_total: int):
+    """nightjar_contraction_plan on numpy arrays (host memory).  Returns
+    (src, dst, new_table, new_free); raises NightjarError (code NJ_EAGAIN when
+    the contraction must be deferred)."""
+    import numpy as np
+    table = np.ascontiguousarray(block_table, dtype=np.int32).copy()
+    free = np.ascontiguousarray(free_list, dtype=np.int32)
+    B, mb = table.shape
+    cap = max(1, int((table >= k_boundary).sum()))
+    src = np.zeros(cap, np.int32)
+    dst = np.zeros(cap, np.int32)
+    new_free = np.zeros(max(1, len(free)), np.int32)
+    nm, nf = _i32(0), _i32(0)
+    _check(lib().nightjar_contraction_plan(table.ctypes.data, B, mb, free.ctypes.data if len(free) else None,
+                                           len(free), k_boundary, k_total, src.ctypes.data, dst.ctypes.data, cap,
+                                           ctypes.byref(nm), new_free.ctypes.data, ctypes.byref(nf)))
+    return src[:nm.value].copy(), dst[:nm.value].copy(), table, new_free[:nf.value].copy()
+
+
+def kv_migrate(desc, kv, src, dst, n, device_error, stream: int = 0) -> None:
+    _check(lib().nightjar_kv_migrate(ctypes.byref(desc), ctypes.byref(kv), src, dst, n, device_error, stream))
 
 
 class Planner:
