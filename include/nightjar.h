@@ -125,6 +125,16 @@ typedef struct nj_kv_cache {
 size_t nightjar_workspace_bytes(const nj_model_desc* desc, int32_t max_B, int32_t max_k);
 
 /*
+ * Whether a verify step of B sequences with k drafts folds its RMSNorms into
+ * the neighbouring GEMMs (1) or runs them as their own kernels (0); < 0 on bad
+ * arguments.  The two differ only in where bf16 rounding happens: folded, a
+ * GEMM input is bf16(h * gain) and the 1/rms row scale is applied to the fp32
+ * product; unfused, the input is bf16(RMSNorm(h) * gain).  Windows of up to
+ * ~64 rows (bf16, every GEMM on the weight-streaming kernel) fold.
+ */
+int nightjar_step_folds_norms(const nj_model_desc* desc, int32_t B, int32_t k);
+
+/*
  * Prepare a fresh workspace: zero-fills it (the device error word and the
  * split-K arrival counters must start at zero).  Call once after allocating
  * it; device memory, 256-byte aligned.

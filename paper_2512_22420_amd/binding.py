@@ -66,6 +66,7 @@ _LIB = None
 _SIGS = {
     "nightjar_workspace_bytes": (_sz, [ctypes.POINTER(ModelDesc), _i32, _i32]),
     "nightjar_workspace_init": (ctypes.c_int, [_vp, _sz, _vp]),
+    "nightjar_step_folds_norms": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _i32, _i32]),
     "nightjar_verify_step": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.POINTER(KvCache),
                                             _vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp,
                                             _vp, _sz, _vp]),
@@ -136,6 +137,10 @@ def workspace_bytes(desc: ModelDesc, max_B: int, max_k: int) -> int:
     if n == 0:
         raise NightjarError(NJ_EINVAL, last_error())
     return n
+
+
+def step_folds_norms(desc: ModelDesc, B: int, k: int) -> bool:
+    return bool(_check(lib().nightjar_step_folds_norms(ctypes.byref(desc), B, k)))
 
 
 def workspace_init(workspace: int, nbytes: int, stream: int = 0) -> None:

@@ -238,6 +238,12 @@ size_t nightjar_workspace_bytes(const nj_model_desc* desc, int32_t max_B, int32_
   return layout(*desc, max_B, max_k).total;
 }
 
+int nightjar_step_folds_norms(const nj_model_desc* desc, int32_t B, int32_t k) {
+  if (!desc_ok(desc)) return NJ_EINVAL;
+  if (B < 1 || k < 0 || k > kMaxK) return fail(NJ_EINVAL, "bad B or k");
+  return fold_norms(*desc, B * (k + 1)) ? 1 : 0;
+}
+
 int nightjar_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
   if (!workspace || workspace_bytes < kAlign) return fail(NJ_EINVAL, "workspace NULL or smaller than %zu", kAlign);
   if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");

@@ -311,3 +311,47 @@ def tiny_inputs(seed: int = 0, k: int = 3) -> Dict:
     c = make_context(TINY_F32, TINY_CTX, k, seed)
     d = make_drafts(TINY_F32, 2, k, seed)
     return {"shape": TINY_F32, "weights": w, **c, **d}
+
+
+# --------------------------------------------------------------------------
+# Inputs generated on the device (the 32-layer and Qwen-shaped stacks, whose
+# weights and caches take tens of GB): torch's seeded generator, the same
+# distributions as the host generators above (not the same bits).
+# --------------------------------------------------------------------------
+def device_normal_bf16(gen, shape_, std: float, device="cuda"):
+    """N(0, std^2) draws rounded to bf16, as int16 bit patterns, generated in
+    bounded chunks."""
+    import torch
+    out = torch.empty(shape_, dtype=torch.bfloat16, device=device)
+    flat = out.view(-1)
+    step = 1 << 26
+    for i in range(0, flat.numel(), step):
+        n = min(step, flat.numel() - i)
+        flat[i:i + n] = (torch.randn(n, generator=gen, device=device) * std).to(torch.bfloat16)
+    return out.view(torch.int16)
+
+
+def device_weights(shape: ModelShape, gen, device="cuda", std: float = 0.02) -> Dict:
+    """Random-init weights of `shape` on the device (bf16 bits as int16,
+    row-major, the layout of make_weights); norm gains 1."""
+    import torch
+    ones = torch.ones(shape.d_model, dtype=torch.bfloat16, device=device).view(torch.int16)
+    w = {"embed": device_normal_bf16(gen, (shape.vocab, shape.d_model), std, device),
+         "lm_head": device_normal_bf16(gen, (shape.vocab, shape.d_model), std, device),
+         "final_norm": ones, "layers": []}
+    for _ in range(shape.n_layers):
+        w["layers"].append({"attn_norm": ones, "ffn_norm": ones,
+                            "w_qkv": device_normal_bf16(gen, (shape.qkv_dim, shape.d_model), std, device),
+                            "w_o": device_normal_bf16(gen, (shape.d_model, shape.n_heads * shape.head_dim), std, device),
+                            "w_gate_up": device_normal_bf16(gen, (2 * shape.ffn_dim, shape.d_model), std, device),
+                            "w_down": device_normal_bf16(gen, (shape.d_model, shape.ffn_dim), std, device)})
+    return w
+
+
+def device_pages(shape: ModelShape, num_blocks: int, gen, device="cuda", kv_std: float = 0.5):
+    """K and V pages of every layer, N(0,1) * kv_std in bf16 (int16 bits)."""
+    kp = [device_normal_bf16(gen, (num_blocks, shape.n_kv_heads, shape.block_size, shape.head_dim), kv_std, device)
+          for _ in range(shape.n_layers)]
+    vp = [device_normal_bf16(gen, (num_blocks, shape.n_kv_heads, shape.head_dim, shape.block_size), kv_std, device)
+          for _ in range(shape.n_layers)]
+    return kp, vp

@@ -1,0 +1,156 @@
+"""Parity at the large configurations (the 8B layer at B=128, the 32-layer 8B
+stack, the 28-layer Qwen2.5-7B shape): the GPU runs the whole batch, the oracle
+checks a subset of its sequences (sequences are independent in the verify
+step).
+
+Inputs: weights and KV pages are generated on the device with torch's seeded
+generator (tens of GB), copied to the host and widened to fp64 once, so the
+oracle's linear layers read them directly.  The checked sequences' drafts come
+from the beta-mixed draft model over the oracle's own target logits, position
+by position (q_i = softmax(beta * l_i + (1 - beta) * N(0, 4)), d_{i+1} ~ q_i),
+so no oracle input is taken from the GPU path; the other sequences get
+softmax(N(0, 4)) drafts generated on the device.
+"""
+from __future__ import annotations
+
+import concurrent.futures as cf
+import dataclasses
+import os
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2512_22420_amd import workload as W
+from paper_2512_22420_amd.device import DeviceCache, DeviceModel, Workspace, device_error, verify
+
+_THREADS = min(16, len(os.sched_getaffinity(0)))
+_ROWS = 4096
+DEVICE = "cuda"
+
+
+def widen_f64(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> fp64 (exact), in row chunks on several threads."""
+    out = np.empty(bits.shape, dtype=np.float64)
+    if bits.ndim == 1:
+        out[:] = oracle.widen(bits, "bf16")
+        return out
+
+    def chunk(r0):
+        out[r0: r0 + _ROWS] = oracle.widen(bits[r0: r0 + _ROWS], "bf16")
+    with cf.ThreadPoolExecutor(_THREADS) as ex:
+        list(ex.map(chunk, range(0, bits.shape[0], _ROWS)))
+    return out
+
+
+def _host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint16)
+
+
+class BigModel:
+    """A bf16 model resident on the device (packed for the library) and its
+    fp64 copy on the host for the oracle (with a shape whose dtype tells the
+    oracle its arrays are already widened)."""
+
+    def __init__(self, shape, seed: int, host: bool = True):
+        gen = torch.Generator(device=DEVICE)
+        gen.manual_seed(seed)
+        w = W.device_weights(shape, gen, device=DEVICE)
+        self.shape = shape
+        self.shape64 = dataclasses.replace(shape, dtype="f32")
+        self.w64 = None
+        if host:
+            self.w64 = {"embed": widen_f64(_host_bits(w["embed"])), "lm_head": widen_f64(_host_bits(w["lm_head"])),
+                        "final_norm": widen_f64(_host_bits(w["final_norm"])), "layers": []}
+            for lw in w["layers"]:
+                self.w64["layers"].append({n: widen_f64(_host_bits(lw[n])) for n in lw})
+        self.dev = DeviceModel(shape, w)
+        # the packed copies are what the library reads; the row-major device
+        # copies of the GEMM weights are dropped with `w`
+        del w
+        torch.cuda.empty_cache()
+
+
+class BigCase:
+    """One verify step of B sequences on the device, with `checked` sequences
+    extracted to a compact host pool for the oracle."""
+
+    def __init__(self, model: BigModel, ctx: np.ndarray, k: int, checked, beta: float, seed: int):
+        shape = model.shape
+        B = len(ctx)
+        self.B, self.k, self.checked = B, k, list(checked)
+        table, num_blocks, max_blocks = W.make_block_table(shape, ctx, k, seed=seed)
+        gen = torch.Generator(device=DEVICE)
+        gen.manual_seed(seed + 1)
+        kp, vp = W.device_pages(shape, num_blocks, gen, device=DEVICE)
+        self.cache = DeviceCache({"k_pages": kp, "v_pages": vp, "block_table": torch.from_numpy(table).to(DEVICE),
+                                  "context_lens": torch.from_numpy(ctx).to(DEVICE), "num_blocks": num_blocks})
+        self.cache.max_blocks = max_blocks
+        # compact host pool of the checked sequences (blocks renumbered in order)
+        sub_tables, blocks = [], []
+        for b in self.checked:
+            own = table[b][table[b] >= 0]
+            sub_tables.append(np.arange(len(blocks), len(blocks) + len(own), dtype=np.int32))
+            blocks.extend(int(x) for x in own)
+        mb = max(len(t) for t in sub_tables)
+        self.sub_table = np.full((len(self.checked), mb), -1, np.int32)
+        for i, t in enumerate(sub_tables):
+            self.sub_table[i, : len(t)] = t
+        idx = torch.tensor(blocks, dtype=torch.long, device=DEVICE)
+        self.sub_k = [widen_f64(_host_bits(kp[l].index_select(0, idx))) for l in range(shape.n_layers)]
+        self.sub_v = [widen_f64(_host_bits(vp[l].index_select(0, idx))) for l in range(shape.n_layers)]
+        self.sub_ctx = ctx[self.checked].astype(np.int32)
+        # step inputs: all sequences on the device
+        V = shape.vocab
+        self.last = torch.randint(0, V, (B,), generator=gen, device=DEVICE, dtype=torch.int32)
+        self.uniforms = torch.rand((B, k + 1), generator=gen, device=DEVICE)
+        self.drafts = torch.zeros((B, k), dtype=torch.int32, device=DEVICE)
+        self.probs = torch.empty((B, k, V), dtype=torch.float32, device=DEVICE)
+        for i in range(k):
+            q = torch.softmax(2.0 * torch.randn((B, V), generator=gen, device=DEVICE), dim=-1)
+            self.probs[:, i] = q
+            self.drafts[:, i] = torch.multinomial(q, 1, generator=gen).squeeze(1).to(torch.int32)
+        # the checked sequences: beta-mixed drafts over the oracle's target logits
+        self.sub_last = self.last.cpu().numpy()[self.checked]
+        sd = np.zeros((len(self.checked), k), np.int32)
+        sq = np.zeros((len(self.checked), k, V), np.float32)
+        for i in range(k):
+            toks = np.concatenate([self.sub_last[:, None], sd[:, :i]], axis=1)
+            lg, _, _ = oracle.forward_window(model.w64, model.shape64, self.sub_k, self.sub_v, self.sub_table,
+                                             self.sub_ctx, toks)
+            for j, b in enumerate(self.checked):
+                sd[j, i], sq[j, i] = W.beta_mix_draft_row(lg[j, i], beta, seed, b, i)
+        self.sub_drafts, self.sub_probs = sd, sq
+        sel = torch.tensor(self.checked, dtype=torch.long, device=DEVICE)
+        if k:
+            self.drafts[sel] = torch.from_numpy(sd).to(DEVICE)
+            self.probs[sel] = torch.from_numpy(sq).to(DEVICE)
+        self.sub_u = self.uniforms.cpu().numpy()[self.checked]
+
+    def run(self, model: BigModel):
+        """The verify step on the device; returns (accepted_len, next_tokens,
+        logits) of the checked sequences and the device error word."""
+        shape = model.shape
+
+        class IO:
+            pass
+        io = IO()
+        io.B, io.k = self.B, self.k
+        io.last_tokens, io.uniforms = self.last, self.uniforms
+        io.draft_tokens = self.drafts if self.k else None
+        io.draft_probs = self.probs if self.k else None
+        io.accepted_len = torch.full((self.B,), -7, dtype=torch.int32, device=DEVICE)
+        io.next_tokens = torch.full((self.B, self.k + 1), -7, dtype=torch.int32, device=DEVICE)
+        io.logits = torch.empty((self.B, self.k + 1, shape.vocab), dtype=torch.float32, device=DEVICE)
+        ws = Workspace(shape, self.B, self.k)
+        verify(model.dev, self.cache, io, ws)
+        err = device_error(ws)
+        sel = torch.tensor(self.checked, dtype=torch.long, device=DEVICE)
+        out = (io.accepted_len[sel].cpu().numpy(), io.next_tokens[sel].cpu().numpy(),
+               io.logits[sel].cpu().numpy(), io.accepted_len.cpu().numpy())
+        del io, ws
+        return out + (err,)
+
+    def oracle(self, model: BigModel):
+        return oracle.verify_step(model.w64, model.shape64, self.sub_k, self.sub_v, self.sub_table, self.sub_ctx,
+                                  self.sub_last, self.sub_drafts, self.sub_probs, self.sub_u)

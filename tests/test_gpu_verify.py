@@ -14,8 +14,10 @@ import torch
 import oracle
 from paper_2512_22420_amd import binding as nb
 from paper_2512_22420_amd import workload as W
-from paper_2512_22420_amd.device import DeviceCache, DeviceModel, StepIO, Workspace, device_error, kv_append, verify
+from paper_2512_22420_amd.device import (DeviceCache, DeviceModel, StepIO, Workspace, device_error, kv_append,
+                                        model_desc, verify)
 
+import rounding_model as RM
 from parity import compare, record, rel_l2_rows, self_check
 
 pytestmark = pytest.mark.gpu
@@ -123,6 +125,16 @@ def test_large_batch_lognormal_contexts():
     assert res["checked"] >= B // 2
 
 
+def _within_storage_model(shape, weights, x, k, ref_logits, gpu_logits):
+    """Per-row logits errors within those of the bf16 storage model of the
+    same path (folded or unfused norms, as the library runs this window)."""
+    B = len(x["context_lens"])
+    fused = nb.step_folds_norms(model_desc(shape), B, k)
+    toks = oracle.window_tokens(x["last_tokens"], x["draft_tokens"])
+    m = RM.forward(weights, shape, x["k_pages"], x["v_pages"], x["block_table"], x["context_lens"], toks, fused)
+    return RM.assert_within_model(gpu_logits, m, ref_logits)
+
+
 @pytest.fixture(scope="module")
 def llama_layer():
     shape = W.LLAMA8B_LAYER
@@ -155,9 +167,10 @@ def test_llama8b_layer_tiled_gemms(llama_layer, B, k):
     """Windows of 128 and 384 rows: the LDS-tiled GEMMs with their inputs written
     k-blocked by the norm, attention and SwiGLU producers, contexts lognormal
     as in the large-batch grid.  The logits bound is the relative L2 over the
-    whole logits tensor; single rows of a window this large reach ~1.1e-2 from
-    bf16 rounding alone (a numpy model of the same roundings with fp64 sums
-    gives 1.07e-2 on row 14 of the 128-row case), so rows are held to 1.5e-2."""
+    whole logits tensor; single rows of a window this large pass 1e-2 from
+    bf16 storage alone (the storage model puts row 14 of the 128-row case at
+    1.08e-2), so rows are held to the storage model's own row errors
+    (rounding_model.assert_within_model)."""
     shape, weights, model = llama_layer
     ctx = W.ctx_lengths("lognormal", B, seed=5, median=768, sigma=0.5, lo=128, hi=2048)
     x = _inputs(shape, ctx, k, seed=1, weights=weights, k_max=5)
@@ -167,7 +180,7 @@ def test_llama8b_layer_tiled_gemms(llama_layer, B, k):
     gl = io.logits.cpu().numpy()
     r = np.asarray(ref["logits"])
     assert np.linalg.norm(gl - r) / np.linalg.norm(r) <= 1e-2
-    assert rel_l2_rows(gl, r).max() <= 1.5e-2
+    _within_storage_model(shape, weights, x, k, r, gl)
     _decisions_ok(io, ref, x, gpu_logits=gl, min_checked=B // 2)
 
 
@@ -176,8 +189,8 @@ def test_llama8b_layer_wide_persistent_lm_head(llama_layer, B, k):
     """Windows of 80 and 96 rows: the persistent LM-head kernel with 5 and 6
     row tiles (one group per workgroup) and its softmax statistics feeding the
     acceptance.  These windows take the unfused path (bf16 normed GEMM inputs),
-    so rows are held to 1.5e-2 as for the tiled windows: row 62 of the 80-row
-    case reaches 1.08e-2, with the tiled LM head as well (same logits bits)."""
+    whose storage roundings alone put row 62 of the 80-row case at 1.06e-2
+    (the storage model); rows are held to the model's row errors."""
     shape, weights, model = llama_layer
     ctx = W.ctx_lengths("lognormal", B, seed=6, median=768, sigma=0.5, lo=128, hi=2048)
     x = _inputs(shape, ctx, k, seed=3, weights=weights, k_max=5)
@@ -187,7 +200,7 @@ def test_llama8b_layer_wide_persistent_lm_head(llama_layer, B, k):
     gl = io.logits.cpu().numpy()
     r = np.asarray(ref["logits"])
     assert np.linalg.norm(gl - r) / np.linalg.norm(r) <= 1e-2
-    assert rel_l2_rows(gl, r).max() <= 1.5e-2
+    _within_storage_model(shape, weights, x, k, r, gl)
     _decisions_ok(io, ref, x, gpu_logits=gl, min_checked=B // 2)
 
 
