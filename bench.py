@@ -1,17 +1,29 @@
 #!/usr/bin/env python3
 """Benchmark of the batched speculative verify step on one MI355X.
 
-Workload: one Llama-3-8B-shaped decoder layer plus the LM head (bf16,
+Headline workload: one Llama-3-8B-shaped decoder layer plus the LM head (bf16,
 random-init N(0, 0.02)), context 1024 for every sequence, KV block 16, draft
-distributions softmax(N(0, 2^2)) -- the small-batch, memory-bound regime.  A
-timed step is the whole hot path: the verify step (embedding, norms, GEMMs,
-RoPE, paged verify attention, LM head, acceptance) and the KV append of the
-accepted rows; the cache's context lengths are restored after each step so
-every step sees the same state.
+distributions softmax(N(0, 2^2)), B=8 sequences with k=5 drafts -- the
+small-batch, memory-bound regime.  A timed step is the whole hot path: the
+verify step (embedding, norms, GEMMs, RoPE, paged verify attention, LM head,
+acceptance) and the KV append of the accepted rows; every step starts from the
+same cache state.
 
-Prints one JSON line: verified tokens/s at the headline point B=8, k=5, the
-(B, k) cost table of the grid B in {1,2,4,8} x k in {0..5}, the LM-head
-GEMM's roofline fraction, and the CPU oracle timed on the host as a baseline.
+Prints one JSON line with:
+* value: verified tokens/s at the headline point (B * (k+1) per step time);
+* roofline: the LM-head kernel as it runs inside the step (folded final norm,
+  softmax-statistics epilogue, the step's own activations), timed with HIP
+  events around its launch on the library's stream (nightjar_profile_*);
+* kernels: every kernel class of the headline step with its time and roofline
+  fraction;
+* grid: the (B, k) cost table of the small-batch grid B in {1,2,4,8} x k in {0..5};
+* large_batch: B in {64, 128} x k in {3, 4, 5} of the same layer with beta-mixed
+  drafts (beta 0.7), contexts lognormal (median 768, clipped to [128, 2048]):
+  step time, step roofline fraction, and the GEMM kernels' fraction of the bf16
+  MFMA peak (from the in-step kernel times);
+* llama8b_32layer: the 32-layer 8B-shaped stack at B=64, k=4 (contexts lognormal,
+  median 1024, clipped to [128, 4096]);
+* cpu_baseline: the CPU oracle timed on the host at the headline workload.
 """
 import argparse
 import json
@@ -49,22 +61,195 @@ def measured_traffic(M):
 
 
 # --------------------------------------------------------------------------
-# Report mode: cost table of the large-batch / full-depth configurations
+# shared pieces
 # --------------------------------------------------------------------------
-def report(args):
-    """Time the verify step over a workload's (B, k) grid and print one JSON
-    line with the cost table.  Inputs are generated on the GPU with torch's
-    seeded generator (same distributions as the CPU generator, not the same
-    bits: these runs are timed, not checked; the parity tests use the CPU
-    generator).  Drafts follow the beta-mixed draft model,
-    q_i = softmax(beta * l_i + (1 - beta) * N(0, 4)), with the target logits l_i
-    of a device pre-pass over the window."""
+class StepInputs:
+    """A step's device inputs and outputs (the fields the device helpers read)."""
+
+
+def device_model(shape, seed):
+    """Random-init weights generated on the device (torch's seeded generator)."""
+    import torch
+
+    from paper_2512_22420_amd import workload as W
+    from paper_2512_22420_amd.device import DeviceModel
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    w = W.device_weights(shape, gen)
+    model = DeviceModel(shape, w)
+    del w
+    torch.cuda.empty_cache()
+    return model
+
+
+def device_case(model, shape, ctx, k, k_max, beta, seed, ws):
+    """Cache with contexts `ctx` (pages generated on the device) and a step's
+    inputs with beta-mixed drafts, q_i = softmax(beta * l_i + (1 - beta) * N(0, 4)),
+    l_i the target logits of window row i from a causal pre-pass through the
+    step itself (these runs are timed, not checked)."""
+    import torch
+
+    from paper_2512_22420_amd import workload as W
+    from paper_2512_22420_amd.device import DeviceCache, verify
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    B = len(ctx)
+    table, num_blocks, max_blocks = W.make_block_table(shape, ctx, k_max, seed=seed)
+    kp, vp = W.device_pages(shape, num_blocks, gen)
+    cache = DeviceCache({"k_pages": kp, "v_pages": vp, "block_table": torch.from_numpy(table).cuda(),
+                         "context_lens": torch.from_numpy(np.asarray(ctx, np.int32)).cuda(),
+                         "num_blocks": num_blocks})
+    cache.max_blocks = max_blocks
+    io = StepInputs()
+    io.B, io.k = B, k
+    V = shape.vocab
+    io.last_tokens = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
+    io.uniforms = torch.rand((B, k + 1), generator=gen, device="cuda")
+    io.accepted_len = torch.zeros(B, dtype=torch.int32, device="cuda")
+    io.next_tokens = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+    io.draft_tokens = torch.zeros((B, k), dtype=torch.int32, device="cuda") if k else None
+    io.draft_probs = torch.full((B, k, V), 1.0 / V, device="cuda") if k else None
+    io.logits = torch.empty((B, k + 1, V), dtype=torch.float32, device="cuda") if k else None
+    for i in range(k):
+        verify(model, cache, io, ws)
+        z = beta * io.logits[:, i, :] + (1.0 - beta) * 2.0 * torch.randn((B, V), generator=gen, device="cuda")
+        q = torch.softmax(z, dim=-1)
+        io.draft_probs[:, i] = q
+        io.draft_tokens[:, i] = torch.multinomial(q, 1, generator=gen).squeeze(1).to(torch.int32)
+    io.logits = None
+    return cache, io
+
+
+def kernel_table(shape, B, k, ctx, prof, steps):
+    """Per kernel class: time per step, its algorithmic bytes / FLOPs per step
+    and the fraction of the roofline bound (HBM 8 TB/s, bf16 MFMA 2.5 PF/s)."""
+    from paper_2512_22420_amd import roofline as R
+    s = shape
+    M = B * (k + 1)
+    L = s.n_layers
+    HD, qkv, F, d, V = s.n_heads * s.head_dim, s.qkv_dim, s.ffn_dim, s.d_model, s.vocab
+    kv_read = sum(int(c) for c in ctx) * s.n_kv_heads * s.head_dim * 2 * 2
+    # (bytes, flops) per launch
+    algo = {
+        "qkv": (R.gemm_bytes(M, qkv, d, 2, 2), 2 * M * qkv * d),
+        "o": (R.gemm_bytes(M, d, HD, 2, 8), 2 * M * d * HD),
+        "gate_up": (R.gemm_bytes(M, 2 * F, d, 2, 0) + M * F * 2, 2 * M * 2 * F * d),
+        "down": (R.gemm_bytes(M, d, F, 2, 8), 2 * M * d * F),
+        "lm_head": (R.lm_head_bytes(s, M), 2 * M * V * d),
+        "attention": (kv_read + M * HD * 2 * 2, 4 * (k + 1) * HD * sum(int(c) + (k + 2) / 2 for c in ctx)),
+        "accept": (2 * B * V * 4 + B * k * 8, 0),
+    }
+    out = {}
+    for name, (us, n) in prof.items():
+        if n == 0:
+            continue
+        row = {"us_per_launch": round(us, 2), "launches_per_step": round(n / steps, 2),
+               "us_per_step": round(us * n / steps, 2)}
+        if name in algo:
+            by, fl = algo[name]
+            t_hbm, t_mfma = by / R.HBM_BYTES_PER_S, fl / R.BF16_MFMA_FLOPS
+            row["bound"] = "mfma" if t_mfma > t_hbm else "hbm"
+            row["gb_s"] = round(by / (us * 1e-6) / 1e9, 1)
+            if fl:
+                row["tflop_s"] = round(fl / (us * 1e-6) / 1e12, 1)
+            row["frac"] = round(max(t_hbm, t_mfma) / (us * 1e-6), 3)
+        out[name] = row
+    return out
+
+
+def profiled(run_step, steps):
+    """Mean in-step kernel times over `steps` steps (HIP events around each
+    launch site inside the library)."""
     import torch
 
     from paper_2512_22420_amd import binding as nb
+    torch.cuda.synchronize()
+    nb.profile_enable(True)
+    for _ in range(steps):
+        run_step()
+    torch.cuda.synchronize()
+    prof = nb.profile_read()
+    nb.profile_enable(False)
+    return prof
+
+
+def gemm_mfma_frac(shape, B, k, prof, steps):
     from paper_2512_22420_amd import roofline as R
+    M = B * (k + 1)
+    flops = 2 * M * (shape.n_layers * R.layer_params(shape) + shape.vocab * shape.d_model)
+    us = sum(prof[n][0] * prof[n][1] for n in ("qkv", "o", "gate_up", "down", "lm_head")) / steps
+    return round(flops / R.BF16_MFMA_FLOPS / (us * 1e-6), 3), round(us, 1)
+
+
+def timed_cold(run, reps, flush, flush_out):
+    """Median event time of `run` with the last-level cache evicted before each
+    rep (reading 640 MB: no dirty lines left to write back in the timed rep)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    ts = []
+    for _ in range(reps):
+        torch.sum(flush, dim=0, keepdim=True, out=flush_out)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        run()
+        b.record(stream)
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b) * 1e3)
+    return float(np.median(ts))
+
+
+def large_point(model, shape, B, k, ctx, ws, beta, seed, reps, flush, flush_out, label):
+    """One (B, k) point with beta-mixed drafts: cold verify time, in-step kernel
+    times, step roofline fraction, GEMM fraction of the MFMA peak."""
+    import torch
+
+    from paper_2512_22420_amd import roofline as R
+    from paper_2512_22420_amd.device import device_error, kv_append, verify
+    cache, io = device_case(model, shape, ctx, k, k, beta, seed, ws)
+    ctx0 = cache.context_lens.clone()  # a copy: the KV append advances cache.context_lens in place
+
+    def vstep():
+        verify(model, cache, io, ws)
+
+    def full():
+        verify(model, cache, io, ws)
+        kv_append(model, cache, io, ws)
+        cache.context_lens.copy_(ctx0)
+    for _ in range(2):
+        full()
+    torch.cuda.synchronize()
+    assert device_error(ws) == 0, f"device error at {label}"
+    t_us = timed_cold(vstep, reps, flush, flush_out)
+    t_step = timed_cold(full, reps, flush, flush_out)
+    psteps = 3
+    prof = profiled(vstep, psteps)
+    acc = io.accepted_len.cpu().numpy()
+    mp = R.step_model(shape, B, k, ctx)
+    gf, gus = gemm_mfma_frac(shape, B, k, prof, psteps)
+    row = {"B": B, "k": k, "M": B * (k + 1), "beta": beta, "verify_us": round(t_us, 1), "step_us": round(t_step, 1),
+           "verified_tok_s": round(B * (k + 1) / (t_us * 1e-6)),
+           "goodput_tok_s": round(float((acc + 1).sum()) / (t_us * 1e-6)),
+           "acceptance": round(float(acc.sum()) / (B * k), 3) if k else None,
+           "roofline_us": round(mp["t_roof_s"] * 1e6, 1), "roofline_frac": round(mp["t_roof_s"] * 1e6 / t_us, 3),
+           "gemm_us_in_step": gus, "gemm_mfma_frac": gf,
+           "kernels": kernel_table(shape, B, k, ctx, prof, psteps), "ctx_mean": round(float(np.mean(ctx)), 1)}
+    log(f"{label} B={B} k={k}: verify {t_us:.1f} us (step {t_step:.1f}), roofline {row['roofline_frac']:.3f}, "
+        f"GEMMs {gus:.1f} us at {gf:.3f} of MFMA peak, acceptance {row['acceptance']}")
+    del cache, io
+    torch.cuda.empty_cache()
+    return row
+
+
+# --------------------------------------------------------------------------
+# Report mode: the full (B, k) cost table of another configuration
+# --------------------------------------------------------------------------
+def report(args):
+    """Time the verify step over a workload's whole (B, k) grid and print one
+    JSON line with the cost table (inputs generated on the device)."""
+    import torch
+
     from paper_2512_22420_amd import workload as W
-    from paper_2512_22420_amd.device import DeviceCache, DeviceModel, Workspace, device_error, kv_append, verify
+    from paper_2512_22420_amd.device import Workspace
 
     wl = W.WORKLOADS[args.workload]
     shape = wl.shape
@@ -74,142 +259,18 @@ def report(args):
         grid = [g for g in grid if g in keep]
     betas = [float(b) for b in args.beta.split(",")]
     torch.cuda.set_device(0)
-    stream = torch.cuda.current_stream()
-    gen = torch.Generator(device="cuda")
-    gen.manual_seed(0)
-
-    def normal_bf16(shape_, std):
-        out = torch.empty(shape_, dtype=torch.bfloat16, device="cuda")
-        flat = out.view(-1)
-        step = 1 << 26
-        for i in range(0, flat.numel(), step):  # bounded fp32 temporaries
-            n = min(step, flat.numel() - i)
-            flat[i:i + n] = (torch.randn(n, generator=gen, device="cuda") * std).to(torch.bfloat16)
-        return out.view(torch.int16)
-
     t0 = time.time()
-    ones = torch.ones(shape.d_model, dtype=torch.bfloat16, device="cuda").view(torch.int16)
-    w = {"embed": normal_bf16((shape.vocab, shape.d_model), 0.02),
-         "lm_head": normal_bf16((shape.vocab, shape.d_model), 0.02), "final_norm": ones, "layers": []}
-    for _ in range(shape.n_layers):
-        w["layers"].append({"attn_norm": ones, "ffn_norm": ones,
-                            "w_qkv": normal_bf16((shape.qkv_dim, shape.d_model), 0.02),
-                            "w_o": normal_bf16((shape.d_model, shape.n_heads * shape.head_dim), 0.02),
-                            "w_gate_up": normal_bf16((2 * shape.ffn_dim, shape.d_model), 0.02),
-                            "w_down": normal_bf16((shape.d_model, shape.ffn_dim), 0.02)})
-    model = DeviceModel(shape, w)
-    torch.cuda.synchronize()
+    model = device_model(shape, 0)
     log(f"{wl.name}: weights generated on the device in {time.time() - t0:.1f} s")
-    B_max = max(B for B, _ in grid)
-    k_max = max(k for _, k in grid)
-    ws = Workspace(shape, B_max, k_max)
-    s = stream.cuda_stream
-
-    class IO:
-        pass
-
+    ws = Workspace(shape, max(B for B, _ in grid), max(k for _, k in grid))
+    flush = torch.zeros(640 * 2 ** 20 // 4, dtype=torch.float32, device="cuda")
+    flush_out = torch.zeros(1, dtype=torch.float32, device="cuda")
     rows = []
     for (B, k) in grid:
         ctx = wl.ctx(B, seed=0)
-        table, num_blocks, max_blocks = W.make_block_table(shape, ctx, k_max, seed=0)
-        c = {"k_pages": [normal_bf16((num_blocks, shape.n_kv_heads, 16, shape.head_dim), 0.5)
-                         for _ in range(shape.n_layers)],
-             "v_pages": [normal_bf16((num_blocks, shape.n_kv_heads, shape.head_dim, 16), 0.5)
-                         for _ in range(shape.n_layers)],
-             "block_table": torch.from_numpy(table).cuda(), "context_lens": torch.from_numpy(ctx).cuda(),
-             "num_blocks": num_blocks}
-        cache = DeviceCache(c)
-        cache.max_blocks = max_blocks
-        ctx0 = cache.context_lens.clone()
         for beta in (betas if k else [None]):
-            io = IO()
-            io.B, io.k = B, k
-            io.last_tokens = torch.randint(0, shape.vocab, (B,), generator=gen, device="cuda", dtype=torch.int32)
-            io.uniforms = torch.rand((B, k + 1), generator=gen, device="cuda")
-            io.accepted_len = torch.zeros(B, dtype=torch.int32, device="cuda")
-            io.next_tokens = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
-            io.draft_tokens = torch.zeros((B, k), dtype=torch.int32, device="cuda") if k else None
-            io.draft_probs = torch.full((B, k, shape.vocab), 1.0 / shape.vocab, device="cuda") if k else None
-            io.logits = torch.empty((B, k + 1, shape.vocab), dtype=torch.float32, device="cuda") if k else None
-            for i in range(k):  # beta-mixed drafts from a causal pre-pass
-                verify(model, cache, io, ws)
-                z = beta * io.logits[:, i, :] + (1.0 - beta) * 2.0 * torch.randn(
-                    (B, shape.vocab), generator=gen, device="cuda")
-                q = torch.softmax(z, dim=-1)
-                io.draft_probs[:, i] = q
-                io.draft_tokens[:, i] = torch.multinomial(q, 1, generator=gen).squeeze(1).to(torch.int32)
-            io.logits = None
-            verify(model, cache, io, ws)
-            torch.cuda.synchronize()
-            assert device_error(ws) == 0, "device error"
-            reps = args.grid_reps
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-            tv, ts = [], []
-            for _ in range(reps):
-                ev[0].record(stream)
-                verify(model, cache, io, ws)
-                ev[1].record(stream)
-                kv_append(model, cache, io, ws)
-                ev[2].record(stream)
-                cache.context_lens.copy_(ctx0)
-                torch.cuda.synchronize()
-                tv.append(ev[0].elapsed_time(ev[1]) * 1e3)
-                ts.append(ev[0].elapsed_time(ev[2]) * 1e3)
-            assert device_error(ws) == 0, "device error"
-            acc = io.accepted_len.cpu().numpy()
-            t_us = float(np.median(tv))
-            mp = R.step_model(shape, B, k, ctx)
-            # the step's GEMMs alone, with layer 0's weights (every layer has the same shapes)
-            M = B * (k + 1)
-            x = normal_bf16((M, max(shape.d_model, shape.ffn_dim, shape.n_heads * shape.head_dim)), 1.0)
-            y = torch.zeros((M, max(shape.vocab, 2 * shape.ffn_dim, shape.qkv_dim)), dtype=torch.float32,
-                            device="cuda")
-            lw = model.layers[0]
-            gl = [(lw["w_qkv"], shape.qkv_dim, shape.d_model, nb.NJ_GEMM_STORE, shape.n_layers),
-                  (lw["w_o"], shape.d_model, shape.n_heads * shape.head_dim, nb.NJ_GEMM_RESIDUAL, shape.n_layers),
-                  (lw["w_gate_up"], 2 * shape.ffn_dim, shape.d_model, nb.NJ_GEMM_SWIGLU, shape.n_layers),
-                  (lw["w_down"], shape.d_model, shape.ffn_dim, nb.NJ_GEMM_RESIDUAL, shape.n_layers),
-                  (model.lm_head, shape.vocab, shape.d_model, nb.NJ_GEMM_STORE, 1)]
-            gemm_us = 0.0
-            for wt, N, K, epi, mult in gl:
-                n = nb.gemm_workspace_bytes(nb.NJ_BF16, M, N, K, epi)
-                gws = torch.empty(n, dtype=torch.uint8, device="cuda")
-                nb.workspace_init(gws.data_ptr(), n, s)
-                # the tiled kernel's inputs in the k-blocked layout, as the step writes them
-                flag = nb.NJ_GEMM_KBLOCKED
-                call = lambda: nb.gemm(nb.NJ_BF16, x.data_ptr(), wt.data_ptr(), y.data_ptr(), M, N, K, epi | flag,
-                                       gws.data_ptr(), n, s)
-                try:
-                    call()
-                except nb.NightjarError:  # a streaming-kernel plan: row-major x
-                    flag = 0
-                    call()
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-                for _ in range(5):
-                    call()
-                e1.record(stream)
-                torch.cuda.synchronize()
-                gemm_us += e0.elapsed_time(e1) / 5 * 1e3 * mult
-            del x, y
-            gemm_roof_us = max(mp["weight_bytes"] / R.HBM_BYTES_PER_S, mp["gemm_flops"] / R.BF16_MFMA_FLOPS) * 1e6
-            row = {"B": B, "k": k, "M": M, "beta": beta, "verify_us": round(t_us, 1),
-                   "step_us": round(float(np.median(ts)), 1),
-                   "verified_tok_s": round(M / (t_us * 1e-6)),
-                   "goodput_tok_s": round(float((acc + 1).sum()) / (t_us * 1e-6)),
-                   "acceptance": round(float(acc.sum()) / (B * k), 3) if k else None,
-                   "roofline_us": round(mp["t_roof_s"] * 1e6, 1),
-                   "roofline_frac": round(mp["t_roof_s"] * 1e6 / t_us, 3),
-                   "gemm_us": round(gemm_us, 1), "gemm_roofline_us": round(gemm_roof_us, 1),
-                   "gemm_mfma_frac": round(mp["gemm_flops"] / R.BF16_MFMA_FLOPS * 1e6 / gemm_us, 3),
-                   "gemm_share": round(gemm_us / t_us, 3),
-                   "kv_gb": round(mp["kv_bytes"] / 1e9, 3), "ctx_mean": round(float(np.mean(ctx)), 1)}
-            rows.append(row)
-            log(f"{wl.name} B={B} k={k} beta={beta}: verify {t_us:.1f} us, step {row['step_us']} us, "
-                f"{row['verified_tok_s']} tok/s, roofline {row['roofline_us']} us ({row['roofline_frac']:.2f}), "
-                f"GEMMs {gemm_us:.1f} us at {row['gemm_mfma_frac']:.2f} of MFMA peak, acceptance {row['acceptance']}")
-        del cache, c
-        torch.cuda.empty_cache()
+            rows.append(large_point(model, shape, B, k, ctx, ws, beta if beta is not None else 0.0, 0,
+                                    args.grid_reps, flush, flush_out, wl.name))
     print(json.dumps({"report": wl.name, "unit": "verified tokens/s", "dtype": "bf16",
                       "data": "synthetic, generated on the device (torch seeded generator)", "grid": rows}),
           flush=True)
@@ -220,15 +281,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--grid-reps", type=int, default=30)
+    ap.add_argument("--grid-reps", type=int, default=20)
     ap.add_argument("--no-grid", action="store_true")
+    ap.add_argument("--no-large", action="store_true", help="skip the large-batch and 32-layer points")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--B", type=int, default=8)
     ap.add_argument("--k", type=int, default=5)
-    ap.add_argument("--calib-copy", action="store_true",
-                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--workload", default="llama8b-layer-small-batch",
-                    help="another workload prints its (B, k) cost table instead of the headline line: "
+                    help="another workload prints its whole (B, k) cost table instead of the headline line: "
                          "llama8b-layer-large-batch, llama8b-32layer, qwen7b-28layer")
     ap.add_argument("--points", default="", help="report mode: only these grid points, e.g. 64x4,128x5")
     ap.add_argument("--beta", default="0.7", help="report mode: beta(s) of the beta-mixed draft model")
@@ -238,14 +298,11 @@ def main():
               "across GPUs without any exchange, which this single-GPU build does not implement.", file=sys.stderr)
         sys.exit(2)
     if args.workload != "llama8b-layer-small-batch":
-        if args.grid_reps == 30:
-            args.grid_reps = 10
         report(args)
         return
 
     import torch
 
-    from paper_2512_22420_amd import binding as nb
     from paper_2512_22420_amd import roofline as R
     from paper_2512_22420_amd import workload as W
     from paper_2512_22420_amd.device import DeviceCache, DeviceModel, StepIO, Workspace, device_error, kv_append, verify
@@ -269,12 +326,7 @@ def main():
         cache = DeviceCache(c)
         io = StepIO(shape, d, keep_logits=False)
         ctx0 = cache.context_lens.clone()
-        return c, d, cache, io, ctx0
-
-    def step(cache, io, ctx0):
-        verify(model, cache, io, ws)
-        kv_append(model, cache, io, ws)
-        cache.context_lens.copy_(ctx0)
+        return cache, io, ctx0
 
     # ---------------- headline: K timed steps at (B, k) ----------------
     # Every step starts from the same state: each one gets its own copy of the
@@ -282,7 +334,7 @@ def main():
     # timed region holds exactly verify_step + kv_append per step; the pages
     # the append writes are rewritten with the same values each step.
     B, k = args.B, args.k
-    _, _, cache, io, ctx0 = setup(B, k)
+    cache, io, ctx0 = setup(B, k)
     ctx_bufs = [ctx0.clone() for _ in range(args.warmup + args.steps)]
     for i in range(args.warmup):
         cache.context_lens = ctx_bufs[i]
@@ -301,103 +353,99 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms_total = ev0.elapsed_time(ev1)
-    ms_per_step = ms_total / args.steps
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
     assert all(torch.equal(c, ctx_bufs[-1]) for c in ctx_bufs[args.warmup:]), "steps diverged"
     cache.context_lens = ctx0
-    acc = io.accepted_len.cpu().numpy()
     verified = B * (k + 1)
     value = verified / (ms_per_step / 1e3)
     log(f"headline B={B} k={k}: {ms_per_step * 1e3:.1f} us/step, {value:.0f} verified tok/s (wall {wall:.3f} s)")
     model_pt = R.step_model(shape, B, k, [1024] * B)
 
-    # ---------------- dominant kernel: the LM-head GEMM ----------------
+    # ---------------- the headline step's kernels, timed inside the step ----------------
     M = B * (k + 1)
-    x = torch.zeros((M, shape.d_model), dtype=torch.int16, device="cuda")
-    y = torch.empty((M, shape.vocab), dtype=torch.float32, device="cuda")
-    s = stream.cuda_stream
-    gws_n = nb.gemm_workspace_bytes(nb.NJ_BF16, M, shape.vocab, shape.d_model, nb.NJ_GEMM_STORE)
-    gws = torch.empty(gws_n, dtype=torch.uint8, device="cuda")
-    nb.workspace_init(gws.data_ptr(), gws_n, s)
+    psteps = max(20, args.steps)
 
-    def lm_head():
-        nb.gemm(nb.NJ_BF16, x.data_ptr(), model.lm_head.data_ptr(), y.data_ptr(), M, shape.vocab, shape.d_model,
-                nb.NJ_GEMM_STORE, gws.data_ptr(), gws_n, s)
+    ctx_start = ctx0.clone()
 
-    for _ in range(5):
-        lm_head()
-    reps = max(20, args.steps)
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    for _ in range(reps):
-        lm_head()
-    g1.record(stream)
-    torch.cuda.synchronize()
-    lm_us = g0.elapsed_time(g1) / reps * 1e3
+    def head_step():
+        verify(model, cache, io, ws)
+        kv_append(model, cache, io, ws)
+        cache.context_lens.copy_(ctx_start)
+    prof = profiled(head_step, psteps)
+    assert device_error(ws) == 0, "device error in the profiled steps"
+    kernels = kernel_table(shape, B, k, [1024] * B, prof, psteps)
+    lm_us = prof["lm_head"][0]
     lm_bytes = R.lm_head_bytes(shape, M)
     lm_gbs = lm_bytes / (lm_us * 1e-6) / 1e9
-    log(f"lm_head gemm M={M}: {lm_us:.1f} us, {lm_gbs:.0f} GB/s")
-    roofline = {"kernel": "gemm_logits_kernel (LM head, M=%d, N=%d, K=%d)" % (M, shape.vocab, shape.d_model),
+    log(f"in-step LM head (M={M}): {lm_us:.1f} us per launch, {lm_gbs:.0f} GB/s")
+    roofline = {"kernel": "LM head inside the step: gemm_stream_kernel<kEpiLogits> (folded final RMSNorm, "
+                          "softmax-statistics epilogue), M=%d, N=%d, K=%d" % (M, shape.vocab, shape.d_model),
                 "bound": "hbm", "achieved": round(lm_gbs, 1), "peak": R.HBM_BYTES_PER_S / 1e9, "unit": "GB/s",
                 "frac": round(lm_gbs / (R.HBM_BYTES_PER_S / 1e9), 4),
                 "traffic": measured_traffic(M),
-                "algorithmic_bytes_per_launch": lm_bytes, "avg_launch_us": round(lm_us, 2)}
-    del x, y, gws
-    if args.calib_copy:
-        src = torch.empty(2 ** 28, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+                "algorithmic_bytes_per_launch": lm_bytes, "avg_launch_us": round(lm_us, 2),
+                "timing": "HIP events around the launch on the library's stream, %d steps" % psteps}
 
-    # ---------------- the (B, k) cost table ----------------
+    # ---------------- the (B, k) cost table of the small-batch grid ----------------
+    flush = torch.zeros(640 * 2 ** 20 // 4, dtype=torch.float32, device="cuda")
+    flush_out = torch.zeros(1, dtype=torch.float32, device="cuda")
     grid = []
     if not args.no_grid:
-        # cold reps: reading 640 MB evicts the 256 MB last-level cache (a read,
-        # so no dirty lines are left to be written back during the timed step)
-        flush = torch.zeros(640 * 2 ** 20 // 4, dtype=torch.float32, device="cuda")
-        flush_sum = torch.zeros(1, dtype=torch.float32, device="cuda")
         for (gB, gk) in wl.grid:
-            _, d, gcache, gio, gctx0 = setup(gB, gk)
+            gcache, gio, gctx0 = setup(gB, gk)
+
+            def gstep():
+                verify(model, gcache, gio, ws)
             for _ in range(3):
-                step(gcache, gio, gctx0)
-            times_cold, times_warm = [], []
-            for rep in range(args.grid_reps):
-                torch.sum(flush, dim=0, keepdim=True, out=flush_sum)
-                a, b2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(stream)
-                verify(model, gcache, gio, ws)
-                b2.record(stream)
-                c1, c2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                c1.record(stream)
-                verify(model, gcache, gio, ws)
-                c2.record(stream)
-                torch.cuda.synchronize()
-                times_cold.append(a.elapsed_time(b2) * 1e3)
-                times_warm.append(c1.elapsed_time(c2) * 1e3)
+                gstep()
+            t_us = timed_cold(gstep, args.grid_reps, flush, flush_out)
+            a, b2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(5):
+                gstep()
+            b2.record(stream)
+            torch.cuda.synchronize()
+            warm = a.elapsed_time(b2) / 5 * 1e3
             assert device_error(ws) == 0
             acc = gio.accepted_len.cpu().numpy()
-            t_us = float(np.median(times_cold))
             mp = R.step_model(shape, gB, gk, [1024] * gB)
-            grid.append({"B": gB, "k": gk, "verify_us": round(t_us, 1),
-                         "verify_us_warm": round(float(np.median(times_warm)), 1),
+            grid.append({"B": gB, "k": gk, "verify_us": round(t_us, 1), "verify_us_warm": round(warm, 1),
                          "verified_tok_s": round(gB * (gk + 1) / (t_us * 1e-6)),
                          "goodput_tok_s": round(float((acc + 1).sum()) / (t_us * 1e-6)),
                          "acceptance": round(float(acc.sum()) / (gB * gk), 3) if gk else None,
                          "roofline_us": round(mp["t_roof_s"] * 1e6, 1),
                          "roofline_frac": round(mp["t_roof_s"] * 1e6 / t_us, 3)})
-            log(f"grid B={gB} k={gk}: {t_us:.1f} us cold, {np.median(times_warm):.1f} us warm, "
-                f"roofline {mp['t_roof_s'] * 1e6:.1f} us")
-        del flush, flush_sum
+            log(f"grid B={gB} k={gk}: {t_us:.1f} us cold, {warm:.1f} us warm, roofline {mp['t_roof_s'] * 1e6:.1f} us")
+            del gcache, gio
+
+    # ---------------- compute-bound points: large batch, 32 layers ----------------
+    large, deep = [], None
+    if not args.no_large:
+        lwl = W.WORKLOADS["llama8b-layer-large-batch"]
+        lmodel = device_model(shape, 0)  # the same layer, weights generated on the device
+        lws = Workspace(shape, 128, 5)
+        for (lB, lk) in [(64, 3), (64, 4), (64, 5), (128, 3), (128, 4), (128, 5)]:
+            large.append(large_point(lmodel, shape, lB, lk, lwl.ctx(lB, seed=0), lws, 0.7, 1, 10, flush, flush_out,
+                                     "large-batch"))
+        del lmodel, lws
+        torch.cuda.empty_cache()
+        dwl = W.WORKLOADS["llama8b-32layer"]
+        t1 = time.time()
+        dmodel = device_model(dwl.shape, 0)
+        log(f"32-layer stack generated on the device in {time.time() - t1:.1f} s")
+        dws = Workspace(dwl.shape, 64, 4)
+        deep = large_point(dmodel, dwl.shape, 64, 4, dwl.ctx(64, seed=0), dws, 0.7, 2, 10, flush, flush_out,
+                           "32-layer")
+        del dmodel, dws
+        torch.cuda.empty_cache()
+    del flush, flush_out
 
     # ---------------- CPU baseline: the oracle on the host ----------------
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
         cores = len(os.sched_getaffinity(0))
-        blas = "unknown BLAS"
-        threads = cores
+        blas, threads = "unknown BLAS", cores
         try:
             from threadpoolctl import threadpool_info
             libs = [p for p in threadpool_info() if p.get("user_api") == "blas"]
@@ -408,9 +456,8 @@ def main():
         except ImportError:  # pragma: no cover
             pass
         # the headline configuration, repeated until at least 10 s of host work
-        cB, ck = B, k
-        c = W.make_context(shape, wl.ctx(cB, seed=0), k_max, seed=0)
-        d = W.make_drafts(shape, cB, ck, seed=0)
+        c = W.make_context(shape, wl.ctx(B, seed=0), k_max, seed=0)
+        d = W.make_drafts(shape, B, k, seed=0)
         n_steps, tc = 0, 0.0
         while tc < 10.0:
             t1 = time.perf_counter()
@@ -418,11 +465,11 @@ def main():
                                d["last_tokens"], d["draft_tokens"], d["draft_probs"], d["uniforms"])
             tc += time.perf_counter() - t1
             n_steps += 1
-        cpu = {"value": round(n_steps * cB * (ck + 1) / tc, 3), "unit": "verified tokens/s", "cores": cores,
+        cpu = {"value": round(n_steps * B * (k + 1) / tc, 3), "unit": "verified tokens/s", "cores": cores,
                "kind": "oracle", "blas": blas, "blas_threads": threads,
-               "sample": f"{n_steps} fp64 oracle verify steps at B={cB} k={ck} ctx 1024 (the headline workload), "
+               "sample": f"{n_steps} fp64 oracle verify steps at B={B} k={k} ctx 1024 (the headline workload), "
                          f"{tc:.1f} s; NumPy with {blas} on {threads} BLAS threads, {cores} cores in the affinity mask"}
-        log(f"cpu oracle: {n_steps} steps in {tc:.1f} s at B={cB} k={ck} on {threads} threads")
+        log(f"cpu oracle: {n_steps} steps in {tc:.1f} s at B={B} k={k} on {threads} threads")
 
     out = {
         "metric": "verified tokens/s per verify step over (batch,k) grid; % HBM or MFMA roofline",
@@ -436,7 +483,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (random-init N(0,0.02) weights, N(0,1)*0.5 KV pages, softmax(N(0,4)) drafts)",
+        "data": "synthetic (random-init N(0,0.02) weights, N(0,1)*0.5 KV pages, softmax(N(0,4)) drafts; "
+                "beta-mixed drafts for the large-batch and 32-layer points)",
         "config": {"workload": "llama3-8b-layer+lm_head verify step, B=%d k=%d ctx 1024 (small-batch grid)" % (B, k),
                    "B": B, "k": k, "ctx": 1024, "M": M, "d_model": shape.d_model, "vocab": shape.vocab,
                    "kv_block": 16, "step": "verify_step + kv_append"},
@@ -444,8 +492,11 @@ def main():
                           "frac": round(model_pt["t_roof_s"] * 1e3 / ms_per_step, 4),
                           "bytes": model_pt["bytes"]},
         "roofline": roofline,
+        "kernels": kernels,
         "cpu_baseline": cpu,
         "grid": grid,
+        "large_batch": large,
+        "llama8b_32layer": deep,
     }
     print(json.dumps(out), flush=True)
 

@@ -214,6 +214,31 @@ int nightjar_device_error(void* workspace, size_t workspace_bytes, void* stream)
 const char* nightjar_last_error(void);
 
 /* ---------------------------------------------------------------------------
+ * Kernel timing of the verify step, for benchmarks: while enabled, every
+ * launch site of nightjar_verify_step and nightjar_kv_append records a pair of
+ * HIP events around its kernels on the call's stream (a little host work and
+ * two event records per launch site; not for use under graph capture).
+ * nightjar_profile_read waits for the recorded events and returns the mean
+ * time per launch of one kernel class since the last nightjar_profile_enable.
+ * ------------------------------------------------------------------------- */
+enum {
+  NJ_PROF_EMBED = 0,     /* token assembly, embedding gather, first norm inputs, RoPE table */
+  NJ_PROF_QKV = 1,       /* QKV GEMM (with its RoPE and window store when the norm is folded) */
+  NJ_PROF_NORM = 2,      /* stand-alone RMSNorm kernels (windows whose norms are not folded) */
+  NJ_PROF_ROPE = 3,      /* stand-alone RoPE + window K/V store (idem)                        */
+  NJ_PROF_ATTENTION = 4, /* paged verify attention (with its split merge)                     */
+  NJ_PROF_O = 5,         /* O GEMM + residual                                                 */
+  NJ_PROF_GATE_UP = 6,   /* gate/up GEMM + SwiGLU                                             */
+  NJ_PROF_DOWN = 7,      /* down GEMM + residual                                              */
+  NJ_PROF_LM_HEAD = 8,   /* final norm (folded) + LM head + softmax statistics                */
+  NJ_PROF_ACCEPT = 9,    /* acceptance (2 or 3 kernels)                                       */
+  NJ_PROF_KV_APPEND = 10,
+  NJ_PROF_COUNT = 11
+};
+int nightjar_profile_enable(int32_t enable); /* also resets the totals */
+int nightjar_profile_read(int32_t kernel, double* mean_us, int64_t* launches);
+
+/* ---------------------------------------------------------------------------
  * Stage entry points: single stages of the verify step, with the kernels the
  * step uses, for stage-level parity tests and kernel timing.
  * ------------------------------------------------------------------------- */

@@ -103,6 +103,8 @@ _SIGS = {
                                                  ctypes.POINTER(_i32), _vp, ctypes.POINTER(_i32)]),
     "nightjar_kv_migrate": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(KvCache), _vp, _vp, _i32, _vp,
                                            _vp]),
+    "nightjar_profile_enable": (ctypes.c_int, [_i32]),
+    "nightjar_profile_read": (ctypes.c_int, [_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
     "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
@@ -318,6 +320,24 @@ class Planner:
         m, n = ctypes.c_double(), ctypes.c_int64()
         _check(lib().nightjar_planner_arm(self._p, B, gamma, ctypes.byref(m), ctypes.byref(n)))
         return m.value, n.value
+
+
+PROF_KERNELS = ("embed", "qkv", "norm", "rope", "attention", "o", "gate_up", "down", "lm_head", "accept",
+                "kv_append")
+
+
+def profile_enable(on: bool) -> None:
+    _check(lib().nightjar_profile_enable(int(on)))
+
+
+def profile_read() -> dict:
+    """{kernel class: (mean us per launch, launches)} since profile_enable."""
+    out = {}
+    for i, name in enumerate(PROF_KERNELS):
+        m, n = ctypes.c_double(), ctypes.c_int64()
+        _check(lib().nightjar_profile_read(i, ctypes.byref(m), ctypes.byref(n)))
+        out[name] = (m.value, n.value)
+    return out
 
 
 def header_functions(header_path: str):

@@ -7,6 +7,7 @@
 #include <mutex>
 #include <string>
 #include <unordered_map>
+#include <vector>
 
 #include "../../include/nightjar.h"
 #include "kernels.h"
@@ -205,6 +206,58 @@ void* g_scratch_ptr[kMaxDevices] = {};
 
 int accept_noalloc_scratch(void** out);
 
+// Kernel timing of the verify step (nightjar_profile_*): while enabled, each
+// launch site of a step records a pair of HIP events on the step's stream;
+// reading synchronises the recorded pairs and accumulates their times per
+// kernel class.  Event pairs are reused.
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_free;
+std::vector<ProfRec> g_prof_pending;
+double g_prof_us[NJ_PROF_COUNT] = {};
+int64_t g_prof_n[NJ_PROF_COUNT] = {};
+
+struct ProfScope {
+  int cls;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  ProfScope(int c, hipStream_t st) : cls(c), s(st) {
+    if (!g_prof_on) return;
+    std::lock_guard<std::mutex> g(g_prof_mu);
+    if (!g_prof_free.empty()) {
+      a = g_prof_free.back().first;
+      b = g_prof_free.back().second;
+      g_prof_free.pop_back();
+    } else if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+      a = b = nullptr;
+      return;
+    }
+    if (hipEventRecord(a, s) != hipSuccess) a = nullptr;
+  }
+  ~ProfScope() {
+    if (!a || !b) return;
+    std::lock_guard<std::mutex> g(g_prof_mu);
+    if (hipEventRecord(b, s) == hipSuccess) g_prof_pending.push_back(ProfRec{cls, a, b});
+    else g_prof_free.emplace_back(a, b);
+  }
+};
+
+void prof_drain() {  // caller holds g_prof_mu
+  for (const ProfRec& r : g_prof_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      g_prof_us[r.cls] += ms * 1e3;
+      ++g_prof_n[r.cls];
+    }
+    g_prof_free.emplace_back(r.a, r.b);
+  }
+  g_prof_pending.clear();
+}
+
 struct StepRecord {
   int B, k, n_layers;
 };
@@ -321,9 +374,10 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   const int nsplit = bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1;
 
   hipError_t e;
-#define NJ_TRY(call, what)                   \
-  do {                                       \
-    e = (call);                              \
+#define NJ_TRY(cls, call, what)                    \
+  do {                                             \
+    ProfScope prof_(cls, s);                       \
+    e = (call);                                    \
     if (e != hipSuccess) return hip_fail(e, what); \
   } while (0)
 
@@ -347,11 +401,11 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   const GemmNorm scale_in{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, nullptr};
 
   if (fused)
-    NJ_TRY(launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
+    NJ_TRY(NJ_PROF_EMBED, launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
                                d.vocab, err, context_lens, d.rope_theta, reinterpret_cast<float*>(ws + L.rope_cs), s),
            "embed");
   else
-    NJ_TRY(launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
+    NJ_TRY(NJ_PROF_EMBED, launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
                              d.vocab, d.rms_eps, err, s, kb_qkv),
            "embed");
   for (int l = 0; l < d.n_layers; ++l) {
@@ -363,12 +417,12 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
     if (fused) {  // RoPE and the window store in the QKV GEMM's epilogue
       const QkvRope rope{context_lens, T, d.n_heads, d.n_kv_heads, reinterpret_cast<const float*>(ws + L.rope_cs), q,
                          wk, wv, snap, acnt};
-      NJ_TRY(launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiQkvRope, scale_in, gcnt, gpart, s, &rope),
+      NJ_TRY(NJ_PROF_QKV, launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiQkvRope, scale_in, gcnt, gpart, s, &rope),
              "qkv gemm");
     } else {
-      if (l > 0) NJ_TRY(launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s, kb_qkv), "attn_norm");
-      NJ_TRY(launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb_qkv), "qkv gemm");
-      NJ_TRY(launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
+      if (l > 0) NJ_TRY(NJ_PROF_NORM, launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s, kb_qkv), "attn_norm");
+      NJ_TRY(NJ_PROF_QKV, launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb_qkv), "qkv gemm");
+      NJ_TRY(NJ_PROF_ROPE, launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
                                 wk, wv, snap, acnt, s),
              "rope");
     }
@@ -376,22 +430,22 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),
                 reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, o, err, kb_o};
-    NJ_TRY(launch_attention(aa, s), "attention");
+    NJ_TRY(NJ_PROF_ATTENTION, launch_attention(aa, s), "attention");
     const void* g_next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : w->final_norm;
     if (fused) {
       const GemmNorm to_ffn{nullptr, 0, 0.f, lw.ffn_norm, x, ssq, nullptr};
-      NJ_TRY(launch_gemm_norm(o, lw.w_o, h, M, d.d_model, HD, kEpiResidualNorm, to_ffn, gcnt, gpart, s), "o gemm");
-      NJ_TRY(launch_gemm_norm(x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, scale_in, gcnt, gpart, s),
+      NJ_TRY(NJ_PROF_O, launch_gemm_norm(o, lw.w_o, h, M, d.d_model, HD, kEpiResidualNorm, to_ffn, gcnt, gpart, s), "o gemm");
+      NJ_TRY(NJ_PROF_GATE_UP, launch_gemm_norm(x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, scale_in, gcnt, gpart, s),
              "gate_up gemm");
       const GemmNorm to_next{nullptr, 0, 0.f, g_next, x, ssq, nullptr};
-      NJ_TRY(launch_gemm_norm(act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidualNorm, to_next, gcnt, gpart, s),
+      NJ_TRY(NJ_PROF_DOWN, launch_gemm_norm(act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidualNorm, to_next, gcnt, gpart, s),
              "down gemm");
     } else {
-      NJ_TRY(launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s, kb_o), "o gemm");
-      NJ_TRY(launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s, kb_gu), "ffn_norm");
-      NJ_TRY(launch_gemm(dt, x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, gcnt, gpart, s, kb_gu, kb_dn),
+      NJ_TRY(NJ_PROF_O, launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s, kb_o), "o gemm");
+      NJ_TRY(NJ_PROF_NORM, launch_rmsnorm(dt, h, lw.ffn_norm, x, M, d.d_model, d.rms_eps, s, kb_gu), "ffn_norm");
+      NJ_TRY(NJ_PROF_GATE_UP, launch_gemm(dt, x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, gcnt, gpart, s, kb_gu, kb_dn),
              "gate_up gemm");
-      NJ_TRY(launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s, kb_dn),
+      NJ_TRY(NJ_PROF_DOWN, launch_gemm(dt, act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidual, gcnt, gpart, s, kb_dn),
              "down gemm");
     }
   }
@@ -399,21 +453,21 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   float* stats = accept_stats_ptr(ws + L.stats);
   if (fused) {
     const GemmNorm lm{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, stats};
-    NJ_TRY(launch_gemm_norm(x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiLogits, lm, gcnt, gpart, s),
+    NJ_TRY(NJ_PROF_LM_HEAD, launch_gemm_norm(x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiLogits, lm, gcnt, gpart, s),
            "lm_head gemm");
     stats_ready = true;
   } else {
-    NJ_TRY(launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s, kb_lm), "final_norm");
+    NJ_TRY(NJ_PROF_NORM, launch_rmsnorm(dt, h, w->final_norm, x, M, d.d_model, d.rms_eps, s, kb_lm), "final_norm");
     if (bf)
-      NJ_TRY(launch_gemm_logits(x, w->lm_head, logits, stats, M, d.vocab, d.d_model, gcnt, gpart, s, &stats_ready,
+      NJ_TRY(NJ_PROF_LM_HEAD, launch_gemm_logits(x, w->lm_head, logits, stats, M, d.vocab, d.d_model, gcnt, gpart, s, &stats_ready,
                                 kb_lm),
              "lm_head gemm");
     else
-      NJ_TRY(launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
+      NJ_TRY(NJ_PROF_LM_HEAD, launch_gemm(dt, x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiStore, gcnt, gpart, s), "lm_head gemm");
   }
   AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, stats_ready,
                 stats_ready ? logits_stat_entries(M, d.vocab, d.d_model) : 0, accepted_len, next_tokens, err};
-  NJ_TRY(launch_accept(ac, s), "accept");
+  NJ_TRY(NJ_PROF_ACCEPT, launch_accept(ac, s), "accept");
 #undef NJ_TRY
   {
     std::lock_guard<std::mutex> g(g_mu);
@@ -448,8 +502,33 @@ int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const i
                  block_table, max_blocks, kv->num_blocks, reinterpret_cast<const int32_t*>(ws + L.ctx_snap),
                  context_lens, accepted_len, d.n_layers, B, k, d.n_kv_heads, d.head_dim,
                  reinterpret_cast<int*>(const_cast<char*>(ws) + L.err)};
-  hipError_t e = launch_kv_append(a, (hipStream_t)stream);
+  hipError_t e;
+  {
+    ProfScope prof_(NJ_PROF_KV_APPEND, (hipStream_t)stream);
+    e = launch_kv_append(a, (hipStream_t)stream);
+  }
   return e == hipSuccess ? NJ_OK : hip_fail(e, "kv_append");
+}
+
+int nightjar_profile_enable(int32_t enable) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  prof_drain();
+  for (int c = 0; c < NJ_PROF_COUNT; ++c) {
+    g_prof_us[c] = 0.0;
+    g_prof_n[c] = 0;
+  }
+  g_prof_on = enable != 0;
+  return NJ_OK;
+}
+
+int nightjar_profile_read(int32_t kernel, double* mean_us, int64_t* launches) {
+  if (kernel < 0 || kernel >= NJ_PROF_COUNT || !mean_us || !launches)
+    return fail(NJ_EINVAL, "profile_read: bad kernel class or NULL output");
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  prof_drain();
+  *launches = g_prof_n[kernel];
+  *mean_us = g_prof_n[kernel] ? g_prof_us[kernel] / (double)g_prof_n[kernel] : 0.0;
+  return NJ_OK;
 }
 
 size_t nightjar_rmsnorm_rope_workspace_bytes(const nj_model_desc* desc, int32_t B, int32_t k) {
