@@ -185,6 +185,61 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nightjar_draft_step -- one token of the draft model's chain (Sec. 2.2: a
+ * small draft model proposes the k tokens one at a time).  The draft model is
+ * a decoder of the same family (descriptor, weights and paged cache as for the
+ * target); this is a k = 0 verify step on it: a forward of last_tokens[b] at
+ * position context_lens[b], the token drawn from its distribution p (softmax
+ * of the logits) with uniforms[b], and p itself recorded as the draft
+ * distribution q that the target's acceptance test divides by.
+ *
+ *   last_tokens   device int32 [B]; uniforms device fp32 [B] in [0, 1)
+ *   token_out     device int32: token of sequence b at token_out[b * token_stride]
+ *   probs_out     device fp32: p of sequence b at probs_out[b * probs_stride + j],
+ *                 j < vocab (probs_stride >= vocab); with strides k and k*V the
+ *                 outputs of chain position i fill column i of the target's
+ *                 draft_tokens [B][k] and draft_probs [B][k][V]
+ *   workspace     as for nightjar_verify_step with (B, 0); a following
+ *                 nightjar_kv_append with k = 0 commits the input token's KV
+ */
+int nightjar_draft_step(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv,
+                        const int32_t* block_table, int32_t max_blocks, const int32_t* context_lens,
+                        const int32_t* last_tokens, const float* uniforms, int32_t B, int32_t* token_out,
+                        int32_t token_stride, float* probs_out, int64_t probs_stride, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * nightjar_sd_step -- one whole speculative-decoding step (Sec. 2.2, Sec. 3.1:
+ * the draft proposes k tokens, the target verifies them in one forward, n
+ * accepted plus one token are committed; k = 0 is plain decoding, Sec. 4).
+ * The draft and target caches share one block table and one context-length
+ * array (a logical block holds the same 16 positions in both pools) and must
+ * be in step when k > 0.  For k > 0: k+1 draft forwards (forward i reads the
+ * previous token and draws draft i+1 with draft_uniforms[b][i]; forward k only
+ * commits draft k's KV, its draw is discarded), each followed by the draft's
+ * KV append; then the target's verify step and KV append.  After the step the
+ * draft cache holds the same committed tokens as the target's (positions past
+ * context_lens are ignored).  With k = 0 the draft does not run and its cache
+ * falls behind: re-enabling speculation then needs the draft KV rebuilt (the
+ * switching cost the planner accounts for, Sec. 5.2), which is the caller's.
+ *
+ *   context_lens     device int32 [B], in/out (advanced by accepted_len + 1)
+ *   draft_uniforms   device fp32 [B][k+1]; uniforms device fp32 [B][k+1] (the target's)
+ *   draft_tokens     device int32 [B][k], out; draft_probs device fp32 [B][k][V], out
+ *   accepted_len, next_tokens: out, as for nightjar_verify_step
+ *   target_ws        >= nightjar_workspace_bytes(target, B, k)
+ *   draft_ws         >= nightjar_sd_workspace_bytes(draft, B); both zero-filled once
+ */
+size_t nightjar_sd_workspace_bytes(const nj_model_desc* draft, int32_t B);
+int nightjar_sd_step(const nj_model_desc* target, const nj_weights* tw, const nj_kv_cache* tkv,
+                     const nj_model_desc* draft, const nj_weights* dw, const nj_kv_cache* dkv,
+                     const int32_t* block_table, int32_t max_blocks, int32_t* context_lens,
+                     const int32_t* last_tokens, const float* draft_uniforms, const float* uniforms, int32_t B,
+                     int32_t k, int32_t* draft_tokens, float* draft_probs, int32_t* accepted_len,
+                     int32_t* next_tokens, void* target_ws, size_t target_ws_bytes, void* draft_ws,
+                     size_t draft_ws_bytes, void* stream);
+
+/*
  * nightjar_kv_append -- commit the accepted window rows (Sec. 6.5: a step is
  * finalised before the next begins; rejected drafts leave no KV behind).
  *

@@ -72,6 +72,14 @@ _SIGS = {
                                             _vp, _sz, _vp]),
     "nightjar_kv_append": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(KvCache), _vp, _i32, _vp, _vp,
                                           _i32, _i32, _vp, _sz, _vp]),
+    "nightjar_draft_step": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.POINTER(KvCache),
+                                           _vp, _i32, _vp, _vp, _vp, _i32, _vp, _i32, _vp, ctypes.c_int64, _vp, _sz,
+                                           _vp]),
+    "nightjar_sd_workspace_bytes": (_sz, [ctypes.POINTER(ModelDesc), _i32]),
+    "nightjar_sd_step": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.POINTER(KvCache),
+                                        ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.POINTER(KvCache),
+                                        _vp, _i32, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp,
+                                        _sz, _vp]),
     "nightjar_device_error": (ctypes.c_int, [_vp, _sz, _vp]),
     "nightjar_last_error": (ctypes.c_char_p, []),
     "nightjar_accept": (ctypes.c_int, [ctypes.POINTER(ModelDesc), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp,
@@ -162,6 +170,30 @@ def kv_append(desc, kv, block_table, max_blocks, context_lens, accepted_len, B, 
               stream: int = 0) -> None:
     _check(lib().nightjar_kv_append(ctypes.byref(desc), ctypes.byref(kv), block_table, max_blocks, context_lens,
                                     accepted_len, B, k, workspace, workspace_nbytes, stream))
+
+
+def draft_step(desc, weights, kv, block_table, max_blocks, context_lens, last_tokens, uniforms, B, token_out,
+               token_stride, probs_out, probs_stride, workspace, workspace_nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_draft_step(ctypes.byref(desc), ctypes.byref(weights), ctypes.byref(kv), block_table,
+                                     max_blocks, context_lens, last_tokens, uniforms, B, token_out, token_stride,
+                                     probs_out, probs_stride, workspace, workspace_nbytes, stream))
+
+
+def sd_workspace_bytes(draft_desc, B) -> int:
+    n = lib().nightjar_sd_workspace_bytes(ctypes.byref(draft_desc), B)
+    if n == 0:
+        raise NightjarError(NJ_EINVAL, last_error())
+    return n
+
+
+def sd_step(tdesc, tw, tkv, ddesc, dw, dkv, block_table, max_blocks, context_lens, last_tokens, draft_uniforms,
+            uniforms, B, k, draft_tokens, draft_probs, accepted_len, next_tokens, target_ws, target_ws_nbytes,
+            draft_ws, draft_ws_nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_sd_step(ctypes.byref(tdesc), ctypes.byref(tw), ctypes.byref(tkv), ctypes.byref(ddesc),
+                                  ctypes.byref(dw), ctypes.byref(dkv), block_table, max_blocks, context_lens,
+                                  last_tokens, draft_uniforms, uniforms, B, k, draft_tokens, draft_probs,
+                                  accepted_len, next_tokens, target_ws, target_ws_nbytes, draft_ws, draft_ws_nbytes,
+                                  stream))
 
 
 def device_error(workspace: int, workspace_nbytes: int, stream: int = 0) -> int:

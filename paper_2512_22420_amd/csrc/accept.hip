@@ -329,6 +329,26 @@ __global__ __launch_bounds__(256) void accept_draw_kernel(AccK a) {
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// A draft step (k = 0): sequence b's drawn token goes to tokens[b * tstride]
+// and its distribution p_j = exp(l_j - m) / sum to probs[b * pstride + j],
+// from the row statistics accept_rows wrote (the same fp32 values the draw
+// summed).  grid (B, ceil(V / 1024)), 4 entries per thread.
+__global__ __launch_bounds__(256) void emit_draft_kernel(const float* __restrict__ logits,
+                                                         const float* __restrict__ rowstat,
+                                                         const int32_t* __restrict__ next, int V,
+                                                         int32_t* __restrict__ tokens, int tstride,
+                                                         float* __restrict__ probs, long long pstride) {
+  const int b = blockIdx.x;
+  const float m = rowstat[b * 2], inv_s = rowstat[b * 2 + 1];
+  if (blockIdx.y == 0 && threadIdx.x == 0) tokens[(size_t)b * tstride] = next[b];
+  const float* l = logits + (size_t)b * V;
+  float* p = probs + (size_t)b * pstride;
+  const int j0 = (blockIdx.y * 256 + threadIdx.x) * 4;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (j0 + e < V) p[j0 + e] = expf(l[j0 + e] - m) * inv_s;
+}
+
 }  // namespace
 
 int accept_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
@@ -341,6 +361,16 @@ size_t accept_workspace_bytes(int rows, int V) {
 }
 
 float* accept_stats_ptr(void* scratch) { return static_cast<float*>(scratch); }
+
+hipError_t launch_emit_draft(const AcceptArgs& x, int32_t* tokens, int tstride, float* probs, long long pstride,
+                             hipStream_t s) {
+  if (x.k != 0) return hipErrorInvalidValue;
+  const int rows = x.B, nch = accept_chunks(x.V);
+  const float* rowstat = reinterpret_cast<const float*>(static_cast<char*>(x.scratch) + al256((size_t)rows * nch * 2 * 4));
+  hipLaunchKernelGGL(emit_draft_kernel, dim3(x.B, (x.V + 1023) / 1024), dim3(256), 0, s, x.logits, rowstat,
+                     x.next_tokens, x.V, tokens, tstride, probs, pstride);
+  return hipGetLastError();
+}
 
 hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
   const int T = x.k + 1, rows = x.B * T, nch = accept_chunks(x.V), ntile = (x.V + kTile - 1) / kTile;

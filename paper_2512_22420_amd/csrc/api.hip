@@ -49,7 +49,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
   size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, ssq, rope_cs, qkv, q, win_k, win_v, part_o, part_ml, o, act,
-      logits, stats, gemm_part, total;
+      logits, stats, gemm_part, dacc, dnext, total;
   size_t win_layer_bytes;
 };
 
@@ -145,6 +145,8 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   L.logits = take(M * d.vocab * 4);
   L.stats = take(accept_workspace_bytes((int)M, d.vocab));
   L.gemm_part = take(part);  // split-K partials (GEMMs run one after another)
+  L.dacc = take((size_t)B * 4);   // draft step: accepted lengths (always 0) and the drawn tokens
+  L.dnext = take((size_t)B * 4);
   L.total = off;
   return L;
 }
@@ -321,11 +323,24 @@ int nightjar_device_error(void* workspace, size_t workspace_bytes, void* stream)
   return v;
 }
 
-int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv,
-                         const int32_t* block_table, int32_t max_blocks, const int32_t* context_lens,
-                         const int32_t* last_tokens, const int32_t* draft_tokens, const float* draft_probs,
-                         const float* uniforms, int32_t B, int32_t k, int32_t* accepted_len, int32_t* next_tokens,
-                         float* target_logits, void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// Outputs of a draft step (nightjar_draft_step): the drawn token and the
+// draft distribution of every sequence, written with strides into the
+// target's draft_tokens [B][k] / draft_probs [B][k][V] layout.
+struct DraftOut {
+  int32_t* tokens;
+  int32_t token_stride;
+  float* probs;
+  int64_t probs_stride;
+};
+
+int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv, const int32_t* block_table,
+                int32_t max_blocks, const int32_t* context_lens, const int32_t* last_tokens,
+                const int32_t* draft_tokens, const float* draft_probs, const float* uniforms, int32_t B, int32_t k,
+                int32_t* accepted_len, int32_t* next_tokens, float* target_logits, void* workspace,
+                size_t workspace_bytes, void* stream, const DraftOut* dout) {
   if (!desc_ok(desc)) return NJ_EINVAL;
   const nj_model_desc& d = *desc;
   if (B < 1) return fail(NJ_EINVAL, "B must be >= 1");
@@ -468,12 +483,113 @@ int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const n
   AcceptArgs ac{logits, draft_tokens, draft_probs, uniforms, B, k, d.vocab, ws + L.stats, stats_ready,
                 stats_ready ? logits_stat_entries(M, d.vocab, d.d_model) : 0, accepted_len, next_tokens, err};
   NJ_TRY(NJ_PROF_ACCEPT, launch_accept(ac, s), "accept");
+  if (dout)
+    NJ_TRY(NJ_PROF_ACCEPT, launch_emit_draft(ac, dout->tokens, dout->token_stride, dout->probs, dout->probs_stride, s),
+           "emit draft");
 #undef NJ_TRY
   {
     std::lock_guard<std::mutex> g(g_mu);
     g_steps[workspace] = StepRecord{B, k, d.n_layers};
   }
   return NJ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nightjar_verify_step(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv,
+                         const int32_t* block_table, int32_t max_blocks, const int32_t* context_lens,
+                         const int32_t* last_tokens, const int32_t* draft_tokens, const float* draft_probs,
+                         const float* uniforms, int32_t B, int32_t k, int32_t* accepted_len, int32_t* next_tokens,
+                         float* target_logits, void* workspace, size_t workspace_bytes, void* stream) {
+  return verify_impl(desc, w, kv, block_table, max_blocks, context_lens, last_tokens, draft_tokens, draft_probs,
+                     uniforms, B, k, accepted_len, next_tokens, target_logits, workspace, workspace_bytes, stream,
+                     nullptr);
+}
+
+int nightjar_draft_step(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cache* kv,
+                        const int32_t* block_table, int32_t max_blocks, const int32_t* context_lens,
+                        const int32_t* last_tokens, const float* uniforms, int32_t B, int32_t* token_out,
+                        int32_t token_stride, float* probs_out, int64_t probs_stride, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc)) return NJ_EINVAL;
+  if (B < 1) return fail(NJ_EINVAL, "B must be >= 1");
+  if (!token_out || !probs_out || !workspace) return fail(NJ_EINVAL, "a required pointer is NULL");
+  if (token_stride < 1 || probs_stride < desc->vocab)
+    return fail(NJ_EINVAL, "token_stride must be >= 1 and probs_stride >= vocab");
+  if (((uintptr_t)workspace & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+  const Layout L = layout(*desc, B, 0);
+  if (workspace_bytes < L.total) return fail(NJ_EINVAL, "workspace too small: %zu < %zu bytes", workspace_bytes, L.total);
+  char* ws = static_cast<char*>(workspace);
+  const DraftOut dout{token_out, token_stride, probs_out, probs_stride};
+  return verify_impl(desc, w, kv, block_table, max_blocks, context_lens, last_tokens, nullptr, nullptr, uniforms, B, 0,
+                     reinterpret_cast<int32_t*>(ws + L.dacc), reinterpret_cast<int32_t*>(ws + L.dnext), nullptr,
+                     workspace, workspace_bytes, stream, &dout);
+}
+
+size_t nightjar_sd_workspace_bytes(const nj_model_desc* draft, int32_t B) {
+  if (!desc_ok(draft) || B < 1) return 0;
+  // the draft's own step workspace, then its context lengths during the
+  // chain, a scratch token and a scratch distribution for the catch-up forward
+  return layout(*draft, B, 0).total + al((size_t)B * 4) * 4 + al((size_t)B * draft->vocab * 4);
+}
+
+int nightjar_sd_step(const nj_model_desc* target, const nj_weights* tw, const nj_kv_cache* tkv,
+                     const nj_model_desc* draft, const nj_weights* dw, const nj_kv_cache* dkv,
+                     const int32_t* block_table, int32_t max_blocks, int32_t* context_lens,
+                     const int32_t* last_tokens, const float* draft_uniforms, const float* uniforms, int32_t B,
+                     int32_t k, int32_t* draft_tokens, float* draft_probs, int32_t* accepted_len,
+                     int32_t* next_tokens, void* target_ws, size_t target_ws_bytes, void* draft_ws,
+                     size_t draft_ws_bytes, void* stream) {
+  if (!desc_ok(target) || !desc_ok(draft)) return NJ_EINVAL;
+  if (target->vocab != draft->vocab) return fail(NJ_EINVAL, "draft and target vocabularies differ");
+  if (B < 1 || k < 0 || k > kMaxK) return fail(NJ_EINVAL, "bad B or k");
+  if (k > 0 && (!draft_tokens || !draft_probs || !draft_uniforms || !dw || !dkv || !draft_ws))
+    return fail(NJ_EINVAL, "k > 0 needs the draft model, its cache, workspace, uniforms and outputs");
+  const int V = target->vocab;
+  hipStream_t s = (hipStream_t)stream;
+  int rc;
+  if (k > 0) {
+    const size_t need = nightjar_sd_workspace_bytes(draft, B);
+    if (draft_ws_bytes < need) return fail(NJ_EINVAL, "draft workspace too small: %zu < %zu", draft_ws_bytes, need);
+    if (((uintptr_t)draft_ws & (kAlign - 1)) != 0) return fail(NJ_EINVAL, "workspace must be 256-byte aligned");
+    char* ws = static_cast<char*>(draft_ws);
+    const size_t base = layout(*draft, B, 0).total;
+    const size_t b4 = al((size_t)B * 4);
+    int32_t* dctx = reinterpret_cast<int32_t*>(ws + base);
+    int32_t* tok_in = reinterpret_cast<int32_t*>(ws + base + b4);
+    int32_t* tok_scratch = reinterpret_cast<int32_t*>(ws + base + 2 * b4);
+    float* u_in = reinterpret_cast<float*>(ws + base + 3 * b4);
+    float* prob_scratch = reinterpret_cast<float*>(ws + base + 4 * b4);
+    const int32_t* dacc = reinterpret_cast<const int32_t*>(ws + layout(*draft, B, 0).dacc);
+    hipError_t e = launch_copy_i32(dctx, context_lens, B, s);  // the draft cache is in step with the target's
+    if (e != hipSuccess) return hip_fail(e, "sd_step: draft context");
+    // the draft chain: forward i takes the previous token, draws draft i+1 and
+    // records q_i; forward k only commits draft k's KV (its draw is not used),
+    // so the draft cache never falls behind the target's
+    for (int i = 0; i <= k; ++i) {
+      // this forward's input token and uniform, gathered from their columns
+      e = launch_gather_u32(tok_in, i == 0 ? last_tokens : draft_tokens + (i - 1), B, i == 0 ? 1 : k, s);
+      if (e == hipSuccess)
+        e = launch_gather_u32(reinterpret_cast<int32_t*>(u_in), reinterpret_cast<const int32_t*>(draft_uniforms) + i,
+                              B, k + 1, s);
+      if (e != hipSuccess) return hip_fail(e, "sd_step: gather");
+      rc = nightjar_draft_step(draft, dw, dkv, block_table, max_blocks, dctx, tok_in, u_in, B,
+                               i < k ? draft_tokens + i : tok_scratch, i < k ? k : 1,
+                               i < k ? draft_probs + (size_t)i * V : prob_scratch, i < k ? (int64_t)k * V : (int64_t)V,
+                               draft_ws, draft_ws_bytes, stream);
+      if (rc != NJ_OK) return rc;
+      rc = nightjar_kv_append(draft, dkv, block_table, max_blocks, dctx, dacc, B, 0, draft_ws, draft_ws_bytes, stream);
+      if (rc != NJ_OK) return rc;
+    }
+  }
+  rc = nightjar_verify_step(target, tw, tkv, block_table, max_blocks, context_lens, last_tokens, draft_tokens,
+                            draft_probs, uniforms, B, k, accepted_len, next_tokens, nullptr, target_ws, target_ws_bytes,
+                            stream);
+  if (rc != NJ_OK) return rc;
+  return nightjar_kv_append(target, tkv, block_table, max_blocks, context_lens, accepted_len, B, k, target_ws,
+                            target_ws_bytes, stream);
 }
 
 int nightjar_kv_append(const nj_model_desc* desc, const nj_kv_cache* kv, const int32_t* block_table,

@@ -298,6 +298,11 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int n) {
   if (i < n) p[i] = v;
 }
 
+__global__ void copy_i32_kernel(int32_t* __restrict__ dst, const int32_t* __restrict__ src, int n, int stride) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[(size_t)i * stride];
+}
+
 // RoPE and the window K/V store for bf16 heads of 128 dims: one workgroup
 // per (sequence, head) covers the window's T rows, so the window blocks are
 // written whole (slots T..15 zero) with 8- and 16-byte stores.  Thread t:
@@ -470,6 +475,16 @@ hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t launch_copy_i32(int32_t* dst, const int32_t* src, int n, hipStream_t s) {
+  hipLaunchKernelGGL(copy_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, dst, src, n, 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_u32(int32_t* dst, const int32_t* src, int n, int stride, hipStream_t s) {
+  hipLaunchKernelGGL(copy_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, dst, src, n, stride);
+  return hipGetLastError();
 }
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s) {

@@ -209,6 +209,10 @@ int accept_chunks(int V);
 float* accept_stats_ptr(void* scratch);  // [B*T][accept_chunks(V)][2] chunk max, sum of exp
 size_t accept_workspace_bytes(int rows, int V);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+// After launch_accept of a k = 0 step: the drawn tokens to tokens[b * tstride]
+// and the distributions p = softmax(logits row) to probs[b * pstride ...].
+hipError_t launch_emit_draft(const AcceptArgs& a, int32_t* tokens, int tstride, float* probs, long long pstride,
+                             hipStream_t s);
 
 struct KvAppendArgs {
   int dtype;
@@ -227,6 +231,9 @@ struct KvAppendArgs {
 hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int n, hipStream_t s);
+hipError_t launch_copy_i32(int32_t* dst, const int32_t* src, int n, hipStream_t s);
+// dst[i] = src[i * stride] for 32-bit words, i < n.
+hipError_t launch_gather_u32(int32_t* dst, const int32_t* src, int n, int stride, hipStream_t s);
 
 // Sets the message nightjar_last_error() returns on this thread; returns code.
 int set_last_error(int code, const char* fmt, ...);
