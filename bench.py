@@ -240,6 +240,92 @@ def large_point(model, shape, B, k, ctx, ws, beta, seed, reps, flush, flush_out,
     return row
 
 
+def sd_table(tmodel, tshape, dshape, B, ctx_len, gammas, reps=10):
+    """Whole speculative-decoding steps (nightjar_sd_step: k+1 draft forwards
+    with their appends, the target's verify step and append) for each k, with
+    the draft chain and the verify step also timed alone.  The random-init
+    draft agrees with the random-init target about as often as chance, so the
+    acceptance here is near 0; goodput at the paper's acceptance rates follows
+    from the step time as (1 - a^(k+1)) / (1 - a) committed tokens per step."""
+    import torch
+
+    from paper_2512_22420_amd import binding as nb
+    from paper_2512_22420_amd import workload as W
+    from paper_2512_22420_amd.device import DeviceCache
+    dmodel = device_model(dshape, 7)
+    kmax = max(gammas)
+    ctx = np.full(B, ctx_len, np.int32)
+    table, num_blocks, max_blocks = W.make_block_table(tshape, ctx, kmax + 1, seed=3)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(3)
+    tk, tv = W.device_pages(tshape, num_blocks, gen)
+    dk, dv = W.device_pages(dshape, num_blocks, gen)
+    bt = torch.from_numpy(table).cuda()
+    ctx_dev = torch.from_numpy(ctx).cuda()
+    ctx0 = ctx_dev.clone()
+    tcache = DeviceCache({"k_pages": tk, "v_pages": tv, "block_table": bt, "context_lens": ctx_dev,
+                          "num_blocks": num_blocks})
+    dcache = DeviceCache({"k_pages": dk, "v_pages": dv, "block_table": bt, "context_lens": ctx_dev,
+                          "num_blocks": num_blocks})
+    s = torch.cuda.current_stream().cuda_stream
+    tn = nb.workspace_bytes(tmodel.desc, B, kmax)
+    tws = torch.empty(tn, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(tws.data_ptr(), tn, s)
+    dn = nb.sd_workspace_bytes(dmodel.desc, B)
+    dws = torch.empty(dn, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(dws.data_ptr(), dn, s)
+    V = tshape.vocab
+    last = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
+    rows = []
+    for k in gammas:
+        du = torch.rand((B, k + 1), generator=gen, device="cuda")
+        u = torch.rand((B, k + 1), generator=gen, device="cuda")
+        dt = torch.zeros((B, max(k, 1)), dtype=torch.int32, device="cuda")
+        dq = torch.zeros((B, max(k, 1), V), device="cuda")
+        acc = torch.zeros(B, dtype=torch.int32, device="cuda")
+        nxt = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+
+        def step():
+            ctx_dev.copy_(ctx0)
+            nb.sd_step(tmodel.desc, tmodel.c, tcache.c, dmodel.desc, dmodel.c, dcache.c, bt.data_ptr(), max_blocks,
+                       ctx_dev.data_ptr(), last.data_ptr(), du.data_ptr(), u.data_ptr(), B, k, dt.data_ptr(),
+                       dq.data_ptr(), acc.data_ptr(), nxt.data_ptr(), tws.data_ptr(), tn, dws.data_ptr(), dn, s)
+
+        def chain():
+            ctx_dev.copy_(ctx0)
+            for i in range(k + 1):
+                nb.draft_step(dmodel.desc, dmodel.c, dcache.c, bt.data_ptr(), max_blocks, ctx_dev.data_ptr(),
+                              last.data_ptr(), du.data_ptr(), B, dt.data_ptr(), max(k, 1), dq.data_ptr(),
+                              max(k, 1) * V, dws.data_ptr(), dn, s)
+        for f in (step, chain):
+            f()
+        torch.cuda.synchronize()
+        assert nb.device_error(tws.data_ptr(), tn, s) == 0 and nb.device_error(dws.data_ptr(), dn, s) == 0
+
+        def timed(f):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                f()
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / reps * 1e3
+        t_step = timed(step)
+        t_chain = timed(chain) if k else 0.0
+        a_n = acc.cpu().numpy()
+        row = {"k": k, "B": B, "sd_step_us": round(t_step, 1), "draft_forwards": k + 1 if k else 0,
+               "draft_chain_us": round(t_chain, 1), "verify_and_append_us": round(t_step - t_chain, 1),
+               "committed_tokens_s": round(float((a_n + 1).sum()) / (t_step * 1e-6)),
+               "goodput_tok_s_at_acceptance": {str(al): round(B * (1 - al ** (k + 1)) / (1 - al) / (t_step * 1e-6))
+                                               for al in (0.53, 0.69)}}
+        rows.append(row)
+        log(f"sd step B={B} k={k}: {t_step:.1f} us (draft chain {t_chain:.1f} us), "
+            f"goodput at acceptance 0.69: {row['goodput_tok_s_at_acceptance']['0.69']} tok/s")
+    del dmodel, tcache, dcache, tws, dws
+    torch.cuda.empty_cache()
+    return {"target": tshape.name, "draft": dshape.name, "ctx": ctx_len, "rows": rows}
+
+
 # --------------------------------------------------------------------------
 # Report mode: the full (B, k) cost table of another configuration
 # --------------------------------------------------------------------------
@@ -436,6 +522,8 @@ def main():
         dws = Workspace(dwl.shape, 64, 4)
         deep = large_point(dmodel, dwl.shape, 64, 4, dwl.ctx(64, seed=0), dws, 0.7, 2, 10, flush, flush_out,
                            "32-layer")
+        # whole speculative-decoding steps: the 32-layer target with a 1B-class draft
+        sd = sd_table(dmodel, dwl.shape, W.LLAMA1B_DRAFT, 8, 1024, [0, 1, 3, 5])
         del dmodel, dws
         torch.cuda.empty_cache()
     del flush, flush_out
@@ -497,6 +585,7 @@ def main():
         "grid": grid,
         "large_batch": large,
         "llama8b_32layer": deep,
+        "sd_step": sd if not args.no_large else None,
     }
     print(json.dumps(out), flush=True)
 

@@ -73,7 +73,11 @@ LLAMA8B = LLAMA8B_LAYER.with_layers(32)
 # Qwen2.5-7B-shaped stack (GQA 28/4, FFN 18944, vocab 152064).
 QWEN7B = ModelShape("qwen2.5-7b", 28, 3584, 28, 4, 128, 18944, 152064, 1e-6, 1e6, "bf16")
 
-SHAPES = {s.name: s for s in (TINY_F32, LLAMA8B_LAYER, LLAMA8B, QWEN7B)}
+# Draft model for the 8B target: Llama-3.2-1B-sized (d 2048, 16 layers, FFN 8192,
+# the target's vocabulary) with 16 heads of 128 dims (the bf16 path's head size).
+LLAMA1B_DRAFT = ModelShape("llama-1b-draft", 16, 2048, 16, 8, 128, 8192, 128256, 1e-5, 5e5, "bf16")
+
+SHAPES = {s.name: s for s in (TINY_F32, LLAMA8B_LAYER, LLAMA8B, QWEN7B, LLAMA1B_DRAFT)}
 
 
 def _rng(seed: int, *keys: int) -> np.random.Generator:
