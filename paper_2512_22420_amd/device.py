@@ -105,7 +105,26 @@ class StepIO:
         self.logits = torch.empty((B, k + 1, shape.vocab), dtype=torch.float32, device=device) if keep_logits else None
 
 
+def _expect(t: Optional[torch.Tensor], dtype, numel: int, name: str) -> None:
+    """The C ABI takes raw pointers: a tensor of another dtype or size would be
+    reinterpreted, so it is refused here."""
+    if t is None:
+        return
+    if t.dtype != dtype or t.numel() != numel or not t.is_contiguous():
+        raise TypeError(f"{name}: need a contiguous {dtype} tensor of {numel} elements, "
+                        f"got {t.dtype} {tuple(t.shape)}")
+
+
 def verify(model: DeviceModel, cache: DeviceCache, io: StepIO, ws: Workspace, stream: Optional[int] = None):
+    B, k, V = io.B, io.k, model.shape.vocab
+    _expect(io.last_tokens, torch.int32, B, "last_tokens")
+    _expect(io.draft_tokens, torch.int32, B * k, "draft_tokens")
+    _expect(io.draft_probs, torch.float32, B * k * V, "draft_probs")
+    _expect(io.uniforms, torch.float32, B * (k + 1), "uniforms")
+    _expect(io.accepted_len, torch.int32, B, "accepted_len")
+    _expect(io.next_tokens, torch.int32, B * (k + 1), "next_tokens")
+    _expect(io.logits, torch.float32, B * (k + 1) * V, "logits")
+    _expect(cache.context_lens, torch.int32, B, "context_lens")
     s = torch.cuda.current_stream().cuda_stream if stream is None else stream
     nb.verify_step(model.desc, model.c, cache.c, _ptr(cache.block_table), cache.max_blocks, _ptr(cache.context_lens),
                    _ptr(io.last_tokens), _ptr(io.draft_tokens), _ptr(io.draft_probs), _ptr(io.uniforms), io.B, io.k,

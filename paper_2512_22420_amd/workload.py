@@ -331,7 +331,7 @@ def device_normal_bf16(gen, shape_, std: float, device="cuda"):
     step = 1 << 26
     for i in range(0, flat.numel(), step):
         n = min(step, flat.numel() - i)
-        flat[i:i + n] = (torch.randn(n, generator=gen, device=device) * std).to(torch.bfloat16)
+        flat[i:i + n] = (torch.randn(n, generator=gen, device=device, dtype=torch.float32) * std).to(torch.bfloat16)
     return out.view(torch.int16)
 
 

@@ -103,11 +103,11 @@ class BigCase:
         # step inputs: all sequences on the device
         V = shape.vocab
         self.last = torch.randint(0, V, (B,), generator=gen, device=DEVICE, dtype=torch.int32)
-        self.uniforms = torch.rand((B, k + 1), generator=gen, device=DEVICE)
+        self.uniforms = torch.rand((B, k + 1), generator=gen, device=DEVICE, dtype=torch.float32)
         self.drafts = torch.zeros((B, k), dtype=torch.int32, device=DEVICE)
         self.probs = torch.empty((B, k, V), dtype=torch.float32, device=DEVICE)
         for i in range(k):
-            q = torch.softmax(2.0 * torch.randn((B, V), generator=gen, device=DEVICE), dim=-1)
+            q = torch.softmax(2.0 * torch.randn((B, V), generator=gen, device=DEVICE, dtype=torch.float32), dim=-1)
             self.probs[:, i] = q
             self.drafts[:, i] = torch.multinomial(q, 1, generator=gen).squeeze(1).to(torch.int32)
         # the checked sequences: beta-mixed drafts over the oracle's target logits

@@ -53,7 +53,7 @@ def test_draft_step_matches_oracle(shape):
     ws, n = _ws(model.desc, B, 0)
     k_t = 3  # write into column 1 of a [B][3] / [B][3][V] layout
     tok = torch.full((B, k_t), -5, dtype=torch.int32, device="cuda")
-    probs = torch.full((B, k_t, shape.vocab), -1.0, device="cuda")
+    probs = torch.full((B, k_t, shape.vocab), -1.0, device="cuda", dtype=torch.float32)
     dl, du = torch.from_numpy(last).cuda(), torch.from_numpy(u).cuda()
     nb.draft_step(model.desc, model.c, cache.c, cache.block_table.data_ptr(), cache.max_blocks,
                   cache.context_lens.data_ptr(), dl.data_ptr(), du.data_ptr(), B, tok.data_ptr() + 4, k_t,
@@ -88,7 +88,7 @@ def _sd_setup(tshape, dshape, k, B, steps, ctx):
 
 def _sd_run(mt, md, cache_t, cache_d, tws, tn, dws, dn, last, du, u, B, k, V):
     dt = torch.zeros((B, k), dtype=torch.int32, device="cuda")
-    dq = torch.zeros((B, k, V), device="cuda")
+    dq = torch.zeros((B, k, V), device="cuda", dtype=torch.float32)
     acc = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     nxt = torch.full((B, k + 1), -7, dtype=torch.int32, device="cuda")
     dl, ddu, dtu = (torch.from_numpy(a).cuda() for a in (last, du, u))

@@ -22,7 +22,16 @@ import torch
 import oracle
 from paper_2512_22420_amd import workload as W
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """The HF reference model is built in fp64; the default dtype is restored
+    afterwards so that no other module sees it (device inputs are fp32)."""
+    old = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(old)
 
 # tiny shapes: the tiny fp32 case, and a 2-layer GQA variant (4 query heads on 2 KV heads)
 SHAPES = [
