@@ -104,15 +104,15 @@ def device_case(model, shape, ctx, k, k_max, beta, seed, ws):
     io.B, io.k = B, k
     V = shape.vocab
     io.last_tokens = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
-    io.uniforms = torch.rand((B, k + 1), generator=gen, device="cuda")
+    io.uniforms = torch.rand((B, k + 1), generator=gen, device="cuda", dtype=torch.float32)
     io.accepted_len = torch.zeros(B, dtype=torch.int32, device="cuda")
     io.next_tokens = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
     io.draft_tokens = torch.zeros((B, k), dtype=torch.int32, device="cuda") if k else None
-    io.draft_probs = torch.full((B, k, V), 1.0 / V, device="cuda") if k else None
+    io.draft_probs = torch.full((B, k, V), 1.0 / V, device="cuda", dtype=torch.float32) if k else None
     io.logits = torch.empty((B, k + 1, V), dtype=torch.float32, device="cuda") if k else None
     for i in range(k):
         verify(model, cache, io, ws)
-        z = beta * io.logits[:, i, :] + (1.0 - beta) * 2.0 * torch.randn((B, V), generator=gen, device="cuda")
+        z = beta * io.logits[:, i, :] + (1.0 - beta) * 2.0 * torch.randn((B, V), generator=gen, device="cuda", dtype=torch.float32)
         q = torch.softmax(z, dim=-1)
         io.draft_probs[:, i] = q
         io.draft_tokens[:, i] = torch.multinomial(q, 1, generator=gen).squeeze(1).to(torch.int32)
@@ -278,10 +278,10 @@ def sd_table(tmodel, tshape, dshape, B, ctx_len, gammas, reps=10):
     last = torch.randint(0, V, (B,), generator=gen, device="cuda", dtype=torch.int32)
     rows = []
     for k in gammas:
-        du = torch.rand((B, k + 1), generator=gen, device="cuda")
-        u = torch.rand((B, k + 1), generator=gen, device="cuda")
+        du = torch.rand((B, k + 1), generator=gen, device="cuda", dtype=torch.float32)
+        u = torch.rand((B, k + 1), generator=gen, device="cuda", dtype=torch.float32)
         dt = torch.zeros((B, max(k, 1)), dtype=torch.int32, device="cuda")
-        dq = torch.zeros((B, max(k, 1), V), device="cuda")
+        dq = torch.zeros((B, max(k, 1), V), device="cuda", dtype=torch.float32)
         acc = torch.zeros(B, dtype=torch.int32, device="cuda")
         nxt = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
 
@@ -324,6 +324,63 @@ def sd_table(tmodel, tshape, dshape, B, ctx_len, gammas, reps=10):
     del dmodel, tcache, dcache, tws, dws
     torch.cuda.empty_cache()
     return {"target": tshape.name, "draft": dshape.name, "ctx": ctx_len, "rows": rows}
+
+
+def elastic_costs(tshape, dshape, moves=292):
+    """Costs of the elastic pool's data movement (Sec. 6.2, 6.4): the draft
+    model's weights (bf16) offloaded to pinned host memory and reloaded, on a
+    side stream, and a contraction migrating `moves` KV blocks of the 32-layer
+    target pool (the paper migrates 292 blocks)."""
+    import torch
+
+    from paper_2512_22420_amd import binding as nb
+    from paper_2512_22420_amd import roofline as R
+    from paper_2512_22420_amd import workload as W
+    from paper_2512_22420_amd.device import DeviceCache, model_desc
+    nbytes = 2 * (dshape.n_layers * R.layer_params(dshape) + 2 * dshape.vocab * dshape.d_model)
+    dev = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+    host = torch.empty(nbytes // 2, dtype=torch.int16, pin_memory=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(side)
+        fn()
+        b.record(side)
+        side.synchronize()
+        return a.elapsed_time(b) * 1e3
+    off = timed(lambda: nb.offload(dev.data_ptr(), host.data_ptr(), nbytes, side.cuda_stream))
+    rel = timed(lambda: nb.reload(host.data_ptr(), dev.data_ptr(), nbytes, side.cuda_stream))
+    del dev, host
+    # contraction: blocks [nb/2, nb/2 + moves) move to [0, moves)
+    nblk = 2 * moves + 8
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    kp, vp = W.device_pages(tshape, nblk, gen)
+    cache = DeviceCache({"k_pages": kp, "v_pages": vp, "block_table": torch.zeros((1, 1), dtype=torch.int32,
+                         device="cuda"), "context_lens": torch.zeros(1, dtype=torch.int32, device="cuda"),
+                         "num_blocks": nblk})
+    src = torch.arange(nblk // 2, nblk // 2 + moves, dtype=torch.int32, device="cuda")
+    dst = torch.arange(0, moves, dtype=torch.int32, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    desc = model_desc(tshape)
+    mig = lambda: nb.kv_migrate(desc, cache.c, src.data_ptr(), dst.data_ptr(), moves, err.data_ptr(),
+                                side.cuda_stream)
+    mig()
+    side.synchronize()
+    assert int(err.item()) == 0
+    t_mig = min(timed(mig) for _ in range(5))
+    mbytes = 2 * moves * tshape.n_layers * 2 * tshape.n_kv_heads * 16 * tshape.head_dim * 2  # read + write
+    out = {"draft_bytes": nbytes, "offload_ms": round(off / 1e3, 2), "offload_gb_s": round(nbytes / off / 1e3, 1),
+           "reload_ms": round(rel / 1e3, 2), "reload_gb_s": round(nbytes / rel / 1e3, 1),
+           "migrate_blocks": moves, "migrate_us": round(t_mig, 1),
+           "migrate_gb_s": round(mbytes / t_mig / 1e3, 1), "migrate_hbm_frac": round(mbytes / t_mig / 1e3 / 8000, 3)}
+    log(f"elastic: offload {out['offload_ms']} ms ({out['offload_gb_s']} GB/s), reload {out['reload_ms']} ms, "
+        f"migrate {moves} blocks in {t_mig:.1f} us ({out['migrate_gb_s']} GB/s)")
+    del cache, kp, vp
+    torch.cuda.empty_cache()
+    return out
 
 
 # --------------------------------------------------------------------------
@@ -524,6 +581,7 @@ def main():
                            "32-layer")
         # whole speculative-decoding steps: the 32-layer target with a 1B-class draft
         sd = sd_table(dmodel, dwl.shape, W.LLAMA1B_DRAFT, 8, 1024, [0, 1, 3, 5])
+        elastic = elastic_costs(dwl.shape, W.LLAMA1B_DRAFT)
         del dmodel, dws
         torch.cuda.empty_cache()
     del flush, flush_out
@@ -586,6 +644,7 @@ def main():
         "large_batch": large,
         "llama8b_32layer": deep,
         "sd_step": sd if not args.no_large else None,
+        "elastic": elastic if not args.no_large else None,
     }
     print(json.dumps(out), flush=True)
 

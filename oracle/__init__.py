@@ -6,4 +6,4 @@ the HIP library never does.
 from .verify_step import (accept, attention, forward_window, gather_cache, invcdf,  # noqa: F401
                           kv_append, linear, rms_norm, rope, silu, softmax, verify_step, widen,
                           window_tokens)
-from . import kv_pool, planner, spec_step  # noqa: F401
+from . import elastic, kv_pool, planner, spec_step  # noqa: F401

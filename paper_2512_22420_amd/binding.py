@@ -55,6 +55,11 @@ class PlannerBState(ctypes.Structure):
                 ("explore_bins", ctypes.c_int64)]
 
 
+class ElasticConfig(ctypes.Structure):
+    _fields_ = [("n_orig", _i32), ("n_draft", _i32), ("tau_low", _i32), ("t_persist", _i32),
+                ("reload_persist", _i32), ("max_migrate", _i32)]
+
+
 class NightjarError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"nightjar error {code}: {msg}")
@@ -113,6 +118,13 @@ _SIGS = {
                                            _vp]),
     "nightjar_profile_enable": (ctypes.c_int, [_i32]),
     "nightjar_profile_read": (ctypes.c_int, [_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
+    "nightjar_elastic_create": (_vp, [ctypes.POINTER(ElasticConfig)]),
+    "nightjar_elastic_destroy": (None, [_vp]),
+    "nightjar_elastic_step": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, ctypes.POINTER(_i32)]),
+    "nightjar_elastic_done": (ctypes.c_int, [_vp, _i32]),
+    "nightjar_elastic_state": (ctypes.c_int, [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
+    "nightjar_offload": (ctypes.c_int, [_vp, _vp, _sz, _vp]),
+    "nightjar_reload": (ctypes.c_int, [_vp, _vp, _sz, _vp]),
     "nightjar_packed_weight_elems": (_sz, [_i32, _i32]),
     "nightjar_pack_weight": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp]),
 }
@@ -302,6 +314,47 @@ def contraction_plan(block_table, free_list, k_boundary: int, k_total: int):
 
 def kv_migrate(desc, kv, src, dst, n, device_error, stream: int = 0) -> None:
     _check(lib().nightjar_kv_migrate(ctypes.byref(desc), ctypes.byref(kv), src, dst, n, device_error, stream))
+
+
+NJ_POOL_RESIDENT, NJ_POOL_OFFLOADING, NJ_POOL_OFFLOADED, NJ_POOL_EXPANDED, NJ_POOL_CONTRACTING, NJ_POOL_RELOADING = \
+    range(6)
+NJ_ACT_NONE, NJ_ACT_OFFLOAD_DRAFT, NJ_ACT_EXPAND, NJ_ACT_CONTRACT, NJ_ACT_RELOAD_DRAFT = range(5)
+
+
+class Elastic:
+    """The elastic pool controller of include/nightjar_memory.h; marshalling only."""
+
+    def __init__(self, n_orig, n_draft, tau_low, t_persist=3, reload_persist=3, max_migrate=1 << 30):
+        cfg = ElasticConfig(n_orig, n_draft, tau_low, t_persist, reload_persist, max_migrate)
+        self._e = lib().nightjar_elastic_create(ctypes.byref(cfg))
+        if not self._e:
+            raise NightjarError(NJ_EINVAL, last_error())
+
+    def __del__(self):
+        if getattr(self, "_e", None) and _LIB is not None:
+            _LIB.nightjar_elastic_destroy(self._e)
+            self._e = None
+
+    def step(self, n_free, n_waiting, speculating, live_above=0) -> int:
+        a = _i32(-1)
+        _check(lib().nightjar_elastic_step(self._e, n_free, n_waiting, int(speculating), live_above, ctypes.byref(a)))
+        return a.value
+
+    def done(self, action) -> None:
+        _check(lib().nightjar_elastic_done(self._e, action))
+
+    def state(self):
+        st, pb, ga = _i32(), _i32(), _i32()
+        _check(lib().nightjar_elastic_state(self._e, ctypes.byref(st), ctypes.byref(pb), ctypes.byref(ga)))
+        return st.value, pb.value, bool(ga.value)
+
+
+def offload(device_src, host_dst, nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_offload(device_src, host_dst, nbytes, stream))
+
+
+def reload(host_src, device_dst, nbytes, stream: int = 0) -> None:
+    _check(lib().nightjar_reload(host_src, device_dst, nbytes, stream))
 
 
 class Planner:

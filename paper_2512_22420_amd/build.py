@@ -18,7 +18,7 @@ OUT = os.path.join(HERE, "libnightjar.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "gemm.hip", "gemm_tile.hip", "attention.hip", "accept.hip", "elementwise.hip", "planner.cpp", "kv_pool.hip"]
+SOURCES = ["api.hip", "gemm.hip", "gemm_tile.hip", "attention.hip", "accept.hip", "elementwise.hip", "planner.cpp", "kv_pool.hip", "elastic.cpp"]
 
 FLAGS = ["-O3", "-std=c++20", f"--offload-arch={ARCH}", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -105,3 +105,25 @@ def test_step_after_contraction_is_bitwise_unchanged(shape, k):
     assert device_error(ws) == 0
     for l in range(shape.n_layers):
         assert torch.all(cache.k_pages[l][kb:].view(-1) == -1)
+
+
+def test_offload_reload_round_trip_on_a_side_stream():
+    """Sec. 6.2: the draft weights go to pinned host memory and back with
+    asynchronous copies on a side stream; the bytes come back unchanged."""
+    n = 48 << 20
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1)
+    src = torch.randint(-30000, 30000, (n // 2,), dtype=torch.int16, device="cuda", generator=g)
+    host = torch.empty(n // 2, dtype=torch.int16, pin_memory=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    nb.offload(src.data_ptr(), host.data_ptr(), n, side.cuda_stream)
+    side.synchronize()
+    assert torch.equal(host, src.cpu())
+    dst = torch.zeros_like(src)
+    side.wait_stream(torch.cuda.current_stream())
+    nb.reload(host.data_ptr(), dst.data_ptr(), n, side.cuda_stream)
+    side.synchronize()
+    assert torch.equal(dst, src)
+    with pytest.raises(nb.NightjarError):
+        nb.offload(0, host.data_ptr(), n, side.cuda_stream)
