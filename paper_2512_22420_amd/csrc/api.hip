@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "../../include/nightjar.h"
+#include "attn_work.h"
 #include "kernels.h"
 
 using namespace nj;
@@ -49,7 +50,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
   size_t err, gemm_cnt, ctx_snap, attn_cnt, h, x, ssq, rope_cs, qkv, q, win_k, win_v, part_o, part_ml, o, act,
-      logits, stats, gemm_part, dacc, dnext, total;
+      logits, stats, gemm_part, dacc, dnext, attn_work, total;
   size_t win_layer_bytes;
 };
 
@@ -147,6 +148,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
   L.gemm_part = take(part);  // split-K partials (GEMMs run one after another)
   L.dacc = take((size_t)B * 4);   // draft step: accepted lengths (always 0) and the drawn tokens
   L.dnext = take((size_t)B * 4);
+  L.attn_work = take(d.dtype == NJ_BF16 ? attention_work_bytes(B, d.n_kv_heads) : 0);  // built once per step
   L.total = off;
   return L;
 }
@@ -177,9 +179,9 @@ PreLayout pre_layout(const nj_model_desc& d, int B, int k) {
   return L;
 }
 
-// Workspace of nightjar_attn_verify: [error word][split arrival counters][partial o][partial (m, l)]
+// Workspace of nightjar_attn_verify: [error word][split arrival counters][partial o][partial (m, l)][work list]
 struct AttnLayout {
-  size_t err, cnt, part_o, part_ml, total;
+  size_t err, cnt, part_o, part_ml, work, total;
 };
 AttnLayout attn_layout(const nj_model_desc& d, int B, int k) {
   AttnLayout L{};
@@ -196,6 +198,7 @@ AttnLayout attn_layout(const nj_model_desc& d, int B, int k) {
                         : 0;
   L.part_o = take(pf * 4);
   L.part_ml = take((pf ? pf / (d.head_dim + 2) * 2 : 0) * 4);
+  L.work = take(d.dtype == NJ_BF16 ? attention_work_bytes(B, d.n_kv_heads) : 0);
   L.total = off;
   return L;
 }
@@ -386,7 +389,7 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   const int dt = bf ? kBF16 : kF32;
   const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
 
-  const int nsplit = bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1;
+  const int attn_wgs = bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1;
 
   hipError_t e;
 #define NJ_TRY(cls, call, what)                    \
@@ -415,13 +418,18 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   const int nt = (d.d_model + 127) / 128;
   const GemmNorm scale_in{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, nullptr};
 
+  // the embedding kernel carries one more workgroup that builds the
+  // attention's work list for every layer of the step (bf16)
+  const AttnPlan plan{context_lens, reinterpret_cast<AttnWork*>(ws + L.attn_work), B, d.n_kv_heads, T, max_blocks,
+                      attn_wgs};
+  const AttnPlan* pl = bf ? &plan : nullptr;
   if (fused)
     NJ_TRY(NJ_PROF_EMBED, launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
-                               d.vocab, err, context_lens, d.rope_theta, reinterpret_cast<float*>(ws + L.rope_cs), s),
+                               d.vocab, err, context_lens, d.rope_theta, reinterpret_cast<float*>(ws + L.rope_cs), s, pl),
            "embed");
   else
     NJ_TRY(NJ_PROF_EMBED, launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
-                             d.vocab, d.rms_eps, err, s, kb_qkv),
+                             d.vocab, d.rms_eps, err, s, kb_qkv, pl),
            "embed");
   for (int l = 0; l < d.n_layers; ++l) {
     const nj_layer_weights& lw = w->layers[l];
@@ -444,7 +452,8 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
                 reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml),
-                reinterpret_cast<int*>(ws + L.attn_cnt), nsplit, o, err, kb_o};
+                reinterpret_cast<int*>(ws + L.attn_cnt), attn_wgs, reinterpret_cast<const AttnWork*>(ws + L.attn_work), o,
+                err, kb_o};
     NJ_TRY(NJ_PROF_ATTENTION, launch_attention(aa, s), "attention");
     const void* g_next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : w->final_norm;
     if (fused) {
@@ -731,12 +740,14 @@ int nightjar_attn_verify(const nj_model_desc* desc, const void* q, const void* k
   char* ws = static_cast<char*>(workspace);
   int* cnt = reinterpret_cast<int*>(ws + L.cnt);
   hipError_t e = hipSuccess;
-  if (bf) e = launch_fill_i32(cnt, 0, (int)(L.part_o - L.cnt) / 4, s);  // split arrivals start at zero
-  if (e != hipSuccess) return hip_fail(e, "attn_verify: clear counters");
+  const int wgs = bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1;
+  // the work list, with the split arrival counters cleared
+  if (bf) e = launch_attn_plan(context_lens, B, d.n_kv_heads, T, max_blocks, wgs, ws + L.work, cnt, s);
+  if (e != hipSuccess) return hip_fail(e, "attn_verify: work list");
   AttnArgs aa{bf ? kBF16 : kF32, q, k_pages, v_pages, win_k, win_v, block_table, max_blocks, context_lens,
               num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,
-              reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml), cnt,
-              bf ? attention_plan(B, d.n_kv_heads, max_blocks) : 1, out, reinterpret_cast<int*>(ws + L.err), false};
+              reinterpret_cast<float*>(ws + L.part_o), reinterpret_cast<float*>(ws + L.part_ml), cnt, wgs,
+              reinterpret_cast<const AttnWork*>(ws + L.work), out, reinterpret_cast<int*>(ws + L.err), false};
   e = launch_attention(aa, s);
   return e == hipSuccess ? NJ_OK : hip_fail(e, "attn_verify");
 }

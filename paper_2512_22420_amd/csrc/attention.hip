@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <climits>
 
+#include "attn_work.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -26,7 +27,6 @@ namespace nj {
 namespace {
 
 constexpr int kD = 128;  // head dim of the bf16 path
-constexpr int kMaxExtraSplits = 4096;  // KV-split workgroups beyond one per (sequence, KV head)
 constexpr int kAttnBuf = 2;    // chunk buffers per workgroup (kAttnBuf - 1 chunks in flight)
 constexpr int kAttnChunk = 4;  // cached blocks per chunk
 // workgroups per CU that the chunk buffers leave room for (160 KB of LDS)
@@ -48,6 +48,7 @@ struct AttnK {
   float* part_o;
   float* part_ml;
   int* counters;  // [B*Hkv][kCounterStride] split arrivals, zero on entry (cleared before each launch)
+  const AttnWork* work;  // [gridDim.x] the work list (attn_work.h)
   bf16_t* out;
   int* err;
   int max_blocks, num_blocks, T, H, Hkv;
@@ -89,7 +90,7 @@ __device__ __forceinline__ int v_lds(int dim, int unit8) {  // element offset in
 // together.  `lds` is the kernel's staging buffer (free by now).
 constexpr int kMergeSplits = 8;   // split partials loaded together per unit
 constexpr int kMergeUnits = 4;    // units merged together per thread
-__device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT, int G, int b, int kvh,
+__device__ void split_arrive(const AttnK& a, int pair, int nsplit, int slot0, int R, int RT, int G, int b, int kvh,
                              __amdgpu_buffer_rsrc_t ors, __amdgpu_buffer_rsrc_t mrs, float* lds, int lds_floats) {
   __shared__ int s_last;
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -99,7 +100,7 @@ __device__ void split_arrive(const AttnK& a, int pair, int nsplit, int R, int RT
   __syncthreads();
   if (!s_last) return;
   const int rpad = RT * 16;
-  const size_t pbase = (size_t)pair * nsplit * rpad;
+  const size_t pbase = (size_t)slot0 * rpad;
   // s_f[qr][sp]: weight 2^(m_sp - M) of split sp for row qr (0 for empty
   // splits); s_w[qr]: 1 / sum_sp weight * l_sp.  The (m, l) of every row and
   // split are loaded in one pass.
@@ -205,24 +206,21 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
   constexpr int UPW = 8 / WPB;  // 1 KB load instructions per wave and chunk
   static_assert(kCB == 2 || kCB == 4, "a chunk's blocks split evenly over the 4 waves");
   __shared__ __attribute__((aligned(16))) bf16_t smem[NBUF * 2 * KV_ELEMS];  // [buf][K|V][chunk], 32 KB per buffer
-  const int pair = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
-  const int b = pair / a.Hkv, kvh = pair % a.Hkv;
+  const AttnWork item = a.work[blockIdx.x];
+  if (item.nsplit == 0) return;  // the list is shorter than the grid
+  const int b = item.b, kvh = item.kvh, split = item.split, nsplit = item.nsplit;
+  const int pair = b * a.Hkv + kvh, slot0 = blockIdx.x - split;
   const int G = a.H / a.Hkv, R = a.T * G, RT = (R + 15) / 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int rt = wave % RTW, tp = wave / RTW;
 
-  int ctx = a.ctx[b];
-  if (ctx < 0 || ctx + a.T > a.max_blocks * kBlock) {
-    if (threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
-    ctx = max(0, min(ctx, a.max_blocks * kBlock - a.T));
-  }
-  // this split's share of the cached blocks, from the actual context length
-  // (shares differ by at most one block); split 0 also takes the window block,
-  // as its first chunk: it is in L2 (just written), so its compute overlaps
-  // the first cached chunk's loads
-  const int nb_ctx = (ctx + kBlock - 1) / kBlock;
-  const int c0 = (int)((long)split * nb_ctx / nsplit), c1 = (int)((long)(split + 1) * nb_ctx / nsplit);
+  const int ctx = item.ctx;
+  if (item.bad_ctx && threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
+  // this split's share of the cached blocks (shares differ by at most one
+  // block); split 0 also takes the window block, as its first chunk: it is in
+  // L2 (just written), so its compute overlaps the first cached chunk's loads
+  const int c0 = item.c0, c1 = item.c1;
   const int ncc = (c1 - c0 + kCB - 1) / kCB;  // cached chunks
   const int wch = split == 0 ? 1 : 0;         // window chunks
   const int nchunks = ncc + wch;
@@ -231,8 +229,8 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
   const __amdgpu_buffer_rsrc_t mrs = coherent_rsrc(a.part_ml, a.part_ml_bytes);
   if (nchunks == 0) {  // no blocks of this sequence for this split: mark its rows empty for the merge
     for (int qr = threadIdx.x; qr < R; qr += 256)
-      coherent_store_f32(mrs, (uint32_t)(((((size_t)pair * nsplit + split) * (RT * 16) + qr) * 2) * 4), -INFINITY);
-    split_arrive(a, pair, nsplit, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
+      coherent_store_f32(mrs, (uint32_t)(((((size_t)slot0 + split) * (RT * 16) + qr) * 2) * 4), -INFINITY);
+    split_arrive(a, pair, nsplit, slot0, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
                  (int)(sizeof(smem) / sizeof(float)));
     return;
   }
@@ -451,7 +449,7 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
           ov[1] = pack_bf16x2(acc[2] / wsum, acc[3] / wsum);
           *out_at(a, b * a.T + i, (kvh * G + hh) * kD + d) = ov;
         } else {
-          const size_t base = ((size_t)pair * nsplit + split) * (RT * 16) + qr;
+          const size_t base = ((size_t)slot0 + split) * (RT * 16) + qr;
           coherent_store(ors, (uint32_t)((base * kD + d) * 4), acc);
           if (d == 0) {
             coherent_store_f32(mrs, (uint32_t)(base * 2 * 4), mx);
@@ -463,7 +461,7 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
     __syncthreads();
   }
   if (nsplit > 1)
-    split_arrive(a, pair, nsplit, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
+    split_arrive(a, pair, nsplit, slot0, R, RT, G, b, kvh, ors, mrs, reinterpret_cast<float*>(smem),
                  (int)(sizeof(smem) / sizeof(float)));
 }
 
@@ -549,28 +547,42 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnF a) {
 }  // namespace
 
 int attention_plan(int B, int Hkv, int max_blocks) {
-  // Enough workgroups to keep ~2048 chunk streams in flight, and no split
-  // longer than 256 blocks (one workgroup streams its chunks one after the
-  // other, so the longest split sets the kernel's duration; shorter splits
-  // cost more in per-split start-up and merging than they win in balance); at
-  // least 8 blocks per split, and at most pairs + kMaxExtraSplits
-  // workgroups, which bounds the partial buffer whatever the context length.
-  // The kernel divides each sequence's actual blocks evenly over the splits.
+  // Workgroups of the work list: one per (sequence, KV head) plus up to
+  // kExtraWorkgroups more, and no more than the splits of kMinSplitBlocks
+  // blocks the longest possible context could use.  The list sizes the
+  // splits from the actual context lengths to fit this grid, so a long
+  // sequence gets proportionally more splits than a short one.
   const int pairs = B * Hkv;
-  const int ns_len = (max_blocks + 255) / 256;
-  int ns = std::max((2048 + pairs - 1) / pairs, ns_len);
-  // keep every workgroup resident at once (2 per CU) when the split-length
-  // bound allows: a split that starts late holds up the merge of its
-  // (sequence, KV head)
-  if (pairs * ns > kResidentWorkgroups) ns = std::max(ns_len, kResidentWorkgroups / pairs);
-  ns = std::min(ns, 1 + kMaxExtraSplits / pairs);
-  ns = std::min(ns, (max_blocks + 7) / 8);
-  return std::max(ns, 1);
+  const long cap = (long)pairs * std::max(1, (max_blocks + kMinSplitBlocks - 1) / kMinSplitBlocks);
+  return (int)std::max<long>(pairs, std::min<long>((long)pairs + kExtraWorkgroups, cap));
 }
+
+size_t attention_work_bytes(int B, int Hkv) { return (size_t)(B * Hkv + kExtraWorkgroups) * sizeof(AttnWork); }
 
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D) {
   const int rpad = ((T * G + 15) / 16) * 16;
-  return (size_t)(B * Hkv + kMaxExtraSplits) * rpad * (D + 2);
+  return (size_t)(B * Hkv + kExtraWorkgroups) * rpad * (D + 2);
+}
+
+namespace {
+// One workgroup: the work list of the next attention launches, and (when
+// counters is given) their split arrival counters cleared.
+__global__ __launch_bounds__(256) void attn_plan_kernel(const int32_t* __restrict__ ctx, int B, int Hkv, int T,
+                                                        int max_blocks, int nwg, AttnWork* __restrict__ work,
+                                                        int* __restrict__ counters) {
+  __shared__ int scratch[attn_work_scratch_ints(256)];
+  if (counters)
+    for (int u = threadIdx.x; u < B * Hkv; u += 256) counters[u * kCounterStride] = 0;
+  build_attn_work<256>(ctx, B, Hkv, T, max_blocks, nwg, work, scratch);
+}
+}  // namespace
+
+hipError_t launch_attn_plan(const int32_t* ctx, int B, int Hkv, int T, int max_blocks, int nwg, void* work,
+                            int* counters, hipStream_t s) {
+  if (nwg < B * Hkv || nwg > B * Hkv + kExtraWorkgroups) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(256), 0, s, ctx, B, Hkv, T, max_blocks, nwg,
+                     static_cast<AttnWork*>(work), counters);
+  return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
@@ -588,12 +600,13 @@ hipError_t launch_attention(const AttnArgs& x, hipStream_t s) {
   AttnK a{static_cast<const bf16_t*>(x.q), static_cast<const bf16_t*>(x.k_pages),
           static_cast<const bf16_t*>(x.v_pages), static_cast<const bf16_t*>(x.win_k),
           static_cast<const bf16_t*>(x.win_v), x.block_table, x.ctx, x.part_o, x.part_ml, x.counters,
-          static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv,
+          x.work, static_cast<bf16_t*>(x.out), x.err, x.max_blocks, x.num_blocks, x.T, x.H, x.Hkv,
           (float)(1.4426950408889634 / sqrt((double)kD)),
           (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * kD * 4, INT32_MAX),
           (int)std::min<size_t>(attention_partial_floats(x.B, x.Hkv, x.T, G, kD) / (kD + 2) * 2 * 4, INT32_MAX),
           x.out_kblocked ? x.B * x.T : 0};
-  dim3 grid(x.B * x.Hkv, x.nsplit);
+  if (!x.work || x.wgs < x.B * x.Hkv || x.wgs > x.B * x.Hkv + kExtraWorkgroups) return hipErrorInvalidValue;
+  dim3 grid(x.wgs);
   switch (RT) {
     case 1: hipLaunchKernelGGL((attn_lds_kernel<1, kAttnBuf, kAttnChunk>), grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((attn_lds_kernel<2, kAttnBuf, kAttnChunk>), grid, dim3(256), 0, s, a); break;

@@ -1,0 +1,168 @@
+// The work list of the bf16 paged attention: which (sequence, KV head, KV
+// split) each workgroup of the attention grid takes.  Built once per step by
+// one workgroup (the QKV GEMM's bookkeeping workgroup, or attn_plan_kernel)
+// from the device context lengths; the attention reads one item per
+// workgroup.
+//
+// Sequence b has nb_b = ceil(ctx_b / 16) cached blocks (ctx_b clamped as the
+// attention clamps it).  With a split length of S blocks it gets
+// s_b = max(1, ceil(nb_b / S)) splits per KV head, and items are numbered
+// (b, KV head, split) in that order, so the splits of one (sequence, KV head)
+// are consecutive and their partials sit in consecutive slots.  S is the
+// smallest of kCand lengths spread over [s_lo, s_hi] whose item count fits the
+// grid: s_lo = max(kMinSplitBlocks, ceil(Hkv * sum nb / nwg)) (no fewer
+// items can fit), s_hi = max(s_lo, ceil(Hkv * sum nb / (nwg - pairs))), which
+// always fits since sum_b ceil(nb_b / S) <= sum nb / S + B.  Items past the
+// list are written with nsplit = 0 (that workgroup exits).
+#pragma once
+
+#include <climits>
+
+#include "common.h"
+
+namespace nj {
+
+#ifndef NJ_ATTN_MIN_SPLIT
+#define NJ_ATTN_MIN_SPLIT 16
+#endif
+#ifndef NJ_ATTN_EXTRA_WGS
+#define NJ_ATTN_EXTRA_WGS 512
+#endif
+constexpr int kMinSplitBlocks = NJ_ATTN_MIN_SPLIT;  // cached blocks a split holds at least
+constexpr int kExtraWorkgroups = NJ_ATTN_EXTRA_WGS; // workgroups beyond one per (sequence, KV head)
+
+struct AttnWork {
+  int b, kvh, split, nsplit;  // nsplit == 0: no item for this workgroup
+  int c0, c1;                 // the split's cached blocks [c0, c1)
+  int ctx;                    // the sequence's context length, clamped into the table
+  int bad_ctx;                // the caller's length was out of range (flagged by split 0)
+};
+static_assert(sizeof(AttnWork) == 32, "one item is two 16-byte loads");
+
+__device__ __forceinline__ int attn_clamp_ctx(int c, int max_blocks, int T) {
+  const int cap = max_blocks * kBlock - T;
+  return (c < 0 || c > cap) ? max(0, min(c, cap)) : c;
+}
+
+// Run by all NT threads of one workgroup (every thread must call it).
+// scratch: at least attn_work_scratch_ints(NT) ints of LDS, not otherwise in use.
+__host__ __device__ constexpr int attn_work_scratch_ints(int NT) { return 8 * (NT / 64) + 2 * NT; }
+template <int NT>
+__device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv, int T, int max_blocks, int nwg,
+                                AttnWork* __restrict__ work, int* scratch) {
+  constexpr int kCand = 8, NWV = NT / 64;
+  constexpr int kKeep = 4;  // context lengths a thread keeps in registers (more are re-read)
+  const int per = (B + NT - 1) / NT;
+  const int b0 = min(B, (int)threadIdx.x * per), b1 = min(B, b0 + per);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
+  int* s_red = scratch;                // [NWV][kCand]
+  int* s_seq = scratch + NWV * kCand;  // small batches: [B][2] first item and context of each sequence
+  int keep[kKeep];
+#pragma unroll
+  for (int j = 0; j < kKeep; ++j) keep[j] = b0 + j < b1 ? ctx[b0 + j] : 0;
+  auto raw_of = [&](int b) {
+    const int i = b - b0;
+    int r = 0;
+#pragma unroll
+    for (int j = 0; j < kKeep; ++j)
+      if (i == j) r = keep[j];
+    return i < kKeep ? r : ctx[b];
+  };
+  auto nblocks_raw = [&](int raw) { return (attn_clamp_ctx(raw, max_blocks, T) + kBlock - 1) / kBlock; };
+  auto wsum = [](int v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+  };
+  // sum of cached blocks
+  int mine = 0;
+  for (int b = b0; b < b1; ++b) mine += nblocks_raw(raw_of(b));
+  mine = wsum(mine);
+  __syncthreads();
+  if (lane == 0) s_red[wave] = mine;
+  __syncthreads();
+  long total = 0;
+  for (int w = 0; w < NWV; ++w) total += s_red[w];
+  const int pairs = B * Hkv;
+  const long work_blocks = (long)Hkv * total;
+  const int s_lo = max(kMinSplitBlocks, (int)((work_blocks + nwg - 1) / nwg));
+  const int s_hi = nwg > pairs ? max(s_lo, (int)((work_blocks + (nwg - pairs) - 1) / (nwg - pairs))) : (1 << 28);
+  auto cand = [&](int c) { return s_lo + (int)(((long)(s_hi - s_lo) * c + kCand - 2) / (kCand - 1)); };
+  int cnt[kCand];
+#pragma unroll
+  for (int c = 0; c < kCand; ++c) cnt[c] = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int n = nblocks_raw(raw_of(b));
+#pragma unroll
+    for (int c = 0; c < kCand; ++c) cnt[c] += max(1, (n + cand(c) - 1) / cand(c));
+  }
+#pragma unroll
+  for (int c = 0; c < kCand; ++c) cnt[c] = wsum(cnt[c]);
+  __syncthreads();  // the block sums above are read
+  if (lane == 0)
+#pragma unroll
+    for (int c = 0; c < kCand; ++c) s_red[wave * kCand + c] = cnt[c];
+  __syncthreads();
+  int S = s_hi;
+  for (int c = kCand - 1; c >= 0; --c) {
+    long items = 0;
+    for (int w = 0; w < NWV; ++w) items += s_red[w * kCand + c];
+    if (items * Hkv <= nwg) S = cand(c);
+  }
+  // exclusive scan of the per-thread item counts (threads own consecutive sequences)
+  int my_items = 0;
+  for (int b = b0; b < b1; ++b) my_items += Hkv * max(1, (nblocks_raw(raw_of(b)) + S - 1) / S);
+  int incl = my_items;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int up = __shfl_up(incl, o);
+    if (lane >= o) incl += up;
+  }
+  __syncthreads();  // the candidate sums are read
+  if (lane == 63) s_red[wave] = incl;
+  __syncthreads();
+  int start = incl - my_items, n_items = 0;
+  for (int w = 0; w < NWV; ++w) {
+    if (w < wave) start += s_red[w];
+    n_items += s_red[w];
+  }
+  // the items: item q of sequence b (q = kv head * s_b + split) goes to
+  // start_b + q.  With fewer sequences than threads, NT / B threads share a
+  // sequence's items; otherwise each thread writes its own sequences'.
+  auto put = [&](int b, int raw, int q, int base) {
+    const int c = attn_clamp_ctx(raw, max_blocks, T), n = (c + kBlock - 1) / kBlock;
+    const int sb = max(1, (n + S - 1) / S);
+    const int g = q / sb, sp = q - g * sb;
+    const int c0 = n < 46341 ? sp * n / sb : (int)((long)sp * n / sb);
+    const int c1 = n < 46341 ? (sp + 1) * n / sb : (int)((long)(sp + 1) * n / sb);
+    work[base + q] = AttnWork{b, g, sp, sb, c0, c1, c, c != raw};
+  };
+  if (B <= NT / 2) {
+    if ((int)threadIdx.x < B) {  // per == 1 here
+      s_seq[2 * threadIdx.x] = start;
+      s_seq[2 * threadIdx.x + 1] = keep[0];
+    }
+    __syncthreads();
+    const int tps = NT / B, b = threadIdx.x / tps, j = threadIdx.x % tps;
+    if (b < B) {
+      const int base = s_seq[2 * b], raw = s_seq[2 * b + 1];
+      const int sb = max(1, (nblocks_raw(raw) + S - 1) / S);
+      for (int q = j; q < Hkv * sb; q += tps) put(b, raw, q, base);
+    }
+  } else {
+    for (int b = b0; b < b1; ++b) {
+      const int raw = raw_of(b), sb = max(1, (nblocks_raw(raw) + S - 1) / S);
+      for (int q = 0; q < Hkv * sb; ++q) put(b, raw, q, start);
+      start += Hkv * sb;
+    }
+  }
+  for (int i = n_items + threadIdx.x; i < nwg; i += NT) work[i] = AttnWork{0, 0, 0, 0, 0, 0, 0, 0};
+  __syncthreads();  // scratch is free again
+}
+
+// The arguments of a work-list build riding along another kernel's launch.
+struct AttnPlan {
+  const int32_t* ctx;
+  AttnWork* work;  // nullptr: no build
+  int B, Hkv, T, max_blocks, nwg;
+};
+
+}  // namespace nj

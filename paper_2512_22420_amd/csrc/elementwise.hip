@@ -1,6 +1,7 @@
 // Small per-row kernels of the verify step: embedding gather fused with the
 // first RMSNorm, RMSNorm, RoPE with the window K/V store, and the KV append
 // of accepted rows.  All are HBM/latency bound and tiny next to the GEMMs.
+#include "attn_work.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -62,8 +63,13 @@ template <typename T>
 __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const T* __restrict__ embed,
     const T* __restrict__ gain, float* __restrict__ h, T* __restrict__ x, int d, int V, float eps,
-    int* __restrict__ err, int kbM) {
+    int* __restrict__ err, int kbM, AttnPlan plan) {
   __shared__ float sh[kNormThreads / kWave];
+  if (plan.work && blockIdx.x == gridDim.x - 1) {  // the extra workgroup: the attention's work list
+    __shared__ int scratch[attn_work_scratch_ints(kNormThreads)];
+    build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.work, scratch);
+    return;
+  }
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
   if (tok < 0 || tok >= V) {
@@ -103,7 +109,12 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const bf16_t* __restrict__ embed,
     const bf16_t* __restrict__ gain, float* __restrict__ h, bf16_t* __restrict__ x, float* __restrict__ ssq, int d,
     int V, int* __restrict__ err, const int32_t* __restrict__ ctx, RopeFreqHead f, float* __restrict__ rope_cs,
-    const float* __restrict__ hin) {
+    const float* __restrict__ hin, AttnPlan plan) {
+  if (plan.work && blockIdx.x == gridDim.x - 1) {  // the extra workgroup: the attention's work list
+    __shared__ int scratch[attn_work_scratch_ints(kNormThreads)];
+    build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.work, scratch);
+    return;
+  }
   const int row = blockIdx.x, b = row / T_, i = row % T_;
   if (rope_cs && threadIdx.x < 64) {
     const int j = threadIdx.x;
@@ -382,27 +393,30 @@ __global__ __launch_bounds__(256) void rope_window_d128_kernel(const float* __re
 
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
                              const void* gain, float* h, void* x, int d, int V, float eps, int* err,
-                             hipStream_t s, bool x_kblocked) {
+                             hipStream_t s, bool x_kblocked, const AttnPlan* plan) {
   const int kbM = x_kblocked ? B * T : 0;
+  const AttnPlan pl = plan ? *plan : AttnPlan{};
+  const dim3 grid(B * T + (pl.work ? 1 : 0));
   if (dtype == kF32)
-    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
+    hipLaunchKernelGGL(embed_norm_kernel<float>, grid, dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const float*>(embed), static_cast<const float*>(gain), h,
-                       static_cast<float*>(x), d, V, eps, err, kbM);
+                       static_cast<float*>(x), d, V, eps, err, kbM, pl);
   else
-    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
+    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, grid, dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h,
-                       static_cast<bf16_t*>(x), d, V, eps, err, kbM);
+                       static_cast<bf16_t*>(x), d, V, eps, err, kbM, pl);
   return hipGetLastError();
 }
 
 hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
                                const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
-                               const int32_t* ctx, float theta, float* rope_cs, hipStream_t s) {
+                               const int32_t* ctx, float theta, float* rope_cs, hipStream_t s, const AttnPlan* plan) {
   RopeFreqHead f{};
   for (int j = 0; j < 64; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / 128);
-  hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, last, drafts, T,
+  const AttnPlan pl = plan ? *plan : AttnPlan{};
+  hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T + (pl.work ? 1 : 0)), dim3(kNormThreads), 0, s, last, drafts, T,
                      static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h, static_cast<bf16_t*>(x),
-                     ssq, d, V, err, ctx, f, rope_cs, nullptr);
+                     ssq, d, V, err, ctx, f, rope_cs, nullptr, pl);
   return hipGetLastError();
 }
 
@@ -412,7 +426,7 @@ hipError_t launch_norm_inputs(const float* h, int B, int T, const void* gain, vo
   for (int j = 0; j < 64; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / 128);
   hipLaunchKernelGGL(embed_gather_kernel, dim3(B * T), dim3(kNormThreads), 0, s, nullptr, nullptr, T, nullptr,
                      static_cast<const bf16_t*>(gain), nullptr, static_cast<bf16_t*>(x), ssq, d, 0, nullptr, ctx, f,
-                     rope_cs, h);
+                     rope_cs, h, AttnPlan{});
   return hipGetLastError();
 }
 

@@ -135,16 +135,21 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
                             float* stats = nullptr, bool x_kblocked = false, bool y_kblocked = false);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
+struct AttnPlan;
+// The embedding kernels can carry one more workgroup that builds the
+// attention's work list (plan nullable; see attn_work.h).
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
                              const void* embed, const void* gain, float* h, void* x, int d, int V,
-                             float eps, int* err, hipStream_t s, bool x_kblocked = false);
+                             float eps, int* err, hipStream_t s, bool x_kblocked = false,
+                             const AttnPlan* plan = nullptr);
 
 // bf16, norm folded into the GEMMs: h[r] = E[id(r)], x[r] = bf16(h[r] * gain),
 // ssq[r][t] = sum of h[r]^2 over columns 128t .. 128t+127; and the step's RoPE
 // table rope_cs[r][j] = (cos, sin) of (ctx[b] + i) * theta^(-j/64) (nullable).
 hipError_t launch_embed_gather(const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
                                const void* gain, float* h, void* x, float* ssq, int d, int V, int* err,
-                               const int32_t* ctx, float theta, float* rope_cs, hipStream_t s);
+                               const int32_t* ctx, float theta, float* rope_cs, hipStream_t s,
+                               const AttnPlan* plan = nullptr);
 
 // The same outputs (x, ssq, rope_cs) for given residual rows h [B*T][d] fp32
 // instead of embedding rows (h is only read).
@@ -167,6 +172,7 @@ hipError_t launch_rope_window(int dtype, const float* qkv, const int32_t* ctx, i
                               int D, float theta, void* q_out, void* win_k, void* win_v, int32_t* ctx_snap,
                               int* attn_counters, hipStream_t s);
 
+struct AttnWork;
 struct AttnArgs {
   int dtype;
   const void* q;        // [M][H][D]
@@ -181,14 +187,21 @@ struct AttnArgs {
   float* part_o;        // split partials (bf16 path)
   float* part_ml;
   int* counters;         // [B*Hkv] split arrivals, zero on entry (bf16 path)
-  int nsplit;  // KV splits per (sequence, KV head); a split's blocks come from the actual context length
+  int wgs;              // bf16: workgroups of the attention work list (attention_plan)
+  const AttnWork* work; // bf16: the list, built by launch_attn_plan or the embedding kernel
   void* out;            // [M][H*D]; k-blocked [H*D/32][M][32] when out_kblocked (bf16 path)
   int* err;
   bool out_kblocked;
 };
-// Number of KV splits the bf16 path uses, and the partial buffer floats it needs.
+// Workgroups of the bf16 path's work list, the bytes of the list, and the
+// partial buffer floats the splits need.
 int attention_plan(int B, int Hkv, int max_blocks);
+size_t attention_work_bytes(int B, int Hkv);
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D);
+// The work list for attention launches over these context lengths (one
+// workgroup), clearing their split counters when `counters` is given.
+hipError_t launch_attn_plan(const int32_t* ctx, int B, int Hkv, int T, int max_blocks, int nwg, void* work,
+                            int* counters, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
 // Acceptance from logits [B*T][V].
