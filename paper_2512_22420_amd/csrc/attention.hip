@@ -27,11 +27,16 @@ namespace nj {
 namespace {
 
 constexpr int kD = 128;  // head dim of the bf16 path
-constexpr int kAttnBuf = 2;    // chunk buffers per workgroup (kAttnBuf - 1 chunks in flight)
-constexpr int kAttnChunk = 4;  // cached blocks per chunk
+#ifndef NJ_ATTN_BUF
+#define NJ_ATTN_BUF 2
+#endif
+#ifndef NJ_ATTN_CHUNK
+#define NJ_ATTN_CHUNK 4
+#endif
+constexpr int kAttnBuf = NJ_ATTN_BUF;      // chunk buffers per workgroup (kAttnBuf - 1 chunks in flight)
+constexpr int kAttnChunk = NJ_ATTN_CHUNK;  // cached blocks per chunk
 // workgroups per CU that the chunk buffers leave room for (160 KB of LDS)
 constexpr int attn_wgs_per_cu(int nbuf, int cb) { return (160 * 1024 - 1024) / (nbuf * cb * 8 * 1024); }
-constexpr int kResidentWorkgroups = 256 * attn_wgs_per_cu(kAttnBuf, kAttnChunk);
 
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));

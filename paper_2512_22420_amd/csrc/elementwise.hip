@@ -65,12 +65,14 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
     const T* __restrict__ gain, float* __restrict__ h, T* __restrict__ x, int d, int V, float eps,
     int* __restrict__ err, int kbM, AttnPlan plan) {
   __shared__ float sh[kNormThreads / kWave];
-  if (plan.work && blockIdx.x == gridDim.x - 1) {  // the extra workgroup: the attention's work list
+  // the extra workgroup (dispatched first, so it overlaps the rows): the
+  // attention's work list
+  if (plan.work && blockIdx.x == 0) {
     __shared__ int scratch[attn_work_scratch_ints(kNormThreads)];
     build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.work, scratch);
     return;
   }
-  const int row = blockIdx.x, b = row / T_, i = row % T_;
+  const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
   int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
   if (tok < 0 || tok >= V) {
     if (threadIdx.x == 0) flag_error(err, kErrToken);
@@ -110,12 +112,14 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     const bf16_t* __restrict__ gain, float* __restrict__ h, bf16_t* __restrict__ x, float* __restrict__ ssq, int d,
     int V, int* __restrict__ err, const int32_t* __restrict__ ctx, RopeFreqHead f, float* __restrict__ rope_cs,
     const float* __restrict__ hin, AttnPlan plan) {
-  if (plan.work && blockIdx.x == gridDim.x - 1) {  // the extra workgroup: the attention's work list
+  // the extra workgroup (dispatched first, so it overlaps the rows): the
+  // attention's work list
+  if (plan.work && blockIdx.x == 0) {
     __shared__ int scratch[attn_work_scratch_ints(kNormThreads)];
     build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.work, scratch);
     return;
   }
-  const int row = blockIdx.x, b = row / T_, i = row % T_;
+  const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
   if (rope_cs && threadIdx.x < 64) {
     const int j = threadIdx.x;
     const double ang = (double)(max(ctx[b], 0) + i) * f.inv_freq[j];
