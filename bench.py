@@ -428,6 +428,9 @@ def main():
     ap.add_argument("--no-grid", action="store_true")
     ap.add_argument("--no-large", action="store_true", help="skip the large-batch and 32-layer points")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also copy a 1 GiB device buffer three times: a dispatch of known HBM traffic "
+                         "(1,048,576 KiB read and written) that scales the FETCH_SIZE / WRITE_SIZE counters")
     ap.add_argument("--B", type=int, default=8)
     ap.add_argument("--k", type=int, default=5)
     ap.add_argument("--workload", default="llama8b-layer-small-batch",
@@ -646,6 +649,13 @@ def main():
         "sd_step": sd if not args.no_large else None,
         "elastic": elastic if not args.no_large else None,
     }
+    if args.calib_copy:
+        src = torch.empty(2 ** 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     print(json.dumps(out), flush=True)
 
 
