@@ -32,7 +32,11 @@ namespace nj {
 namespace {
 
 constexpr int kTile = 256;          // weights per tile (4 per lane of a wave)
-constexpr int kTilesPerBlock = 8;   // tiles per accept_draw workgroup (two per wave)
+// Tiles a wave of accept_draw sums (its loads issued together): two while few
+// sequences leave the grid small, four from kDrawWideBatch sequences up
+// (fewer, longer workgroups: B=128 at the 8B vocabulary 53 -> 48 us, B=256
+// at the 7B vocabulary 109 -> 87 us; at B=8 two are faster).
+constexpr int kDrawWideBatch = 32;
 constexpr int kMaxTiles = 2048;     // V <= 524288
 
 struct AccK {
@@ -264,7 +268,9 @@ __device__ void draw_token(const AccK& a, int b, int n, bool resid, float m, flo
   if (lane == 0) a.accepted_len[b] = n;
 }
 
+template <int kTilesPerWave>
 __global__ __launch_bounds__(256) void accept_draw_kernel(AccK a) {
+  constexpr int kTilesPerBlock = 4 * kTilesPerWave;
   __shared__ double s_ts[kMaxTiles];
   __shared__ double s_fb[kMaxTiles];  // only for an all-zero residual
   __shared__ int s_last;
@@ -291,18 +297,29 @@ __global__ __launch_bounds__(256) void accept_draw_kernel(AccK a) {
   const float* lrow = a.logits + (size_t)(b * T + n) * a.V;
   const float* qrow = resid ? a.dprobs + ((size_t)b * a.k + n) * a.V : lrow;
   const __amdgpu_buffer_rsrc_t trs = coherent_rsrc(a.tsum, a.tsum_bytes);
-  const int t0 = blockIdx.y * kTilesPerBlock, t1 = min(t0 + kTilesPerBlock, a.ntile);
+  // this wave's tiles t0 + wave + 4 j: every tile's loads are issued before
+  // any is summed (whole vec4 pieces; the row's ragged end takes the scalar path)
+  const int t0 = blockIdx.y * kTilesPerBlock;
   const bool vec = (a.V & 3) == 0;
-  for (int t = t0 + wave; t < t1; t += 4) {
+  f32x4 l4[kTilesPerWave], q4[kTilesPerWave];
+#pragma unroll
+  for (int j = 0; j < kTilesPerWave; ++j) {
+    const int t = t0 + wave + 4 * j, j0 = t * kTile + lane * 4;
+    const bool full = vec && t < a.ntile && j0 + 3 < a.V;
+    l4[j] = full ? *reinterpret_cast<const f32x4*>(lrow + j0) : f32x4{0.f, 0.f, 0.f, 0.f};
+    q4[j] = full && resid ? *reinterpret_cast<const f32x4*>(qrow + j0) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int j = 0; j < kTilesPerWave; ++j) {
+    const int t = t0 + wave + 4 * j;
+    if (t >= a.ntile) break;
     const int j0 = t * kTile + lane * 4;
     double ls = 0.0;
     if (vec && j0 + 3 < a.V) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lrow + j0);
-      const f32x4 q4 = *reinterpret_cast<const f32x4*>(qrow + j0);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p = expf(l4[e] - m) * inv_s;
-        ls += (double)(resid ? fmaxf(0.f, p - q4[e]) : p);
+        const float p = expf(l4[j][e] - m) * inv_s;
+        ls += (double)(resid ? fmaxf(0.f, p - q4[j][e]) : p);
       }
     } else {
 #pragma unroll
@@ -399,8 +416,10 @@ hipError_t launch_accept(const AcceptArgs& x, hipStream_t s) {
   hipLaunchKernelGGL(accept_rows_kernel, dim3(rows), dim3(kRowThreads), 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_draw_kernel, dim3(x.B, (ntile + kTilesPerBlock - 1) / kTilesPerBlock), dim3(256), 0, s,
-                     a);
+  if (x.B >= kDrawWideBatch)
+    hipLaunchKernelGGL(accept_draw_kernel<4>, dim3(x.B, (ntile + 15) / 16), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(accept_draw_kernel<2>, dim3(x.B, (ntile + 7) / 8), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
