@@ -86,14 +86,16 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
   const long work_blocks = (long)Hkv * total;
   const int s_lo = max(kMinSplitBlocks, (int)((work_blocks + nwg - 1) / nwg));
   const int s_hi = nwg > pairs ? max(s_lo, (int)((work_blocks + (nwg - pairs) - 1) / (nwg - pairs))) : (1 << 28);
-  auto cand = [&](int c) { return s_lo + (int)(((long)(s_hi - s_lo) * c + kCand - 2) / (kCand - 1)); };
-  int cnt[kCand];
+  int cand[kCand], cnt[kCand];
 #pragma unroll
-  for (int c = 0; c < kCand; ++c) cnt[c] = 0;
+  for (int c = 0; c < kCand; ++c) {
+    cand[c] = s_lo + (int)(((long)(s_hi - s_lo) * c + kCand - 2) / (kCand - 1));
+    cnt[c] = 0;
+  }
   for (int b = b0; b < b1; ++b) {
-    const int n = nblocks_raw(raw_of(b));
+    const unsigned n = (unsigned)nblocks_raw(raw_of(b));
 #pragma unroll
-    for (int c = 0; c < kCand; ++c) cnt[c] += max(1, (n + cand(c) - 1) / cand(c));
+    for (int c = 0; c < kCand; ++c) cnt[c] += max(1u, (n + (unsigned)cand[c] - 1u) / (unsigned)cand[c]);
   }
 #pragma unroll
   for (int c = 0; c < kCand; ++c) cnt[c] = wsum(cnt[c]);
@@ -103,10 +105,11 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
     for (int c = 0; c < kCand; ++c) s_red[wave * kCand + c] = cnt[c];
   __syncthreads();
   int S = s_hi;
+#pragma unroll
   for (int c = kCand - 1; c >= 0; --c) {
     long items = 0;
     for (int w = 0; w < NWV; ++w) items += s_red[w * kCand + c];
-    if (items * Hkv <= nwg) S = cand(c);
+    if (items * Hkv <= nwg) S = cand[c];
   }
   // exclusive scan of the per-thread item counts (threads own consecutive sequences)
   int my_items = 0;
