@@ -423,13 +423,17 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   const AttnPlan plan{context_lens, reinterpret_cast<AttnWork*>(ws + L.attn_work), B, d.n_kv_heads, T, max_blocks,
                       attn_wgs};
   const AttnPlan* pl = bf ? &plan : nullptr;
+  // Norms not folded, but a QKV GEMM that still streams: RoPE and the window
+  // store in its epilogue (no row scale), from the table the embedding kernel writes
+  const bool rope_in_qkv = !fused && bf && gemm_streams(M, QKV, d.d_model, kEpiStore);
   if (fused)
     NJ_TRY(NJ_PROF_EMBED, launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
                                d.vocab, err, context_lens, d.rope_theta, reinterpret_cast<float*>(ws + L.rope_cs), s, pl),
            "embed");
   else
     NJ_TRY(NJ_PROF_EMBED, launch_embed_norm(dt, last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, d.d_model,
-                             d.vocab, d.rms_eps, err, s, kb_qkv, pl),
+                             d.vocab, d.rms_eps, err, s, kb_qkv, pl, context_lens, d.rope_theta,
+                             rope_in_qkv ? reinterpret_cast<float*>(ws + L.rope_cs) : nullptr),
            "embed");
   for (int l = 0; l < d.n_layers; ++l) {
     const nj_layer_weights& lw = w->layers[l];
@@ -444,10 +448,18 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
              "qkv gemm");
     } else {
       if (l > 0) NJ_TRY(NJ_PROF_NORM, launch_rmsnorm(dt, h, lw.attn_norm, x, M, d.d_model, d.rms_eps, s, kb_qkv), "attn_norm");
-      NJ_TRY(NJ_PROF_QKV, launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb_qkv), "qkv gemm");
-      NJ_TRY(NJ_PROF_ROPE, launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
-                                wk, wv, snap, acnt, s),
-             "rope");
+      if (rope_in_qkv) {
+        const QkvRope rope{context_lens, T, d.n_heads, d.n_kv_heads, reinterpret_cast<const float*>(ws + L.rope_cs), q,
+                           wk, wv, snap, acnt};
+        const GemmNorm unscaled{nullptr, 0, 0.f, nullptr, nullptr, nullptr, nullptr};
+        NJ_TRY(NJ_PROF_QKV, launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiQkvRope, unscaled, gcnt, gpart, s, &rope),
+               "qkv gemm");
+      } else {
+        NJ_TRY(NJ_PROF_QKV, launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb_qkv), "qkv gemm");
+        NJ_TRY(NJ_PROF_ROPE, launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
+                                  wk, wv, snap, acnt, s),
+               "rope");
+      }
     }
     AttnArgs aa{dt, q, kv->k_pages[l], kv->v_pages[l], wk, wv, block_table, max_blocks, context_lens,
                 kv->num_blocks, B, T, d.n_heads, d.n_kv_heads, d.head_dim,

@@ -59,11 +59,34 @@ __device__ __forceinline__ void norm_row(const float (&hv)[kNormMaxPer][4], cons
   }
 }
 
+struct RopeFreqHead {  // theta^(-2j/128) for the 64 rotation pairs of a 128-dim head, from the host in fp64
+  double inv_freq[64];
+};
+
+// Row `row` (window position i of sequence b) of the step's RoPE table:
+// rope_cs[row][j] = (cos, sin) of (ctx_b + i) * theta^(-2j/128), the angle in
+// fp64 with the range reduction done against 2 pi in two parts, the sincos in
+// fp32 on the reduced argument.  Threads 0..63 of the workgroup.
+__device__ __forceinline__ void rope_table_row(const int32_t* __restrict__ ctx, const RopeFreqHead& f, int row, int b,
+                                               int i, float* __restrict__ rope_cs) {
+  if (threadIdx.x < 64) {
+    const int j = threadIdx.x;
+    const double ang = (double)(max(ctx[b], 0) + i) * f.inv_freq[j];
+    const double kq = rint(ang * 0.15915494309189535);
+    const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
+    float sn, cs;
+    sincosf((float)red, &sn, &cs);
+    rope_cs[((size_t)row * 64 + j) * 2] = cs;
+    rope_cs[((size_t)row * 64 + j) * 2 + 1] = sn;
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
     const int32_t* __restrict__ last, const int32_t* __restrict__ drafts, int T_, const T* __restrict__ embed,
     const T* __restrict__ gain, float* __restrict__ h, T* __restrict__ x, int d, int V, float eps,
-    int* __restrict__ err, int kbM, AttnPlan plan) {
+    int* __restrict__ err, int kbM, AttnPlan plan, const int32_t* __restrict__ ctx, RopeFreqHead f,
+    float* __restrict__ rope_cs) {
   __shared__ float sh[kNormThreads / kWave];
   // the extra workgroup (dispatched first, so it overlaps the rows): the
   // attention's work list
@@ -73,6 +96,7 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
     return;
   }
   const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
+  if (rope_cs) rope_table_row(ctx, f, row, b, i, rope_cs);
   int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
   if (tok < 0 || tok >= V) {
     if (threadIdx.x == 0) flag_error(err, kErrToken);
@@ -100,9 +124,6 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
 // pos * theta^(-j/64), pos = ctx[b] + i, for the 64 rotation pairs of a
 // 128-dim head (angle formed and reduced to [-pi, pi] in fp64, then fp32
 // sin/cos, as in rope_window_kernel); every head and layer of the step uses it.
-struct RopeFreqHead {  // theta^(-2j/128) for the 64 rotation pairs of a 128-dim head, from the host in fp64
-  double inv_freq[64];
-};
 
 // With hin (fp32 [rows][d]) the rows are read from there instead of the
 // embedding and h is not written: the same inputs for a given residual stream
@@ -120,16 +141,7 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     return;
   }
   const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
-  if (rope_cs && threadIdx.x < 64) {
-    const int j = threadIdx.x;
-    const double ang = (double)(max(ctx[b], 0) + i) * f.inv_freq[j];
-    const double kq = rint(ang * 0.15915494309189535);
-    const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
-    float sn, cs;
-    sincosf((float)red, &sn, &cs);
-    rope_cs[((size_t)row * 64 + j) * 2] = cs;
-    rope_cs[((size_t)row * 64 + j) * 2 + 1] = sn;
-  }
+  if (rope_cs) rope_table_row(ctx, f, row, b, i, rope_cs);
   const bf16_t* e = nullptr;
   if (!hin) {
     int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
@@ -397,18 +409,22 @@ __global__ __launch_bounds__(256) void rope_window_d128_kernel(const float* __re
 
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T, const void* embed,
                              const void* gain, float* h, void* x, int d, int V, float eps, int* err,
-                             hipStream_t s, bool x_kblocked, const AttnPlan* plan) {
+                             hipStream_t s, bool x_kblocked, const AttnPlan* plan, const int32_t* ctx, float theta,
+                             float* rope_cs) {
   const int kbM = x_kblocked ? B * T : 0;
   const AttnPlan pl = plan ? *plan : AttnPlan{};
+  RopeFreqHead f{};
+  if (rope_cs)
+    for (int j = 0; j < 64; ++j) f.inv_freq[j] = pow((double)theta, -2.0 * j / 128);
   const dim3 grid(B * T + (pl.work ? 1 : 0));
   if (dtype == kF32)
     hipLaunchKernelGGL(embed_norm_kernel<float>, grid, dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const float*>(embed), static_cast<const float*>(gain), h,
-                       static_cast<float*>(x), d, V, eps, err, kbM, pl);
+                       static_cast<float*>(x), d, V, eps, err, kbM, pl, ctx, f, rope_cs);
   else
     hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, grid, dim3(kNormThreads), 0, s, last, drafts, T,
                        static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(gain), h,
-                       static_cast<bf16_t*>(x), d, V, eps, err, kbM, pl);
+                       static_cast<bf16_t*>(x), d, V, eps, err, kbM, pl, ctx, f, rope_cs);
   return hipGetLastError();
 }
 

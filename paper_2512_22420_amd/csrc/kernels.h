@@ -138,10 +138,13 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
 struct AttnPlan;
 // The embedding kernels can carry one more workgroup that builds the
 // attention's work list (plan nullable; see attn_work.h).
+// With rope_cs (bf16, 128-dim heads) it also writes the step's RoPE table, as
+// launch_embed_gather does, for a QKV GEMM with the RoPE epilogue.
 hipError_t launch_embed_norm(int dtype, const int32_t* last, const int32_t* drafts, int B, int T,
                              const void* embed, const void* gain, float* h, void* x, int d, int V,
                              float eps, int* err, hipStream_t s, bool x_kblocked = false,
-                             const AttnPlan* plan = nullptr);
+                             const AttnPlan* plan = nullptr, const int32_t* ctx = nullptr, float theta = 0.f,
+                             float* rope_cs = nullptr);
 
 // bf16, norm folded into the GEMMs: h[r] = E[id(r)], x[r] = bf16(h[r] * gain),
 // ssq[r][t] = sum of h[r]^2 over columns 128t .. 128t+127; and the step's RoPE
