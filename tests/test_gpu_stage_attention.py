@@ -105,6 +105,15 @@ def _attn_gpu(shape, c, q, wk, wv, ctx, k, table=None):
     return _host(out, shape.dtype).reshape(B * T, shape.n_heads, shape.head_dim), err
 
 
+def _many(B, seed):
+    """B short contexts (0..40 tokens) with every 50th one long (1500..2047): the
+    work list gives the long ones several splits and the short ones one."""
+    rng = np.random.default_rng(seed)
+    ctx = rng.integers(0, 41, size=B)
+    ctx[::50] = rng.integers(1500, 2048, size=len(ctx[::50]))
+    return ctx.tolist()
+
+
 @pytest.mark.parametrize("shape,ctx,k", [
     (L8, [0, 5, 16, 37, 1000, 2047], 3),          # ragged: empty, partial, exact block, long
     (L8, [2047, 0, 3], 15),                       # R = 16 x 4 = 64 query rows; empty KV splits of short rows
@@ -113,7 +122,10 @@ def _attn_gpu(shape, c, q, wk, wv, ctx, k, table=None):
     (QW, [300, 0, 47, 4000], 8),                  # G = 7: 63 query rows
     (QW, [129, 1], 2),
     (TF, [32, 48, 0], 3),                         # fp32 path
-], ids=["8b-ragged", "8b-r64", "8b-headline", "8b-window-only", "g7-r63", "g7-k2", "f32"])
+    (L8, _many(600, 1), 3),                       # work list: more sequences than half its threads
+    (L8, _many(1100, 2), 1),                      # work list: five sequences per thread (contexts re-read)
+], ids=["8b-ragged", "8b-r64", "8b-headline", "8b-window-only", "g7-r63", "g7-k2", "f32", "8b-b600-work-list",
+        "8b-b1100-work-list"])
 def test_attn_verify_matches_oracle(shape, ctx, k):
     ctx = np.asarray(ctx, np.int32)
     c, q, wk, wv = _attn_case(shape, ctx, k, seed=int(ctx.sum()) + k)
