@@ -451,8 +451,11 @@ enum {
  * caller, for parity tests of every kernel shape and for tuning.  split_k = 0
  * lets the kernel's planner choose; split_k >= 1 is capped so that every chunk
  * has work (128 k per chunk at least for NJ_GEMM_STREAM, 64 for the tiled
- * kernels).  The tiled kernels need K % 64 == 0, and a split run may cover at
- * most 1024 output tiles; otherwise NJ_EINVAL.  Operands, epilogues and errors
+ * kernels).  For the tiled kernels split_k = -G runs G workgroups that share
+ * the output tiles x K/64 units of work evenly (stream-K; G capped at the unit
+ * count), tiles cut between workgroups being summed in k order.  The tiled
+ * kernels need K % 64 == 0, and a run that cuts tiles may have at most 1024
+ * workgroups; otherwise NJ_EINVAL.  Operands, epilogues and errors
  * as in nightjar_gemm; the workspace must hold
  * nightjar_gemm_plan_workspace_bytes(...) bytes (0 = invalid arguments).
  */

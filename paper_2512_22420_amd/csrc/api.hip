@@ -882,7 +882,8 @@ int nightjar_gemm(int32_t dtype, const void* x, const void* w, void* y, int32_t 
 static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epilogue, int32_t kernel, int32_t split,
                      GemmPlan* out) {
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
-  if (split < 0) return fail(NJ_EINVAL, "split_k must be >= 0");
+  if (split < 0 && (kernel == NJ_GEMM_AUTO || kernel == NJ_GEMM_STREAM || kernel == NJ_GEMM_STREAM_DEEP))
+    return fail(NJ_EINVAL, "split_k < 0 (stream-K) needs a tiled kernel");
   if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_TILE_192x256) return fail(NJ_EINVAL, "bad kernel choice");
   if (dtype != NJ_BF16) {
     if (kernel != NJ_GEMM_AUTO || split) return fail(NJ_EINVAL, "the fp32 GEMM has a single kernel and no split");
@@ -904,11 +905,14 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
                      : kernel == NJ_GEMM_TILE_192x256 ? kTile192x256
                      : kernel == NJ_GEMM_TILE_128x256 ? kTile128x256
                                                       : kTile128x128;
-    p = split ? gemm_tile_plan(M, N, K, epilogue, tile, std::min(split, K / 64))
-              : gemm_tile_choose(M, N, K, epilogue, tile);
+    p = split > 0   ? gemm_tile_plan(M, N, K, epilogue, tile, std::min(split, K / 64))
+        : split < 0 ? gemm_tile_plan_sk(M, N, K, epilogue, tile, -split)
+                    : gemm_tile_choose(M, N, K, epilogue, tile);
   }
   if (p.nkc > 1 && p.counter_bytes > kGemmCounterBytes)
-    return fail(NJ_EINVAL, "a split-K run may cover at most %zu output tiles", kGemmCounterBytes / (kCounterStride * 4));
+    return fail(NJ_EINVAL, "a run that splits tiles may have at most %d workgroups", kGemmMaxSplitGrid);
+  if (p.tile == kTile256x256 && !tile_one_segment(p, K))
+    return fail(NJ_EINVAL, "the 256x256 tile runs one tile (or one K chunk of it) per workgroup: no stream-K grid");
   if (p.part_bytes >= kMaxPartBytes) return fail(NJ_EINVAL, "split-K partials would take 2 GiB or more");
   *out = p;
   return NJ_OK;

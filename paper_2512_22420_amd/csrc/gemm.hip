@@ -778,7 +778,21 @@ hipError_t launch_logits(const GemmK& a, const GemmPlan& p, hipStream_t s) {
 
 static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc) {
+namespace {
+// Buffers of a stream-K schedule: the most segments any tile is cut into
+// (partials: that many M x N fp32 copies) and one counter per workgroup.
+void tile_sk_buffers(GemmPlan& p, int M, int N, int K) {
+  const long KU = K / 64, U = (long)p.ntiles * KU, GS = p.grid / p.mblocks;
+  auto owner = [&](long X) { return ((X + 1) * GS + U - 1) / U - 1; };
+  long smax = 1;
+  for (long t = 0; t < p.ntiles; ++t) smax = std::max(smax, owner(t * KU + KU - 1) - owner(t * KU) + 1);
+  p.nkc = (int)smax;
+  p.part_bytes = smax > 1 ? al256((size_t)smax * M * N * 4) : 0;
+  p.counter_bytes = smax > 1 ? al256((size_t)p.grid * kCounterStride * 4) : 0;
+}
+}  // namespace
+
+GemmPlan gemm_tile_plan_sk(int M, int N, int K, int epi, int tile, int grid) {
   GemmPlan p{};
   const int NG = epi == kEpiSwiglu ? 2 : 1;
   const int Nout = N / NG;
@@ -786,13 +800,20 @@ GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc) {
   const int bm = tile_bm(tile), bno = tile_bn(tile) / NG;
   p.mblocks = (M + bm - 1) / bm;
   p.ntiles = (Nout + bno - 1) / bno;
-  const int nst = K / 64;
-  p.stages_per_chunk = (nst + nkc - 1) / nkc;
-  p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
+  // shares per M tile: the grid rounded down to a multiple of the M tiles
+  const long units = (long)p.ntiles * (K / 64);
+  const long shares = std::max(1L, std::min({(long)grid / p.mblocks, units, ((1L << 20) - 1) / p.mblocks}));
+  p.grid = (int)(shares * p.mblocks);
+  p.stages_per_chunk = (int)((units + shares - 1) / shares);  // units per workgroup, at most
   p.depth = 1;
-  p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
-  p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * kCounterStride * 4) : 0;
+  tile_sk_buffers(p, M, N, K);
   return p;
+}
+
+GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc) {
+  const int NG = epi == kEpiSwiglu ? 2 : 1;
+  const int tiles = ((M + tile_bm(tile) - 1) / tile_bm(tile)) * ((N / NG + tile_bn(tile) / NG - 1) / (tile_bn(tile) / NG));
+  return gemm_tile_plan_sk(M, N, K, epi, tile, tiles * std::max(1, std::min(nkc, K / 64)));
 }
 
 namespace {
@@ -809,7 +830,7 @@ double tile_cost(const GemmPlan& p, int M, int N, int K) {
   // sustained fraction of a CU's MFMA peak with k-blocked x; 128x128 tiles
   // reach about the same with one or two workgroups on a CU
   const double eff = p.tile == kTile256x256 ? 0.49 : p.tile == kTile192x256 ? 0.44 : p.tile == kTile128x256 ? 0.37 : 0.31;
-  const double wgs = (double)p.ntiles * p.mblocks * p.nkc;
+  const double wgs = (double)p.grid;
   const double per_cu = p.tile == kTile128x128 && wgs > 256.0 ? 2.0 : 1.0;  // resident workgroups per CU
   const double rounds = std::ceil(wgs / (256.0 * per_cu));
   double t = rounds * per_cu * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (2.5e15 / 256.0 * eff);
@@ -832,6 +853,18 @@ GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile) {
     for (int nkc = 1; nkc <= 8; nkc *= 2) {
       if (nkc > 1 && K / 64 / nkc < 8) break;
       const GemmPlan p = gemm_tile_plan(M, N, K, epi, tile, nkc);
+      if (p.nkc > 1 && (p.counter_bytes > kGemmCounterBytes || p.part_bytes >= kMaxPartBytes)) continue;
+      const double c = tile_cost(p, M, N, K);
+      if (c < bc) bc = c, best = p;
+    }
+    // Stream-K on one workgroup per CU, when the tiles leave CUs idle: only
+    // for the long reductions of the down projection (K >= 8192), the one
+    // place where a sweep of the 8B and 7B shapes at 320..2048 rows found it
+    // ahead (4-5%); on the other GEMMs the cut tiles' partials cost more than
+    // the balance gains.
+    if (tile != kTile256x256 && epi == kEpiResidual && K >= 8192 &&
+        (long)gemm_tile_plan(M, N, K, epi, tile, 1).grid % 256 != 0) {
+      const GemmPlan p = gemm_tile_plan_sk(M, N, K, epi, tile, 256);
       if (p.nkc > 1 && (p.counter_bytes > kGemmCounterBytes || p.part_bytes >= kMaxPartBytes)) continue;
       const double c = tile_cost(p, M, N, K);
       if (c < bc) bc = c, best = p;

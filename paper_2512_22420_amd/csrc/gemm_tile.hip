@@ -20,9 +20,12 @@
 //   the linear ID is remapped to give each XCD a contiguous run of tiles, with
 //   the M tiles of one weight tile adjacent.  The weight tile is then fetched
 //   from HBM once and re-read by its neighbours from that XCD's L2.
-// - When there are too few tiles to fill the chip, K is split across
-//   workgroups with the same fixed-order, last-arriver reduction as the
-//   weight-streaming kernel.
+// - Work is scheduled stream-K: the tiles x K/64 units go to the grid's
+//   workgroups in equal contiguous shares, so a tile count that does not
+//   divide the chip still keeps every CU busy to the end; a tile cut between
+//   workgroups is summed in k order by the last to arrive (fixed order, as
+//   in the weight-streaming kernel's split K).  A plain K split (or none) is
+//   the special case grid = tiles x c.
 // - Epilogues as in the weight-streaming kernel: fp32 store, fp32 residual
 //   add, and SwiGLU, for which the first half of the weight tile holds gate
 //   rows and the second half the matching up rows.
@@ -42,18 +45,23 @@ struct TileK {
   const bf16_t* X;
   const bf16_t* W;
   void* Y;
-  float* part;    // [nkc][M][NG][Nout] fp32 partials (split K only)
-  int* counters;  // [tiles_n * tiles_m][kCounterStride] arrival counters (split K only), zero between launches
-  int M, Nout, K, tiles_m, tiles_n, nkc, stages_per_chunk;
+  float* part;    // [segments][M][NG][Nout] fp32 partials (tiles split over workgroups only)
+  int* counters;  // [grid][kCounterStride] arrival counters (idem), zero between launches
+  int M, Nout, K, tiles_m, tiles_n;
   int part_bytes;
   float* stats;   // kEpiStore, nullable: [M][nch][2] (max, sum of exp) of each row over this tile's columns, entry tn
   int nch;
   int xkb, ykb;   // x (SwiGLU: y) stored k-blocked, [K/32][M][32]
+  int grid;       // workgroups (launch only; the kernel reads gridDim)
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int BM, int BN, int WM, int WN, int NBUF, int NG, int EPI>
+// SK: the stream-K loop over several segments per workgroup; without it a
+// workgroup runs exactly one segment (the host launches such shapes only on
+// grids whose shares never cross a tile boundary), which keeps the segment
+// state out of the register budget of the 256 x 256 tiles.
+template <int BM, int BN, int WM, int WN, int NBUF, int NG, int EPI, bool SK>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM / 16;                 // x fragments per wave
@@ -69,24 +77,58 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[NBUF * STAGE];
   __shared__ int s_last;
 
-  // XCD-aware tile order: workgroup b runs on XCD b % 8; XCD x takes the
-  // x-th contiguous share of the logical tiles.
-  const int total = a.tiles_m * a.tiles_n * a.nkc;
-  const int bid = blockIdx.x;
-  const int per = total >> 3, rem = total & 7, xcd = bid & 7, loc = bid >> 3;
-  const int t = xcd < rem ? xcd * (per + 1) + loc : rem * (per + 1) + (xcd - rem) * per + loc;
-  const int tm = t % a.tiles_m;
-  const int tk = t / a.tiles_m;
-  const int kc = tk % a.nkc;
-  const int tn = tk / a.nkc;
+  // Stream-K schedule over weight-tile columns.  The work of one M tile is
+  // tiles_n x KU units (a unit: one output tile, 64 of k; units k-major
+  // inside a weight tile).  Workgroup w = s tiles_m + tm takes M tile tm and
+  // share s of the G' = G / tiles_m shares: units [s U' / G', (s+1) U' / G')
+  // of the U' = tiles_n KU, so every workgroup gets the same amount of work
+  // whatever the tile count, and the tiles_m workgroups of a share walk the
+  // same weights at the same k (read once from HBM, then from L2).  A tile
+  // covered by more than one share is a run of segments in k order; each
+  // writes its partial and the last to arrive adds them in that order (fixed,
+  // so the result does not depend on timing).  With G' = tiles_n x c for c
+  // dividing KU this is a plain c-way split of K; with c = 1, one tile per
+  // workgroup.
+  // XCD-aware order: workgroup b runs on XCD b % 8; XCD x takes the x-th
+  // contiguous run of w, so the M tiles of a share run on one XCD.
+  const unsigned G = gridDim.x, bid = blockIdx.x;
+  const unsigned gper = G >> 3, grem = G & 7, xcd = bid & 7, loc = bid >> 3;
+  const unsigned w = xcd < grem ? xcd * (gper + 1) + loc : grem * (gper + 1) + (xcd - grem) * gper + loc;
+  const int tm = __builtin_amdgcn_readfirstlane(w % a.tiles_m);
+  const unsigned sh = w / a.tiles_m, GS = G / a.tiles_m;
+  // The host keeps U' < 2^31 and G < 2^20.  The first unit of share v is
+  // floor(v U' / G') = v q + floor(v r / G'), and the owner of unit X, the
+  // largest v with floor(v U' / G') <= X, is floor(((X+1) G' - 1) / U') (in
+  // fp64, exact below 2^53; the quotient is never within 1/U' of an integer it
+  // is not).
+  const unsigned KU = a.K / 64, U = (unsigned)a.tiles_n * KU;
+  const unsigned uq = U / GS, ur = U % GS;
+  auto first_unit = [&](unsigned v) { return v * uq + (unsigned)((unsigned long long)v * ur / GS); };
+  auto owner = [&](unsigned X) { return (unsigned)((((double)X + 1.0) * GS - 1.0) / U); };
+  unsigned unit = first_unit(sh);
+  const unsigned unit_end = first_unit(sh + 1);
 
   const int M = a.M, Nout = a.Nout, K = a.K;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int r = lane & 15, g = lane >> 4;
+  const int KS = K / 32, nto = Nout / 16;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+
+  for (int seg = 0; unit < unit_end; ++seg) {
+  // the segment's values are uniform: readfirstlane keeps them in scalar
+  // registers across the main loop
+  const int tn = __builtin_amdgcn_readfirstlane(unit / KU);
+  const int ku0 = __builtin_amdgcn_readfirstlane(unit - tn * KU);
+  const int ku1 = __builtin_amdgcn_readfirstlane(min(KU, ku0 + (unit_end - unit)));
+  unit += ku1 - ku0;
+  const int s_first = __builtin_amdgcn_readfirstlane(owner(tn * KU));
+  const int nseg = __builtin_amdgcn_readfirstlane(owner(tn * KU + KU - 1)) - s_first + 1;
+  const int slot = (int)sh - s_first;  // this segment's place in the tile's k order
+  const int w_first = s_first * a.tiles_m + tm;  // owns the tile's counter
+  if (seg > 0) __syncthreads();  // the previous tile's epilogue is done with LDS
   const int m0 = tm * BM;
   const int n0 = tn * (NG == 1 ? BN : HALF);
-  const int KS = K / 32, nto = Nout / 16;
 
   // The units this wave loads: u = wave * UPW + q; u < XU is x row tile u
   // (rows clamped into range: rows past the end are computed and never
@@ -94,7 +136,6 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   // tiles past the edge clamped to the last one).  Address of stage st: the
   // uniform base ubase[q] + st * ustep[q] bytes plus the lane's 32-bit
   // offset vofs[q].
-  const int wv = __builtin_amdgcn_readfirstlane(wave);
   const char* ubase[UPW];
   uint32_t ustep[UPW], vofs[UPW];
 #pragma unroll
@@ -156,9 +197,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   // from LDS while stage st is multiplied.
   bf16x8 xf[2][TM], wf[2][TN];
 
-  // the plan counts K in 64-wide stages; here a stage is one 32-wide k-step
-  const int spc = a.stages_per_chunk * 2;
-  const int st0 = kc * spc, st1 = min(KS, st0 + spc);
+  // a unit is two stages here (a stage is one 32-wide k-step)
+  const int st0 = 2 * ku0, st1 = min(KS, 2 * ku1);
   // Prologue: stages st0 .. st0+NBUF-1 in flight, stage st0 read.  Stages
   // past the chunk re-load its last stage into a buffer nobody reads, so
   // every iteration issues the same number of loads and the wait counts
@@ -223,9 +263,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   };
   auto out_q = [&](int j) { return NG == 1 ? 0 : j / (TN / 2); };
 
-  if (a.nkc > 1) {
-    // Split K: publish the partial with device-coherent stores, count arrivals,
-    // and let the last workgroup of the tile add the partials in chunk order.
+  if (nseg > 1) {
+    // A split tile: publish the partial with device-coherent stores, count
+    // arrivals, and let the last workgroup of the tile add the partials in k
+    // order.  The counter of a split tile is that of its first workgroup
+    // (no two split tiles share one).
     const __amdgpu_buffer_rsrc_t prs = coherent_rsrc(a.part, a.part_bytes);
     auto poff = [&](int c, int m, int j) {
       return (uint32_t)((((size_t)c * M + m) * NG + out_q(j)) * Nout + out_n(j)) * 4u;
@@ -236,22 +278,25 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
       if (m >= M) continue;
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        if (out_n(j) < Nout) coherent_store(prs, poff(kc, m, j), acc[i][j]);
+        if (out_n(j) < Nout) coherent_store(prs, poff(slot, m, j), acc[i][j]);
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    int* cnt = a.counters + ((size_t)tn * a.tiles_m + tm) * kCounterStride;
+    int* cnt = a.counters + (size_t)w_first * kCounterStride;
     if (threadIdx.x == 0)
-      s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.nkc - 1);
+      s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
     __syncthreads();
-    if (!s_last) return;
+    if (!s_last) {
+      if constexpr (SK) continue;
+      else return;
+    }
     if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
-    // Sum all nkc partials (this workgroup's own included, read back) in chunk
+    // Sum all partials (this workgroup's own included, read back) in k
     // order; half of the fragments at a time keeps 16 loads in flight.
     // Fragments past the edge read a clamped in-range address and are dropped.
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      for (int c = 0; c < a.nkc; ++c) {
+      for (int c = 0; c < nseg; ++c) {
 #pragma unroll
         for (int i = h * (TM / 2); i < (h + 1) * (TM / 2); ++i) {
           const int m = min(out_m(i), M - 1);
@@ -346,19 +391,31 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
       }
     }
   }
+  if constexpr (!SK) break;
+  }  // segments
 }
 
-template <int BM, int BN, int WM, int WN, int NBUF>
+template <int BM, int BN, int WM, int WN, int NBUF, bool SK>
 hipError_t launch_shape(const TileK& a, int epi, hipStream_t s) {
-  const dim3 grid(a.tiles_m * a.tiles_n * a.nkc), block(WM * WN * 64);
-  if (epi == kEpiStore) hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 1, kEpiStore>), grid, block, 0, s, a);
+  const dim3 grid(a.grid), block(WM * WN * 64);
+  if (epi == kEpiStore) hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 1, kEpiStore, SK>), grid, block, 0, s, a);
   else if (epi == kEpiResidual)
-    hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 1, kEpiResidual>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 2, kEpiSwiglu>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 1, kEpiResidual, SK>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((gemm_tile_kernel<BM, BN, WM, WN, NBUF, 2, kEpiSwiglu, SK>), grid, block, 0, s, a);
   return hipGetLastError();
+}
+template <int BM, int BN, int WM, int WN, int NBUF>
+hipError_t launch_shape_any(const TileK& a, int epi, bool one_segment, hipStream_t s) {
+  return one_segment ? launch_shape<BM, BN, WM, WN, NBUF, false>(a, epi, s)
+                     : launch_shape<BM, BN, WM, WN, NBUF, true>(a, epi, s);
 }
 
 }  // namespace
+
+bool tile_one_segment(const GemmPlan& p, int K) {
+  const long tiles = (long)p.ntiles * p.mblocks;
+  return p.grid % tiles == 0 && p.grid / tiles <= K / 64;
+}
 
 int tile_bm(int cfg) { return cfg == kTile256x256 ? 256 : cfg == kTile192x256 ? 192 : 128; }
 int tile_bn(int cfg) { return cfg == kTile128x128 ? 128 : 256; }
@@ -367,20 +424,29 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
                             int* counters, float* part, hipStream_t s, float* stats, bool x_kblocked,
                             bool y_kblocked) {
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
-  TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
-          p.nkc > 1 ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles, p.nkc, p.stages_per_chunk,
+  const bool split = p.part_bytes > 0;
+  const long units = (long)p.ntiles * (K / 64);  // per M tile
+  if (p.grid < p.mblocks || p.grid % p.mblocks || p.grid / p.mblocks > units || p.grid >= (1 << 20) ||
+      units >= (1L << 31) || (split && (!part || !counters)))
+    return hipErrorInvalidValue;
+  TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, split ? part : nullptr,
+          split ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles,
           (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk,
-          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0};
+          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid};
+  const bool one_segment = tile_one_segment(p, K);
   switch (p.tile) {
     // 4 waves of 128 x 128 (a quarter fewer LDS reads per MFMA; all 512
     // registers per lane), 8 waves of 128 x 64 for SwiGLU, whose epilogue
-    // would not fit beside the larger accumulators
+    // would not fit beside the larger accumulators; one segment per
+    // workgroup only (the stream-K loop's state does not fit beside them)
     case kTile256x256:
-      return epi == kEpiSwiglu ? launch_shape<256, 256, 2, 4, 4>(a, epi, s) : launch_shape<256, 256, 2, 2, 4>(a, epi, s);
+      if (!one_segment) return hipErrorInvalidValue;
+      return epi == kEpiSwiglu ? launch_shape<256, 256, 2, 4, 4, false>(a, epi, s)
+                               : launch_shape<256, 256, 2, 2, 4, false>(a, epi, s);
     // 4 waves of 96 x 128: windows of 3 x 128 (or 6 x 64) rows without a padded tile
-    case kTile192x256: return launch_shape<192, 256, 2, 2, 4>(a, epi, s);
-    case kTile128x256: return launch_shape<128, 256, 2, 4, 4>(a, epi, s);
-    default: return launch_shape<128, 128, 2, 2, 4>(a, epi, s);
+    case kTile192x256: return launch_shape_any<192, 256, 2, 2, 4>(a, epi, one_segment, s);
+    case kTile128x256: return launch_shape_any<128, 256, 2, 4, 4>(a, epi, one_segment, s);
+    default: return launch_shape_any<128, 128, 2, 2, 4>(a, epi, one_segment, s);
   }
 }
 

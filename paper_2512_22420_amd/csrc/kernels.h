@@ -31,10 +31,18 @@ struct GemmPlan {
   int mt, nw, ntiles, mblocks, nkc, stages_per_chunk;
   int depth;  // streaming kernel: weight stages in flight ahead of the one being multiplied (1 or 3)
   size_t part_bytes, counter_bytes;
+  int grid;   // tiled kernel: workgroups of the stream-K schedule
 };
 GemmPlan gemm_plan(int M, int N, int K, int epi);
-// Plan of the LDS-tiled kernel with a given tile shape and K split.
+// Plan of the LDS-tiled kernel with a given tile shape and K split (grid =
+// tiles x nkc).
 GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc);
+// Plan of the LDS-tiled kernel with a given tile shape on `grid` workgroups
+// that share the tiles x K/64 units of work evenly (stream-K).
+GemmPlan gemm_tile_plan_sk(int M, int N, int K, int epi, int tile, int grid);
+// Whether every workgroup of a tiled plan works inside one tile (grid = tiles
+// x c, c <= K/64), as the 256 x 256 tile requires.
+bool tile_one_segment(const GemmPlan& p, int K);
 // The tiled kernel needs K % 64 == 0 and operands of fewer than 2^31 elements.
 bool tile_fits(int M, int N, int K);
 // Best tiled plan by the cost model (only_tile = kTileNone: any tile shape).
@@ -50,13 +58,16 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split, int depth);
 GemmPlan gemm_logits_widen(const GemmPlan& p, int M, int N);
 int tile_bm(int tile);
 int tile_bn(int tile);
-// Split K only happens when ntiles * mblocks <= 256, so every GEMM's arrival
-// counters fit in this many bytes (a fixed region, whatever M, N, K).
+// Arrival counters of split-K hand-offs live in one fixed region, whatever
+// M, N, K: the streaming kernel splits K only when ntiles * mblocks <= 256,
+// and a tiled run that splits tiles has at most kGemmMaxSplitGrid workgroups
+// (one counter per workgroup at most).
 // Arrival counters that many workgroups increment are kept 256 bytes apart:
 // device-scope atomics on one cache line are serialised, so counters that
 // share a line make every workgroup of a launch wait for all the others'.
 constexpr int kCounterStride = 64;  // ints
-constexpr size_t kGemmCounterBytes = 128 * kCounterStride * 4;  // split-K counters of up to 128 output tiles
+constexpr int kGemmMaxSplitGrid = 1024;
+constexpr size_t kGemmCounterBytes = (size_t)kGemmMaxSplitGrid * kCounterStride * 4;
 // Split-K partials are addressed with 32-bit buffer offsets.
 constexpr size_t kMaxPartBytes = (size_t)1 << 31;
 

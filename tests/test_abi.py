@@ -99,9 +99,20 @@ def test_gemm_with_plan_rejects_impossible_plans_on_host():
     assert L.nightjar_gemm_with_plan(nb.NJ_BF16, 16, 16, 16, 200, 256, 96, st, nb.NJ_GEMM_TILE_128x128, 0, 256, ws, 0) \
         == nb.NJ_EINVAL
     assert "K % 64" in nb.last_error()
-    # a split run may cover at most 1024 output tiles
+    # a run that cuts tiles between workgroups may have at most 1024 of them
     assert nb.lib().nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 768, 128256, 4096, st, nb.NJ_GEMM_TILE_128x128, 2) == 0
-    assert "output tiles" in nb.last_error()
+    assert "at most 1024 workgroups" in nb.last_error()
+    assert nb.lib().nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 768, 4096, 4096, st, nb.NJ_GEMM_TILE_128x128,
+                                                       -1100) == 0
+    # stream-K grids: tiled kernels only, and not the 256x256 tile
+    assert nb.lib().nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 768, 4096, 4096, st, nb.NJ_GEMM_TILE_256x256,
+                                                       -100) == 0
+    assert "256x256" in nb.last_error()
+    assert nb.lib().nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 768, 4096, 4096, st, nb.NJ_GEMM_TILE_128x256,
+                                                       -100) > 0
+    # a grid of 3 x 12 workgroups on 12 tiles is a plain 3-way split, which the 256x256 tile runs
+    assert nb.lib().nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 768, 1024, 4096, st, nb.NJ_GEMM_TILE_256x256,
+                                                       -36) > 0
     # auto plan takes no split; fp32 has one kernel; bad kernel id
     assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, nb.NJ_GEMM_AUTO, 2) == 0
     assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_F32, 64, 256, 256, st, nb.NJ_GEMM_STREAM, 0) == 0

@@ -123,6 +123,14 @@ def _gemm_tol(ref, epi):
     (nb.NJ_GEMM_TILE_128x128, 3, 257, 1024, 2048, nb.NJ_GEMM_RESIDUAL),    # split that is not a power of 2
     (nb.NJ_GEMM_TILE_128x128, 0, 768, 2 * 1024, 512, nb.NJ_GEMM_SWIGLU),
     (nb.NJ_GEMM_TILE_128x128, 0, 1, 272, 64, nb.NJ_GEMM_STORE),            # one row, one stage
+    # stream-K: workgroups that span several tiles, tiles cut into many
+    # segments, one unit per workgroup, shares crossing ragged tiles
+    (nb.NJ_GEMM_TILE_128x128, -7, 257, 1024, 2048, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_TILE_128x256, -100, 130, 2 * 704, 1024, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_192x256, -37, 384, 4096, 1024, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_128x128, -5, 65, 384, 256, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_128x256, -1000, 129, 512, 4096, nb.NJ_GEMM_STORE),   # capped at 256 units: one each
+    (nb.NJ_GEMM_TILE_192x256, -300, 500, 2 * 1008, 2048, nb.NJ_GEMM_SWIGLU),
     (nb.NJ_GEMM_STREAM, 3, 48, 4096, 4096, nb.NJ_GEMM_STORE),              # streaming kernel, forced split
     (nb.NJ_GEMM_STREAM, 1, 200, 1024, 1024, nb.NJ_GEMM_RESIDUAL),          # streaming kernel past 64 rows
     (nb.NJ_GEMM_STREAM, 0, 80, 4112, 1024, nb.NJ_GEMM_STORE),              # persistent, 5 row tiles, ragged group
@@ -318,6 +326,32 @@ def test_accept_edge_uniforms():
     acc, nxt = _run_accept(V, logits, drafts, q, u)
     assert acc[0] == 0 and nxt[0, 0] != 5 and nxt[0, 0] == V - 1  # residual p - q > 0 everywhere but token 5
     assert acc[1] == 2 and nxt[1, 2] == 0  # bonus draw with u = 0 takes the first positive weight
+
+
+@pytest.mark.parametrize("kernel,split,M,N,K", [
+    (nb.NJ_GEMM_TILE_128x256, -200, 768, 4096, 14336),
+    (nb.NJ_GEMM_TILE_128x128, -300, 300, 1024, 4096),
+])
+def test_gemm_stream_k_is_deterministic_and_reusable(kernel, split, M, N, K):
+    """Stream-K segments of a cut tile are summed in k order by whichever
+    workgroup arrives last, and the counters are left at zero: repeated calls
+    on one workspace give bitwise-identical results."""
+    rng = np.random.default_rng(98)
+    dx = _dev(W.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32)))
+    dw = _devw(W.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02))
+    nbytes = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, M, N, K, nb.NJ_GEMM_STORE, kernel, split)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    nb.workspace_init(ws.data_ptr(), nbytes, _stream())
+    outs = []
+    for _ in range(4):
+        y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        nb.gemm_with_plan(nb.NJ_BF16, dx.data_ptr(), dw.data_ptr(), y.data_ptr(), M, N, K, nb.NJ_GEMM_STORE, kernel,
+                          split, ws.data_ptr(), nbytes, _stream())
+        outs.append(y)
+    torch.cuda.synchronize()
+    for y in outs[1:]:
+        assert torch.equal(y, outs[0])
+    assert not torch.isnan(outs[0]).any()
 
 
 def test_gemm_split_k_is_deterministic_and_reusable():
