@@ -377,7 +377,7 @@ def test_stale_workspace_contents_never_reach_the_outputs(k):
     x = _inputs(SMALL_BF16, ctx, k, seed=21)
     model, _, io_f, _, err_f = _run(SMALL_BF16, x)
     ws = Workspace(SMALL_BF16, len(ctx), k)
-    zero_prefix = 256 + 128 * 256  # error word, split-K arrival counters (128, 256 bytes apart)
+    zero_prefix = 256 + 1024 * 256  # error word, split-K arrival counters (1024, 256 bytes apart)
     ws.buf[zero_prefix:].fill_(255)
     _, _, io_s, _, err_s = _run(SMALL_BF16, x, model=model, ws=ws)
     assert err_f == 0 and err_s == 0
