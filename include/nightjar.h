@@ -443,7 +443,10 @@ enum {
   NJ_GEMM_TILE_128x256 = 3,
   NJ_GEMM_TILE_128x128 = 4,
   NJ_GEMM_STREAM_DEEP = 5,  /* weight-streaming kernel, 3 stages in flight per wave  */
-  NJ_GEMM_TILE_192x256 = 6  /* LDS-tiled kernel, 192-row x tiles (windows of 3 x 64 rows)    */
+  NJ_GEMM_TILE_192x256 = 6, /* LDS-tiled kernel, 192-row x tiles (windows of 3 x 64 rows)    */
+  NJ_GEMM_TILE_160x256 = 7, /* LDS-tiled kernel, 160-row x tiles (windows of 2 x 160 rows)   */
+  NJ_GEMM_TILE_96x256 = 8,  /* LDS-tiled kernels with small tiles, for weight matrices      */
+  NJ_GEMM_TILE_96x128 = 9   /* with few rows (more tiles to fill the chip)                  */
 };
 
 /*

@@ -18,6 +18,7 @@ NJ_GEMM_STORE, NJ_GEMM_RESIDUAL, NJ_GEMM_SWIGLU = 0, 1, 2
 NJ_GEMM_KBLOCKED = 16  # flag: x (and a SwiGLU y) k-blocked, [K/32][M][32]
 NJ_GEMM_AUTO, NJ_GEMM_STREAM, NJ_GEMM_TILE_256x256, NJ_GEMM_TILE_128x256, NJ_GEMM_TILE_128x128 = 0, 1, 2, 3, 4
 NJ_GEMM_TILE_192x256 = 6
+NJ_GEMM_TILE_160x256, NJ_GEMM_TILE_96x256, NJ_GEMM_TILE_96x128 = 7, 8, 9
 NJ_GEMM_STREAM_DEEP = 5
 
 _vp = ctypes.c_void_p

@@ -60,7 +60,7 @@ struct GemmShape {
 };
 void step_gemms(const nj_model_desc& d, GemmShape out[5]) {
   const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
-  out[0] = {QKV, d.d_model, kEpiStore};
+  out[0] = {QKV, d.d_model, kEpiQkvRope};  // planned as the QKV projection (a streaming plan carries RoPE)
   out[1] = {d.d_model, HD, kEpiResidual};
   out[2] = {2 * d.ffn_dim, d.d_model, kEpiSwiglu};
   out[3] = {d.d_model, d.ffn_dim, kEpiResidual};
@@ -93,10 +93,18 @@ bool desc_ok(const nj_model_desc* d) {
 
 // Whether a window of M rows runs with the RMSNorms folded into the GEMMs:
 // bf16 with every GEMM of the step on the weight-streaming kernel.
+// The QKV projection without RoPE in its epilogue (fp32 q/k/v rows for the
+// RoPE kernel), on the plan chosen for the QKV projection.
+hipError_t launch_qkv_store(int dt, const void* x, const void* w, void* y, int M, int N, int K, int* gcnt, float* gpart,
+                            hipStream_t s, bool x_kblocked) {
+  if (dt != kBF16) return launch_gemm(dt, x, w, y, M, N, K, kEpiStore, gcnt, gpart, s, x_kblocked);
+  return launch_gemm_plan(x, w, y, M, N, K, kEpiStore, gemm_plan(M, N, K, kEpiQkvRope), gcnt, gpart, s, x_kblocked);
+}
+
 bool fold_norms(const nj_model_desc& d, int M) {
   if (d.dtype != NJ_BF16) return false;
   const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
-  return gemm_streams(M, QKV, d.d_model, kEpiStore) && gemm_streams(M, d.d_model, HD, kEpiResidual) &&
+  return gemm_streams(M, QKV, d.d_model, kEpiQkvRope) && gemm_streams(M, d.d_model, HD, kEpiResidual) &&
          gemm_streams(M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu) &&
          gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual) && gemm_streams(M, d.vocab, d.d_model, kEpiStore);
 }
@@ -127,6 +135,7 @@ Layout layout(const nj_model_desc& d, int B, int k) {
     GemmShape gs[5];
     step_gemms(d, gs);
     for (const GemmShape& g : gs) part = std::max(part, gemm_plan((int)M, g.N, g.K, g.epi).part_bytes);
+    if (M >= (size_t)kTileMinRows) part = std::max(part, kSplitPartCap);  // any smaller window's plans fit
   }
   L.h = take(M * d.d_model * 4);
   L.x = take(M * d.d_model * e);
@@ -174,7 +183,9 @@ PreLayout pre_layout(const nj_model_desc& d, int B, int k) {
   L.ssq = take(M * ((d.d_model + 127) / 128) * 4);
   L.rope_cs = take(M * 64 * 2 * 4);
   L.qkv = take(M * QKV * 4);
-  L.gemm_part = take(d.dtype == NJ_BF16 ? gemm_plan((int)M, QKV, d.d_model, kEpiStore).part_bytes : 0);
+  size_t part = d.dtype == NJ_BF16 ? gemm_plan((int)M, QKV, d.d_model, kEpiQkvRope).part_bytes : 0;
+  if (d.dtype == NJ_BF16 && M >= (size_t)kTileMinRows) part = std::max(part, kSplitPartCap);
+  L.gemm_part = take(part);
   L.total = off;
   return L;
 }
@@ -409,7 +420,7 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   // Without the folded norm, the input of each GEMM that runs on the
   // LDS-tiled kernel is written k-blocked by its producer (norm, attention,
   // SwiGLU epilogue), so the tile loads read 1 KB contiguous units.
-  const bool kb_qkv = bf && !fused && !gemm_streams(M, QKV, d.d_model, kEpiStore);
+  const bool kb_qkv = bf && !fused && !gemm_streams(M, QKV, d.d_model, kEpiQkvRope);
   const bool kb_o = bf && !fused && !gemm_streams(M, d.d_model, HD, kEpiResidual);
   const bool kb_gu = bf && !fused && !gemm_streams(M, F2, d.d_model, kEpiSwiglu);
   const bool kb_dn = bf && !fused && d.ffn_dim % 32 == 0 && !gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual);
@@ -425,7 +436,7 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   const AttnPlan* pl = bf ? &plan : nullptr;
   // Norms not folded, but a QKV GEMM that still streams: RoPE and the window
   // store in its epilogue (no row scale), from the table the embedding kernel writes
-  const bool rope_in_qkv = !fused && bf && gemm_streams(M, QKV, d.d_model, kEpiStore);
+  const bool rope_in_qkv = !fused && bf && gemm_streams(M, QKV, d.d_model, kEpiQkvRope);
   if (fused)
     NJ_TRY(NJ_PROF_EMBED, launch_embed_gather(last_tokens, draft_tokens, B, T, w->embed, w->layers[0].attn_norm, h, x, ssq, d.d_model,
                                d.vocab, err, context_lens, d.rope_theta, reinterpret_cast<float*>(ws + L.rope_cs), s, pl),
@@ -455,7 +466,7 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
         NJ_TRY(NJ_PROF_QKV, launch_gemm_norm(x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiQkvRope, unscaled, gcnt, gpart, s, &rope),
                "qkv gemm");
       } else {
-        NJ_TRY(NJ_PROF_QKV, launch_gemm(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb_qkv), "qkv gemm");
+        NJ_TRY(NJ_PROF_QKV, launch_qkv_store(dt, x, lw.w_qkv, qkv, M, QKV, d.d_model, gcnt, gpart, s, kb_qkv), "qkv gemm");
         NJ_TRY(NJ_PROF_ROPE, launch_rope_window(dt, qkv, context_lens, B, T, d.n_heads, d.n_kv_heads, d.head_dim, d.rope_theta, q,
                                   wk, wv, snap, acnt, s),
                "rope");
@@ -709,10 +720,9 @@ int nightjar_rmsnorm_rope(const nj_model_desc* desc, const float* h, const void*
     e = launch_gemm_norm(ws + L.x, w_qkv, ws + L.qkv, M, QKV, d.d_model, kEpiQkvRope, scale_in, gcnt, gpart, s, &rope);
     return e == hipSuccess ? NJ_OK : hip_fail(e, "rmsnorm_rope: qkv gemm");
   }
-  const bool kb = bf && !gemm_streams(M, QKV, d.d_model, kEpiStore);
+  const bool kb = bf && !gemm_streams(M, QKV, d.d_model, kEpiQkvRope);
   e = launch_rmsnorm(dt, h, attn_norm, ws + L.x, M, d.d_model, d.rms_eps, s, kb);
-  if (e == hipSuccess)
-    e = launch_gemm(dt, ws + L.x, w_qkv, ws + L.qkv, M, QKV, d.d_model, kEpiStore, gcnt, gpart, s, kb);
+  if (e == hipSuccess) e = launch_qkv_store(dt, ws + L.x, w_qkv, ws + L.qkv, M, QKV, d.d_model, gcnt, gpart, s, kb);
   if (e == hipSuccess)
     e = launch_rope_window(dt, reinterpret_cast<const float*>(ws + L.qkv), context_lens, B, T, d.n_heads,
                            d.n_kv_heads, d.head_dim, d.rope_theta, q_out, win_k, win_v, nullptr, nullptr, s);
@@ -884,7 +894,7 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
   if (gemm_args_ok(dtype, M, N, K, epilogue) != NJ_OK) return NJ_EINVAL;
   if (split < 0 && (kernel == NJ_GEMM_AUTO || kernel == NJ_GEMM_STREAM || kernel == NJ_GEMM_STREAM_DEEP))
     return fail(NJ_EINVAL, "split_k < 0 (stream-K) needs a tiled kernel");
-  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_TILE_192x256) return fail(NJ_EINVAL, "bad kernel choice");
+  if (kernel < NJ_GEMM_AUTO || kernel > NJ_GEMM_TILE_96x128) return fail(NJ_EINVAL, "bad kernel choice");
   if (dtype != NJ_BF16) {
     if (kernel != NJ_GEMM_AUTO || split) return fail(NJ_EINVAL, "the fp32 GEMM has a single kernel and no split");
     *out = GemmPlan{};
@@ -903,6 +913,9 @@ static int plan_with(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t epi
     if (!tile_fits(M, N, K)) return fail(NJ_EINVAL, "the tiled kernels need K %% 64 == 0 and M*K, N*K < 2^31");
     const int tile = kernel == NJ_GEMM_TILE_256x256   ? kTile256x256
                      : kernel == NJ_GEMM_TILE_192x256 ? kTile192x256
+                     : kernel == NJ_GEMM_TILE_160x256 ? kTile160x256
+                     : kernel == NJ_GEMM_TILE_96x256  ? kTile96x256
+                     : kernel == NJ_GEMM_TILE_96x128  ? kTile96x128
                      : kernel == NJ_GEMM_TILE_128x256 ? kTile128x256
                                                       : kTile128x128;
     p = split > 0   ? gemm_tile_plan(M, N, K, epilogue, tile, std::min(split, K / 64))

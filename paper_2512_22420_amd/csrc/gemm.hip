@@ -40,6 +40,8 @@
 // product unchanged.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
+#include <unordered_map>
 #include <utility>
 
 #include "common.h"
@@ -52,7 +54,6 @@ constexpr int kSU = 4;                   // 32-wide k-steps per stage
 constexpr int kSK = 32 * kSU;            // 128 k per stage
 constexpr int kXStride = kSK + 8;        // LDS row stride in elements (+16 bytes)
 constexpr int kNW = 8;                   // waves per workgroup
-constexpr int kTileMinRows = 65;         // windows of more than 64 rows may use the LDS-tiled kernel
 constexpr int kSplitTargetWorkgroups = 256;
 constexpr int kRedBatch = 4;             // split-K partials loaded together by the reducing workgroup
 
@@ -817,58 +818,78 @@ GemmPlan gemm_tile_plan(int M, int N, int K, int epi, int tile, int nkc) {
 }
 
 namespace {
-// Cost models (seconds) used to pick the kernel for windows of 64+ rows,
-// with constants fitted to a sweep of the 8B- and 7B-shaped GEMMs at 64..2048
-// rows (the chosen plan is within 15% of the best measured one everywhere).
+// Cost models (seconds) used to pick the kernel for windows of 65+ rows,
+// with constants fitted to sweeps of the 8B- and 7B-shaped GEMMs (QKV, O,
+// gate/up, down, LM head) at 65..2048 rows over both kernels, every tile
+// shape, K split and a 256-workgroup stream-K grid: the plan chosen is the
+// fastest measured one, or within 3% of it, at 68 of 77 points and within
+// 11% at the others.
 // Tiled kernel: rounds of resident workgroups times one tile's MFMA time at
-// the tile shape's sustained fraction of peak, plus, when K is split, the
+// the tile shape's sustained fraction of peak, plus, when tiles are cut, the
 // last arriver's reduction (one CU reads nkc partial tiles) and the partial
 // traffic.
 constexpr double kLaunch = 5e-6;
+constexpr double kCuPeak = 2.5e15 / 256.0;  // bf16 MFMA FLOP/s of one CU
+constexpr int kTileShapes[] = {kTile256x256, kTile192x256, kTile160x256, kTile128x256, kTile96x256, kTile96x128,
+                               kTile128x128};
+// sustained fraction of a CU's MFMA peak with k-blocked x
+double tile_eff(int tile) {
+  switch (tile) {
+    case kTile256x256: return 0.56;
+    case kTile192x256: return 0.46;
+    case kTile160x256: return 0.52;
+    case kTile128x256: return 0.46;
+    case kTile96x256: return 0.42;
+    default: return 0.32;  // 96 x 128 and 128 x 128
+  }
+}
+// workgroups of the shape a CU holds at once (LDS and registers): two of the
+// small tiles, one of the others
+int tile_occupancy(int tile) { return tile == kTile128x128 || tile == kTile96x128 ? 2 : 1; }
 double tile_cost(const GemmPlan& p, int M, int N, int K) {
   const int bm = tile_bm(p.tile), bn = tile_bn(p.tile);
-  // sustained fraction of a CU's MFMA peak with k-blocked x; 128x128 tiles
-  // reach about the same with one or two workgroups on a CU
-  const double eff = p.tile == kTile256x256 ? 0.49 : p.tile == kTile192x256 ? 0.44 : p.tile == kTile128x256 ? 0.37 : 0.31;
   const double wgs = (double)p.grid;
-  const double per_cu = p.tile == kTile128x128 && wgs > 256.0 ? 2.0 : 1.0;  // resident workgroups per CU
+  // a CU takes a second workgroup only when the grid has more than one per CU
+  const double per_cu = std::max(1.0, std::min((double)tile_occupancy(p.tile), std::ceil(wgs / 256.0)));
   const double rounds = std::ceil(wgs / (256.0 * per_cu));
-  double t = rounds * per_cu * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (2.5e15 / 256.0 * eff);
-  if (p.nkc > 1) t += 2.0 * p.nkc * bm * bn * 4 / 1e11 + 2.0 * p.nkc * (double)M * N * 4 / 5e12;
+  double t = rounds * per_cu * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (kCuPeak * tile_eff(p.tile));
+  if (p.nkc > 1) t += 2.0 * p.nkc * bm * bn * 4 / 5e10 + 2.0 * p.nkc * (double)M * N * 4 / 5e12;
   return t + kLaunch;
 }
-// Weight-streaming kernel: one pass over the weights per 64-row block, later
-// passes partly served from the caches.
-double stream_cost(int M, int N, int K) {
-  const int mb = (M + 63) / 64;
-  return (double)N * K * 2 * (1.0 + 0.7 * (mb - 1)) / 4e12 + kLaunch;
+// Weight-streaming kernel: rounds of workgroups (one per CU), each streaming
+// 128 weight rows of its K chunk at ~40 GB/s per CU or multiplying them by
+// its 16..64 x rows at ~0.22 of the CU's MFMA peak (LDS-bound), whichever is
+// longer.
+double stream_cost(int M, int N, int K, int epi) {
+  const GemmPlan p = gemm_stream_plan(M, N, K, epi, 0, 1);
+  const double rounds = std::ceil((double)p.ntiles * p.mblocks * p.nkc / 256.0);
+  const double kchunk = 128.0 * p.stages_per_chunk;
+  const double t_wg = std::max(128.0 * kchunk * 2 / 40e9, 2.0 * 128 * (16.0 * p.mt) * kchunk / (kCuPeak * 0.22));
+  return 8e-6 + rounds * t_wg + (p.nkc > 1 ? 3e-6 : 0.0);
 }
+// A QKV projection that streams applies RoPE and stores the window K/V in its
+// epilogue; a tiled one leaves that to a kernel of its own.
+double rope_kernel_cost(int M) { return 5e-6 + 9e-9 * M; }
 }  // namespace
 
 GemmPlan gemm_tile_choose(int M, int N, int K, int epi, int only_tile) {
   GemmPlan best{};
   double bc = 1e30;
-  for (int tile : {kTile256x256, kTile192x256, kTile128x256, kTile128x128}) {
+  auto consider = [&](const GemmPlan& p) {
+    if (p.nkc > 1 && (p.counter_bytes > kGemmCounterBytes || p.part_bytes > kSplitPartCap)) return;
+    const double c = tile_cost(p, M, N, K);
+    if (c < bc) bc = c, best = p;
+  };
+  for (int tile : kTileShapes) {
     if (only_tile != kTileNone && tile != only_tile) continue;
     for (int nkc = 1; nkc <= 8; nkc *= 2) {
       if (nkc > 1 && K / 64 / nkc < 8) break;
-      const GemmPlan p = gemm_tile_plan(M, N, K, epi, tile, nkc);
-      if (p.nkc > 1 && (p.counter_bytes > kGemmCounterBytes || p.part_bytes >= kMaxPartBytes)) continue;
-      const double c = tile_cost(p, M, N, K);
-      if (c < bc) bc = c, best = p;
+      consider(gemm_tile_plan(M, N, K, epi, tile, nkc));
     }
-    // Stream-K on one workgroup per CU, when the tiles leave CUs idle: only
-    // for the long reductions of the down projection (K >= 8192), the one
-    // place where a sweep of the 8B and 7B shapes at 320..2048 rows found it
-    // ahead (4-5%); on the other GEMMs the cut tiles' partials cost more than
-    // the balance gains.
-    if (tile != kTile256x256 && epi == kEpiResidual && K >= 8192 &&
-        (long)gemm_tile_plan(M, N, K, epi, tile, 1).grid % 256 != 0) {
-      const GemmPlan p = gemm_tile_plan_sk(M, N, K, epi, tile, 256);
-      if (p.nkc > 1 && (p.counter_bytes > kGemmCounterBytes || p.part_bytes >= kMaxPartBytes)) continue;
-      const double c = tile_cost(p, M, N, K);
-      if (c < bc) bc = c, best = p;
-    }
+    // Stream-K on one workgroup per CU when the tiles leave CUs idle (not for
+    // the 256 x 256 tile, which runs one segment per workgroup).
+    if (tile != kTile256x256 && (long)gemm_tile_plan(M, N, K, epi, tile, 1).grid % 256 != 0)
+      consider(gemm_tile_plan_sk(M, N, K, epi, tile, 256));
   }
   return best;
 }
@@ -885,7 +906,8 @@ GemmPlan gemm_logits_widen(const GemmPlan& p, int M, int N) {
   return logits_persistent_grid(q, N) > 0 ? q : p;
 }
 
-GemmPlan gemm_plan(int M, int N, int K, int epi) {
+namespace {
+GemmPlan gemm_plan_uncached(int M, int N, int K, int epi) {
   if (M >= kTileMinRows && tile_fits(M, N, K)) {
     // wide fp32-store GEMMs (the LM head) of up to 96 rows: the persistent
     // kernel reads the weights once and runs ~10% ahead of the best tile
@@ -895,10 +917,36 @@ GemmPlan gemm_plan(int M, int N, int K, int epi) {
       if (sp.mt > 4 && logits_persistent_grid(sp, N) >= 256) return sp;
     }
     const GemmPlan t = gemm_tile_choose(M, N, K, epi, kTileNone);
-    // the tiled kernel only when clearly ahead: the two models err by ~15%
-    if (tile_cost(t, M, N, K) < 0.85 * stream_cost(M, N, K)) return t;
+    const double extra = epi == kEpiQkvRope ? rope_kernel_cost(M) : 0.0;
+    if (tile_cost(t, M, N, K) + extra < stream_cost(M, N, K, epi)) return t;
   }
   return gemm_stream_plan(M, N, K, epi, 0, 1);
+}
+}  // namespace
+
+// The plan depends only on (M, N, K, epilogue) and a verify step asks for
+// the same few plans several times per launch (workspace layout, which
+// kernels the norms fold into, the launches), while scoring every tile shape
+// and stream-K grid costs tens of microseconds of host time for the LM head:
+// plans are kept in a small table (cleared when it fills).
+GemmPlan gemm_plan(int M, int N, int K, int epi) {
+  static std::mutex mu;
+  static std::unordered_map<uint64_t, GemmPlan> memo;
+  const uint64_t key = ((uint64_t)(uint32_t)M << 40) ^ ((uint64_t)(uint32_t)N << 20) ^ ((uint64_t)(uint32_t)K << 4) ^
+                       (uint64_t)(uint32_t)epi;
+  {
+    std::lock_guard<std::mutex> g(mu);
+    const auto it = memo.find(key);
+    if (it != memo.end() && it->second.key_m == M && it->second.key_n == N && it->second.key_k == K &&
+        it->second.key_epi == epi)
+      return it->second;
+  }
+  GemmPlan p = gemm_plan_uncached(M, N, K, epi);
+  p.key_m = M, p.key_n = N, p.key_k = K, p.key_epi = epi;
+  std::lock_guard<std::mutex> g(mu);
+  if (memo.size() >= 4096) memo.clear();
+  memo[key] = p;
+  return p;
 }
 
 GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split, int depth) {
@@ -918,7 +966,8 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split, int depth) {
   if (split > 0) nkc = std::min(split, nst);
   else
     while (base * nkc * 2 <= kSplitTargetWorkgroups && nst / (nkc * 2) >= 8) nkc *= 2;
-  if (split <= 0 && (size_t)nkc * M * N * 4 >= kMaxPartBytes) nkc = 1;
+  if (split <= 0)
+    while (nkc > 1 && (size_t)nkc * M * N * 4 > kSplitPartCap) nkc /= 2;
   p.stages_per_chunk = (nst + nkc - 1) / nkc;
   p.nkc = (nst + p.stages_per_chunk - 1) / p.stages_per_chunk;
   p.depth = depth;
@@ -966,7 +1015,7 @@ int logits_stat_entries(int M, int N, int K) {
 
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
                             int* counters, float* part, hipStream_t s, const QkvRope* rope) {
-  const int pe = epi == kEpiResidualNorm ? kEpiResidual : (epi == kEpiLogits || epi == kEpiQkvRope) ? kEpiStore : epi;
+  const int pe = epi == kEpiResidualNorm ? kEpiResidual : epi == kEpiLogits ? kEpiStore : epi;
   const GemmPlan p = gemm_plan(M, N, K, pe);
   if (p.tile != kTileNone) return hipErrorInvalidValue;  // the caller checks gemm_streams first
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;

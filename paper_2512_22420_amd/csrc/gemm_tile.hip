@@ -57,6 +57,17 @@ struct TileK {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// stage buffers of the smaller tile shapes (compile-time settings)
+#ifndef NJ_NBUF_192x256
+#define NJ_NBUF_192x256 4
+#endif
+#ifndef NJ_NBUF_128x256
+#define NJ_NBUF_128x256 4
+#endif
+#ifndef NJ_NBUF_128x128
+#define NJ_NBUF_128x128 4
+#endif
+
 // SK: the stream-K loop over several segments per workgroup; without it a
 // workgroup runs exactly one segment (the host launches such shapes only on
 // grids whose shares never cross a tile boundary), which keeps the segment
@@ -67,11 +78,14 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   constexpr int TM = BM / WM / 16;                 // x fragments per wave
   constexpr int TN = BN / WN / 16;                 // weight fragments per wave
   constexpr int XU = BM / 16, WU = BN / 16;        // 1 KB units per stage
-  constexpr int UPW = (XU + WU) / NW;              // units each wave loads per stage
+  // units each wave loads per stage; when they do not split evenly, the
+  // surplus slots of the last waves load the stage's last unit again, to the
+  // same LDS address (the same bytes), so every wave issues the same number
+  // of loads and the load-counter waits below stay exact
+  constexpr int UPW = (XU + WU + NW - 1) / NW;
   constexpr int STAGE = (XU + WU) * 512;           // bf16 elements per stage buffer
   constexpr int DIST = NBUF - 1;                   // stages in flight ahead of the one multiplied
   constexpr int HALF = BN / 2;                     // SwiGLU: gate rows, then up rows
-  static_assert(UPW * NW == XU + WU, "a stage's units must split evenly over the waves");
   static_assert(NG == 1 || (TN % 2 == 0), "SwiGLU waves hold gate and up fragments in pairs");
   static_assert(DIST * UPW <= 63, "load counter range");
   __shared__ __attribute__((aligned(16))) bf16_t lds[NBUF * STAGE];
@@ -130,7 +144,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   const int m0 = tm * BM;
   const int n0 = tn * (NG == 1 ? BN : HALF);
 
-  // The units this wave loads: u = wave * UPW + q; u < XU is x row tile u
+  // The units this wave loads: u = min(wave * UPW + q, XU + WU - 1); u < XU is x row tile u
   // (rows clamped into range: rows past the end are computed and never
   // stored), else weight tile u - XU (SwiGLU: gate tiles, then up tiles;
   // tiles past the edge clamped to the last one).  Address of stage st: the
@@ -140,7 +154,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   uint32_t ustep[UPW], vofs[UPW];
 #pragma unroll
   for (int q = 0; q < UPW; ++q) {
-    const int u = wv * UPW + q;
+    const int u = min(wv * UPW + q, XU + WU - 1);
     if (u < XU) {
       // row-major x: 64 bytes of each of 16 rows; k-blocked x: one 1 KB run
       const uint32_t row = (uint32_t)min(m0 + u * 16 + r, M - 1);
@@ -163,7 +177,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void*)lds;
   auto issue1 = [&](int q, int st, int buf) {
     const char* sb = ubase[q] + (size_t)st * ustep[q];
-    const uint32_t dst = lds_base + (uint32_t)(buf * STAGE + (wv * UPW + q) * 512) * 2u;
+    const uint32_t dst = lds_base + (uint32_t)(buf * STAGE + min(wv * UPW + q, XU + WU - 1) * 512) * 2u;
     asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(vofs[q]), "s"(sb), "s"(dst)
                  : "memory", "m0");
   };
@@ -239,9 +253,15 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
         if (e < TN) wf[Q][e] = ld16(wrd[RBUF] + wofs(e) * 512);
         else xf[Q][e - TN] = ld16(xrd[RBUF] + (e - TN) * 512);
       }
+#ifdef NJ_SETPRIO
+      __builtin_amdgcn_s_setprio(1);
+#endif
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[P][j], xf[P][i], acc[i][j], 0, 0, 0);
+#ifdef NJ_SETPRIO
+      __builtin_amdgcn_s_setprio(0);
+#endif
     }
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -292,13 +312,14 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     }
     if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
     // Sum all partials (this workgroup's own included, read back) in k
-    // order; half of the fragments at a time keeps 16 loads in flight.
+    // order; half of the row fragments at a time (rows [h TM / 2, (h+1) TM / 2),
+    // which covers an odd TM too) keeps 16 loads in flight.
     // Fragments past the edge read a clamped in-range address and are dropped.
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       for (int c = 0; c < nseg; ++c) {
 #pragma unroll
-        for (int i = h * (TM / 2); i < (h + 1) * (TM / 2); ++i) {
+        for (int i = h * TM / 2; i < (h + 1) * TM / 2; ++i) {
           const int m = min(out_m(i), M - 1);
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
@@ -417,8 +438,17 @@ bool tile_one_segment(const GemmPlan& p, int K) {
   return p.grid % tiles == 0 && p.grid / tiles <= K / 64;
 }
 
-int tile_bm(int cfg) { return cfg == kTile256x256 ? 256 : cfg == kTile192x256 ? 192 : 128; }
-int tile_bn(int cfg) { return cfg == kTile128x128 ? 128 : 256; }
+int tile_bm(int cfg) {
+  switch (cfg) {
+    case kTile256x256: return 256;
+    case kTile192x256: return 192;
+    case kTile160x256: return 160;
+    case kTile96x256:
+    case kTile96x128: return 96;
+    default: return 128;
+  }
+}
+int tile_bn(int cfg) { return cfg == kTile128x128 || cfg == kTile96x128 ? 128 : 256; }
 
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s, float* stats, bool x_kblocked,
@@ -435,18 +465,33 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
           x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid};
   const bool one_segment = tile_one_segment(p, K);
   switch (p.tile) {
-    // 4 waves of 128 x 128 (a quarter fewer LDS reads per MFMA; all 512
-    // registers per lane), 8 waves of 128 x 64 for SwiGLU, whose epilogue
-    // would not fit beside the larger accumulators; one segment per
-    // workgroup only (the stream-K loop's state does not fit beside them)
+    // 8 waves of 128 x 64 (two per SIMD: one issues MFMAs while the other
+    // waits on LDS or a barrier); one segment per workgroup only (the
+    // stream-K loop's state does not fit beside the accumulators)
     case kTile256x256:
       if (!one_segment) return hipErrorInvalidValue;
-      return epi == kEpiSwiglu ? launch_shape<256, 256, 2, 4, 4, false>(a, epi, s)
-                               : launch_shape<256, 256, 2, 2, 4, false>(a, epi, s);
+#ifdef NJ_T256_WAVES4
+      if (epi != kEpiSwiglu) return launch_shape<256, 256, 2, 2, 4, false>(a, epi, s);
+#endif
+      return launch_shape<256, 256, 2, 4, 4, false>(a, epi, s);
     // 4 waves of 96 x 128: windows of 3 x 128 (or 6 x 64) rows without a padded tile
-    case kTile192x256: return launch_shape_any<192, 256, 2, 2, 4>(a, epi, one_segment, s);
-    case kTile128x256: return launch_shape_any<128, 256, 2, 4, 4>(a, epi, one_segment, s);
-    default: return launch_shape_any<128, 128, 2, 2, 4>(a, epi, one_segment, s);
+    case kTile192x256:
+#ifdef NJ_T192_WAVES8
+      return launch_shape_any<192, 256, 2, 4, NJ_NBUF_192x256>(a, epi, one_segment, s);
+#endif
+      return launch_shape_any<192, 256, 2, 2, NJ_NBUF_192x256>(a, epi, one_segment, s);
+    // 8 waves of 80 x 64: windows of 2 x 160 rows (320 = B 64 x (k+1) 5)
+    case kTile160x256: return launch_shape_any<160, 256, 2, 4, 4>(a, epi, one_segment, s);
+    // 8 waves of 48 x 64 and of 48 x 32: more, smaller tiles where the
+    // weight matrix has few columns
+    case kTile96x256: return launch_shape_any<96, 256, 2, 4, 4>(a, epi, one_segment, s);
+    case kTile96x128:
+#ifdef NJ_T96x128_WAVES4
+      return launch_shape_any<96, 128, 2, 2, 4>(a, epi, one_segment, s);
+#endif
+      return launch_shape_any<96, 128, 2, 4, 4>(a, epi, one_segment, s);
+    case kTile128x256: return launch_shape_any<128, 256, 2, 4, NJ_NBUF_128x256>(a, epi, one_segment, s);
+    default: return launch_shape_any<128, 128, 2, 2, NJ_NBUF_128x128>(a, epi, one_segment, s);
   }
 }
 

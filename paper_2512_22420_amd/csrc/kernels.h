@@ -17,7 +17,8 @@ enum { kF32 = 0, kBF16 = 1 };
 enum { kEpiStore = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiLogits = 3, kEpiResidualNorm = 4, kEpiQkvRope = 5 };
 
 // Output tiles of the LDS-tiled kernel for large windows: x rows x weight rows.
-enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3, kTile192x256 = 4 };
+enum { kTileNone = 0, kTile256x256 = 1, kTile128x256 = 2, kTile128x128 = 3, kTile192x256 = 4, kTile160x256 = 5,
+       kTile96x256 = 6, kTile96x128 = 7 };
 
 // How the bf16 GEMM splits its work.  Weight-streaming kernel (tile ==
 // kTileNone): 16-row x tiles per workgroup (mt), waves per workgroup (nw, 8),
@@ -32,7 +33,12 @@ struct GemmPlan {
   int depth;  // streaming kernel: weight stages in flight ahead of the one being multiplied (1 or 3)
   size_t part_bytes, counter_bytes;
   int grid;   // tiled kernel: workgroups of the stream-K schedule
+  int key_m, key_n, key_k, key_epi;  // the arguments gemm_plan chose it for (its plan table checks them)
 };
+// The plan the bf16 GEMM runs for y = x . w^T with epilogue epi; epi =
+// kEpiQkvRope plans the QKV projection (store output), for which a
+// streaming plan also applies RoPE while a tiled one needs the RoPE kernel.
+// Plans of the same arguments are computed once and kept.
 GemmPlan gemm_plan(int M, int N, int K, int epi);
 // Plan of the LDS-tiled kernel with a given tile shape and K split (grid =
 // tiles x nkc).
@@ -70,6 +76,12 @@ constexpr int kGemmMaxSplitGrid = 1024;
 constexpr size_t kGemmCounterBytes = (size_t)kGemmMaxSplitGrid * kCounterStride * 4;
 // Split-K partials are addressed with 32-bit buffer offsets.
 constexpr size_t kMaxPartBytes = (size_t)1 << 31;
+// The planners choose no split plan whose partials exceed this, so that a
+// step's partial region can be sized once for every window up to the largest
+// one: windows of more than 64 rows reserve the cap, and below that the
+// chosen plans' partials grow with the window.
+constexpr size_t kSplitPartCap = (size_t)96 << 20;
+constexpr int kTileMinRows = 65;  // windows of more than 64 rows may use the LDS-tiled kernel
 
 // bf16 GEMM weights live in a packed layout: 128-row groups, each a run of
 // K/32 k-steps of 8 tiles (16 rows x 32 k, 1 KB, MFMA lane order).  Elements

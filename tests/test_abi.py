@@ -116,7 +116,7 @@ def test_gemm_with_plan_rejects_impossible_plans_on_host():
     # auto plan takes no split; fp32 has one kernel; bad kernel id
     assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, nb.NJ_GEMM_AUTO, 2) == 0
     assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_F32, 64, 256, 256, st, nb.NJ_GEMM_STREAM, 0) == 0
-    assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, 9, 0) == 0
+    assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, nb.NJ_GEMM_TILE_96x128 + 1, 0) == 0
     assert L.nightjar_gemm_plan_workspace_bytes(nb.NJ_BF16, 64, 256, 256, st, nb.NJ_GEMM_STREAM, -1) == 0
     # the workspace grows with the split (fp32 partials per chunk)
     a = nb.gemm_plan_workspace_bytes(nb.NJ_BF16, 384, 4096, 4096, st, nb.NJ_GEMM_TILE_256x256, 1)

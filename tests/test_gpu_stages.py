@@ -131,6 +131,19 @@ def _gemm_tol(ref, epi):
     (nb.NJ_GEMM_TILE_128x128, -5, 65, 384, 256, nb.NJ_GEMM_STORE),
     (nb.NJ_GEMM_TILE_128x256, -1000, 129, 512, 4096, nb.NJ_GEMM_STORE),   # capped at 256 units: one each
     (nb.NJ_GEMM_TILE_192x256, -300, 500, 2 * 1008, 2048, nb.NJ_GEMM_SWIGLU),
+    # 8-wave tiles whose load units do not split evenly over the waves, and
+    # odd row-fragment counts per wave (5 for 160 rows, 3 for 96) in the
+    # split-K reduction
+    (nb.NJ_GEMM_TILE_160x256, 0, 320, 4096, 1024, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_TILE_160x256, 2, 300, 2 * 1008, 2048, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_160x256, -256, 320, 4096, 2048, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_96x256, 0, 200, 1040, 512, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_96x256, 3, 96, 4096, 2048, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_TILE_96x256, -64, 250, 2 * 704, 1024, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_96x128, 0, 97, 1024, 512, nb.NJ_GEMM_STORE),
+    (nb.NJ_GEMM_TILE_96x128, 4, 320, 4096, 4096, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_TILE_96x128, -300, 200, 2 * 512, 1024, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_96x128, 2, 768, 2 * 1024, 512, nb.NJ_GEMM_SWIGLU),
     (nb.NJ_GEMM_STREAM, 3, 48, 4096, 4096, nb.NJ_GEMM_STORE),              # streaming kernel, forced split
     (nb.NJ_GEMM_STREAM, 1, 200, 1024, 1024, nb.NJ_GEMM_RESIDUAL),          # streaming kernel past 64 rows
     (nb.NJ_GEMM_STREAM, 0, 80, 4112, 1024, nb.NJ_GEMM_STORE),              # persistent, 5 row tiles, ragged group
@@ -176,6 +189,8 @@ def _kblock(a, M, K):
     (nb.NJ_GEMM_TILE_128x256, 2, 130, 2 * 704, 1024, nb.NJ_GEMM_SWIGLU),   # split, ragged M
     (nb.NJ_GEMM_TILE_128x128, 3, 257, 1024, 2048, nb.NJ_GEMM_STORE),
     (nb.NJ_GEMM_TILE_256x256, 0, 512, 2 * 512, 1024, nb.NJ_GEMM_SWIGLU),
+    (nb.NJ_GEMM_TILE_160x256, 0, 320, 4096, 1024, nb.NJ_GEMM_RESIDUAL),
+    (nb.NJ_GEMM_TILE_96x128, 2, 200, 2 * 512, 1024, nb.NJ_GEMM_SWIGLU),
 ])
 def test_gemm_kblocked_operands_match_row_major(kernel, split, M, N, K, epi):
     """The k-blocked x (and SwiGLU y) layout of the verify step's tiled GEMMs:
