@@ -836,7 +836,7 @@ constexpr int kTileShapes[] = {kTile256x256, kTile192x256, kTile160x256, kTile12
 double tile_eff(int tile) {
   switch (tile) {
     case kTile256x256: return 0.56;
-    case kTile192x256: return 0.46;
+    case kTile192x256: return 0.50;
     case kTile160x256: return 0.52;
     case kTile128x256: return 0.46;
     case kTile96x256: return 0.42;

@@ -57,16 +57,6 @@ struct TileK {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// stage buffers of the smaller tile shapes (compile-time settings)
-#ifndef NJ_NBUF_192x256
-#define NJ_NBUF_192x256 4
-#endif
-#ifndef NJ_NBUF_128x256
-#define NJ_NBUF_128x256 4
-#endif
-#ifndef NJ_NBUF_128x128
-#define NJ_NBUF_128x128 4
-#endif
 
 // SK: the stream-K loop over several segments per workgroup; without it a
 // workgroup runs exactly one segment (the host launches such shapes only on
@@ -253,15 +243,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
         if (e < TN) wf[Q][e] = ld16(wrd[RBUF] + wofs(e) * 512);
         else xf[Q][e - TN] = ld16(xrd[RBUF] + (e - TN) * 512);
       }
-#ifdef NJ_SETPRIO
-      __builtin_amdgcn_s_setprio(1);
-#endif
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[P][j], xf[P][i], acc[i][j], 0, 0, 0);
-#ifdef NJ_SETPRIO
-      __builtin_amdgcn_s_setprio(0);
-#endif
     }
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -470,28 +454,17 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
     // stream-K loop's state does not fit beside the accumulators)
     case kTile256x256:
       if (!one_segment) return hipErrorInvalidValue;
-#ifdef NJ_T256_WAVES4
-      if (epi != kEpiSwiglu) return launch_shape<256, 256, 2, 2, 4, false>(a, epi, s);
-#endif
       return launch_shape<256, 256, 2, 4, 4, false>(a, epi, s);
-    // 4 waves of 96 x 128: windows of 3 x 128 (or 6 x 64) rows without a padded tile
-    case kTile192x256:
-#ifdef NJ_T192_WAVES8
-      return launch_shape_any<192, 256, 2, 4, NJ_NBUF_192x256>(a, epi, one_segment, s);
-#endif
-      return launch_shape_any<192, 256, 2, 2, NJ_NBUF_192x256>(a, epi, one_segment, s);
+    // 8 waves of 96 x 64: windows of 3 x 128 (or 6 x 64) rows without a padded tile
+    case kTile192x256: return launch_shape_any<192, 256, 2, 4, 4>(a, epi, one_segment, s);
     // 8 waves of 80 x 64: windows of 2 x 160 rows (320 = B 64 x (k+1) 5)
     case kTile160x256: return launch_shape_any<160, 256, 2, 4, 4>(a, epi, one_segment, s);
     // 8 waves of 48 x 64 and of 48 x 32: more, smaller tiles where the
-    // weight matrix has few columns
+    // weight matrix has few rows
     case kTile96x256: return launch_shape_any<96, 256, 2, 4, 4>(a, epi, one_segment, s);
-    case kTile96x128:
-#ifdef NJ_T96x128_WAVES4
-      return launch_shape_any<96, 128, 2, 2, 4>(a, epi, one_segment, s);
-#endif
-      return launch_shape_any<96, 128, 2, 4, 4>(a, epi, one_segment, s);
-    case kTile128x256: return launch_shape_any<128, 256, 2, 4, NJ_NBUF_128x256>(a, epi, one_segment, s);
-    default: return launch_shape_any<128, 128, 2, 2, NJ_NBUF_128x128>(a, epi, one_segment, s);
+    case kTile96x128: return launch_shape_any<96, 128, 2, 4, 4>(a, epi, one_segment, s);
+    case kTile128x256: return launch_shape_any<128, 256, 2, 4, 4>(a, epi, one_segment, s);
+    default: return launch_shape_any<128, 128, 2, 2, 4>(a, epi, one_segment, s);
   }
 }
 
