@@ -349,58 +349,96 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
     const bf16_t* ks = smem + (ch % NBUF) * 2 * KV_ELEMS;
     const bf16_t* vs = ks + KV_ELEMS;
     if (rt < RT) {
-      for (int bi = tp; bi < nblk; bi += NTP) {
-        const int nvalid = win ? a.T : min(kBlock, ctx - (j0 + bi) * kBlock);
-        const bf16_t* kb = ks + bi * kBlock * kD;
-        const bf16_t* vb = vs + bi * kBlock * kD;
-        bf16x8 kf[4];
+      // Blocks bi and bi + NTP together: their score products are two
+      // independent chains, and one cross-lane max, one exp2 of the running
+      // max and one rescale of the accumulators serve both.
+      for (int bi = tp; bi < nblk; bi += 2 * NTP) {
+        const bool two = bi + NTP < nblk;  // uniform
+        bf16x8 kf[2][4];
+        u32x2 vf[2][8];
+        int nvalid[2];
 #pragma unroll
-        for (int s = 0; s < 4; ++s) kf[s] = ld8(kb + k_lds(r16, 4 * g + s));
-        u32x2 vf[8];
+        for (int h = 0; h < 2; ++h) {
+          if (h == 1 && !two) break;
+          const int blk = bi + h * NTP;
+          nvalid[h] = win ? a.T : min(kBlock, ctx - (j0 + blk) * kBlock);
+          const bf16_t* kb = ks + blk * kBlock * kD;
+          const bf16_t* vb = vs + blk * kBlock * kD;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) vf[dt] = *reinterpret_cast<const u32x2*>(vb + v_lds(16 * dt + r16, g));
-        if (4 * g + 3 >= nvalid) {  // tokens past the valid ones may hold anything: zero them
-          const int keep = nvalid - 4 * g;
+          for (int s = 0; s < 4; ++s) kf[h][s] = ld8(kb + k_lds(r16, 4 * g + s));
 #pragma unroll
-          for (int dt = 0; dt < 8; ++dt) {
-            uint32_t lo = vf[dt][0], hi = vf[dt][1];
-            if (keep <= 0) lo = 0u;
-            else if (keep == 1) lo &= 0xffffu;
-            if (keep <= 2) hi = 0u;
-            else if (keep == 3) hi &= 0xffffu;
-            vf[dt][0] = lo;
-            vf[dt][1] = hi;
+          for (int dt = 0; dt < 8; ++dt) vf[h][dt] = *reinterpret_cast<const u32x2*>(vb + v_lds(16 * dt + r16, g));
+          if (4 * g + 3 >= nvalid[h]) {  // tokens past the valid ones may hold anything: zero them
+            const int keep = nvalid[h] - 4 * g;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+              uint32_t lo = vf[h][dt][0], hi = vf[h][dt][1];
+              if (keep <= 0) lo = 0u;
+              else if (keep == 1) lo &= 0xffffu;
+              if (keep <= 2) hi = 0u;
+              else if (keep == 3) hi &= 0xffffu;
+              vf[h][dt][0] = lo;
+              vf[h][dt][1] = hi;
+            }
           }
         }
-        f32x4 st = f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 st[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-        for (int s = 0; s < 4; ++s) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qf[s], st, 0, 0, 0);
-        float sc[4];
-        float bm = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int tok = 4 * g + i;
-          const bool ok = tok < nvalid && (!win || tok <= qpos);
-          sc[i] = ok ? st[i] * a.scale_log2 : -INFINITY;
-          bm = fmaxf(bm, sc[i]);
+        for (int s = 0; s < 4; ++s) {
+          st[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0][s], qf[s], st[0], 0, 0, 0);
+          if (two) st[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1][s], qf[s], st[1], 0, 0, 0);
         }
+        float sc[2][4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sc[h][i] = st[h][i] * a.scale_log2;
+          if (h == 1 && !two) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sc[h][i] = -INFINITY;
+          } else if (win || nvalid[h] < kBlock) {  // uniform: only a partial or the window block masks tokens
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int tok = 4 * g + i;
+              if (!(tok < nvalid[h] && (!win || tok <= qpos))) sc[h][i] = -INFINITY;
+            }
+          }
+        }
+        float bm = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
+                         fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
         bm = fmaxf(bm, __shfl_xor(bm, 16));
         bm = fmaxf(bm, __shfl_xor(bm, 32));
         const float mn = fmaxf(m_run, bm);
-        const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m_run - mn);
-        float p[4];
+        // exponents are <= 0 here: the hardware exp2 (v_exp_f32) gives
+        // exp2(-inf) = 0 for masked tokens; a row with nothing valid yet
+        // (mn = -inf) keeps p = 0
+        const float ms = mn == -INFINITY ? 0.f : mn;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - ms);
+        float p[2][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) p[i] = (sc[i] == -INFINITY) ? 0.f : exp2f(sc[i] - mn);
-        l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) p[h][i] = __builtin_amdgcn_exp2f(sc[h][i] - ms);
+        l_run = l_run * alpha + (((p[0][0] + p[0][1]) + (p[0][2] + p[0][3])) + ((p[1][0] + p[1][1]) + (p[1][2] + p[1][3])));
         m_run = mn;
-        u32x2 pp;
-        pp[0] = pack_bf16x2(p[0], p[1]);
-        pp[1] = pack_bf16x2(p[2], p[3]);
-        const bf16x4 pf = __builtin_bit_cast(bf16x4, pp);
+        bf16x4 pf[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          u32x2 pp;
+          pp[0] = pack_bf16x2(p[h][0], p[h][1]);
+          pp[1] = pack_bf16x2(p[h][2], p[h][3]);
+          pf[h] = __builtin_bit_cast(bf16x4, pp);
+        }
+        // the accumulators move only when some row's running max rose (uniform branch)
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+        }
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          o[dt] *= alpha;
-          o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vf[dt]), pf, o[dt], 0, 0, 0);
+          o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vf[0][dt]), pf[0], o[dt], 0, 0, 0);
+          if (two)
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, vf[1][dt]), pf[1], o[dt], 0, 0, 0);
         }
       }
     }
