@@ -143,3 +143,19 @@ def test_stage_entries_reject_bad_arguments_on_host():
     assert rc == nb.NJ_EINVAL and "aligned" in nb.last_error()
     rc = nb.lib().nightjar_rmsnorm_rope(ctypes.byref(d8), 16, 16, 16, 16, 2, 16, 16, 16, 16, 256, m, 0)
     assert rc == nb.NJ_EINVAL
+
+
+@pytest.mark.parametrize("shape,max_B,max_k", [(W.LLAMA8B_LAYER, 128, 5), (W.QWEN7B, 256, 7), (W.LLAMA1B_DRAFT, 64, 4)],
+                         ids=["8b-layer", "qwen7b", "1b-draft"])
+def test_max_workspace_serves_every_smaller_window(shape, max_B, max_k):
+    """nightjar_workspace_bytes(max_B, max_k) is enough for every (B, k) below
+    it, whatever GEMM plan (split partials included) the smaller window picks."""
+    L = nb.lib()
+    d = model_desc(shape)
+    top = L.nightjar_workspace_bytes(ctypes.byref(d), max_B, max_k)
+    assert top > 0
+    Bs = sorted(set(list(range(1, 17)) + list(range(16, max_B + 1, 7)) + [max_B]))
+    for B in Bs:
+        for k in range(max_k + 1):
+            need = L.nightjar_workspace_bytes(ctypes.byref(d), B, k)
+            assert 0 < need <= top, (B, k, need, top)
