@@ -72,7 +72,10 @@ enum {
   NJ_DEV_BAD_TOKEN = 1,   /* a window or draft token id outside [0, V)                 */
   NJ_DEV_BAD_BLOCK = 2,   /* a needed block-table entry outside [0, num_blocks)          */
   NJ_DEV_BAD_CONTEXT = 4, /* context_lens[b] < 0 or context_lens[b]+k+1 > max_blocks*16  */
-  NJ_DEV_BAD_ACCEPT = 8   /* kv_append: accepted_len[b] outside [0, k]                   */
+  NJ_DEV_BAD_ACCEPT = 8,  /* kv_append: accepted_len[b] outside [0, k]                   */
+  NJ_DEV_SPLIT_WAIT = 16  /* a split GEMM's workgroups did not all arrive within the wait
+                             bound (the GPU ran fewer of them at once than the plan
+                             assumes); the GEMM's output is not valid                     */
 };
 
 typedef struct nj_model_desc {

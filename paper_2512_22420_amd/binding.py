@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(HERE, "libnightjar.so")
 
 NJ_F32, NJ_BF16 = 0, 1
 NJ_OK, NJ_EINVAL, NJ_EDEVICE, NJ_EHIP, NJ_EAGAIN = 0, -1, -2, -3, -4
-NJ_DEV_BAD_TOKEN, NJ_DEV_BAD_BLOCK, NJ_DEV_BAD_CONTEXT, NJ_DEV_BAD_ACCEPT = 1, 2, 4, 8
+NJ_DEV_BAD_TOKEN, NJ_DEV_BAD_BLOCK, NJ_DEV_BAD_CONTEXT, NJ_DEV_BAD_ACCEPT, NJ_DEV_SPLIT_WAIT = 1, 2, 4, 8, 16
 NJ_GEMM_STORE, NJ_GEMM_RESIDUAL, NJ_GEMM_SWIGLU = 0, 1, 2
 NJ_GEMM_KBLOCKED = 16  # flag: x (and a SwiGLU y) k-blocked, [K/32][M][32]
 NJ_GEMM_AUTO, NJ_GEMM_STREAM, NJ_GEMM_TILE_256x256, NJ_GEMM_TILE_128x256, NJ_GEMM_TILE_128x128 = 0, 1, 2, 3, 4

@@ -68,7 +68,7 @@ __device__ __forceinline__ void chunk_stats(const float (&v)[kStatPer], float& m
 constexpr int kBlock = 16;  // tokens per KV block
 
 // Device error bits (mirror NJ_DEV_* of the public header).
-constexpr int kErrToken = 1, kErrBlock = 2, kErrContext = 4, kErrAccept = 8;
+constexpr int kErrToken = 1, kErrBlock = 2, kErrContext = 4, kErrAccept = 8, kErrSplitWait = 16;
 
 __device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float((uint32_t)v << 16); }
 

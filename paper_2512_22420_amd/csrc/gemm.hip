@@ -793,6 +793,16 @@ void tile_sk_buffers(GemmPlan& p, int M, int N, int K) {
 }
 }  // namespace
 
+int device_cus() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    return n;
+  }();
+  return cus;
+}
+
 GemmPlan gemm_tile_plan_sk(int M, int N, int K, int epi, int tile, int grid) {
   GemmPlan p{};
   const int NG = epi == kEpiSwiglu ? 2 : 1;
@@ -808,6 +818,7 @@ GemmPlan gemm_tile_plan_sk(int M, int N, int K, int epi, int tile, int grid) {
   p.stages_per_chunk = (int)((units + shares - 1) / shares);  // units per workgroup, at most
   p.depth = 1;
   tile_sk_buffers(p, M, N, K);
+  p.par = p.nkc > 1 && p.grid <= kParMaxGrid && tile_one_segment(p, K) ? 1 : 0;
   return p;
 }
 
@@ -821,25 +832,27 @@ namespace {
 // Cost models (seconds) used to pick the kernel for windows of 65+ rows,
 // with constants fitted to sweeps of the 8B- and 7B-shaped GEMMs (QKV, O,
 // gate/up, down, LM head) at 65..2048 rows over both kernels, every tile
-// shape, K split and a 256-workgroup stream-K grid: the plan chosen is the
-// fastest measured one, or within 3% of it, at 68 of 77 points and within
-// 11% at the others.
+// shape, K splits of 1..8 (slice-reduced) and a 256-workgroup stream-K grid:
+// the plan chosen is the fastest measured one, or within 3% of it, at 70 of
+// 83 points and within 15% at the others (the sustained fractions below are
+// fitted for ranking plans, so they sit above the measured ones).
 // Tiled kernel: rounds of resident workgroups times one tile's MFMA time at
 // the tile shape's sustained fraction of peak, plus, when tiles are cut, the
 // last arriver's reduction (one CU reads nkc partial tiles) and the partial
 // traffic.
 constexpr double kLaunch = 5e-6;
+constexpr double kParFixed = 3e-6;  // the wait for a tile's slowest workgroup and the departure
 constexpr double kCuPeak = 2.5e15 / 256.0;  // bf16 MFMA FLOP/s of one CU
 constexpr int kTileShapes[] = {kTile256x256, kTile192x256, kTile160x256, kTile128x256, kTile96x256, kTile96x128,
                                kTile128x128};
 // sustained fraction of a CU's MFMA peak with k-blocked x
 double tile_eff(int tile) {
   switch (tile) {
-    case kTile256x256: return 0.56;
-    case kTile192x256: return 0.50;
-    case kTile160x256: return 0.52;
-    case kTile128x256: return 0.46;
-    case kTile96x256: return 0.42;
+    case kTile256x256: return 0.64;
+    case kTile192x256:
+    case kTile160x256: return 0.58;
+    case kTile128x256: return 0.50;
+    case kTile96x256: return 0.40;
     default: return 0.32;  // 96 x 128 and 128 x 128
   }
 }
@@ -853,7 +866,12 @@ double tile_cost(const GemmPlan& p, int M, int N, int K) {
   const double per_cu = std::max(1.0, std::min((double)tile_occupancy(p.tile), std::ceil(wgs / 256.0)));
   const double rounds = std::ceil(wgs / (256.0 * per_cu));
   double t = rounds * per_cu * 2.0 * bm * bn * (64.0 * p.stages_per_chunk) / (kCuPeak * tile_eff(p.tile));
-  if (p.nkc > 1) t += 2.0 * p.nkc * bm * bn * 4 / 5e10 + 2.0 * p.nkc * (double)M * N * 4 / 5e12;
+  if (p.nkc > 1) {
+    // cut tiles: one CU reads the nkc partial tiles (last arriver), or, with
+    // the slice reduction, each of the nkc workgroups reads one tile's worth
+    t += (p.par ? kParFixed + bm * bn * 4 / 1e11 : 2.0 * p.nkc * bm * bn * 4 / 5e10) +
+         2.0 * p.nkc * (double)M * N * 4 / 5e12;
+  }
   return t + kLaunch;
 }
 // Weight-streaming kernel: rounds of workgroups (one per CU), each streaming

@@ -53,10 +53,63 @@ struct TileK {
   int nch;
   int xkb, ykb;   // x (SwiGLU: y) stored k-blocked, [K/32][M][32]
   int grid;       // workgroups (launch only; the kernel reads gridDim)
+  int par;        // one-segment split plans: every workgroup of a tile reduces a slice of its rows
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+
+// Split partials of a tile cut into nseg segments: [segment][M][NG][Nout]
+// fp32, segment = position in k order.  Workgroup `slot` of the tile sums
+// rows [m0 + slot * rs, m0 + (slot+1) * rs) of the tile (rs = ceil(BM / nseg))
+// over all segments in k order, four columns per unit, and applies the
+// epilogue to them.
+constexpr int kSplitSpinMax = 1 << 21;          // wait bound (~2^21 short sleeps, well over 100 ms)
+constexpr int kSplitErrOffset = 64;             // ints from the error word to the counter region
+template <int BM, int BN, int NG, int EPI>
+__device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nseg, int slot, int m0, int n0) {
+  constexpr int NC = NG == 1 ? BN : BN / 2;  // output columns of the tile (per group)
+  constexpr int C4 = NC / 4;
+  const int M = a.M, Nout = a.Nout;
+  const int rs = (BM + nseg - 1) / nseg;
+  const int r0 = m0 + slot * rs, r1 = min(min(m0 + (slot + 1) * rs, m0 + BM), M);
+  const int units = max(0, r1 - r0) * C4;
+  auto poff = [&](int c, int m, int q, int n) { return (uint32_t)((((size_t)c * M + m) * NG + q) * Nout + n) * 4u; };
+  for (int u = threadIdx.x; u < units; u += blockDim.x) {
+    const int m = r0 + u / C4, n = n0 + (u % C4) * 4;
+    if (n >= Nout) continue;
+    f32x4 v[NG];
+#pragma unroll
+    for (int q = 0; q < NG; ++q) v[q] = coherent_load(prs, poff(0, m, q, n));
+    // the other segments, four loads in flight per group at a time, added in k order
+    for (int c0 = 1; c0 < nseg; c0 += 4) {
+      f32x4 t[4][NG];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int q = 0; q < NG; ++q) t[j][q] = coherent_load(prs, poff(min(c0 + j, nseg - 1), m, q, n));
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (c0 + j < nseg)
+#pragma unroll
+          for (int q = 0; q < NG; ++q) v[q] = v[q] + t[j][q];
+    }
+    if constexpr (EPI == kEpiStore) {
+      *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) = v[0];
+    } else if constexpr (EPI == kEpiResidual) {
+      f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
+      *p = *p + v[0];
+    } else {
+      const f32x4 gt = v[0], up = v[NG - 1];
+      u32x2 o;
+      o[0] = pack_bf16x2(silu_mul(gt[0], up[0]), silu_mul(gt[1], up[1]));
+      o[1] = pack_bf16x2(silu_mul(gt[2], up[2]), silu_mul(gt[3], up[3]));
+      bf16_t* yp = a.ykb ? static_cast<bf16_t*>(a.Y) + ((size_t)(n >> 5) * M + m) * 32 + (n & 31)
+                         : static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n;
+      *reinterpret_cast<u32x2*>(yp) = o;
+    }
+  }
+}
 
 // SK: the stream-K loop over several segments per workgroup; without it a
 // workgroup runs exactly one segment (the host launches such shapes only on
@@ -287,6 +340,39 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     int* cnt = a.counters + (size_t)w_first * kCounterStride;
+    if constexpr (!SK) {
+      if (a.par) {
+        // Every workgroup of the tile waits for the tile's nseg partials,
+        // then reduces its own slice of the tile's rows (the same k order
+        // as the last-arriver reduction, so the same bits): nseg CUs share
+        // the reduction instead of one reading all partials.  The host
+        // launches this only on grids of at most one workgroup per CU, so
+        // all of them are resident; the wait is still bounded, and a
+        // timeout is flagged in the workspace's error word, which sits
+        // right before the counter region.
+        if (threadIdx.x == 0) {
+          __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int it = 0; __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < nseg; ++it) {
+            if (it >= kSplitSpinMax) {
+              atomicOr(a.counters - kSplitErrOffset, kErrSplitWait);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+          }
+        }
+        __syncthreads();
+        slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, slot, m0, n0);
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        // the last to leave resets both counters for the next launch
+        if (threadIdx.x == 0 &&
+            __hip_atomic_fetch_add(cnt + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nseg - 1) {
+          __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(cnt + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return;
+      }
+    }
     if (threadIdx.x == 0)
       s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
     __syncthreads();
@@ -446,8 +532,9 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
   TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, split ? part : nullptr,
           split ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles,
           (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk,
-          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid};
+          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid, 0};
   const bool one_segment = tile_one_segment(p, K);
+  a.par = split && one_segment && p.par && !a.stats && p.grid <= device_cus() ? 1 : 0;
   switch (p.tile) {
     // 8 waves of 128 x 64 (two per SIMD: one issues MFMAs while the other
     // waits on LDS or a barrier); one segment per workgroup only (the

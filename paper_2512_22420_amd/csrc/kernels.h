@@ -34,7 +34,14 @@ struct GemmPlan {
   size_t part_bytes, counter_bytes;
   int grid;   // tiled kernel: workgroups of the stream-K schedule
   int key_m, key_n, key_k, key_epi;  // the arguments gemm_plan chose it for (its plan table checks them)
+  // tiled kernel, one-segment split plans on at most kParMaxGrid workgroups:
+  // every workgroup of a cut tile reduces a slice of its rows (the launch
+  // also checks that the GPU has a CU for each workgroup)
+  int par;
 };
+constexpr int kParMaxGrid = 256;
+// CUs of the current device (queried once; 0 when there is no device).
+int device_cus();
 // The plan the bf16 GEMM runs for y = x . w^T with epilogue epi; epi =
 // kEpiQkvRope plans the QKV projection (store output), for which a
 // streaming plan also applies RoPE while a tiled one needs the RoPE kernel.
@@ -91,7 +98,9 @@ size_t packed_weight_elems(int N, int K);
 hipError_t launch_pack_weight(const void* src, void* dst, int N, int K, hipStream_t s);
 
 // y = x . w^T, x [M][K], w [N][K] (for SwiGLU N = 2F, y [M][F]); bf16 w
-// packed, fp32 w row-major.  `counters`
+// packed, fp32 w row-major.  The 256 bytes before `counters` are the
+// workspace's device-error word (a split GEMM whose workgroups time out
+// waiting for each other sets kErrSplitWait there).  `counters`
 // (plan.counter_bytes, zero on entry and on exit) and `part`
 // (plan.part_bytes) are scratch; GEMMs that run one after another on a stream
 // may share both as long as the counters are never overwritten by anything else.
