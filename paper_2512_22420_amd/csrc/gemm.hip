@@ -82,6 +82,7 @@ struct GemmK {
   float* ssq_out;
   QkvRope rope;     // kEpiQkvRope
   int ykbM;         // kEpiSwiglu: nonzero = y stored k-blocked, [Nout/32][M][32] (M = ykbM)
+  int par;          // split K: every chunk's workgroup reduces and finishes a slice of the block's rows
 };
 
 // The weight stream of one 16-row weight tile (wp: this lane's piece of k-step
@@ -265,6 +266,9 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
   stream_tile<MT, NB, PT>(acc, wp, xp, xc, xo, K, KS, st0, st1, &xs[0][0]);
 
   const int ncol = wtile * 16 + 4 * g;  // weight rows of this lane's results
+  // rows [mlo, mhi) of the window are this workgroup's to finish (all of the
+  // block's, but for the slice-reduced split K)
+  int mlo = m0, mhi = min(M, m0 + ROWS);
   if (nkc > 1) {
     // Split K: publish this chunk's partial, and the last chunk to arrive
     // finishes the tile.  Partials are written and read with device-coherent
@@ -284,6 +288,51 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     int* cnt = a.counters + ((size_t)mb * gridDim.x + blockIdx.x) * kCounterStride;
+    if (a.par) {
+      // Every chunk's workgroup waits for all nkc partials of the tile, then
+      // sums rows [mlo, mhi) of the block over them in chunk order (the same
+      // additions as the last-arriver form, so the same bits) and runs the
+      // epilogue on those rows only.  The host runs this only when every
+      // workgroup of the grid has a CU of its own; the wait is bounded, and a
+      // timeout sets kErrSplitWait in the workspace's error word, which sits
+      // right before the counter region.  Each workgroup leaves (and the last
+      // resets both counters) before reading, so none can still be waiting
+      // when the counters go back to zero.
+      if (threadIdx.x == 0) {
+        __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int it = 0; __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < nkc; ++it) {
+          if (it >= kSplitSpinMax) {
+            atomicOr(a.counters - kSplitErrOffset, kErrSplitWait);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+        if (__hip_atomic_fetch_add(cnt + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nkc - 1) {
+          __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(cnt + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+      __syncthreads();
+      const int valid = min(ROWS, M - m0), rs = (valid + nkc - 1) / nkc;
+      mlo = min(m0 + kc * rs, m0 + valid);
+      mhi = min(mlo + rs, m0 + valid);
+      for (int j0 = 0; j0 < nkc; j0 += kRedBatch) {
+        f32x4 v[kRedBatch][MT];
+#pragma unroll
+        for (int q = 0; q < kRedBatch; ++q)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const int m = m0 + mt * 16 + r;
+            v[q][mt] = m >= mlo && m < mhi ? coherent_load(prs, poff(min(j0 + q, nkc - 1), m)) : f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+        for (int q = 0; q < kRedBatch; ++q)
+          if (j0 + q < nkc) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[mt] = j0 + q == 0 ? v[q][mt] : acc[mt] + v[q][mt];
+          }
+      }
+    } else {
     if (threadIdx.x == 0)
       s_last = (__hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nkc - 1);
     __syncthreads();
@@ -307,6 +356,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) acc[mt] = j0 + q == 0 ? v[q][mt] : acc[mt] + v[q][mt];
         }
+    }
     }
   }
 
@@ -340,7 +390,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = m0 + mt * 16 + r;
-      if (m >= M) continue;
+      if (m < mlo || m >= mhi) continue;
       const f32x4 gt = acc[mt], up = ex[(wave * MT + mt) * 64 + lane];
       u32x2 o;
       o[0] = pack_bf16x2(silu_mul(gt[0], up[0]), silu_mul(gt[1], up[1]));
@@ -373,7 +423,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       float cm, cs;
       chunk_stats(v, cm, cs);
       const int m = m0 + row;
-      if (c == 0 && (int)threadIdx.x / kStatLanes < ROWS && m < M) {
+      if (c == 0 && (int)threadIdx.x / kStatLanes < ROWS && m >= mlo && m < mhi) {
         a.stats[((size_t)m * a.nch + blockIdx.x) * 2] = cm;
         a.stats[((size_t)m * a.nch + blockIdx.x) * 2 + 1] = cs;
       }
@@ -384,7 +434,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       const int idx = threadIdx.x + it * NTH;
       const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
       const int m = m0 + row, n = n0 + c4;
-      if (idx < PIECES && m < M && n < Nout)
+      if (idx < PIECES && m >= mlo && m < mhi && n < Nout)
         *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) =
             *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
     }
@@ -400,13 +450,14 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     __syncthreads();
     const QkvRope& rp = a.rope;
     const int hd = blockIdx.x, T = rp.T, H = rp.H, Hkv = rp.Hkv;
-    const int rows = min(ROWS, M - m0);
+    const int r_lo = mlo - m0, r_hi = mhi - m0;  // this workgroup's rows of the tile
     if (hd < H + Hkv) {
       bf16_t* base = static_cast<bf16_t*>(hd < H ? rp.q_out : rp.win_k);
 #pragma unroll
       for (int it = 0; it < RP_IT; ++it) {
         const int u = threadIdx.x + it * NTH, row = u / 64, j = u % 64, m = m0 + row;
-        if (row >= rows) break;
+        if (row >= r_hi) break;
+        if (row < r_lo) continue;
         const int b = m / T, i = m % T;
         const float cs = __uint_as_float(cs_pre[it][0]), sn = __uint_as_float(cs_pre[it][1]);
         const float x1 = ot[row * OS + j], x2 = ot[row * OS + j + 64];
@@ -419,7 +470,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       if (hd >= H) {
         bf16_t* wb0 = static_cast<bf16_t*>(rp.win_k);
         const int nz = (kBlock - T) * 128 / 8;  // 16-byte pieces
-        for (int b = (m0 + T - 1) / T; b * T < m0 + rows; ++b)
+        for (int b = (mlo + T - 1) / T; b * T < mhi; ++b)
           for (int u = threadIdx.x; u < nz; u += NTH)
             *reinterpret_cast<u32x4*>(wb0 + (((size_t)b * Hkv + (hd - H)) * kBlock + T) * 128 + u * 8) =
                 u32x4{0u, 0u, 0u, 0u};
@@ -431,7 +482,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       // written one value at a time)
       bf16_t* vb = static_cast<bf16_t*>(rp.win_v);
       const int gv = hd - H - Hkv;
-      const int b0 = (m0 + T - 1) / T, b1 = (m0 + rows) / T;  // whole sequences [b0, b1)
+      const int b0 = (mlo + T - 1) / T, b1 = mhi / T;  // whole sequences [b0, b1)
       for (int u = threadIdx.x; u < (b1 - b0) * 128; u += NTH) {
         const int b = b0 + u / 128, dd = u % 128;
         uint32_t w[8];
@@ -446,15 +497,15 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
         dst[0] = u32x4{w[0], w[1], w[2], w[3]};
         dst[1] = u32x4{w[4], w[5], w[6], w[7]};
       }
-      for (int u = threadIdx.x; u < rows * 128; u += NTH) {  // rows of sequences cut by the block edge
-        const int row = u / 128, dd = u % 128, m = m0 + row, b = m / T, i = m % T;
+      for (int u = threadIdx.x; u < (r_hi - r_lo) * 128; u += NTH) {  // rows of sequences cut by an edge
+        const int row = r_lo + u / 128, dd = u % 128, m = m0 + row, b = m / T, i = m % T;
         if (b >= b0 && b < b1) continue;
         vb[(((size_t)b * Hkv + gv) * 128 + dd) * kBlock + i] = f2bf(ot[row * OS + dd]);
         if (i == 0)
           for (int sl = T; sl < kBlock; ++sl) vb[(((size_t)b * Hkv + gv) * 128 + dd) * kBlock + sl] = 0;
       }
     }
-    if (hd == 0 && m0 == 0) {
+    if (hd == 0 && mlo == 0) {
       const int B = M / T;
       for (int u = threadIdx.x; u < B; u += NTH)
         if (rp.ctx_snap) rp.ctx_snap[u] = rp.ctx[u];
@@ -482,7 +533,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       const int row = idx / (TPW * 4), c4 = (idx % (TPW * 4)) * 4;
       const int m = m0 + row, n = n0 + c4;
       float part = 0.f;
-      const bool ok = idx < PIECES && m < M && n < Nout;
+      const bool ok = idx < PIECES && m >= mlo && m < mhi && n < Nout;
       if (ok) {
         f32x4* hp = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
         const f32x4 hv = h_pre[it] + *reinterpret_cast<const f32x4*>(&ot[row * OS + c4]);
@@ -502,7 +553,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       part += __shfl_xor(part, 4);
       part += __shfl_xor(part, 8);
       part += __shfl_xor(part, 16);
-      if ((idx % (TPW * 4)) == 0 && idx < PIECES && m < M) a.ssq_out[(size_t)m * a.nch + blockIdx.x] = part;
+      if ((idx % (TPW * 4)) == 0 && idx < PIECES && m >= mlo && m < mhi) a.ssq_out[(size_t)m * a.nch + blockIdx.x] = part;
     }
   } else {
     if (!active) return;
@@ -510,7 +561,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = m0 + mt * 16 + r;
-      if (m >= M) continue;
+      if (m < mlo || m >= mhi) continue;
       f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
       *p = *p + acc[mt];
     }
@@ -730,8 +781,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }
 
 template <int EPI, int NB>
-hipError_t launch_stream_nb(const GemmK& a, const GemmPlan& p, hipStream_t s) {
+hipError_t launch_stream_nb(const GemmK& a0, const GemmPlan& p, hipStream_t s) {
   const dim3 grid(p.ntiles, p.mblocks, p.nkc), block(kNW * 64);
+  GemmK a = a0;
+  a.par = p.par && p.nkc > 1 && (long)p.ntiles * p.mblocks * p.nkc <= device_cus() ? 1 : 0;
   switch (p.mt) {
     case 1: hipLaunchKernelGGL((gemm_stream_kernel<1, EPI, NB>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((gemm_stream_kernel<2, EPI, NB>), grid, block, 0, s, a); break;
@@ -991,6 +1044,7 @@ GemmPlan gemm_stream_plan(int M, int N, int K, int epi, int split, int depth) {
   p.depth = depth;
   p.part_bytes = p.nkc > 1 ? al256((size_t)p.nkc * M * N * 4) : 0;
   p.counter_bytes = p.nkc > 1 ? al256((size_t)p.ntiles * p.mblocks * kCounterStride * 4) : 0;
+  p.par = p.nkc > 1 && (long)p.ntiles * p.mblocks * p.nkc <= kParMaxGrid ? 1 : 0;
   static_assert(kSplitTargetWorkgroups / 2 * kCounterStride * 4 <= kGemmCounterBytes, "counter region too small");
   return p;
 }

@@ -64,8 +64,6 @@ typedef __attribute__((address_space(3))) void lds_void;
 // rows [m0 + slot * rs, m0 + (slot+1) * rs) of the tile (rs = ceil(BM / nseg))
 // over all segments in k order, four columns per unit, and applies the
 // epilogue to them.
-constexpr int kSplitSpinMax = 1 << 21;          // wait bound (~2^21 short sleeps, well over 100 ms)
-constexpr int kSplitErrOffset = 64;             // ints from the error word to the counter region
 template <int BM, int BN, int NG, int EPI>
 __device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nseg, int slot, int m0, int n0) {
   constexpr int NC = NG == 1 ? BN : BN / 2;  // output columns of the tile (per group)

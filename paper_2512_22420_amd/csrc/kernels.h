@@ -40,6 +40,8 @@ struct GemmPlan {
   int par;
 };
 constexpr int kParMaxGrid = 256;
+constexpr int kSplitSpinMax = 1 << 21;  // wait bound of the slice-reduced splits (~2^21 short sleeps, > 100 ms)
+constexpr int kSplitErrOffset = 64;     // ints from the workspace's device-error word to a GEMM counter region
 // CUs of the current device (queried once; 0 when there is no device).
 int device_cus();
 // The plan the bf16 GEMM runs for y = x . w^T with epilogue epi; epi =
