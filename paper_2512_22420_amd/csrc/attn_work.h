@@ -57,6 +57,62 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
   const int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
   int* s_red = scratch;                // [NWV][kCand]
   int* s_seq = scratch + NWV * kCand;  // small batches: [B][2] first item and context of each sequence
+  auto nblocks_raw = [&](int raw) { return (attn_clamp_ctx(raw, max_blocks, T) + kBlock - 1) / kBlock; };
+  auto wsum = [](int v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+  };
+  // Up to 64 sequences: one wave sizes the list with shuffles (the same
+  // integer steps as the block-wide path below, so the same list), and one
+  // barrier hands each sequence's first item and context to the writers.
+  if (B <= kWave && B <= NT / 2) {
+    if (wave == 0) {
+      const int raw = lane < B ? ctx[lane] : 0;
+      const unsigned n = lane < B ? (unsigned)nblocks_raw(raw) : 0u;
+      const long total = wsum((int)n);
+      const int pairs = B * Hkv;
+      const long work_blocks = (long)Hkv * total;
+      const int s_lo = max(kMinSplitBlocks, (int)((work_blocks + nwg - 1) / nwg));
+      const int s_hi = nwg > pairs ? max(s_lo, (int)((work_blocks + (nwg - pairs) - 1) / (nwg - pairs))) : (1 << 28);
+      int S = s_hi;
+      for (int c = kCand - 1; c >= 0; --c) {
+        const int cand = s_lo + (int)(((long)(s_hi - s_lo) * c + kCand - 2) / (kCand - 1));
+        const int cnt = wsum(lane < B ? (int)max(1u, (n + (unsigned)cand - 1u) / (unsigned)cand) : 0);
+        if ((long)cnt * Hkv <= nwg) S = cand;
+      }
+      const int items = lane < B ? Hkv * max(1, ((int)n + S - 1) / S) : 0;
+      int incl = items;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int up = __shfl_up(incl, o);
+        if (lane >= o) incl += up;
+      }
+      if (lane < B) {
+        s_seq[2 * lane] = incl - items;
+        s_seq[2 * lane + 1] = raw;
+      }
+      if (lane == 63) {
+        s_red[0] = S;
+        s_red[1] = incl;
+      }
+    }
+    __syncthreads();
+    const int S = s_red[0], n_items = s_red[1];
+    const int tps = NT / B, b = threadIdx.x / tps, j = threadIdx.x % tps;
+    if (b < B) {
+      const int base = s_seq[2 * b], raw = s_seq[2 * b + 1];
+      const int c = attn_clamp_ctx(raw, max_blocks, T), n = (c + kBlock - 1) / kBlock;
+      const int sb = max(1, (n + S - 1) / S);
+      for (int q = j; q < Hkv * sb; q += tps) {
+        const int g = q / sb, sp = q - g * sb;
+        const int c0 = n < 46341 ? sp * n / sb : (int)((long)sp * n / sb);
+        const int c1 = n < 46341 ? (sp + 1) * n / sb : (int)((long)(sp + 1) * n / sb);
+        work[base + q] = AttnWork{b, g, sp, sb, c0, c1, c, c != raw};
+      }
+    }
+    for (int i = n_items + threadIdx.x; i < nwg; i += NT) work[i] = AttnWork{0, 0, 0, 0, 0, 0, 0, 0};
+    __syncthreads();  // scratch is free again
+    return;
+  }
   int keep[kKeep];
 #pragma unroll
   for (int j = 0; j < kKeep; ++j) keep[j] = b0 + j < b1 ? ctx[b0 + j] : 0;
@@ -67,11 +123,6 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
     for (int j = 0; j < kKeep; ++j)
       if (i == j) r = keep[j];
     return i < kKeep ? r : ctx[b];
-  };
-  auto nblocks_raw = [&](int raw) { return (attn_clamp_ctx(raw, max_blocks, T) + kBlock - 1) / kBlock; };
-  auto wsum = [](int v) {
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
   };
   // sum of cached blocks
   int mine = 0;

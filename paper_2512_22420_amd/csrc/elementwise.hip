@@ -67,11 +67,12 @@ struct RopeFreqHead {  // theta^(-2j/128) for the 64 rotation pairs of a 128-dim
 // rope_cs[row][j] = (cos, sin) of (ctx_b + i) * theta^(-2j/128), the angle in
 // fp64 with the range reduction done against 2 pi in two parts, the sincos in
 // fp32 on the reduced argument.  Threads 0..63 of the workgroup.
-__device__ __forceinline__ void rope_table_row(const int32_t* __restrict__ ctx, const RopeFreqHead& f, int row, int b,
-                                               int i, float* __restrict__ rope_cs) {
+// c: the sequence's context length (already loaded); run by threads 0..63.
+__device__ __forceinline__ void rope_table_row(int c, const RopeFreqHead& f, int row, int i,
+                                               float* __restrict__ rope_cs) {
   if (threadIdx.x < 64) {
     const int j = threadIdx.x;
-    const double ang = (double)(max(ctx[b], 0) + i) * f.inv_freq[j];
+    const double ang = (double)(max(c, 0) + i) * f.inv_freq[j];
     const double kq = rint(ang * 0.15915494309189535);
     const double red = fma(-kq, 6.283185307179586, ang) - kq * 2.4492935982947064e-16;
     float sn, cs;
@@ -96,8 +97,10 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
     return;
   }
   const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
-  if (rope_cs) rope_table_row(ctx, f, row, b, i, rope_cs);
+  // the token id and the context length load together; the RoPE math runs
+  // while the embedding row is in flight
   int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
+  const int c = rope_cs && threadIdx.x < 64 ? ctx[b] : 0;
   if (tok < 0 || tok >= V) {
     if (threadIdx.x == 0) flag_error(err, kErrToken);
     tok = 0;
@@ -108,10 +111,13 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
 #pragma unroll
   for (int it = 0; it < kNormMaxPer; ++it) {
     const int j = (it * kNormThreads + threadIdx.x) * 4;
-    if (j < d) {
-      load4(e + j, hv[it]);
-      store4(hr + j, hv[it]);
-    }
+    if (j < d) load4(e + j, hv[it]);
+  }
+  if (rope_cs) rope_table_row(c, f, row, i, rope_cs);
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+    if (j < d) store4(hr + j, hv[it]);
   }
   norm_row<T>(hv, gain, x, row, kbM, d, eps, sh);
 }
@@ -141,10 +147,15 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     return;
   }
   const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
-  if (rope_cs) rope_table_row(ctx, f, row, b, i, rope_cs);
+  // Every load of the row goes out before any store: the token id and the
+  // context length together, then the embedding (or residual) row and the
+  // gains, under which the RoPE math runs.
+  int tok = 0;
+  if (!hin) tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
+  const int c = rope_cs && threadIdx.x < 64 ? ctx[b] : 0;
+  const float* src32 = hin ? hin + (size_t)row * d : nullptr;
   const bf16_t* e = nullptr;
   if (!hin) {
-    int tok = (i == 0) ? last[b] : drafts[b * (T_ - 1) + i - 1];
     if (tok < 0 || tok >= V) {
       if (threadIdx.x == 0) flag_error(err, kErrToken);
       tok = 0;
@@ -152,28 +163,34 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
     e = embed + (size_t)tok * d;
   }
   const int nt = (d + 127) / 128;
+  float hv[kNormMaxPer][4], gv[kNormMaxPer][4];
+#pragma unroll
+  for (int it = 0; it < kNormMaxPer; ++it) {
+    const int j = (it * kNormThreads + threadIdx.x) * 4;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) hv[it][q] = gv[it][q] = 0.f;
+    if (j < d) {
+      if (hin) load4(src32 + j, hv[it]);
+      else load4(e + j, hv[it]);
+      load4(gain + j, gv[it]);
+    }
+  }
+  if (rope_cs) rope_table_row(c, f, row, i, rope_cs);
 #pragma unroll
   for (int it = 0; it < kNormMaxPer; ++it) {
     const int j = (it * kNormThreads + threadIdx.x) * 4;
     if (j >= ((d + 127) / 128) * 128) break;  // uniform per 32-lane tile
-    float hv[4] = {0.f, 0.f, 0.f, 0.f};
     float part = 0.f;
     if (j < d) {
-      float gv[4], o[4];
-      if (hin) {
-        load4(hin + (size_t)row * d + j, hv);
-      } else {
-        load4(e + j, hv);
-        store4(h + (size_t)row * d + j, hv);
-      }
-      load4(gain + j, gv);
+      float o[4];
+      if (!hin) store4(h + (size_t)row * d + j, hv[it]);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = hv[q] * gv[q];
+      for (int q = 0; q < 4; ++q) o[q] = hv[it][q] * gv[it][q];
       store4(x + (size_t)row * d + j, o);
-      part = hv[0] * hv[0];
-      part = fmaf(hv[1], hv[1], part);
-      part = fmaf(hv[2], hv[2], part);
-      part = fmaf(hv[3], hv[3], part);
+      part = hv[it][0] * hv[it][0];
+      part = fmaf(hv[it][1], hv[it][1], part);
+      part = fmaf(hv[it][2], hv[it][2], part);
+      part = fmaf(hv[it][3], hv[it][3], part);
     }
     part += __shfl_xor(part, 1);
     part += __shfl_xor(part, 2);

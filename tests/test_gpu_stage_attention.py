@@ -122,10 +122,12 @@ def _many(B, seed):
     (QW, [300, 0, 47, 4000], 8),                  # G = 7: 63 query rows
     (QW, [129, 1], 2),
     (TF, [32, 48, 0], 3),                         # fp32 path
+    (L8, _many(64, 3), 4),                        # work list: the one-wave path at its largest batch
+    (L8, _many(65, 4), 2),                        # work list: the block-wide path at its smallest batch
     (L8, _many(600, 1), 3),                       # work list: more sequences than half its threads
     (L8, _many(1100, 2), 1),                      # work list: five sequences per thread (contexts re-read)
-], ids=["8b-ragged", "8b-r64", "8b-headline", "8b-window-only", "g7-r63", "g7-k2", "f32", "8b-b600-work-list",
-        "8b-b1100-work-list"])
+], ids=["8b-ragged", "8b-r64", "8b-headline", "8b-window-only", "g7-r63", "g7-k2", "f32", "8b-b64-work-list",
+        "8b-b65-work-list", "8b-b600-work-list", "8b-b1100-work-list"])
 def test_attn_verify_matches_oracle(shape, ctx, k):
     ctx = np.asarray(ctx, np.int32)
     c, q, wk, wv = _attn_case(shape, ctx, k, seed=int(ctx.sum()) + k)
