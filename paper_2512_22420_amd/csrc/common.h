@@ -29,6 +29,23 @@ __device__ __forceinline__ f32x4 coherent_load(__amdgpu_buffer_rsrc_t r, uint32_
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 16 /* sc1 */));
 }
 
+// Split-K partials inside one XCD (accelerator die: its CUs share one L2):
+// a plain store reaches that L2, and an sc0 load skips the CU's L1 but may
+// hit the L2, so workgroups on the same XCD exchange partials without a trip
+// to memory.  Only valid between workgroups that are on the same XCD, which
+// xcd_id() tells.
+__device__ __forceinline__ void xcd_store(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, 0);
+}
+__device__ __forceinline__ f32x4 xcd_load(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 1 /* sc0 */));
+}
+__device__ __forceinline__ unsigned xcd_id() {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & 0xfu;
+}
+
 __device__ __forceinline__ void coherent_store_f32(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, byte_off, 0, 16 /* sc1 */);
 }

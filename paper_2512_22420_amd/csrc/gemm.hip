@@ -40,6 +40,7 @@
 // product unchanged.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <mutex>
 #include <unordered_map>
 #include <utility>
@@ -83,6 +84,8 @@ struct GemmK {
   QkvRope rope;     // kEpiQkvRope
   int ykbM;         // kEpiSwiglu: nonzero = y stored k-blocked, [Nout/32][M][32] (M = ykbM)
   int par;          // split K: every chunk's workgroup reduces and finishes a slice of the block's rows
+  int par_l2;       // par, and round-robin dispatch puts every chunk of a block on one XCD (see below)
+  unsigned foreign; // chunks that act as if dispatched elsewhere (tests of the fallback; normally 0)
 };
 
 // The weight stream of one 16-row weight tile (wp: this lane's piece of k-step
@@ -275,14 +278,28 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
     // accesses, so the hand-off needs neither an L2 writeback nor an L2
     // invalidate: each thread waits until its partial stores are acknowledged,
     // then one counter increment publishes them.
+    // With par_l2 the host has laid the grid out so that round-robin dispatch
+    // (workgroup i to XCD i mod 8) puts every chunk of a block on one XCD;
+    // a chunk that finds itself there exchanges its partial through that
+    // XCD's L2 (xcd_store / xcd_load), one that does not ("foreign") writes
+    // through to memory and says so with its arrival (bit 16 + kc of the
+    // counter), so that its partial is read from memory and, when the block's
+    // chunks are mixed, one chunk that is on the expected XCD finishes the
+    // whole block.  The sums are the same in every case.
     const int Ntot = Nout * NG;
     const __amdgpu_buffer_rsrc_t prs = coherent_rsrc(a.part, a.part_bytes);
     auto poff = [&](int j, int m) { return (uint32_t)(((size_t)j * M + m) * Ntot + ncol) * 4u; };
+    const unsigned lbid = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const bool foreign = a.par_l2 && (xcd_id() != (lbid & 7u) || ((a.foreign >> kc) & 1u));
+    const bool l2 = a.par_l2 && !foreign;
     if (active) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = m0 + mt * 16 + r;
-        if (m < M) coherent_store(prs, poff(kc, m), acc[mt]);
+        if (m < M) {
+          if (l2) xcd_store(prs, poff(kc, m), acc[mt]);
+          else coherent_store(prs, poff(kc, m), acc[mt]);
+        }
       }
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -299,32 +316,46 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
       // resets both counters) before reading, so none can still be waiting
       // when the counters go back to zero.
       if (threadIdx.x == 0) {
-        __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        for (int it = 0; __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < nkc; ++it) {
+        __hip_atomic_fetch_add(cnt, 1 + (foreign ? 1 << (16 + kc) : 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int v = 0;
+        for (int it = 0; ((v = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffff) < nkc; ++it) {
           if (it >= kSplitSpinMax) {
             atomicOr(a.counters - kSplitErrOffset, kErrSplitWait);
             break;
           }
           __builtin_amdgcn_s_sleep(2);
         }
+        s_last = (int)((unsigned)v >> 16);  // the foreign chunks
         if (__hip_atomic_fetch_add(cnt + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nkc - 1) {
           __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           __hip_atomic_store(cnt + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
       }
       __syncthreads();
-      const int valid = min(ROWS, M - m0), rs = (valid + nkc - 1) / nkc;
-      mlo = min(m0 + kc * rs, m0 + valid);
-      mhi = min(mlo + rs, m0 + valid);
+      const unsigned fmask = (unsigned)s_last, all = (1u << nkc) - 1u;
+      const int valid = min(ROWS, M - m0);
+      if (fmask != 0 && fmask != all) {
+        // mixed: the first chunk on the expected XCD finishes the block
+        if (kc != __builtin_ctz(~fmask & all)) return;
+        mhi = m0 + valid;
+      } else {
+        const int rs = (valid + nkc - 1) / nkc;
+        mlo = min(m0 + kc * rs, m0 + valid);
+        mhi = min(mlo + rs, m0 + valid);
+      }
       for (int j0 = 0; j0 < nkc; j0 += kRedBatch) {
         f32x4 v[kRedBatch][MT];
 #pragma unroll
-        for (int q = 0; q < kRedBatch; ++q)
+        for (int q = 0; q < kRedBatch; ++q) {
+          const int j = min(j0 + q, nkc - 1);
+          const bool jl2 = a.par_l2 && !((fmask >> j) & 1u);
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             const int m = m0 + mt * 16 + r;
-            v[q][mt] = m >= mlo && m < mhi ? coherent_load(prs, poff(min(j0 + q, nkc - 1), m)) : f32x4{0.f, 0.f, 0.f, 0.f};
+            v[q][mt] = m >= mlo && m < mhi ? (jl2 ? xcd_load(prs, poff(j, m)) : coherent_load(prs, poff(j, m)))
+                                           : f32x4{0.f, 0.f, 0.f, 0.f};
           }
+        }
 #pragma unroll
         for (int q = 0; q < kRedBatch; ++q)
           if (j0 + q < nkc) {
@@ -785,6 +816,10 @@ hipError_t launch_stream_nb(const GemmK& a0, const GemmPlan& p, hipStream_t s) {
   const dim3 grid(p.ntiles, p.mblocks, p.nkc), block(kNW * 64);
   GemmK a = a0;
   a.par = p.par && p.nkc > 1 && (long)p.ntiles * p.mblocks * p.nkc <= device_cus() ? 1 : 0;
+  // chunks kc of block (t, mb) are workgroups t + ntiles (mb + mblocks kc):
+  // one XCD under round-robin dispatch when ntiles * mblocks is a multiple of 8
+  a.par_l2 = a.par && p.nkc <= kSplitL2MaxChunks && ((long)p.ntiles * p.mblocks) % 8 == 0 ? 1 : 0;
+  a.foreign = split_foreign_mask();
   switch (p.mt) {
     case 1: hipLaunchKernelGGL((gemm_stream_kernel<1, EPI, NB>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((gemm_stream_kernel<2, EPI, NB>), grid, block, 0, s, a); break;
@@ -845,6 +880,14 @@ void tile_sk_buffers(GemmPlan& p, int M, int N, int K) {
   p.counter_bytes = smax > 1 ? al256((size_t)p.grid * kCounterStride * 4) : 0;
 }
 }  // namespace
+
+unsigned split_foreign_mask() {
+  static const unsigned mask = [] {
+    const char* e = getenv("NJ_TEST_SPLIT_FOREIGN");
+    return e ? (unsigned)strtoul(e, nullptr, 0) : 0u;
+  }();
+  return mask;
+}
 
 int device_cus() {
   static const int cus = [] {

@@ -54,38 +54,45 @@ struct TileK {
   int xkb, ykb;   // x (SwiGLU: y) stored k-blocked, [K/32][M][32]
   int grid;       // workgroups (launch only; the kernel reads gridDim)
   int par;        // one-segment split plans: every workgroup of a tile reduces a slice of its rows
+  int par_l2;     // par, and partials may go through one XCD's L2 (see the split hand-off)
+  unsigned foreign;  // segments that act as if dispatched elsewhere (tests of the fallback; normally 0)
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
 
 
 // Split partials of a tile cut into nseg segments: [segment][M][NG][Nout]
-// fp32, segment = position in k order.  Workgroup `slot` of the tile sums
-// rows [m0 + slot * rs, m0 + (slot+1) * rs) of the tile (rs = ceil(BM / nseg))
-// over all segments in k order, four columns per unit, and applies the
-// epilogue to them.
+// fp32, segment = position in k order.  The tile's rows are cut into nslice
+// slices (rs = ceil(BM / nslice) rows each); slice sl, rows [m0 + sl * rs,
+// m0 + (sl+1) * rs), is summed over all segments in k order, four columns per
+// unit, and the epilogue applied to it.  Segment c's partial is read from
+// this XCD's L2 when bit c of l2seg is set, else from memory.
 template <int BM, int BN, int NG, int EPI>
-__device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nseg, int slot, int m0, int n0) {
+__device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nseg, unsigned l2seg, int nslice, int sl,
+                             int m0, int n0) {
   constexpr int NC = NG == 1 ? BN : BN / 2;  // output columns of the tile (per group)
   constexpr int C4 = NC / 4;
   const int M = a.M, Nout = a.Nout;
-  const int rs = (BM + nseg - 1) / nseg;
-  const int r0 = m0 + slot * rs, r1 = min(min(m0 + (slot + 1) * rs, m0 + BM), M);
+  const int rs = (BM + nslice - 1) / nslice;
+  const int r0 = m0 + sl * rs, r1 = min(min(m0 + (sl + 1) * rs, m0 + BM), M);
   const int units = max(0, r1 - r0) * C4;
   auto poff = [&](int c, int m, int q, int n) { return (uint32_t)((((size_t)c * M + m) * NG + q) * Nout + n) * 4u; };
   for (int u = threadIdx.x; u < units; u += blockDim.x) {
     const int m = r0 + u / C4, n = n0 + (u % C4) * 4;
     if (n >= Nout) continue;
+    auto ld = [&](int c, int q) {
+      return (l2seg >> c) & 1u ? xcd_load(prs, poff(c, m, q, n)) : coherent_load(prs, poff(c, m, q, n));
+    };
     f32x4 v[NG];
 #pragma unroll
-    for (int q = 0; q < NG; ++q) v[q] = coherent_load(prs, poff(0, m, q, n));
+    for (int q = 0; q < NG; ++q) v[q] = ld(0, q);
     // the other segments, four loads in flight per group at a time, added in k order
     for (int c0 = 1; c0 < nseg; c0 += 4) {
       f32x4 t[4][NG];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int q = 0; q < NG; ++q) t[j][q] = coherent_load(prs, poff(min(c0 + j, nseg - 1), m, q, n));
+        for (int q = 0; q < NG; ++q) t[j][q] = ld(min(c0 + j, nseg - 1), q);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (c0 + j < nseg)
@@ -323,17 +330,34 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
     // arrivals, and let the last workgroup of the tile add the partials in k
     // order.  The counter of a split tile is that of its first workgroup
     // (no two split tiles share one).
+    // With par_l2, a tile whose segments the XCD-aware order above puts in
+    // one XCD's run exchanges its partials through that XCD's L2 (xcd_store /
+    // xcd_load); a segment that did not land on the XCD round-robin dispatch
+    // gives it ("foreign") writes through to memory and says so with its
+    // arrival (bit 16 + slot of the counter), so that its partial is read from
+    // memory and, when the tile's segments are mixed, one segment that is on
+    // the expected XCD reduces the whole tile.  The sums are the same in every
+    // case.
     const __amdgpu_buffer_rsrc_t prs = coherent_rsrc(a.part, a.part_bytes);
     auto poff = [&](int c, int m, int j) {
       return (uint32_t)((((size_t)c * M + m) * NG + out_q(j)) * Nout + out_n(j)) * 4u;
     };
+    auto xcd_of = [&](unsigned v) {  // the XCD whose run holds logical workgroup v
+      return v < grem * (gper + 1) ? v / (gper + 1) : grem + (v - grem * (gper + 1)) / max(gper, 1u);
+    };
+    const bool tile_l2 = a.par_l2 && !SK &&
+                         xcd_of((unsigned)w_first) == xcd_of((unsigned)((s_first + nseg - 1) * a.tiles_m + tm));
+    const bool foreign = tile_l2 && (xcd_id() != xcd || ((a.foreign >> slot) & 1u));
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = out_m(i);
       if (m >= M) continue;
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        if (out_n(j) < Nout) coherent_store(prs, poff(slot, m, j), acc[i][j]);
+        if (out_n(j) < Nout) {
+          if (tile_l2 && !foreign) xcd_store(prs, poff(slot, m, j), acc[i][j]);
+          else coherent_store(prs, poff(slot, m, j), acc[i][j]);
+        }
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -349,17 +373,26 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
         // timeout is flagged in the workspace's error word, which sits
         // right before the counter region.
         if (threadIdx.x == 0) {
-          __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          for (int it = 0; __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < nseg; ++it) {
+          __hip_atomic_fetch_add(cnt, 1 + (foreign ? 1 << (16 + slot) : 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          int v = 0;
+          for (int it = 0; ((v = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffff) < nseg; ++it) {
             if (it >= kSplitSpinMax) {
               atomicOr(a.counters - kSplitErrOffset, kErrSplitWait);
               break;
             }
             __builtin_amdgcn_s_sleep(2);
           }
+          s_last = (int)((unsigned)v >> 16);  // the foreign segments
         }
         __syncthreads();
-        slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, slot, m0, n0);
+        const unsigned fmask = (unsigned)s_last, all = (1u << nseg) - 1u;
+        const unsigned l2seg = tile_l2 ? ~fmask & all : 0u;
+        if (fmask != 0 && fmask != all) {
+          // mixed: the first segment on the expected XCD reduces the whole tile
+          if (slot == __builtin_ctz(l2seg)) slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, l2seg, 1, 0, m0, n0);
+        } else {
+          slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, l2seg, nseg, slot, m0, n0);
+        }
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         // the last to leave resets both counters for the next launch
@@ -530,9 +563,11 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
   TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, split ? part : nullptr,
           split ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles,
           (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk,
-          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid, 0};
+          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid, 0, 0, 0u};
   const bool one_segment = tile_one_segment(p, K);
   a.par = split && one_segment && p.par && !a.stats && p.grid <= device_cus() ? 1 : 0;
+  a.par_l2 = a.par && p.grid / ((long)p.ntiles * p.mblocks) <= kSplitL2MaxChunks ? 1 : 0;
+  a.foreign = split_foreign_mask();
   switch (p.tile) {
     // 8 waves of 128 x 64 (two per SIMD: one issues MFMAs while the other
     // waits on LDS or a barrier); one segment per workgroup only (the

@@ -42,6 +42,13 @@ struct GemmPlan {
 constexpr int kParMaxGrid = 256;
 constexpr int kSplitSpinMax = 1 << 21;  // wait bound of the slice-reduced splits (~2^21 short sleeps, > 100 ms)
 constexpr int kSplitErrOffset = 64;     // ints from the workspace's device-error word to a GEMM counter region
+// Split-K partials through one XCD's L2 (see xcd_store): at most this many
+// chunks per tile (each arrival carries a "not where round-robin dispatch put
+// it" bit, bits 16 + chunk of the tile's counter).
+constexpr int kSplitL2MaxChunks = 15;
+// Chunks (bit c: chunk c) that act as if dispatched to a foreign XCD, for
+// tests of the fallback: 0 unless NJ_TEST_SPLIT_FOREIGN is set.
+unsigned split_foreign_mask();
 // CUs of the current device (queried once; 0 when there is no device).
 int device_cus();
 // The plan the bf16 GEMM runs for y = x . w^T with epilogue epi; epi =
