@@ -432,7 +432,7 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   // the embedding kernel carries one more workgroup that builds the
   // attention's work list for every layer of the step (bf16)
   const AttnPlan plan{context_lens, reinterpret_cast<AttnWork*>(ws + L.attn_work), B, d.n_kv_heads, T, max_blocks,
-                      attn_wgs};
+                      attn_wgs, bf && attention_orders(attn_wgs) ? 1 : 0};
   const AttnPlan* pl = bf ? &plan : nullptr;
   // Norms not folded, but a QKV GEMM that still streams: RoPE and the window
   // store in its epilogue (no row scale), from the table the embedding kernel writes

@@ -214,14 +214,14 @@ __global__ __launch_bounds__(256, attn_wgs_per_cu(NBUF, kCB)) void attn_lds_kern
   const AttnWork item = a.work[blockIdx.x];
   if (item.nsplit == 0) return;  // the list is shorter than the grid
   const int b = item.b, kvh = item.kvh, split = item.split, nsplit = item.nsplit;
-  const int pair = b * a.Hkv + kvh, slot0 = blockIdx.x - split;
+  const int pair = b * a.Hkv + kvh, slot0 = item.slot0;
   const int G = a.H / a.Hkv, R = a.T * G, RT = (R + 15) / 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int rt = wave % RTW, tp = wave / RTW;
 
-  const int ctx = item.ctx;
-  if (item.bad_ctx && threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
+  const int ctx = item.ctx >= 0 ? item.ctx : ~item.ctx;
+  if (item.ctx < 0 && threadIdx.x == 0 && split == 0) flag_error(a.err, kErrContext);
   // this split's share of the cached blocks (shares differ by at most one
   // block); split 0 also takes the window block, as its first chunk: it is in
   // L2 (just written), so its compute overlaps the first cached chunk's loads
@@ -600,6 +600,8 @@ int attention_plan(int B, int Hkv, int max_blocks) {
   return (int)std::max<long>(pairs, std::min<long>((long)pairs + kExtraWorkgroups, cap));
 }
 
+bool attention_orders(int nwg) { return nwg > attn_wgs_per_cu(kAttnBuf, kAttnChunk) * device_cus(); }
+
 size_t attention_work_bytes(int B, int Hkv) { return (size_t)(B * Hkv + kExtraWorkgroups) * sizeof(AttnWork); }
 
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D) {
@@ -611,12 +613,12 @@ namespace {
 // One workgroup: the work list of the next attention launches, and (when
 // counters is given) their split arrival counters cleared.
 __global__ __launch_bounds__(256) void attn_plan_kernel(const int32_t* __restrict__ ctx, int B, int Hkv, int T,
-                                                        int max_blocks, int nwg, AttnWork* __restrict__ work,
+                                                        int max_blocks, int nwg, int order, AttnWork* __restrict__ work,
                                                         int* __restrict__ counters) {
   __shared__ int scratch[attn_work_scratch_ints(256)];
   if (counters)
     for (int u = threadIdx.x; u < B * Hkv; u += 256) counters[u * kCounterStride] = 0;
-  build_attn_work<256>(ctx, B, Hkv, T, max_blocks, nwg, work, scratch);
+  build_attn_work<256>(ctx, B, Hkv, T, max_blocks, nwg, order != 0, work, scratch);
 }
 }  // namespace
 
@@ -624,7 +626,7 @@ hipError_t launch_attn_plan(const int32_t* ctx, int B, int Hkv, int T, int max_b
                             int* counters, hipStream_t s) {
   if (nwg < B * Hkv || nwg > B * Hkv + kExtraWorkgroups) return hipErrorInvalidValue;
   hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(256), 0, s, ctx, B, Hkv, T, max_blocks, nwg,
-                     static_cast<AttnWork*>(work), counters);
+                     attention_orders(nwg) ? 1 : 0, static_cast<AttnWork*>(work), counters);
   return hipGetLastError();
 }
 

@@ -14,6 +14,15 @@
 // items can fit), s_hi = max(s_lo, ceil(Hkv * sum nb / (nwg - pairs))), which
 // always fits since sum_b ceil(nb_b / S) <= sum nb / S + B.  Items past the
 // list are written with nsplit = 0 (that workgroup exits).
+//
+// The partials of a (sequence, KV head)'s splits sit in consecutive slots
+// numbered in (b, KV head, split) order (slot0 of the item: its pair's first),
+// but the items run in the order of the list, which, when the grid is more
+// than one round of resident workgroups, puts the longest splits first
+// (longest-processing-time order: short items left for last fill the final
+// round instead of a long one holding it open).  Items of equal length take the
+// order their sequences' atomic increments give them; which workgroup runs an
+// item does not change its result.
 #pragma once
 
 #include <climits>
@@ -34,10 +43,12 @@ constexpr int kExtraWorkgroups = NJ_ATTN_EXTRA_WGS; // workgroups beyond one per
 struct AttnWork {
   int b, kvh, split, nsplit;  // nsplit == 0: no item for this workgroup
   int c0, c1;                 // the split's cached blocks [c0, c1)
-  int ctx;                    // the sequence's context length, clamped into the table
-  int bad_ctx;                // the caller's length was out of range (flagged by split 0)
+  int ctx;                    // the sequence's context length clamped into the table, or its bitwise
+                              // complement when the caller's length was out of range (flagged by split 0)
+  int slot0;                  // partial slot of the pair's split 0
 };
 static_assert(sizeof(AttnWork) == 32, "one item is two 16-byte loads");
+constexpr int kOrderBuckets = 256;  // split lengths (in blocks) the list orders by; longer ones share the last
 
 __device__ __forceinline__ int attn_clamp_ctx(int c, int max_blocks, int T) {
   const int cap = max_blocks * kBlock - T;
@@ -46,25 +57,80 @@ __device__ __forceinline__ int attn_clamp_ctx(int c, int max_blocks, int T) {
 
 // Run by all NT threads of one workgroup (every thread must call it).
 // scratch: at least attn_work_scratch_ints(NT) ints of LDS, not otherwise in use.
-__host__ __device__ constexpr int attn_work_scratch_ints(int NT) { return 8 * (NT / 64) + 2 * NT; }
+__host__ __device__ constexpr int attn_work_scratch_ints(int NT) { return 8 * (NT / 64) + 3 * NT / 2 + kOrderBuckets; }
 template <int NT>
 __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv, int T, int max_blocks, int nwg,
-                                AttnWork* __restrict__ work, int* scratch) {
+                                bool order, AttnWork* __restrict__ work, int* scratch) {
   constexpr int kCand = 8, NWV = NT / 64;
   constexpr int kKeep = 4;  // context lengths a thread keeps in registers (more are re-read)
   const int per = (B + NT - 1) / NT;
   const int b0 = min(B, (int)threadIdx.x * per), b1 = min(B, b0 + per);
   const int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
   int* s_red = scratch;                // [NWV][kCand]
-  int* s_seq = scratch + NWV * kCand;  // small batches: [B][2] first item and context of each sequence
+  int* s_seq = scratch + NWV * kCand;  // small batches: [B][3] first slot, context, first list position
+  int* s_hist = s_seq + 3 * NT / 2;    // [kOrderBuckets] items per split-length bucket, then list cursors
   auto nblocks_raw = [&](int raw) { return (attn_clamp_ctx(raw, max_blocks, T) + kBlock - 1) / kBlock; };
   auto wsum = [](int v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     return v;
   };
+  auto bucket = [&](int n, int sb) {    // longest splits first
+    return kOrderBuckets - 1 - min((n + sb - 1) / sb, kOrderBuckets - 1);
+  };
+  // Exclusive scan of s_hist into list positions (every thread calls it).
+  auto scan_hist = [&]() {
+    __syncthreads();
+    if (wave == 0) {
+      constexpr int PER = kOrderBuckets / 64;
+      int h[PER], sum = 0;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) sum += (h[e] = s_hist[lane * PER + e]);
+      int incl = sum;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int up = __shfl_up(incl, o);
+        if (lane >= o) incl += up;
+      }
+      int run = incl - sum;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        s_hist[lane * PER + e] = run;
+        run += h[e];
+      }
+    }
+    __syncthreads();
+  };
+  // Small batches (B <= NT / 2, s_seq holding each sequence's first slot and
+  // context): list positions, then the items, NT / B threads per sequence.
+  auto put_small = [&](int S) {
+    if (order) {
+      for (int i = threadIdx.x; i < kOrderBuckets; i += NT) s_hist[i] = 0;
+      __syncthreads();
+      int n = 0, sb = 0;
+      if ((int)threadIdx.x < B) {
+        n = nblocks_raw(s_seq[3 * threadIdx.x + 1]);
+        sb = max(1, (n + S - 1) / S);
+        atomicAdd(&s_hist[bucket(n, sb)], Hkv * sb);
+      }
+      scan_hist();
+      if ((int)threadIdx.x < B) s_seq[3 * threadIdx.x + 2] = atomicAdd(&s_hist[bucket(n, sb)], Hkv * sb);
+      __syncthreads();
+    }
+    const int tps = NT / B, b = threadIdx.x / tps, j = threadIdx.x % tps;
+    if (b < B) {
+      const int slot = s_seq[3 * b], raw = s_seq[3 * b + 1], pos = order ? s_seq[3 * b + 2] : slot;
+      const int c = attn_clamp_ctx(raw, max_blocks, T), nb = (c + kBlock - 1) / kBlock;
+      const int sbb = max(1, (nb + S - 1) / S);
+      for (int q = j; q < Hkv * sbb; q += tps) {
+        const int g = q / sbb, sp = q - g * sbb;
+        const int c0 = nb < 46341 ? sp * nb / sbb : (int)((long)sp * nb / sbb);
+        const int c1 = nb < 46341 ? (sp + 1) * nb / sbb : (int)((long)(sp + 1) * nb / sbb);
+        work[pos + q] = AttnWork{b, g, sp, sbb, c0, c1, c != raw ? ~c : c, slot + g * sbb};
+      }
+    }
+  };
   // Up to 64 sequences: one wave sizes the list with shuffles (the same
-  // integer steps as the block-wide path below, so the same list), and one
-  // barrier hands each sequence's first item and context to the writers.
+  // integer steps as the block-wide path below, so the same list) and hands
+  // each sequence's first slot and context to the writers.
   if (B <= kWave && B <= NT / 2) {
     if (wave == 0) {
       const int raw = lane < B ? ctx[lane] : 0;
@@ -87,8 +153,8 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
         if (lane >= o) incl += up;
       }
       if (lane < B) {
-        s_seq[2 * lane] = incl - items;
-        s_seq[2 * lane + 1] = raw;
+        s_seq[3 * lane] = incl - items;
+        s_seq[3 * lane + 1] = raw;
       }
       if (lane == 63) {
         s_red[0] = S;
@@ -97,19 +163,8 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
     }
     __syncthreads();
     const int S = s_red[0], n_items = s_red[1];
-    const int tps = NT / B, b = threadIdx.x / tps, j = threadIdx.x % tps;
-    if (b < B) {
-      const int base = s_seq[2 * b], raw = s_seq[2 * b + 1];
-      const int c = attn_clamp_ctx(raw, max_blocks, T), n = (c + kBlock - 1) / kBlock;
-      const int sb = max(1, (n + S - 1) / S);
-      for (int q = j; q < Hkv * sb; q += tps) {
-        const int g = q / sb, sp = q - g * sb;
-        const int c0 = n < 46341 ? sp * n / sb : (int)((long)sp * n / sb);
-        const int c1 = n < 46341 ? (sp + 1) * n / sb : (int)((long)(sp + 1) * n / sb);
-        work[base + q] = AttnWork{b, g, sp, sb, c0, c1, c, c != raw};
-      }
-    }
-    for (int i = n_items + threadIdx.x; i < nwg; i += NT) work[i] = AttnWork{0, 0, 0, 0, 0, 0, 0, 0};
+    put_small(S);
+    for (int i = n_items + threadIdx.x; i < nwg; i += NT) work[i] = AttnWork{};
     __syncthreads();  // scratch is free again
     return;
   }
@@ -178,37 +233,40 @@ __device__ void build_attn_work(const int32_t* __restrict__ ctx, int B, int Hkv,
     if (w < wave) start += s_red[w];
     n_items += s_red[w];
   }
-  // the items: item q of sequence b (q = kv head * s_b + split) goes to
-  // start_b + q.  With fewer sequences than threads, NT / B threads share a
-  // sequence's items; otherwise each thread writes its own sequences'.
-  auto put = [&](int b, int raw, int q, int base) {
-    const int c = attn_clamp_ctx(raw, max_blocks, T), n = (c + kBlock - 1) / kBlock;
-    const int sb = max(1, (n + S - 1) / S);
-    const int g = q / sb, sp = q - g * sb;
-    const int c0 = n < 46341 ? sp * n / sb : (int)((long)sp * n / sb);
-    const int c1 = n < 46341 ? (sp + 1) * n / sb : (int)((long)(sp + 1) * n / sb);
-    work[base + q] = AttnWork{b, g, sp, sb, c0, c1, c, c != raw};
-  };
+  // the items: item q of sequence b (q = kv head * s_b + split) has partial
+  // slot start_b + q and goes to the list position its split length gives.
   if (B <= NT / 2) {
     if ((int)threadIdx.x < B) {  // per == 1 here
-      s_seq[2 * threadIdx.x] = start;
-      s_seq[2 * threadIdx.x + 1] = keep[0];
+      s_seq[3 * threadIdx.x] = start;
+      s_seq[3 * threadIdx.x + 1] = keep[0];
     }
     __syncthreads();
-    const int tps = NT / B, b = threadIdx.x / tps, j = threadIdx.x % tps;
-    if (b < B) {
-      const int base = s_seq[2 * b], raw = s_seq[2 * b + 1];
-      const int sb = max(1, (nblocks_raw(raw) + S - 1) / S);
-      for (int q = j; q < Hkv * sb; q += tps) put(b, raw, q, base);
-    }
+    put_small(S);
   } else {
+    if (order) {
+      for (int i = threadIdx.x; i < kOrderBuckets; i += NT) s_hist[i] = 0;
+      __syncthreads();
+      for (int b = b0; b < b1; ++b) {
+        const int n = nblocks_raw(raw_of(b)), sb = max(1, (n + S - 1) / S);
+        atomicAdd(&s_hist[bucket(n, sb)], Hkv * sb);
+      }
+      scan_hist();
+    }
     for (int b = b0; b < b1; ++b) {
-      const int raw = raw_of(b), sb = max(1, (nblocks_raw(raw) + S - 1) / S);
-      for (int q = 0; q < Hkv * sb; ++q) put(b, raw, q, start);
+      const int raw = raw_of(b);
+      const int c = attn_clamp_ctx(raw, max_blocks, T), n = (c + kBlock - 1) / kBlock;
+      const int sb = max(1, (n + S - 1) / S);
+      const int pos = order ? atomicAdd(&s_hist[bucket(n, sb)], Hkv * sb) : start;
+      for (int q = 0; q < Hkv * sb; ++q) {
+        const int g = q / sb, sp = q - g * sb;
+        const int c0 = n < 46341 ? sp * n / sb : (int)((long)sp * n / sb);
+        const int c1 = n < 46341 ? (sp + 1) * n / sb : (int)((long)(sp + 1) * n / sb);
+        work[pos + q] = AttnWork{b, g, sp, sb, c0, c1, c != raw ? ~c : c, start + g * sb};
+      }
       start += Hkv * sb;
     }
   }
-  for (int i = n_items + threadIdx.x; i < nwg; i += NT) work[i] = AttnWork{0, 0, 0, 0, 0, 0, 0, 0};
+  for (int i = n_items + threadIdx.x; i < nwg; i += NT) work[i] = AttnWork{};
   __syncthreads();  // scratch is free again
 }
 
@@ -217,6 +275,7 @@ struct AttnPlan {
   const int32_t* ctx;
   AttnWork* work;  // nullptr: no build
   int B, Hkv, T, max_blocks, nwg;
+  int order;       // longest splits first (attention_orders(nwg))
 };
 
 }  // namespace nj

@@ -93,7 +93,8 @@ __global__ __launch_bounds__(kNormThreads) void embed_norm_kernel(
   // attention's work list
   if (plan.work && blockIdx.x == 0) {
     __shared__ int scratch[attn_work_scratch_ints(kNormThreads)];
-    build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.work, scratch);
+    build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.order != 0, plan.work,
+                                  scratch);
     return;
   }
   const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;
@@ -143,7 +144,8 @@ __global__ __launch_bounds__(kNormThreads) void embed_gather_kernel(
   // attention's work list
   if (plan.work && blockIdx.x == 0) {
     __shared__ int scratch[attn_work_scratch_ints(kNormThreads)];
-    build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.work, scratch);
+    build_attn_work<kNormThreads>(plan.ctx, plan.B, plan.Hkv, plan.T, plan.max_blocks, plan.nwg, plan.order != 0, plan.work,
+                                  scratch);
     return;
   }
   const int row = blockIdx.x - (plan.work ? 1 : 0), b = row / T_, i = row % T_;

@@ -240,6 +240,9 @@ struct AttnArgs {
 // Workgroups of the bf16 path's work list, the bytes of the list, and the
 // partial buffer floats the splits need.
 int attention_plan(int B, int Hkv, int max_blocks);
+// Whether a work list of nwg workgroups is ordered longest split first: when
+// the grid is more than one round of resident attention workgroups.
+bool attention_orders(int nwg);
 size_t attention_work_bytes(int B, int Hkv);
 size_t attention_partial_floats(int B, int Hkv, int T, int G, int D);
 // The work list for attention launches over these context lengths (one
