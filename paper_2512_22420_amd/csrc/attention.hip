@@ -594,10 +594,16 @@ int attention_plan(int B, int Hkv, int max_blocks) {
   // kExtraWorkgroups more, and no more than the splits of kMinSplitBlocks
   // blocks the longest possible context could use.  The list sizes the
   // splits from the actual context lengths to fit this grid, so a long
-  // sequence gets proportionally more splits than a short one.
+  // sequence gets proportionally more splits than a short one.  Once the
+  // pairs alone fill half of the resident attention workgroups, fewer extra
+  // ones: the grid runs in rounds anyway, and longer splits pay their fixed
+  // start-up and merge once per more blocks (measured: 8B B=64 k=4 and the
+  // 7B shape at B=256 k=7 fastest with 128 extra, B=8 with 512).
   const int pairs = B * Hkv;
   const long cap = (long)pairs * std::max(1, (max_blocks + kMinSplitBlocks - 1) / kMinSplitBlocks);
-  return (int)std::max<long>(pairs, std::min<long>((long)pairs + kExtraWorkgroups, cap));
+  const int extra = 2 * pairs <= attn_wgs_per_cu(kAttnBuf, kAttnChunk) * device_cus() ? kExtraWorkgroups
+                                                                                      : std::min(kExtraWorkgroups, kExtraWorkgroupsLarge);
+  return (int)std::max<long>(pairs, std::min<long>((long)pairs + extra, cap));
 }
 
 bool attention_orders(int nwg) { return nwg > attn_wgs_per_cu(kAttnBuf, kAttnChunk) * device_cus(); }

@@ -38,7 +38,8 @@ namespace nj {
 #define NJ_ATTN_EXTRA_WGS 512
 #endif
 constexpr int kMinSplitBlocks = NJ_ATTN_MIN_SPLIT;  // cached blocks a split holds at least
-constexpr int kExtraWorkgroups = NJ_ATTN_EXTRA_WGS; // workgroups beyond one per (sequence, KV head)
+constexpr int kExtraWorkgroups = NJ_ATTN_EXTRA_WGS; // workgroups beyond one per (sequence, KV head), at most
+constexpr int kExtraWorkgroupsLarge = 128;          // ... once the pairs fill half of the resident workgroups
 
 struct AttnWork {
   int b, kvh, split, nsplit;  // nsplit == 0: no item for this workgroup
