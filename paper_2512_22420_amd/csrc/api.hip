@@ -101,12 +101,28 @@ hipError_t launch_qkv_store(int dt, const void* x, const void* w, void* y, int M
   return launch_gemm_plan(x, w, y, M, N, K, kEpiStore, gemm_plan(M, N, K, kEpiQkvRope), gcnt, gpart, s, x_kblocked);
 }
 
+// Whether a window of M rows runs with the RMSNorms folded into the GEMMs
+// (the producer of h writes bf16(h * gain) and per-tile sums of h^2, the
+// consumer scales its output rows by 1/rms): bf16, the QKV projection on the
+// weight-streaming kernel (RoPE in its epilogue), and each residual GEMM (O,
+// down) either streaming or on a tiled plan whose split tiles are reduced by
+// all their workgroups (the epilogue that writes the next norm's inputs);
+// gate/up and the LM head take the row scale on either kernel.
 bool fold_norms(const nj_model_desc& d, int M) {
-  if (d.dtype != NJ_BF16) return false;
+  if (d.dtype != NJ_BF16 || d.d_model % 32) return false;
   const int HD = d.n_heads * d.head_dim, QKV = (d.n_heads + 2 * d.n_kv_heads) * d.head_dim;
-  return gemm_streams(M, QKV, d.d_model, kEpiQkvRope) && gemm_streams(M, d.d_model, HD, kEpiResidual) &&
-         gemm_streams(M, 2 * d.ffn_dim, d.d_model, kEpiSwiglu) &&
-         gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual) && gemm_streams(M, d.vocab, d.d_model, kEpiStore);
+  if (!gemm_streams(M, QKV, d.d_model, kEpiQkvRope)) return false;
+  // a tiled consumer reads each row's partials in 16-byte pieces
+  const int F2 = 2 * d.ffn_dim;
+  if ((!gemm_streams(M, F2, d.d_model, kEpiSwiglu) || !gemm_streams(M, d.vocab, d.d_model, kEpiStore)) &&
+      ((d.d_model + 127) / 128) % 4)
+    return false;
+  auto producer_ok = [&](int K) {
+    const GemmPlan p = gemm_plan(M, d.d_model, K, kEpiResidual);
+    return p.tile == kTileNone ||
+           (p.par && p.part_bytes > 0 && tile_one_segment(p, K) && p.grid <= device_cus());
+  };
+  return producer_ok(HD) && producer_ok(d.ffn_dim);
 }
 
 Layout layout(const nj_model_desc& d, int B, int k) {
@@ -420,11 +436,11 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   // Without the folded norm, the input of each GEMM that runs on the
   // LDS-tiled kernel is written k-blocked by its producer (norm, attention,
   // SwiGLU epilogue), so the tile loads read 1 KB contiguous units.
-  const bool kb_qkv = bf && !fused && !gemm_streams(M, QKV, d.d_model, kEpiQkvRope);
-  const bool kb_o = bf && !fused && !gemm_streams(M, d.d_model, HD, kEpiResidual);
-  const bool kb_gu = bf && !fused && !gemm_streams(M, F2, d.d_model, kEpiSwiglu);
-  const bool kb_dn = bf && !fused && d.ffn_dim % 32 == 0 && !gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual);
-  const bool kb_lm = bf && !fused && !gemm_streams(M, d.vocab, d.d_model, kEpiStore);
+  const bool kb_qkv = bf && !gemm_streams(M, QKV, d.d_model, kEpiQkvRope);
+  const bool kb_o = bf && !gemm_streams(M, d.d_model, HD, kEpiResidual);
+  const bool kb_gu = bf && !gemm_streams(M, F2, d.d_model, kEpiSwiglu);
+  const bool kb_dn = bf && d.ffn_dim % 32 == 0 && !gemm_streams(M, d.d_model, d.ffn_dim, kEpiResidual);
+  const bool kb_lm = bf && !gemm_streams(M, d.vocab, d.d_model, kEpiStore);
   float* ssq = reinterpret_cast<float*>(ws + L.ssq);
   const int nt = (d.d_model + 127) / 128;
   const GemmNorm scale_in{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, nullptr};
@@ -480,12 +496,16 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
     NJ_TRY(NJ_PROF_ATTENTION, launch_attention(aa, s), "attention");
     const void* g_next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : w->final_norm;
     if (fused) {
-      const GemmNorm to_ffn{nullptr, 0, 0.f, lw.ffn_norm, x, ssq, nullptr};
-      NJ_TRY(NJ_PROF_O, launch_gemm_norm(o, lw.w_o, h, M, d.d_model, HD, kEpiResidualNorm, to_ffn, gcnt, gpart, s), "o gemm");
-      NJ_TRY(NJ_PROF_GATE_UP, launch_gemm_norm(x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, scale_in, gcnt, gpart, s),
+      // each input in the layout its consumer's kernel reads (k-blocked for a tiled plan)
+      const GemmNorm to_ffn{nullptr, 0, 0.f, lw.ffn_norm, x, ssq, nullptr, kb_gu};
+      NJ_TRY(NJ_PROF_O, launch_gemm_norm(o, lw.w_o, h, M, d.d_model, HD, kEpiResidualNorm, to_ffn, gcnt, gpart, s, nullptr, kb_o),
+             "o gemm");
+      NJ_TRY(NJ_PROF_GATE_UP, launch_gemm_norm(x, lw.w_gate_up, act, M, F2, d.d_model, kEpiSwiglu, scale_in, gcnt, gpart, s,
+                                               nullptr, kb_gu, kb_dn),
              "gate_up gemm");
-      const GemmNorm to_next{nullptr, 0, 0.f, g_next, x, ssq, nullptr};
-      NJ_TRY(NJ_PROF_DOWN, launch_gemm_norm(act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidualNorm, to_next, gcnt, gpart, s),
+      const GemmNorm to_next{nullptr, 0, 0.f, g_next, x, ssq, nullptr, l + 1 < d.n_layers ? kb_qkv : kb_lm};
+      NJ_TRY(NJ_PROF_DOWN, launch_gemm_norm(act, lw.w_down, h, M, d.d_model, d.ffn_dim, kEpiResidualNorm, to_next, gcnt, gpart,
+                                            s, nullptr, kb_dn),
              "down gemm");
     } else {
       NJ_TRY(NJ_PROF_O, launch_gemm(dt, o, lw.w_o, h, M, d.d_model, HD, kEpiResidual, gcnt, gpart, s, kb_o), "o gemm");
@@ -500,7 +520,8 @@ int verify_impl(const nj_model_desc* desc, const nj_weights* w, const nj_kv_cach
   float* stats = accept_stats_ptr(ws + L.stats);
   if (fused) {
     const GemmNorm lm{ssq, nt, d.rms_eps, nullptr, nullptr, nullptr, stats};
-    NJ_TRY(NJ_PROF_LM_HEAD, launch_gemm_norm(x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiLogits, lm, gcnt, gpart, s),
+    NJ_TRY(NJ_PROF_LM_HEAD, launch_gemm_norm(x, w->lm_head, logits, M, d.vocab, d.d_model, kEpiLogits, lm, gcnt, gpart, s,
+                                             nullptr, kb_lm),
            "lm_head gemm");
     stats_ready = true;
   } else {

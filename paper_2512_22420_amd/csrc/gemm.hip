@@ -86,6 +86,7 @@ struct GemmK {
   int par;          // split K: every chunk's workgroup reduces and finishes a slice of the block's rows
   int par_l2;       // par, and round-robin dispatch puts every chunk of a block on one XCD (see below)
   unsigned foreign; // chunks that act as if dispatched elsewhere (tests of the fallback; normally 0)
+  int xg_kb;        // kEpiResidualNorm: xg stored k-blocked, [Nout/32][M][32]
 };
 
 // The weight stream of one 16-row weight tile (wp: this lane's piece of k-step
@@ -573,7 +574,7 @@ __global__ __launch_bounds__(kNW * 64) void gemm_stream_kernel(GemmK a) {
         u32x2 o;
         o[0] = pack_bf16x2(hv[0] * bf2f((bf16_t)(gw[0] & 0xffffu)), hv[1] * bf2f((bf16_t)(gw[0] >> 16)));
         o[1] = pack_bf16x2(hv[2] * bf2f((bf16_t)(gw[1] & 0xffffu)), hv[3] * bf2f((bf16_t)(gw[1] >> 16)));
-        *reinterpret_cast<u32x2*>(a.xg + (size_t)m * Nout + n) = o;
+        *reinterpret_cast<u32x2*>(a.xg_kb ? a.xg + ((size_t)(n >> 5) * M + m) * 32 + (n & 31) : a.xg + (size_t)m * Nout + n) = o;
         part = hv[0] * hv[0];
         part = fmaf(hv[1], hv[1], part);
         part = fmaf(hv[2], hv[2], part);
@@ -1129,15 +1130,26 @@ int logits_stat_entries(int M, int N, int K) {
 }
 
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
-                            int* counters, float* part, hipStream_t s, const QkvRope* rope) {
+                            int* counters, float* part, hipStream_t s, const QkvRope* rope, bool x_kblocked,
+                            bool y_kblocked) {
   const int pe = epi == kEpiResidualNorm ? kEpiResidual : epi == kEpiLogits ? kEpiStore : epi;
-  const GemmPlan p = gemm_plan(M, N, K, pe);
-  if (p.tile != kTileNone) return hipErrorInvalidValue;  // the caller checks gemm_streams first
+  const GemmPlan p = gemm_plan(M, N, K, epi == kEpiQkvRope ? kEpiQkvRope : pe);
+  if (p.tile != kTileNone) {
+    // the tiled kernel: the row scale in every epilogue, the next norm's
+    // inputs from the slice-reduced residual epilogue (it checks the plan);
+    // RoPE lives in the streaming epilogue only
+    if (epi == kEpiQkvRope) return hipErrorInvalidValue;
+    return launch_gemm_tile(x, w, y, M, N, K, pe, p, counters, part, s, epi == kEpiLogits ? nm.stats : nullptr,
+                            x_kblocked, y_kblocked, &nm);
+  }
+  if (x_kblocked) return hipErrorInvalidValue;  // the streaming kernel reads row-major x
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   GemmK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, p.nkc > 1 ? part : nullptr,
           p.nkc > 1 ? counters : nullptr, M, Nout, K, K / 32, p.stages_per_chunk, (int)p.part_bytes, nm.stats,
           (Nout + kStatChunk - 1) / kStatChunk, nm.ssq_in, nm.nt_in, nm.eps,
           static_cast<const bf16_t*>(nm.gain), static_cast<bf16_t*>(nm.xg), nm.ssq_out, rope ? *rope : QkvRope{}};
+  a.ykbM = y_kblocked ? M : 0;
+  a.xg_kb = nm.xg_kb;
   switch (epi) {
     case kEpiQkvRope: return launch_stream<kEpiQkvRope>(a, p, s);
     case kEpiStore: return launch_stream<kEpiStore>(a, p, s);

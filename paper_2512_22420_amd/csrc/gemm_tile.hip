@@ -56,9 +56,22 @@ struct TileK {
   int par;        // one-segment split plans: every workgroup of a tile reduces a slice of its rows
   int par_l2;     // par, and partials may go through one XCD's L2 (see the split hand-off)
   unsigned foreign;  // segments that act as if dispatched elsewhere (tests of the fallback; normally 0)
+  // RMSNorm folded into the neighbours (nullable).  Consumer: every output row
+  // m is scaled by 1 / sqrt(sum_t ssq_in[m][t] / K + eps) (x was stored as
+  // bf16(h * gain)).  Producer (kEpiResidual, slice-reduced splits only): with
+  // h = y + x . w^T also xg = bf16(h * gain) (k-blocked [N/32][M][32] when
+  // xg_kb) and ssq_out[m][t] = sum of h^2 over columns 128t .. 128t+127.
+  const float* ssq_in;
+  int nt_in;
+  float eps;
+  const bf16_t* gain;
+  bf16_t* xg;
+  float* ssq_out;
+  int xg_kb, nt_out;
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
+constexpr int kMaxSsq4 = 16;  // folded-norm consumer: up to 64 sums-of-squares partials per row
 
 
 // Split partials of a tile cut into nseg segments: [segment][M][NG][Nout]
@@ -69,17 +82,23 @@ typedef __attribute__((address_space(3))) void lds_void;
 // this XCD's L2 when bit c of l2seg is set, else from memory.
 template <int BM, int BN, int NG, int EPI>
 __device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nseg, unsigned l2seg, int nslice, int sl,
-                             int m0, int n0) {
+                             int m0, int n0, const float* s_rinv) {
   constexpr int NC = NG == 1 ? BN : BN / 2;  // output columns of the tile (per group)
   constexpr int C4 = NC / 4;
+  static_assert(EPI != kEpiResidual || C4 % 32 == 0, "a row's 128-column segments are whole half-waves of units");
   const int M = a.M, Nout = a.Nout;
   const int rs = (BM + nslice - 1) / nslice;
   const int r0 = m0 + sl * rs, r1 = min(min(m0 + (sl + 1) * rs, m0 + BM), M);
   const int units = max(0, r1 - r0) * C4;
   auto poff = [&](int c, int m, int q, int n) { return (uint32_t)((((size_t)c * M + m) * NG + q) * Nout + n) * 4u; };
-  for (int u = threadIdx.x; u < units; u += blockDim.x) {
-    const int m = r0 + u / C4, n = n0 + (u % C4) * 4;
-    if (n >= Nout) continue;
+  // whole passes of the workgroup (every lane takes part in the norm
+  // epilogue's butterfly), units past the slice or the matrix idle
+  for (int u0 = 0; u0 < units; u0 += blockDim.x) {
+    const int u = u0 + (int)threadIdx.x;
+    const int m = r0 + min(u, units - 1) / C4, n = n0 + (u % C4) * 4;
+    const bool ok = u < units && n < Nout;
+    float part = 0.f;
+    if (ok) {
     auto ld = [&](int c, int q) {
       return (l2seg >> c) & 1u ? xcd_load(prs, poff(c, m, q, n)) : coherent_load(prs, poff(c, m, q, n));
     };
@@ -99,11 +118,29 @@ __device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nse
 #pragma unroll
           for (int q = 0; q < NG; ++q) v[q] = v[q] + t[j][q];
     }
+    if (a.ssq_in) {
+      const float sc = s_rinv[m - m0];
+#pragma unroll
+      for (int q = 0; q < NG; ++q) v[q] *= sc;
+    }
     if constexpr (EPI == kEpiStore) {
       *reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n) = v[0];
     } else if constexpr (EPI == kEpiResidual) {
       f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(a.Y) + (size_t)m * Nout + n);
-      *p = *p + v[0];
+      const f32x4 hv = *p + v[0];
+      *p = hv;
+      if (a.xg) {  // the next RMSNorm's inputs
+        const u32x2 gw = *reinterpret_cast<const u32x2*>(a.gain + n);
+        u32x2 o;
+        o[0] = pack_bf16x2(hv[0] * bf2f((bf16_t)(gw[0] & 0xffffu)), hv[1] * bf2f((bf16_t)(gw[0] >> 16)));
+        o[1] = pack_bf16x2(hv[2] * bf2f((bf16_t)(gw[1] & 0xffffu)), hv[3] * bf2f((bf16_t)(gw[1] >> 16)));
+        bf16_t* xp = a.xg_kb ? a.xg + ((size_t)(n >> 5) * M + m) * 32 + (n & 31) : a.xg + (size_t)m * Nout + n;
+        *reinterpret_cast<u32x2*>(xp) = o;
+        part = hv[0] * hv[0];
+        part = fmaf(hv[1], hv[1], part);
+        part = fmaf(hv[2], hv[2], part);
+        part = fmaf(hv[3], hv[3], part);
+      }
     } else {
       const f32x4 gt = v[0], up = v[NG - 1];
       u32x2 o;
@@ -112,6 +149,17 @@ __device__ void slice_reduce(const TileK& a, __amdgpu_buffer_rsrc_t prs, int nse
       bf16_t* yp = a.ykb ? static_cast<bf16_t*>(a.Y) + ((size_t)(n >> 5) * M + m) * 32 + (n & 31)
                          : static_cast<bf16_t*>(a.Y) + (size_t)m * Nout + n;
       *reinterpret_cast<u32x2*>(yp) = o;
+    }
+    }
+    if constexpr (EPI == kEpiResidual) {
+      if (a.xg) {  // sum of h^2 over each 128-column segment: lane order, then a 5-step butterfly over its 32 units
+        part += __shfl_xor(part, 1);
+        part += __shfl_xor(part, 2);
+        part += __shfl_xor(part, 4);
+        part += __shfl_xor(part, 8);
+        part += __shfl_xor(part, 16);
+        if (u < units && (u % 32) == 0 && n < Nout) a.ssq_out[(size_t)m * a.nt_out + n / 128] = part;
+      }
     }
   }
 }
@@ -138,6 +186,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   static_assert(DIST * UPW <= 63, "load counter range");
   __shared__ __attribute__((aligned(16))) bf16_t lds[NBUF * STAGE];
   __shared__ int s_last;
+  __shared__ float s_rinv[BM];  // consumer of a folded RMSNorm: 1/rms of the tile's rows
 
   // Stream-K schedule over weight-tile columns.  The work of one M tile is
   // tiles_n x KU units (a unit: one output tile, 64 of k; units k-major
@@ -265,9 +314,33 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
   // past the chunk re-load its last stage into a buffer nobody reads, so
   // every iteration issues the same number of loads and the wait counts
   // below are exact.
+  // Folded-norm consumer: this thread's row of sums-of-squares partials
+  // (thread t: row m0 + t), loaded ahead of the stages as assembly so that
+  // the compiler adds no wait of its own (which would also drain the stages);
+  // the prologue's wait below leaves only stage loads outstanding, so these
+  // have landed by then.
+  f32x4 ssq_v[kMaxSsq4];
+  const bool rinv_row = a.ssq_in && seg == 0 && (int)threadIdx.x < BM;
+  if (rinv_row) {
+    const float* sp = a.ssq_in + (size_t)min(m0 + (int)threadIdx.x, M - 1) * a.nt_in;
+#pragma unroll
+    for (int q = 0; q < kMaxSsq4; ++q)
+      if (q * 4 < a.nt_in) asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(ssq_v[q]) : "v"(sp + 4 * q) : "memory");
+  }
 #pragma unroll
   for (int d = 0; d < NBUF; ++d) issue(min(st0 + d, st1 - 1), d);
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NBUF - 1) * UPW) : "memory");
+  if (rinv_row) {  // 1/rms of row m0 + t (partials summed in order); read after later barriers
+#pragma unroll
+    for (int q = 0; q < kMaxSsq4; ++q) asm volatile("" : "+v"(ssq_v[q]));
+    float sum = 0.f;
+#pragma unroll
+    for (int q = 0; q < kMaxSsq4; ++q)
+      if (q * 4 < a.nt_in)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += ssq_v[q][e];
+    s_rinv[threadIdx.x] = 1.0f / sqrtf(sum / (float)K + a.eps);
+  }
 #pragma unroll
   for (int j = 0; j < TN; ++j) wf[0][j] = ld16(wrd[0] + wofs(j) * 512);
 #pragma unroll
@@ -389,9 +462,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
         const unsigned l2seg = tile_l2 ? ~fmask & all : 0u;
         if (fmask != 0 && fmask != all) {
           // mixed: the first segment on the expected XCD reduces the whole tile
-          if (slot == __builtin_ctz(l2seg)) slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, l2seg, 1, 0, m0, n0);
+          if (slot == __builtin_ctz(l2seg)) slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, l2seg, 1, 0, m0, n0, s_rinv);
         } else {
-          slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, l2seg, nseg, slot, m0, n0);
+          slice_reduce<BM, BN, NG, EPI>(a, prs, nseg, l2seg, nseg, slot, m0, n0, s_rinv);
         }
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
@@ -430,6 +503,15 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tile_kernel(TileK a) {
           }
         }
       }
+    }
+  }
+
+  if (a.ssq_in) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const float sc = s_rinv[min(out_m(i), M - 1) - m0];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] *= sc;
     }
   }
 
@@ -553,7 +635,7 @@ int tile_bn(int cfg) { return cfg == kTile128x128 || cfg == kTile96x128 ? 128 : 
 
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s, float* stats, bool x_kblocked,
-                            bool y_kblocked) {
+                            bool y_kblocked, const GemmNorm* nm) {
   const int Nout = (epi == kEpiSwiglu) ? N / 2 : N;
   const bool split = p.part_bytes > 0;
   const long units = (long)p.ntiles * (K / 64);  // per M tile
@@ -563,11 +645,26 @@ hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N,
   TileK a{static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), y, split ? part : nullptr,
           split ? counters : nullptr, M, Nout, K, p.mblocks, p.ntiles,
           (int)p.part_bytes, epi == kEpiStore ? stats : nullptr, (Nout + kStatChunk - 1) / kStatChunk,
-          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid, 0, 0, 0u};
+          x_kblocked ? 1 : 0, y_kblocked ? 1 : 0, p.grid, 0, 0, 0u,
+          nullptr, 0, 0.f, nullptr, nullptr, nullptr, 0, 0};
   const bool one_segment = tile_one_segment(p, K);
   a.par = split && one_segment && p.par && !a.stats && p.grid <= device_cus() ? 1 : 0;
   a.par_l2 = a.par && p.grid / ((long)p.ntiles * p.mblocks) <= kSplitL2MaxChunks ? 1 : 0;
   a.foreign = split_foreign_mask();
+  if (nm) {
+    if (nm->ssq_in) {
+      // whole 16-byte loads of a row's partials
+      if (nm->nt_in < 1 || nm->nt_in > 4 * kMaxSsq4 || nm->nt_in % 4) return hipErrorInvalidValue;
+      a.ssq_in = nm->ssq_in, a.nt_in = nm->nt_in, a.eps = nm->eps;
+    }
+    if (nm->xg) {
+      // the producer side lives in the slice reduction: residual plans whose
+      // split tiles are reduced by all their workgroups
+      if (epi != kEpiResidual || !a.par || !nm->gain || !nm->ssq_out || Nout % 32) return hipErrorInvalidValue;
+      a.gain = static_cast<const bf16_t*>(nm->gain), a.xg = static_cast<bf16_t*>(nm->xg), a.ssq_out = nm->ssq_out;
+      a.xg_kb = nm->xg_kb, a.nt_out = (Nout + 127) / 128;
+    }
+  }
   switch (p.tile) {
     // 8 waves of 128 x 64 (two per SIMD: one issues MFMAs while the other
     // waits on LDS or a barrier); one segment per workgroup only (the

@@ -136,9 +136,10 @@ struct GemmNorm {
   int nt_in;            // partials per row (<= 64)
   float eps;
   const void* gain;     // producer side: bf16 [N]
-  void* xg;             // bf16 [M][N]
+  void* xg;             // bf16 [M][N], or k-blocked [N/32][M][32] with xg_kb
   float* ssq_out;       // [M][ceil(N / 128)]
   float* stats;         // kEpiLogits only
+  int xg_kb = 0;
 };
 // kEpiQkvRope: the QKV GEMM's 128-column groups are its heads (head_dim 128):
 // q heads are rotated and stored to q_out [M][H][128], k heads rotated into
@@ -164,8 +165,12 @@ bool gemm_streams(int M, int N, int K, int epi);
 // (max, sum of exp) pairs per row that the LM-head GEMM's statistics epilogue
 // writes: one per 128-column chunk, per persistent workgroup, or per column tile
 int logits_stat_entries(int M, int N, int K);
+// A tiled plan takes the row scale in any epilogue and the next norm's inputs
+// only from a slice-reduced residual plan (not QKV + RoPE); x_kblocked: x is
+// k-blocked (tiled plans only); y_kblocked: the SwiGLU output k-blocked.
 hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmNorm& nm,
-                            int* counters, float* part, hipStream_t s, const QkvRope* rope = nullptr);
+                            int* counters, float* part, hipStream_t s, const QkvRope* rope = nullptr,
+                            bool x_kblocked = false, bool y_kblocked = false);
 // The LDS-tiled kernel alone (K % 64 == 0).  x_kblocked: x is stored
 // k-blocked, [K/32][M][32] (element (m, k) at ((k / 32) * M + m) * 32 + k % 32),
 // so that each 16-row x 32-column operand unit is 1 KB of contiguous memory;
@@ -173,7 +178,8 @@ hipError_t launch_gemm_norm(const void* x, const void* w, void* y, int M, int N,
 // tiled GEMM's input).
 hipError_t launch_gemm_tile(const void* x, const void* w, void* y, int M, int N, int K, int epi, const GemmPlan& p,
                             int* counters, float* part, hipStream_t s,
-                            float* stats = nullptr, bool x_kblocked = false, bool y_kblocked = false);
+                            float* stats = nullptr, bool x_kblocked = false, bool y_kblocked = false,
+                            const GemmNorm* nm = nullptr);
 
 // h[r] = E[id(r)], x[r] = rmsnorm(h[r]) * gain, ids from last/draft tokens.
 struct AttnPlan;
